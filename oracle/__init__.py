@@ -1,0 +1,167 @@
+"""CPU oracle for the Mamba-3 SSM hot path (fp64, plain sequential recurrence).
+
+TEST INFRASTRUCTURE.  Only the tests, the smoke check and the benchmark's CPU
+baseline may import it; the library and its Python binding never do.  It
+shares no code with the HIP path.  The arithmetic lives in m3_oracle.c (see
+its header for the equations and the readings of the paper it follows); this
+module builds it with gcc, marshals arrays and extracts (batch, head) slices
+from tensors in the library layout.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "m3_oracle.c")
+_LIB = os.path.join(_HERE, "libm3_oracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile the oracle with gcc (OpenMP over slices).  The target ISA is
+    the portable x86-64-v3 so the library runs on any AVX2 host."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", "-O2", "-march=x86-64-v3", "-fopenmp", "-shared",
+                        "-fPIC", "-std=c11", _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build()
+        lib = ctypes.CDLL(_LIB)
+        i64, dp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+        lib.m3o_scan.argtypes = [i64] * 5 + [dp] * 8 + [dp] * 3 + [dp] * 4 + [ci]
+        lib.m3o_scan.restype = ci
+        lib.m3o_step.argtypes = [i64] * 4 + [dp] * 3 + [dp] * 8 + [dp, ci]
+        lib.m3o_step.restype = ci
+        _lib = lib
+    return _lib
+
+
+def _f64(a):
+    return np.ascontiguousarray(np.asarray(a, dtype=np.float64))
+
+
+def _ptr(a):
+    return None if a is None else a.ctypes.data
+
+
+def scan(x, B, C, dt, A, lam, theta, D, init_state=None, init_B=None,
+         init_X=None, nthreads=0, return_threads=False):
+    """Sequential scan over S independent slices.
+
+    x [S,L,R,P], B/C [S,L,R,N], dt/A/lam [S,L], theta [S,L,N/2], D [S],
+    optional init_state [S,N,P] and carry init_B [S,R,N], init_X [S,R,P].
+    Returns y [S,L,R,P], state [S,N,P], carryB [S,R,N], carryX [S,R,P].
+    """
+    x, B, C = _f64(x), _f64(B), _f64(C)
+    dt, A, lam, theta, D = _f64(dt), _f64(A), _f64(lam), _f64(theta), _f64(D)
+    S, L, R, P = x.shape
+    N = B.shape[-1]
+    assert B.shape == (S, L, R, N) and C.shape == (S, L, R, N)
+    assert dt.shape == (S, L) and A.shape == (S, L) and lam.shape == (S, L)
+    assert theta.shape == (S, L, N // 2) and D.shape == (S,)
+    if (init_B is None) != (init_X is None):
+        raise ValueError("give both carry halves or neither")
+    init_state = None if init_state is None else _f64(init_state)
+    init_B = None if init_B is None else _f64(init_B)
+    init_X = None if init_X is None else _f64(init_X)
+    y = np.empty((S, L, R, P))
+    state = np.empty((S, N, P))
+    cB = np.empty((S, R, N))
+    cX = np.empty((S, R, P))
+    used = _load().m3o_scan(S, L, N, P, R, _ptr(x), _ptr(B), _ptr(C), _ptr(dt),
+                            _ptr(A), _ptr(lam), _ptr(theta), _ptr(D),
+                            _ptr(init_state), _ptr(init_B), _ptr(init_X),
+                            _ptr(y), _ptr(state), _ptr(cB), _ptr(cX),
+                            int(nthreads))
+    out = (y, state, cB, cX)
+    return (out, used) if return_threads else out
+
+
+def step(state, carryB, carryX, x, B, C, dt, A, lam, theta, D, nthreads=0):
+    """One decode step on S slices.  Returns (y [S,R,P], state', carryB',
+    carryX'); the inputs are not modified."""
+    state, carryB, carryX = _f64(state).copy(), _f64(carryB).copy(), _f64(carryX).copy()
+    x, B, C = _f64(x), _f64(B), _f64(C)
+    dt, A, lam, theta, D = _f64(dt), _f64(A), _f64(lam), _f64(theta), _f64(D)
+    S, R, P = x.shape
+    N = B.shape[-1]
+    assert state.shape == (S, N, P) and theta.shape == (S, N // 2)
+    y = np.empty((S, R, P))
+    _load().m3o_step(S, N, P, R, _ptr(state), _ptr(carryB), _ptr(carryX),
+                     _ptr(x), _ptr(B), _ptr(C), _ptr(dt), _ptr(A), _ptr(lam),
+                     _ptr(theta), _ptr(D), _ptr(y), int(nthreads))
+    return y, state, carryB, carryX
+
+
+# ---------------------------------------------------------------------------
+# Slice extraction from tensors in the library layout.
+# ---------------------------------------------------------------------------
+
+def _np(t):
+    """torch tensor (any device, any float dtype) or array -> fp64 numpy,
+    exactly (bf16 values are representable in fp64)."""
+    try:
+        import torch
+        if isinstance(t, torch.Tensor):
+            return t.detach().to("cpu", torch.float64).numpy()
+    except ImportError:  # pragma: no cover
+        pass
+    return np.asarray(t, dtype=np.float64)
+
+
+def slices_of_scan(x, Bm, Cm, dt, A, lam, theta, D, slices, t0=0, t1=None):
+    """Gather the oracle's per-slice arrays for (b, h) pairs in `slices` from
+    library-layout tensors x [B,L,H,R,P], Bm/Cm [B,L,H,R,N], dt/lam [B,L,H],
+    A [H] (per head), theta [B,L,H,N/2], D [H]; tokens t0..t1."""
+    t1 = x.shape[1] if t1 is None else t1
+    bs = [b for b, _ in slices]
+    hs = [h for _, h in slices]
+
+    def take(t):
+        # stack of t[b, t0:t1, h, ...] over (b, h) in slices
+        return np.stack([_np(t[b, t0:t1, h]) for b, h in zip(bs, hs)])
+
+    xs, Bs, Cs = take(x), take(Bm), take(Cm)
+    dts, lams, ths = take(dt), take(lam), take(theta)
+    A_np, D_np = _np(A), _np(D)
+    As = np.repeat(A_np[hs][:, None], dts.shape[1], axis=1)
+    Ds = D_np[hs]
+    return dict(x=xs, B=Bs, C=Cs, dt=dts, A=As, lam=lams, theta=ths, D=Ds)
+
+
+def slices_of_state(t, slices):
+    """state-like tensor [B,H,...] -> numpy [S,...] for the given (b, h)."""
+    return np.stack([_np(t[b, h]) for b, h in slices])
+
+
+def slices_of_step(x, Bm, Cm, dt, lam, theta, slices):
+    """Per-step tensors x [B,H,R,P], Bm/Cm [B,H,R,N], dt/lam [B,H],
+    theta [B,H,N/2] -> per-slice arrays."""
+    return dict(x=slices_of_state(x, slices), B=slices_of_state(Bm, slices),
+                C=slices_of_state(Cm, slices),
+                dt=np.array([_np(dt[b, h]) for b, h in slices], dtype=np.float64).reshape(-1),
+                lam=np.array([_np(lam[b, h]) for b, h in slices], dtype=np.float64).reshape(-1),
+                theta=slices_of_state(theta, slices))
+
+
+def rel_err(got, ref):
+    """Infinity-norm relative error max|got - ref| / max|ref| (0 if both are
+    zero).  Applied per slice by the parity tests."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    den = np.max(np.abs(ref)) if ref.size else 0.0
+    num = np.max(np.abs(got - ref)) if ref.size else 0.0
+    if den == 0.0:
+        return float(num)
+    return float(num / den)
