@@ -1,0 +1,221 @@
+"""Benchmark of the Mamba-3 SSM hot path on one MI355X.
+
+One timed step = one pass of the whole hot path:
+  * one m3_scan_fwd over the SISO bf16 prefill batch (B=4, L=2048, H=16,
+    P=64, N=128, R=1, chunk 64), inputs rotated over 4 resident copies so the
+    256 MB Infinity Cache cannot hold them between steps;
+  * one m3_step over the decode batch (B=256, H=32, P=64, N=128, R=4, fp32
+    state from a 1024-token prefill), each step with fresh seeded inputs.
+`value` is the prefill tokens/s; `decode_us_per_step` the decode step time.
+Both come from HIP events recorded on the stream the kernels run on.  The
+CPU oracle is timed on a bounded sample of the same workloads on the host.
+
+Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "prefill scan tokens/s + decode step µs @B=256; % of MFMA/HBM roofline"
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=200)
+    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); every (batch, head) "
+              "slice is independent, so more GPUs would only split the batch.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_2603_15569_amd import m3, roofline
+    from paper_2603_15569_amd.inputs import WORKLOADS, make_step_inputs, workload_inputs
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    # ---------------- prefill workload (SISO bf16) ----------------
+    wp = WORKLOADS[1]
+    base = workload_inputs(1, device=dev)
+    copies = [base] + [type(base)(**{k: (v.clone() if isinstance(v, torch.Tensor) else v)
+                                     for k, v in base.__dict__.items()}) for _ in range(3)]
+    Bp, Lp, Hp, Rp, Pp = base.x.shape
+    Np = base.Bm.shape[-1]
+    Qp = wp["chunk"]
+    dims = m3.scan_dims(base.x, base.Bm, Qp, base.A)
+    ws = torch.empty(max(m3.workspace_bytes(dims), 1), dtype=torch.uint8, device=dev)
+    out = (torch.empty_like(base.x), torch.empty(Bp, Hp, Np, Pp, device=dev),
+           torch.empty(Bp, Hp, Rp, Np, device=dev, dtype=base.x.dtype),
+           torch.empty(Bp, Hp, Rp, Pp, device=dev, dtype=base.x.dtype))
+
+    def scan(i):
+        c = copies[i % len(copies)]
+        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.theta, c.D, chunk=Qp, out=out,
+                    workspace=ws)
+
+    # ---------------- decode workload (B=256, MIMO R=4) ----------------
+    wd = WORKLOADS[4]
+    layer = workload_inputs(4, device=dev)
+    _, dstate, (dcB, dcX) = m3.scan_fwd(layer.x, layer.Bm, layer.Cm, layer.dt, layer.A,
+                                        layer.lam, layer.theta, layer.D, chunk=wd["chunk"])
+    del layer.x, layer.Bm, layer.Cm, layer.theta, layer.lam, layer.dt  # free the prefill inputs
+    torch.cuda.synchronize()
+    n_step_inputs = max(1, min(args.steps + args.warmup, wd["steps"]))
+    step_in = []
+    for s in range(n_step_inputs):
+        step_in.append(make_step_inputs(_LayerView(layer, wd), s, device=dev))
+    yd = torch.empty_like(step_in[0].x)
+
+    def dstep(i):
+        st = step_in[i % n_step_inputs]
+        m3.step(dstate, (dcB, dcX), st.x, st.Bm, st.Cm, st.dt, layer.A, st.lam, st.theta, layer.D,
+                y=yd)
+
+    # ---------------- timed loop ----------------
+    for i in range(args.warmup):
+        scan(i)
+        dstep(i)
+    torch.cuda.synchronize()
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    for i in range(args.steps):
+        ev[i][0].record(stream)
+        scan(i)
+        ev[i][1].record(stream)
+        dstep(args.warmup + i)
+        ev[i][2].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    scan_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
+    step_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
+    tot_ms = np.array([e[0].elapsed_time(e[2]) for e in ev])
+
+    tokens = Bp * Lp
+    prefill_tok_s = tokens / (scan_ms.mean() * 1e-3)
+    dec_us = step_ms.mean() * 1e3
+
+    # rooflines (algorithmic bytes / FLOPs per launch, see roofline.py)
+    Bd, Hd, Rd, Pd = step_in[0].x.shape
+    Nd = step_in[0].Bm.shape[-1]
+    dec_bytes = Bd * Hd * roofline.decode_bytes_per_slice(Nd, Pd, Rd, 2)
+    dec_gbs = dec_bytes / (step_ms.mean() * 1e-3) / 1e9
+    pre_bytes = roofline.prefill_bytes(Bp, Lp, Hp, Np, Pp, Rp, 2)
+    pre_flops = Bp * Hp * roofline.chunked_flops(Lp, Np, Pp, Rp, Qp)
+    pre_gbs = pre_bytes / (scan_ms.mean() * 1e-3) / 1e9
+    pre_tfs = pre_flops / (scan_ms.mean() * 1e-3) / 1e12
+    peak_gbs = roofline.HBM_BYTES_PER_S / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(prefill_tok_s, 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(float(tot_ms.mean()), 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"prefill B={Bp} L={Lp} H={Hp} P={Pp} N={Np} R={Rp} chunk={Qp} bf16 "
+                         f"+ decode step B={Bd} H={Hd} P={Pd} N={Nd} R={Rd} fp32 state"),
+            "prefill": {"batch": Bp, "seqlen": Lp, "nheads": Hp, "headdim": Pp, "dstate": Np,
+                        "rank": Rp, "chunk": Qp, "io": "bf16"},
+            "decode": {"batch": Bd, "nheads": Hd, "headdim": Pd, "dstate": Nd, "rank": Rd,
+                       "io": "bf16", "state": "fp32"},
+        },
+        "prefill_ms": round(float(scan_ms.mean()), 5),
+        "prefill_ms_p10_p90": [round(float(np.percentile(scan_ms, 10)), 5),
+                               round(float(np.percentile(scan_ms, 90)), 5)],
+        "decode_us_per_step": round(dec_us, 3),
+        "decode_us_p10_p90": [round(float(np.percentile(step_ms, 10)) * 1e3, 3),
+                              round(float(np.percentile(step_ms, 90)) * 1e3, 3)],
+        "roofline": {
+            "kernel": "k_step (m3_step, one launch per step)",
+            "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": peak_gbs, "unit": "GB/s",
+            "frac": round(dec_gbs / peak_gbs, 4), "traffic": None,
+            "bytes_per_launch": dec_bytes,
+        },
+        "roofline_prefill": {
+            "kernel": "m3_scan_fwd (all launches of one scan)",
+            "bound": "hbm", "achieved": round(pre_gbs, 1), "peak": peak_gbs, "unit": "GB/s",
+            "frac": round(pre_gbs / peak_gbs, 4), "traffic": None, "bytes_per_launch": pre_bytes,
+            "mfma_tflops": round(pre_tfs, 2),
+            "mfma_frac": round(pre_tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
+        },
+        "wall_s_timed_loop": round(wall, 3),
+    }
+    if not args.no_cpu:
+        result["cpu_baseline"] = cpu_baseline(base, layer, step_in, wp, wd)
+    print(json.dumps(result), flush=True)
+
+
+class _LayerView:
+    """Shape/dtype view of the decode layer for the step-input generator."""
+
+    def __init__(self, layer, w):
+        import torch
+        self.x = torch.empty((w["batch"], 1, w["nheads"], w["rank"], w["headdim"]),
+                             dtype=torch.bfloat16, device=layer.A.device)
+        self.Bm = torch.empty((w["batch"], 1, w["nheads"], w["rank"], w["dstate"]),
+                              dtype=torch.bfloat16, device=layer.A.device)
+        self.dt_bias = layer.dt_bias
+        self.omega = layer.omega
+
+
+def cpu_baseline(base, layer, step_in, wp, wd):
+    """The fp64 oracle on the host: all 64 slices of the whole prefill batch
+    (tokens/s), and one decode step on 64 of the 8192 slices (scaled to the
+    whole batch)."""
+    import numpy as np
+    import oracle
+    sl = [(b, h) for b in range(wp["batch"]) for h in range(wp["nheads"])]
+    Ls = wp["seqlen"]
+    ref = oracle.slices_of_scan(base.x, base.Bm, base.Cm, base.dt, base.A, base.lam, base.theta,
+                                base.D, sl, 0, Ls)
+    t0 = time.perf_counter()
+    _, used = oracle.scan(**ref, return_threads=True)
+    dt = time.perf_counter() - t0
+    tok_s = wp["batch"] * Ls / dt
+    dsl = [(b, h) for b in range(0, wd["batch"], 4) for h in range(0, wd["nheads"], 8)][:64]
+    st = step_in[0]
+    p = oracle.slices_of_step(st.x, st.Bm, st.Cm, st.dt, st.lam, st.theta, dsl)
+    N, P, R = wd["dstate"], wd["headdim"], wd["rank"]
+    rng = np.random.default_rng(0)
+    S = len(dsl)
+    state = rng.standard_normal((S, N, P))
+    cb, cx = rng.standard_normal((S, R, N)), rng.standard_normal((S, R, P))
+    A_s = np.array([float(layer.A[h]) for _, h in dsl])
+    D_s = np.array([float(layer.D[h]) for _, h in dsl])
+    reps = 20
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        oracle.step(state, cb, cx, p["x"], p["B"], p["C"], p["dt"], A_s, p["lam"], p["theta"], D_s)
+    ddt = (time.perf_counter() - t0) / reps
+    dec_us = ddt * (wd["batch"] * wd["nheads"] / S) * 1e6
+    return {"value": round(tok_s, 1), "unit": "tokens/s", "cores": int(used), "kind": "oracle",
+            "sample": (f"prefill: all {len(sl)} (batch, head) slices of the SISO bf16 batch, "
+                       f"first {Ls} of {wp['seqlen']} tokens, fp64, {dt:.2f} s; decode: one step "
+                       f"on {S} of {wd['batch'] * wd['nheads']} slices x {reps} reps, scaled"),
+            "decode_us_per_step": round(dec_us, 1)}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,152 @@
+/*
+ * libm3 - the Mamba-3 SSM layer's data-parallel hot path on AMD MI355X
+ * (gfx950): the chunked prefill scan and the single-token decode step.
+ *
+ * The operation (Mamba-3, Sec. 3.1 Prop. "Exponential-Trapezoidal
+ * Discretization"; Sec. 3.2 Props. "Complex-to-Real SSM Equivalence" and
+ * "Rotary Embedding Equivalence with Exponential-Trapezoidal
+ * Discretization"; Sec. 3.3 and App. "MIMO for Mamba-3"), for every batch
+ * row b and head h independently, over tokens t = 0 .. L-1:
+ *
+ *     alpha_t = exp(dt_t A_t)
+ *     beta_t  = (1 - lambda_t) dt_t alpha_t
+ *     gamma_t = lambda_t dt_t
+ *     h_t = alpha_t R_t h_{t-1} + beta_t R_t B_{t-1} X_{t-1}^T + gamma_t B_t X_t^T
+ *     Y_t = h_t^T C_t + D X_t
+ *
+ * h is the N x P fp32 state (N even: N/2 complex entries stored as real
+ * parts in rows 0 .. N/2-1 and imaginary parts in rows N/2 .. N-1).  B_t and
+ * C_t are N x R, X_t and Y_t are P x R (R = 1 is the SISO layer).  R_t
+ * rotates every row pair (i, i + N/2) by the angle theta_t[i]:
+ *     [h_i; h_{i+N/2}] <- [[cos, -sin], [sin, cos]] [h_i; h_{i+N/2}].
+ * theta is the per-step angle (the paper's Delta_t theta_t[i]); the library
+ * does not multiply it by dt.  D is a per-head skip (Mamba convention; the
+ * paper has no skip term).  With no initial state, h_{-1} = 0 and
+ * B_{-1} X_{-1}^T = 0 (the unrolled state starts at gamma_0 B_0 x_0).
+ *
+ * The persistent decode state is (h, B_{t-1}, X_{t-1}): h in the physical
+ * (unrotated) frame plus the "carry", the previous token's B and X, which
+ * the next step's beta term needs.
+ *
+ * Memory layouts (all row-major, contiguous, innermost last):
+ *     x, y        [batch][seqlen][nheads][rank][headdim]     io dtype
+ *     B, C        [batch][seqlen][nheads][rank][dstate]      io dtype
+ *     dt, lambda  [batch][seqlen][nheads]                    fp32
+ *     theta       [batch][seqlen][nheads][dstate/2]          fp32
+ *     A           A[b*a_stride_b + t*a_stride_t + h*a_stride_h]  fp32 (< 0)
+ *     D           [nheads]                                   fp32
+ *     state       [batch][nheads][dstate][headdim]           fp32
+ *     carryB      [batch][nheads][rank][dstate]              io dtype
+ *     carryX      [batch][nheads][rank][headdim]             io dtype
+ * Decode-step tensors drop the seqlen axis.
+ *
+ * Ownership and errors: every data pointer is a DEVICE pointer owned by the
+ * caller; the library allocates no device memory.  Calls are asynchronous
+ * on `stream` (a hipStream_t; NULL is the default stream).  Every argument
+ * error is detected on the host before any launch and leaves all outputs
+ * untouched; a failed launch returns M3_ERR_HIP.  No call prints, throws or
+ * aborts.  Results are deterministic (no floating-point atomics).  Calls on
+ * disjoint buffers may run concurrently; the library has no mutable global
+ * state besides a once-initialised cache of device properties.
+ */
+#ifndef M3_H
+#define M3_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    M3_OK = 0,
+    M3_ERR_NULL = 1,        /* a required pointer is NULL                      */
+    M3_ERR_SHAPE = 2,       /* a size is out of range or inconsistent          */
+    M3_ERR_DTYPE = 3,       /* unknown io dtype                                */
+    M3_ERR_UNSUPPORTED = 4, /* valid, but no kernel is built for this shape    */
+    M3_ERR_ALIGN = 5,       /* a pointer is misaligned (see each call)         */
+    M3_ERR_WORKSPACE = 6,   /* workspace missing or smaller than required      */
+    M3_ERR_HIP = 7          /* the HIP runtime reported an error               */
+} m3_status;
+
+typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
+
+typedef struct {
+    int64_t batch;     /* >= 1                                              */
+    int64_t seqlen;    /* L >= 0 (ignored by m3_step)                        */
+    int64_t nheads;    /* >= 1                                              */
+    int64_t headdim;   /* P                                                  */
+    int64_t dstate;    /* N, even                                            */
+    int64_t rank;      /* R >= 1 (MIMO rank)                                 */
+    int64_t chunk;     /* Q: tokens per chunk of the prefill scan            */
+    int32_t io;        /* m3_dtype of x, B, C, y and the carry               */
+    int32_t reserved;  /* must be 0                                          */
+    int64_t a_stride_b, a_stride_t, a_stride_h; /* strides of A, in floats   */
+} m3_dims;
+
+/*
+ * Bytes of device workspace m3_scan_fwd needs for `dims` (0 on invalid
+ * dims).  The workspace holds the per-chunk state contributions and the
+ * states entering each chunk.
+ */
+size_t m3_scan_workspace_bytes(const m3_dims *dims);
+
+/*
+ * Chunked prefill scan (Sec. 3.3 "Chunked Algorithm for MIMO SSMs"; the
+ * recurrence above).  Writes y for every token, final_state = h_{L-1}, and
+ * the carry (B_{L-1}, X_{L-1}) ready for m3_step or a further m3_scan_fwd.
+ *
+ * init_state (may be NULL) is h_{-1}; init_carryB / init_carryX (both NULL
+ * or both set) are B_{-1}, X_{-1}: passing the state and carry returned by
+ * an earlier call continues that sequence exactly.  With seqlen == 0 the
+ * outputs are the initial state and carry (zeros when not given), and the
+ * token arrays (x, B, C, dt, lambda, theta, y) may be NULL.
+ *
+ * Supported shapes (else M3_ERR_UNSUPPORTED): io bf16 with dstate 128,
+ * headdim 64, rank 1/2/4 and chunk*rank a multiple of 64 with chunk in
+ * {32, 64, 128}; io fp32 with (dstate, headdim) = (16, 16) or (128, 64),
+ * rank 1/2/4, chunk in {16, 32, 64} and chunk*rank a multiple of 64.
+ * x, B, C, theta, y, the states, the carries and the workspace must be
+ * 16-byte aligned; dt, A, lambda and D 4-byte aligned (else M3_ERR_ALIGN).
+ * Output buffers must not overlap the inputs.  A must be <= 0 (a positive
+ * log-decay can overflow the chunk-local decay factors); dt and lambda are
+ * expected in (0, inf) and [0, 1].
+ */
+m3_status m3_scan_fwd(const m3_dims *dims,
+                      const void *x, const void *B, const void *C,
+                      const float *dt, const float *A, const float *lambda,
+                      const float *theta, const float *D,
+                      const float *init_state, const void *init_carryB,
+                      const void *init_carryX,
+                      void *y, float *final_state, void *carryB, void *carryX,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * One decode step (one iteration of the recurrence) for every (b, h):
+ * state <- h_t, carry <- (B_t, X_t) in place, y_t written.  dims->seqlen
+ * and dims->chunk are ignored; A is read at t = 0 (a_stride_t unused).
+ * Tensors: x_t [batch][nheads][rank][headdim], B_t and C_t
+ * [batch][nheads][rank][dstate] (io dtype), dt_t and lambda_t
+ * [batch][nheads], theta_t [batch][nheads][dstate/2] (fp32),
+ * y_t [batch][nheads][rank][headdim] (io dtype).  Supported shapes: those
+ * of m3_scan_fwd (chunk ignored).
+ */
+m3_status m3_step(const m3_dims *dims,
+                  float *state, void *carryB, void *carryX,
+                  const void *x_t, const void *B_t, const void *C_t,
+                  const float *dt_t, const float *A, const float *lambda_t,
+                  const float *theta_t, const float *D,
+                  void *y_t, void *stream);
+
+/* Static description of a status code. */
+const char *m3_status_string(m3_status status);
+
+/* The hipError_t of the last M3_ERR_HIP returned on this thread (0 if none). */
+int m3_last_hip_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* M3_H */

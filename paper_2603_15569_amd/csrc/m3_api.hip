@@ -1,0 +1,163 @@
+// C-ABI front end of libm3: argument validation on the host (before any HIP
+// call), workspace layout, dispatch to the shape-specialised kernels.
+#include <limits.h>
+
+#include "m3.h"
+#include "m3_internal.h"
+
+namespace m3 {
+
+static thread_local int g_last_hip_error = 0;
+
+static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N, int64_t P,
+                                          int io_bytes, int acc_bytes) {
+    ScanWorkspaceLayout w;
+    const size_t per = (size_t)BH * (size_t)nchunks;
+    w.off_M = 0;
+    w.off_Sin = align_up(per * (size_t)(N * P) * sizeof(float), 256);
+    w.off_tot = align_up(w.off_Sin + per * (size_t)(N * P) * (size_t)io_bytes, 256);
+    w.total = align_up(w.off_tot + per * (size_t)(N / 2 + 1) * (size_t)acc_bytes, 256);
+    return w;
+}
+
+static bool aligned16(const void *p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
+static bool aligned4(const void *p) { return p == nullptr || ((uintptr_t)p & 3u) == 0; }
+
+static int io_bytes_of(int32_t io) { return io == M3_F32 ? 4 : io == M3_BF16 ? 2 : 0; }
+
+// Sizes shared by both entry points.  Limits keep every element offset and
+// the 1-D grid of one workgroup per (slice, chunk) inside 31/63-bit ranges.
+static m3_status check_dims_common(const m3_dims *d) {
+    if (!d) return M3_ERR_NULL;
+    if (d->io != M3_F32 && d->io != M3_BF16) return M3_ERR_DTYPE;
+    if (d->reserved != 0) return M3_ERR_SHAPE;
+    if (d->batch < 1 || d->nheads < 1 || d->headdim < 1 || d->dstate < 2 || d->rank < 1)
+        return M3_ERR_SHAPE;
+    if (d->dstate % 2) return M3_ERR_SHAPE;
+    if (d->batch > INT_MAX || d->nheads > INT_MAX || d->batch * d->nheads > INT_MAX / 16)
+        return M3_ERR_SHAPE;
+    return M3_OK;
+}
+
+}  // namespace m3
+
+using namespace m3;
+
+extern "C" const char *m3_status_string(m3_status s) {
+    switch (s) {
+    case M3_OK: return "ok";
+    case M3_ERR_NULL: return "a required pointer is NULL";
+    case M3_ERR_SHAPE: return "a size is out of range or inconsistent";
+    case M3_ERR_DTYPE: return "unknown io dtype";
+    case M3_ERR_UNSUPPORTED: return "no kernel is built for this shape";
+    case M3_ERR_ALIGN: return "a pointer is misaligned";
+    case M3_ERR_WORKSPACE: return "workspace missing or too small";
+    case M3_ERR_HIP: return "HIP runtime error";
+    }
+    return "unknown status";
+}
+
+extern "C" int m3_last_hip_error(void) { return g_last_hip_error; }
+
+static m3_status check_scan_dims(const m3_dims *d, ScanImpl *impl, int64_t *nchunks) {
+    m3_status s = check_dims_common(d);
+    if (s != M3_OK) return s;
+    if (d->seqlen < 0 || d->chunk < 1) return M3_ERR_SHAPE;
+    // element offsets of the largest tensors must fit in int64 comfortably
+    const int64_t per_tok = d->nheads * d->rank * (d->dstate > d->headdim ? d->dstate : d->headdim);
+    if (d->seqlen > (INT64_MAX / 4) / (d->batch * per_tok)) return M3_ERR_SHAPE;
+    const int64_t nc = (d->seqlen + d->chunk - 1) / d->chunk;
+    if (d->batch * d->nheads * nc > (int64_t)INT_MAX) return M3_ERR_SHAPE;
+    *impl = find_scan_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
+    if (!impl->launch) return M3_ERR_UNSUPPORTED;
+    *nchunks = nc;
+    return M3_OK;
+}
+
+extern "C" size_t m3_scan_workspace_bytes(const m3_dims *d) {
+    ScanImpl impl;
+    int64_t nc = 0;
+    if (check_scan_dims(d, &impl, &nc) != M3_OK) return 0;
+    return scan_workspace_layout(d->batch * d->nheads, nc, d->dstate, d->headdim,
+                                 io_bytes_of(d->io), impl.acc_bytes)
+        .total;
+}
+
+extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B, const void *C,
+                                 const float *dt, const float *A, const float *lambda,
+                                 const float *theta, const float *D, const float *init_state,
+                                 const void *init_carryB, const void *init_carryX, void *y,
+                                 float *final_state, void *carryB, void *carryX, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    ScanImpl impl;
+    int64_t nc = 0;
+    m3_status s = check_scan_dims(d, &impl, &nc);
+    if (s != M3_OK) return s;
+    // token arrays may be NULL only for an empty sequence (empty tensors)
+    const bool tok_ok = d->seqlen == 0 || (x && B && C && dt && lambda && theta && y);
+    if (!tok_ok || !A || !D || !final_state || !carryB || !carryX) return M3_ERR_NULL;
+    if ((init_carryB == nullptr) != (init_carryX == nullptr)) return M3_ERR_NULL;
+    const void *vec[] = {x, B, C, theta, init_state, init_carryB, init_carryX,
+                         y, final_state, carryB, carryX, workspace};
+    for (const void *p : vec)
+        if (!aligned16(p)) return M3_ERR_ALIGN;
+    const void *scal[] = {dt, A, lambda, D};
+    for (const void *p : scal)
+        if (!aligned4(p)) return M3_ERR_ALIGN;
+    const ScanWorkspaceLayout wl = scan_workspace_layout(d->batch * d->nheads, nc, d->dstate,
+                                                         d->headdim, io_bytes_of(d->io),
+                                                         impl.acc_bytes);
+    if (nc > 0 && (workspace == nullptr || workspace_bytes < wl.total)) return M3_ERR_WORKSPACE;
+
+    ScanArgs a;
+    a.x = x; a.B = B; a.C = C;
+    a.dt = dt; a.A = A; a.lam = lambda; a.theta = theta; a.D = D;
+    a.init_state = init_state; a.init_cB = init_carryB; a.init_cX = init_carryX;
+    a.y = y; a.final_state = final_state; a.cB = carryB; a.cX = carryX;
+    char *ws = static_cast<char *>(workspace);
+    a.M = nc > 0 ? reinterpret_cast<float *>(ws + wl.off_M) : nullptr;
+    a.Sin = nc > 0 ? ws + wl.off_Sin : nullptr;
+    a.tot = nc > 0 ? ws + wl.off_tot : nullptr;
+    a.batch = d->batch; a.L = d->seqlen; a.H = d->nheads; a.nchunks = nc;
+    a.a_sb = d->a_stride_b; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
+    const hipError_t e = impl.launch(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return M3_ERR_HIP;
+    }
+    return M3_OK;
+}
+
+extern "C" m3_status m3_step(const m3_dims *d, float *state, void *carryB, void *carryX,
+                             const void *x_t, const void *B_t, const void *C_t,
+                             const float *dt_t, const float *A, const float *lambda_t,
+                             const float *theta_t, const float *D, void *y_t, void *stream) {
+    m3_status s = check_dims_common(d);
+    if (s != M3_OK) return s;
+    step_launch_fn fn = find_step_impl(d->io, d->dstate, d->headdim, d->rank);
+    if (!fn) return M3_ERR_UNSUPPORTED;
+    if (!state || !carryB || !carryX || !x_t || !B_t || !C_t || !dt_t || !A || !lambda_t ||
+        !theta_t || !D || !y_t)
+        return M3_ERR_NULL;
+    const void *vec[] = {state, carryB, carryX, x_t, B_t, C_t, theta_t, y_t};
+    for (const void *p : vec)
+        if (!aligned16(p)) return M3_ERR_ALIGN;
+    const void *scal[] = {dt_t, A, lambda_t, D};
+    for (const void *p : scal)
+        if (!aligned4(p)) return M3_ERR_ALIGN;
+    StepArgs a;
+    a.state = state; a.cB = carryB; a.cX = carryX;
+    a.x = x_t; a.B = B_t; a.C = C_t;
+    a.dt = dt_t; a.A = A; a.lam = lambda_t; a.theta = theta_t; a.D = D;
+    a.y = y_t;
+    a.batch = d->batch; a.H = d->nheads;
+    a.a_sb = d->a_stride_b; a.a_sh = d->a_stride_h;
+    const hipError_t e = fn(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return M3_ERR_HIP;
+    }
+    return M3_OK;
+}

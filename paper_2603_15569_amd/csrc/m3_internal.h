@@ -1,0 +1,56 @@
+// Internal interface between the C-ABI front end (m3_api.hip) and the
+// kernel translation units.  Not installed; include/m3.h is the public API.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace m3 {
+
+// Arguments of one prefill scan, already validated by the front end.
+struct ScanArgs {
+    const void *x, *B, *C;
+    const float *dt, *A, *lam, *theta, *D;
+    const float *init_state;
+    const void *init_cB, *init_cX;      // both null or both set
+    void *y;
+    float *final_state;
+    void *cB, *cX;
+    // workspace regions (see scan_workspace_layout)
+    float *M;        // [BH][nchunks][N][P] fp32  per-chunk state contributions
+    void *Sin;       // [BH][nchunks][P][N] io    state entering each chunk
+    void *tot;       // [BH][nchunks][1+N/2] acc  chunk log-decay and angle totals
+    int64_t batch, L, H, nchunks;
+    int64_t a_sb, a_st, a_sh;
+};
+
+struct StepArgs {
+    float *state;
+    void *cB, *cX;
+    const void *x, *B, *C;
+    const float *dt, *A, *lam, *theta, *D;
+    void *y;
+    int64_t batch, H;
+    int64_t a_sb, a_sh;
+};
+
+typedef hipError_t (*scan_launch_fn)(const ScanArgs &, hipStream_t);
+typedef hipError_t (*step_launch_fn)(const StepArgs &, hipStream_t);
+
+struct ScanImpl {
+    scan_launch_fn launch;
+    int acc_bytes;   // bytes of the prologue scalar type (4: fp32, 8: fp64)
+};
+
+// Kernel lookup by shape; null launch when no kernel is built for it.
+ScanImpl find_scan_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+step_launch_fn find_step_impl(int io, int64_t N, int64_t P, int64_t R);
+
+// Byte offsets of the workspace regions for a scan.
+struct ScanWorkspaceLayout {
+    size_t off_M, off_Sin, off_tot, total;
+};
+ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N,
+                                          int64_t P, int io_bytes, int acc_bytes);
+
+}  // namespace m3

@@ -1,0 +1,162 @@
+"""Python binding of libm3 (ctypes): argument marshalling only.
+
+Every step of the path runs in the HIP kernels behind the C ABI declared in
+include/m3.h; PyTorch supplies device memory and the current HIP stream.
+There is no fallback: when libm3.so is missing or a call fails, an exception
+is raised.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libm3.so")
+
+M3_OK, M3_ERR_NULL, M3_ERR_SHAPE, M3_ERR_DTYPE = 0, 1, 2, 3
+M3_ERR_UNSUPPORTED, M3_ERR_ALIGN, M3_ERR_WORKSPACE, M3_ERR_HIP = 4, 5, 6, 7
+M3_F32, M3_BF16 = 0, 1
+_IO = {torch.float32: M3_F32, torch.bfloat16: M3_BF16}
+
+
+class M3Dims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int64), ("seqlen", ctypes.c_int64),
+                ("nheads", ctypes.c_int64), ("headdim", ctypes.c_int64),
+                ("dstate", ctypes.c_int64), ("rank", ctypes.c_int64),
+                ("chunk", ctypes.c_int64), ("io", ctypes.c_int32),
+                ("reserved", ctypes.c_int32), ("a_stride_b", ctypes.c_int64),
+                ("a_stride_t", ctypes.c_int64), ("a_stride_h", ctypes.c_int64)]
+
+
+class M3Error(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"libm3 status {status}: {msg}")
+        self.status = status
+
+
+EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_step", "m3_status_string",
+           "m3_last_hip_error")
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libm3.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with "
+                               "`python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(LIB_PATH)
+        vp, dims_p = ctypes.c_void_p, ctypes.POINTER(M3Dims)
+        L.m3_scan_workspace_bytes.argtypes = [dims_p]
+        L.m3_scan_workspace_bytes.restype = ctypes.c_size_t
+        L.m3_scan_fwd.argtypes = [dims_p] + [vp] * 15 + [vp, ctypes.c_size_t, vp]
+        L.m3_scan_fwd.restype = ctypes.c_int
+        L.m3_step.argtypes = [dims_p] + [vp] * 12 + [vp]
+        L.m3_step.restype = ctypes.c_int
+        L.m3_status_string.argtypes = [ctypes.c_int]
+        L.m3_status_string.restype = ctypes.c_char_p
+        L.m3_last_hip_error.argtypes = []
+        L.m3_last_hip_error.restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def _check(status: int):
+    if status != M3_OK:
+        msg = lib().m3_status_string(status).decode()
+        if status == M3_ERR_HIP:
+            msg += f" (hipError {lib().m3_last_hip_error()})"
+        raise M3Error(status, msg)
+
+
+def _p(t: Optional[torch.Tensor]):
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise ValueError("libm3 takes contiguous tensors")
+    return t.data_ptr()
+
+
+def _stream(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream)
+
+
+def _a_strides(A: torch.Tensor, batch: int, seqlen: int, nheads: int):
+    """A is per head [H] or per token [B, L, H] (Mamba-3's data-dependent A)."""
+    if A.dim() == 1 and A.shape[0] == nheads:
+        return 0, 0, 1
+    if A.dim() == 3 and tuple(A.shape) == (batch, seqlen, nheads):
+        s = A.stride()
+        return s[0], s[1], s[2]
+    raise ValueError(f"A must be [H] or [B, L, H], got {tuple(A.shape)}")
+
+
+def scan_dims(x: torch.Tensor, Bm: torch.Tensor, chunk: int, A: Optional[torch.Tensor] = None) -> M3Dims:
+    batch, seqlen, nheads, rank, headdim = x.shape
+    dstate = Bm.shape[-1]
+    sb, st, sh = _a_strides(A, batch, seqlen, nheads) if A is not None else (0, 0, 1)
+    return M3Dims(batch, seqlen, nheads, headdim, dstate, rank, int(chunk),
+                  _IO[x.dtype], 0, sb, st, sh)
+
+
+def workspace_bytes(dims: M3Dims) -> int:
+    return int(lib().m3_scan_workspace_bytes(ctypes.byref(dims)))
+
+
+def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
+             init_state=None, init_carry=None, out=None, workspace=None,
+             stream=None) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
+    """m3_scan_fwd: returns y [B,L,H,R,P], final_state [B,H,N,P] fp32 and the
+    carry (B_{L-1} [B,H,R,N], X_{L-1} [B,H,R,P]).  `out` may supply
+    (y, final_state, carryB, carryX) to write into."""
+    d = scan_dims(x, Bm, chunk, A)
+    batch, seqlen, nheads, rank, headdim = x.shape
+    dstate = Bm.shape[-1]
+    dev = x.device
+    if out is None:
+        y = torch.empty_like(x)
+        fs = torch.empty((batch, nheads, dstate, headdim), dtype=torch.float32, device=dev)
+        cB = torch.empty((batch, nheads, rank, dstate), dtype=x.dtype, device=dev)
+        cX = torch.empty((batch, nheads, rank, headdim), dtype=x.dtype, device=dev)
+    else:
+        y, fs, cB, cX = out
+    nbytes = workspace_bytes(d)
+    if workspace is None and nbytes > 0:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    icB, icX = (None, None) if init_carry is None else init_carry
+    _check(lib().m3_scan_fwd(ctypes.byref(d), _p(x), _p(Bm), _p(Cm), _p(dt), _p(A), _p(lam),
+                             _p(theta), _p(D), _p(init_state), _p(icB), _p(icX), _p(y), _p(fs),
+                             _p(cB), _p(cX), _p(workspace),
+                             workspace.numel() if workspace is not None else 0,
+                             _stream(stream)))
+    return y, fs, (cB, cX)
+
+
+def step_dims(x_t: torch.Tensor, B_t: torch.Tensor, A: torch.Tensor) -> M3Dims:
+    batch, nheads, rank, headdim = x_t.shape
+    dstate = B_t.shape[-1]
+    if A.dim() == 1 and A.shape[0] == nheads:
+        sb, sh = 0, 1
+    elif A.dim() == 2 and tuple(A.shape) == (batch, nheads):
+        sb, sh = A.stride()
+    else:
+        raise ValueError(f"A must be [H] or [B, H], got {tuple(A.shape)}")
+    return M3Dims(batch, 1, nheads, headdim, dstate, rank, 1, _IO[x_t.dtype], 0, sb, 0, sh)
+
+
+def step(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, y=None, stream=None):
+    """m3_step: advances `state` [B,H,N,P] and `carry` (B [B,H,R,N],
+    X [B,H,R,P]) in place by one token; returns y_t [B,H,R,P]."""
+    d = step_dims(x_t, B_t, A)
+    if y is None:
+        y = torch.empty_like(x_t)
+    cB, cX = carry
+    _check(lib().m3_step(ctypes.byref(d), _p(state), _p(cB), _p(cX), _p(x_t), _p(B_t), _p(C_t),
+                         _p(dt_t), _p(A), _p(lam_t), _p(theta_t), _p(D), _p(y), _stream(stream)))
+    return y

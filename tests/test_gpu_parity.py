@@ -1,0 +1,330 @@
+"""GPU parity: libm3 (through the C ABI) against the fp64 CPU oracle.
+
+Metric: per (batch, head) slice, max|gpu - oracle| / max|oracle| (infinity
+norm relative error), for y, the final state and (decode) every step's y.
+Bars: 1e-5 for the fp32 build, 2e-2 for bf16 inputs.  The oracle reads the
+exact (bf16-rounded) inputs the GPU received.  Integer-like results (the
+carry, a copy of the last token's B and x) must match bit for bit.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_15569_amd import m3
+from paper_2603_15569_amd.inputs import (WORKLOADS, make_scan_inputs, make_step_inputs,
+                                         workload_inputs)
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-5, "bf16": 2e-2}
+DEV = "cuda:0"
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True):
+    """Scan with every output pre-filled with NaN, so an unwritten element fails."""
+    x = inp.x
+    B_, L, H, R, P = x.shape
+    N = inp.Bm.shape[-1]
+    out = None
+    if nan_fill:
+        out = (torch.full_like(x, float("nan")),
+               torch.full((B_, H, N, P), float("nan"), device=x.device),
+               torch.full((B_, H, R, N), float("nan"), device=x.device, dtype=x.dtype),
+               torch.full((B_, H, R, P), float("nan"), device=x.device, dtype=x.dtype))
+    y, fs, (cB, cX) = m3.scan_fwd(x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta, inp.D,
+                                  chunk=chunk, init_state=init_state, init_carry=init_carry,
+                                  out=out)
+    torch.cuda.synchronize()
+    return y, fs, cB, cX
+
+
+def check_slices(inp, y, fs, cB, cX, slices, tol, init_state=None, init_carry=None, label=""):
+    ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                inp.D, slices)
+    kw = {}
+    if init_state is not None:
+        kw["init_state"] = oracle.slices_of_state(init_state, slices)
+    if init_carry is not None:
+        kw["init_B"] = oracle.slices_of_state(init_carry[0], slices)
+        kw["init_X"] = oracle.slices_of_state(init_carry[1], slices)
+    ry, rs, rb, rx = oracle.scan(**ref, **kw)
+    worst = 0.0
+    for k, (b, h) in enumerate(slices):
+        gy = y[b, :, h].double().cpu().numpy()
+        gs = fs[b, h].double().cpu().numpy()
+        assert np.all(np.isfinite(gy)) and np.all(np.isfinite(gs)), f"{label} non-finite {(b, h)}"
+        e = max(oracle.rel_err(gy, ry[k]), oracle.rel_err(gs, rs[k]))
+        worst = max(worst, e)
+        assert e <= tol, f"{label} slice {(b, h)}: rel err {e:.3g} > {tol}"
+        assert np.array_equal(cB[b, h].double().cpu().numpy(), rb[k]), f"{label} carry B {(b, h)}"
+        assert np.array_equal(cX[b, h].double().cpu().numpy(), rx[k]), f"{label} carry X {(b, h)}"
+    say(f"{label}: worst rel err {worst:.3g} over {len(slices)} slices")
+    return worst
+
+
+def sample_slices(batch, nheads, count, seed):
+    rng = np.random.default_rng(seed)
+    allsl = [(b, h) for b in range(batch) for h in range(nheads)]
+    if len(allsl) <= count:
+        return allsl
+    pick = {allsl[0], allsl[-1]}
+    for i in rng.permutation(len(allsl)):
+        if len(pick) >= count:
+            break
+        pick.add(allsl[i])
+    return sorted(pick)
+
+
+# ---------------------------------------------------------------------------
+# Workloads
+# ---------------------------------------------------------------------------
+
+def test_workload0_tiny_siso_fp32():
+    say("workload 0: tiny SISO fp32, full check")
+    inp = workload_inputs(0, device=DEV)
+    y, fs, cB, cX = run_scan(inp, WORKLOADS[0]["chunk"])
+    check_slices(inp, y, fs, cB, cX, sample_slices(1, 2, 99, 0), TOL["f32"], label="w0")
+
+
+def test_workload1_siso_bf16():
+    say("workload 1: SISO bf16 prefill, all 64 slices")
+    w = WORKLOADS[1]
+    inp = workload_inputs(1, device=DEV)
+    y, fs, cB, cX = run_scan(inp, w["chunk"])
+    check_slices(inp, y, fs, cB, cX, sample_slices(w["batch"], w["nheads"], 10**6, 1),
+                 TOL["bf16"], label="w1")
+
+
+def test_workload2_mimo_bf16():
+    say("workload 2: MIMO R=4 bf16 prefill, 18 sampled slices")
+    w = WORKLOADS[2]
+    inp = workload_inputs(2, device=DEV)
+    y, fs, cB, cX = run_scan(inp, w["chunk"])
+    check_slices(inp, y, fs, cB, cX, sample_slices(w["batch"], w["nheads"], 18, 2),
+                 TOL["bf16"], label="w2")
+
+
+def test_workload3_long_mimo_bf16():
+    say("workload 3: long-context MIMO prefill L=65536, 4 sampled slices")
+    w = WORKLOADS[3]
+    inp = workload_inputs(3, device=DEV)
+    y, fs, cB, cX = run_scan(inp, w["chunk"])
+    check_slices(inp, y, fs, cB, cX, sample_slices(w["batch"], w["nheads"], 4, 3),
+                 TOL["bf16"], label="w3")
+
+
+def test_workload4_decode_loop():
+    """State from a 1024-token prefill (B=256, H=32, R=4), then 1024 decode
+    steps with fresh inputs; every step's y and the final state checked on 16
+    sampled slices."""
+    w = WORKLOADS[4]
+    say("workload 4: prefill B=256 L=1024 then 1024 steps, 16 sampled slices")
+    inp = workload_inputs(4, device=DEV)
+    y, fs, cB, cX = run_scan(inp, w["chunk"], nan_fill=False)
+    slices = sample_slices(w["batch"], w["nheads"], 16, 4)
+    ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                inp.D, slices)
+    ry, rs, rb, rx = oracle.scan(**ref)
+    del y
+    bi = torch.tensor([b for b, _ in slices], device=DEV)
+    hi = torch.tensor([h for _, h in slices], device=DEV)
+    A_s, D_s = ref["A"][:, 0], ref["D"]
+    worst = 0.0
+    for s in range(w["steps"]):
+        st = make_step_inputs(inp, s)
+        yt = m3.step(fs, (cB, cX), st.x, st.Bm, st.Cm, st.dt, inp.A, st.lam, st.theta, inp.D)
+        g = lambda t: t[bi, hi].double().cpu().numpy()
+        ryt, rs, rb, rx = oracle.step(rs, rb, rx, g(st.x), g(st.Bm), g(st.Cm), g(st.dt),
+                                      A_s, g(st.lam), g(st.theta), D_s)
+        gy = g(yt)
+        for k in range(len(slices)):
+            e = oracle.rel_err(gy[k], ryt[k])
+            worst = max(worst, e)
+            assert e <= TOL["bf16"], f"step {s} slice {slices[k]} rel err {e:.3g}"
+    gs = fs[bi, hi].double().cpu().numpy()
+    for k in range(len(slices)):
+        e = oracle.rel_err(gs[k], rs[k])
+        worst = max(worst, e)
+        assert e <= TOL["bf16"], f"final state slice {slices[k]} rel err {e:.3g}"
+    assert np.array_equal(cB[bi, hi].double().cpu().numpy(), rb)
+    assert np.array_equal(cX[bi, hi].double().cpu().numpy(), rx)
+    say(f"w4: worst rel err {worst:.3g}")
+
+
+# ---------------------------------------------------------------------------
+# Shapes, ragged lengths and edge cases
+# ---------------------------------------------------------------------------
+
+SHAPES = [  # io, N, P, R, Q
+    ("f32", 16, 16, 1, 64), ("f32", 16, 16, 2, 32), ("f32", 16, 16, 4, 16),
+    ("f32", 16, 16, 4, 64), ("f32", 128, 64, 2, 32), ("f32", 128, 64, 4, 16),
+    ("f32", 128, 64, 4, 32),
+    ("bf16", 128, 64, 1, 64), ("bf16", 128, 64, 1, 128), ("bf16", 128, 64, 2, 64),
+    ("bf16", 128, 64, 4, 32), ("bf16", 128, 64, 4, 64), ("bf16", 128, 64, 4, 128),
+]
+
+
+@pytest.mark.parametrize("io,N,P,R,Q", SHAPES)
+def test_shapes_ragged(io, N, P, R, Q):
+    """Several chunks plus a ragged tail, two batch rows and three heads."""
+    L = 3 * Q + Q // 2 + 3
+    say(f"shape io={io} N={N} P={P} R={R} Q={Q} L={L}")
+    inp = make_scan_inputs(2, L, 3, P, N, R, io=io, seed=11 + N + R + Q, device=DEV, chunk=Q)
+    y, fs, cB, cX = run_scan(inp, Q)
+    check_slices(inp, y, fs, cB, cX, sample_slices(2, 3, 99, 5), TOL[io], label=f"{io}/{N}/{R}/{Q}")
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+@pytest.mark.parametrize("L", [1, 2, 63, 64, 65])
+def test_short_sequences(io, L):
+    N, P, R, Q = (16, 16, 1, 64) if io == "f32" else (128, 64, 4, 64)
+    say(f"short io={io} L={L}")
+    inp = make_scan_inputs(2, L, 2, P, N, R, io=io, seed=100 + L, device=DEV, chunk=Q)
+    y, fs, cB, cX = run_scan(inp, Q)
+    check_slices(inp, y, fs, cB, cX, sample_slices(2, 2, 99, 6), TOL[io], label=f"short{L}")
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_empty_sequence(io):
+    N, P, R, Q = (16, 16, 2, 32) if io == "f32" else (128, 64, 2, 64)
+    say(f"empty io={io}")
+    dt = torch.float32 if io == "f32" else torch.bfloat16
+    inp = make_scan_inputs(2, 0, 2, P, N, R, io=io, seed=3, device=DEV, chunk=Q)
+    st0 = torch.randn(2, 2, N, P, device=DEV)
+    c0 = (torch.randn(2, 2, R, N, device=DEV).to(dt), torch.randn(2, 2, R, P, device=DEV).to(dt))
+    y, fs, cB, cX = run_scan(inp, Q, init_state=st0, init_carry=c0)
+    assert y.numel() == 0
+    assert torch.equal(fs, st0) and torch.equal(cB, c0[0]) and torch.equal(cX, c0[1])
+    y, fs, cB, cX = run_scan(inp, Q)
+    assert torch.count_nonzero(fs) == 0 and torch.count_nonzero(cB.float()) == 0
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_segment_resume_and_decode_consistency(io):
+    """scan(0:L1) -> (state, carry) -> scan(L1:L) equals scan(0:L); and
+    scan(0:L) then one m3_step equals scan(0:L+1) at token L (the decode
+    state is the physical-frame state plus the previous token's B and x)."""
+    N, P, R, Q = (16, 16, 2, 32) if io == "f32" else (128, 64, 4, 64)
+    L, L1 = 200, 77
+    say(f"segment resume io={io}")
+    inp = make_scan_inputs(2, L + 1, 2, P, N, R, io=io, seed=42, device=DEV, chunk=Q)
+
+    def part(t0, t1):
+        return type(inp)(x=inp.x[:, t0:t1].contiguous(), Bm=inp.Bm[:, t0:t1].contiguous(),
+                         Cm=inp.Cm[:, t0:t1].contiguous(), dt=inp.dt[:, t0:t1].contiguous(),
+                         A=inp.A, lam=inp.lam[:, t0:t1].contiguous(),
+                         theta=inp.theta[:, t0:t1].contiguous(), D=inp.D, chunk=Q)
+    yf, fsf, _, _ = run_scan(part(0, L + 1), Q)
+    ya, fsa, cBa, cXa = run_scan(part(0, L1), Q)
+    yb, fsb, cBb, cXb = run_scan(part(L1, L), Q, init_state=fsa, init_carry=(cBa, cXa))
+    check_slices(part(L1, L), yb, fsb, cBb, cXb, sample_slices(2, 2, 99, 7), TOL[io],
+                 init_state=fsa, init_carry=(cBa, cXa), label="resume")
+    # decode consistency: one step from the state after L tokens
+    yl, fsl, cBl, cXl = run_scan(part(0, L), Q)
+    xt, Bt, Ct = inp.x[:, L].contiguous(), inp.Bm[:, L].contiguous(), inp.Cm[:, L].contiguous()
+    yt = m3.step(fsl, (cBl, cXl), xt, Bt, Ct, inp.dt[:, L].contiguous(), inp.A,
+                 inp.lam[:, L].contiguous(), inp.theta[:, L].contiguous(), inp.D)
+    torch.cuda.synchronize()
+    tol = TOL[io] if io == "bf16" else 1e-5
+    for b in range(2):
+        for h in range(2):
+            assert oracle.rel_err(yt[b, h].double().cpu().numpy(),
+                                  yf[b, L, h].double().cpu().numpy()) <= tol
+            assert oracle.rel_err(fsl[b, h].cpu().numpy(), fsf[b, h].cpu().numpy()) <= tol
+
+
+@pytest.mark.parametrize("io", ["f32", "bf16"])
+def test_chunk_boundary_impulse(io):
+    """Only x at the last token of a chunk is nonzero and lambda there is 0,
+    so every later output flows through the cross-chunk previous-input term
+    (sigma of that token reads the next chunk's lambda and dt)."""
+    N, P, R, Q = (16, 16, 1, 64) if io == "f32" else (128, 64, 2, 64)
+    L = 3 * Q
+    say(f"boundary impulse io={io}")
+    inp = make_scan_inputs(1, L, 2, P, N, R, io=io, seed=9, device=DEV, chunk=Q)
+    j = Q - 1
+    keep = inp.x[:, j].clone()
+    inp.x.zero_()
+    inp.x[:, j] = keep
+    inp.lam[:, j] = 0.0
+    y, fs, cB, cX = run_scan(inp, Q)
+    assert torch.count_nonzero(y[:, :j].float()) == 0
+    check_slices(inp, y, fs, cB, cX, [(0, 0), (0, 1)], TOL[io], label="impulse")
+    # beyond the boundary the output is large (not a trivially small residue)
+    assert y[:, j + 1:].float().abs().max() > 1e-3
+
+
+def test_chunk_size_invariance():
+    """Results do not depend on the chunk length (Sec. 3.3)."""
+    say("chunk invariance bf16 R=4 Q in {32, 64, 128}")
+    inp = make_scan_inputs(2, 700, 2, 64, 128, 4, io="bf16", seed=5, device=DEV)
+    ys = [run_scan(inp, Q) for Q in (32, 64, 128)]
+    for y, fs, _, _ in ys[1:]:
+        for b in range(2):
+            for h in range(2):
+                assert oracle.rel_err(y[b, :, h].double().cpu().numpy(),
+                                      ys[0][0][b, :, h].double().cpu().numpy()) <= 2e-2
+                assert oracle.rel_err(fs[b, h].cpu().numpy(), ys[0][1][b, h].cpu().numpy()) <= 2e-2
+
+
+def test_per_token_A():
+    """Mamba-3's data-dependent A_t passed as a [B, L, H] tensor."""
+    say("per-token A fp32")
+    inp = make_scan_inputs(2, 150, 2, 16, 16, 2, io="f32", seed=21, device=DEV, chunk=32)
+    A_t = -torch.rand(2, 150, 2, device=DEV) * 4 - 0.1
+    y, fs, (cB, cX) = m3.scan_fwd(inp.x, inp.Bm, inp.Cm, inp.dt, A_t, inp.lam, inp.theta, inp.D,
+                                  chunk=32)
+    torch.cuda.synchronize()
+    sl = [(0, 0), (1, 1)]
+    ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                inp.D, sl)
+    ref["A"] = np.stack([A_t[b, :, h].double().cpu().numpy() for b, h in sl])
+    ry, rs, _, _ = oracle.scan(**ref)
+    for k, (b, h) in enumerate(sl):
+        assert oracle.rel_err(y[b, :, h].double().cpu().numpy(), ry[k]) <= 1e-5
+        assert oracle.rel_err(fs[b, h].cpu().numpy(), rs[k]) <= 1e-5
+
+
+def test_determinism():
+    """Two runs give bitwise-identical outputs (no atomics in reductions)."""
+    say("determinism bf16 R=4")
+    inp = make_scan_inputs(2, 300, 4, 64, 128, 4, io="bf16", seed=8, device=DEV)
+    a = run_scan(inp, 64)
+    b = run_scan(inp, 64)
+    for u, v in zip(a, b):
+        assert torch.equal(u, v)
+
+
+@pytest.mark.parametrize("io,N,P,R", [("f32", 16, 16, 1), ("f32", 128, 64, 4),
+                                      ("bf16", 128, 64, 1), ("bf16", 128, 64, 4)])
+def test_decode_steps_small(io, N, P, R):
+    """A few decode steps from a random state and carry, every output checked."""
+    say(f"decode small io={io} N={N} R={R}")
+    dt = torch.float32 if io == "f32" else torch.bfloat16
+    inp = make_scan_inputs(3, 4, 5, P, N, R, io=io, seed=31, device=DEV)
+    state = torch.randn(3, 5, N, P, device=DEV)
+    cB = torch.randn(3, 5, R, N, device=DEV).to(dt)
+    cX = torch.randn(3, 5, R, P, device=DEV).to(dt)
+    sl = [(b, h) for b in range(3) for h in range(5)]
+    rs = oracle.slices_of_state(state, sl)
+    rb, rx = oracle.slices_of_state(cB, sl), oracle.slices_of_state(cX, sl)
+    A_s = np.array([float(inp.A[h]) for _, h in sl])
+    D_s = np.array([float(inp.D[h]) for _, h in sl])
+    tol = TOL[io]
+    for s in range(4):
+        st = make_step_inputs(inp, s)
+        y = torch.full_like(st.x, float("nan"))
+        m3.step(state, (cB, cX), st.x, st.Bm, st.Cm, st.dt, inp.A, st.lam, st.theta, inp.D, y=y)
+        torch.cuda.synchronize()
+        p = oracle.slices_of_step(st.x, st.Bm, st.Cm, st.dt, st.lam, st.theta, sl)
+        ry, rs, rb, rx = oracle.step(rs, rb, rx, p["x"], p["B"], p["C"], p["dt"], A_s, p["lam"],
+                                     p["theta"], D_s)
+        for k, (b, h) in enumerate(sl):
+            assert oracle.rel_err(y[b, h].double().cpu().numpy(), ry[k]) <= tol
+            assert oracle.rel_err(state[b, h].cpu().numpy(), rs[k]) <= tol
+        assert np.array_equal(oracle.slices_of_state(cB, sl), rb)

@@ -1,0 +1,148 @@
+"""CPU tests of the host side: the C-ABI library loads and exports every
+symbol of include/m3.h, every argument error is caught on the host before a
+launch, and the benchmark's accounting matches the paper's printed forms."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2603_15569_amd import m3, roofline
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def golden():
+    vals = {}
+    with open(os.path.join(ROOT, "tests", "golden", "paper_formulas.txt")) as f:
+        for line in f:
+            line = line.strip()
+            if line and not line.startswith("#"):
+                k, v = line.split()[:2]
+                vals[k] = float(v)
+    return vals
+
+
+@pytest.fixture(scope="module")
+def L():
+    return m3.lib()
+
+
+def test_exports_match_header(L):
+    hdr = open(os.path.join(ROOT, "include", "m3.h")).read()
+    declared = set(re.findall(r"^\S.*?\b(m3_\w+)\s*\(", hdr, flags=re.M))
+    assert declared == set(m3.EXPORTS)
+    for name in declared:
+        assert hasattr(L, name), name
+
+
+def test_status_strings(L):
+    for s in range(8):
+        assert L.m3_status_string(s)
+    assert L.m3_last_hip_error() == 0
+
+
+FAKE = 0x100000  # 16-byte aligned fake device address; never dereferenced
+
+
+def dims(**kw):
+    d = dict(batch=1, seqlen=256, nheads=2, headdim=16, dstate=16, rank=1, chunk=64,
+             io=m3.M3_F32, reserved=0, a_stride_b=0, a_stride_t=0, a_stride_h=1)
+    d.update(kw)
+    return m3.M3Dims(**d)
+
+
+def scan_call(L, d, over=None, ws_bytes=None):
+    ptrs = [FAKE] * 15
+    for k, v in (over or {}).items():
+        ptrs[k] = v
+    # init_state / init carry default to NULL
+    for k in (8, 9, 10):
+        if not over or k not in over:
+            ptrs[k] = None
+    need = L.m3_scan_workspace_bytes(ctypes.byref(d)) if d is not None else 0
+    ws = FAKE
+    wsb = need if ws_bytes is None else ws_bytes
+    return L.m3_scan_fwd(ctypes.byref(d) if d is not None else None, *ptrs, ws, wsb, None)
+
+
+def test_scan_host_validation(L):
+    assert scan_call(L, None) == m3.M3_ERR_NULL
+    assert scan_call(L, dims(io=7)) == m3.M3_ERR_DTYPE
+    assert scan_call(L, dims(dstate=15)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(rank=0)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(batch=0)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(seqlen=-1)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(chunk=0)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(reserved=1)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(dstate=64, headdim=64)) == m3.M3_ERR_UNSUPPORTED
+    assert scan_call(L, dims(chunk=48)) == m3.M3_ERR_UNSUPPORTED
+    assert scan_call(L, dims(io=m3.M3_BF16)) == m3.M3_ERR_UNSUPPORTED
+    assert scan_call(L, dims(), {0: None}) == m3.M3_ERR_NULL
+    assert scan_call(L, dims(), {14: None}) == m3.M3_ERR_NULL
+    assert scan_call(L, dims(), {11: None}) == m3.M3_ERR_NULL       # y with seqlen > 0
+    assert scan_call(L, dims(), {9: FAKE}) == m3.M3_ERR_NULL        # one carry half only
+    assert scan_call(L, dims(), {0: FAKE + 4}) == m3.M3_ERR_ALIGN
+    assert scan_call(L, dims(), {3: FAKE + 2}) == m3.M3_ERR_ALIGN
+    assert scan_call(L, dims(), ws_bytes=0) == m3.M3_ERR_WORKSPACE
+    need = L.m3_scan_workspace_bytes(ctypes.byref(dims()))
+    assert scan_call(L, dims(), ws_bytes=need - 1) == m3.M3_ERR_WORKSPACE
+    assert L.m3_last_hip_error() == 0
+
+
+def test_workspace_bytes(L):
+    assert L.m3_scan_workspace_bytes(None) == 0
+    assert L.m3_scan_workspace_bytes(ctypes.byref(dims(dstate=64, headdim=64))) == 0
+    d = dims(io=m3.M3_BF16, dstate=128, headdim=64, rank=4, chunk=64, seqlen=4096, batch=8,
+             nheads=32)
+    nb = L.m3_scan_workspace_bytes(ctypes.byref(d))
+    per = 8 * 32 * 64
+    assert nb >= per * 128 * 64 * (4 + 2) + per * 65 * 4
+    assert nb % 256 == 0
+
+
+def test_step_host_validation(L):
+    def call(d, over=None):
+        ptrs = [FAKE] * 12
+        for k, v in (over or {}).items():
+            ptrs[k] = v
+        return L.m3_step(ctypes.byref(d) if d is not None else None, *ptrs, None)
+    assert call(None) == m3.M3_ERR_NULL
+    assert call(dims(io=9)) == m3.M3_ERR_DTYPE
+    assert call(dims(dstate=32, headdim=16)) == m3.M3_ERR_UNSUPPORTED
+    assert call(dims(), {0: None}) == m3.M3_ERR_NULL
+    assert call(dims(), {11: None}) == m3.M3_ERR_NULL
+    assert call(dims(), {0: FAKE + 8}) == m3.M3_ERR_ALIGN
+    assert call(dims(), {6: FAKE + 1}) == m3.M3_ERR_ALIGN
+
+
+def test_accounting_against_paper():
+    g = golden()
+    # Tab. arith_intensity (a): about 2.5 for large N, P
+    assert abs(roofline.decode_ai_siso(4096, 4096) - g["siso_decode_ai_approx"]) < 0.01
+    assert 2.3 < roofline.decode_ai_siso(128, 64) < g["siso_decode_ai_approx"]
+    # MIMO intensity grows linearly with R (Tab. arith_intensity (b))
+    a1, a4 = roofline.decode_ai_mimo(128, 64, 1), roofline.decode_ai_mimo(128, 64, 4)
+    assert 3.0 < a4 / a1 < 3.3
+    assert abs(roofline.decode_ai_mimo(128, 64, 1) - roofline.decode_ai_siso(128, 64)) < 0.2
+    # Sec. 3.3: C = P = N gives 8 T N^2 (ignoring the 2 (T/C) N P term)
+    T, N = 4096, 64
+    f = roofline.chunked_flops(T, N, N, 1, N)
+    assert abs(f - g["chunked_siso_total_coeff"] * T * N * N) == 2 * T * N
+    # Sec. 3.3: C R = N = P gives 8 T R N^2
+    R = 4
+    f = roofline.chunked_flops(T, N, N, R, N // R)
+    assert abs(f - g["chunked_mimo_total_coeff"] * T * R * N * N) == 2 * (T * R // N) * N * N
+    # intra-chunk FLOPs grow R^2, inter-chunk projections R times
+    intra = lambda R: 2 * (T / 64) * (64 * R) ** 2 * (128 + 64)
+    assert intra(4) / intra(1) == 4 ** g["mimo_intra_growth_power"]
+
+
+def test_prefill_bytes_workloads():
+    # SISO bf16 prefill (B=4, L=2048, H=16, N=128, P=64): 1032 B per token-head
+    per = roofline.prefill_bytes(1, 1, 1, 128, 64, 1, 2) - (128 * 64 * 4 + (128 + 64) * 2)
+    assert per == 1032
+    # MIMO R=4: 3336 B per token-head
+    per4 = roofline.prefill_bytes(1, 1, 1, 128, 64, 4, 2) - (128 * 64 * 4 + 4 * (128 + 64) * 2)
+    assert per4 == 3336
+    assert roofline.decode_bytes_per_slice(128, 64, 4, 2) == 71944
