@@ -72,6 +72,12 @@ typedef enum {
 
 typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
 
+/* m3_dims.flags: run the prefill as three kernels (chunk states, a state
+ * pass over chunks, chunk outputs) instead of the single-pass kernel with a
+ * look-back across chunks.  Same results up to rounding; the single-pass
+ * kernel is the default wherever it is built (dstate 128, headdim 64). */
+#define M3_SCAN_SPLIT 1
+
 typedef struct {
     int64_t batch;     /* >= 1                                              */
     int64_t seqlen;    /* L >= 0 (ignored by m3_step)                        */
@@ -81,7 +87,7 @@ typedef struct {
     int64_t rank;      /* R >= 1 (MIMO rank)                                 */
     int64_t chunk;     /* Q: tokens per chunk of the prefill scan            */
     int32_t io;        /* m3_dtype of x, B, C, y and the carry               */
-    int32_t reserved;  /* must be 0                                          */
+    int32_t flags;     /* 0 or M3_SCAN_SPLIT; other bits must be 0           */
     int64_t a_stride_b, a_stride_t, a_stride_h; /* strides of A, in floats   */
 } m3_dims;
 

@@ -12,13 +12,24 @@ static thread_local int g_last_hip_error = 0;
 static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
 ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N, int64_t P,
-                                          int io_bytes, int acc_bytes) {
-    ScanWorkspaceLayout w;
+                                          int io_bytes, int acc_bytes, bool fused) {
+    ScanWorkspaceLayout w = {};
     const size_t per = (size_t)BH * (size_t)nchunks;
-    w.off_M = 0;
-    w.off_Sin = align_up(per * (size_t)(N * P) * sizeof(float), 256);
-    w.off_tot = align_up(w.off_Sin + per * (size_t)(N * P) * (size_t)io_bytes, 256);
-    w.total = align_up(w.off_tot + per * (size_t)(N / 2 + 1) * (size_t)acc_bytes, 256);
+    const size_t tot_bytes = per * (size_t)(N / 2 + 1) * (size_t)acc_bytes;
+    const size_t state_bytes = per * (size_t)(N * P) * sizeof(float);
+    if (!fused) {
+        w.off_M = 0;
+        w.off_Sin = align_up(state_bytes, 256);
+        w.off_tot = align_up(w.off_Sin + per * (size_t)(N * P) * (size_t)io_bytes, 256);
+        w.total = align_up(w.off_tot + tot_bytes, 256);
+    } else {
+        w.off_ctl = 0;
+        w.off_flags = 256;
+        w.off_tot = align_up(w.off_flags + per * sizeof(uint32_t), 256);
+        w.off_agg = align_up(w.off_tot + tot_bytes, 256);
+        w.off_inc = align_up(w.off_agg + state_bytes, 256);
+        w.total = align_up(w.off_inc + state_bytes, 256);
+    }
     return w;
 }
 
@@ -32,7 +43,7 @@ static int io_bytes_of(int32_t io) { return io == M3_F32 ? 4 : io == M3_BF16 ? 2
 static m3_status check_dims_common(const m3_dims *d) {
     if (!d) return M3_ERR_NULL;
     if (d->io != M3_F32 && d->io != M3_BF16) return M3_ERR_DTYPE;
-    if (d->reserved != 0) return M3_ERR_SHAPE;
+    if (d->flags & ~M3_SCAN_SPLIT) return M3_ERR_SHAPE;
     if (d->batch < 1 || d->nheads < 1 || d->headdim < 1 || d->dstate < 2 || d->rank < 1)
         return M3_ERR_SHAPE;
     if (d->dstate % 2) return M3_ERR_SHAPE;
@@ -72,6 +83,12 @@ static m3_status check_scan_dims(const m3_dims *d, ScanImpl *impl, int64_t *nchu
     if (d->batch * d->nheads * nc > (int64_t)INT_MAX) return M3_ERR_SHAPE;
     *impl = find_scan_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
     if (!impl->launch) return M3_ERR_UNSUPPORTED;
+    // the single-pass kernel serves every shape it is built for, except the
+    // empty sequence (handled by the three-kernel path's state kernel alone)
+    if (nc > 0 && !(d->flags & M3_SCAN_SPLIT)) {
+        scan_launch_fn f = find_fused_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
+        if (f) { impl->launch = f; impl->fused = true; }
+    }
     *nchunks = nc;
     return M3_OK;
 }
@@ -81,7 +98,7 @@ extern "C" size_t m3_scan_workspace_bytes(const m3_dims *d) {
     int64_t nc = 0;
     if (check_scan_dims(d, &impl, &nc) != M3_OK) return 0;
     return scan_workspace_layout(d->batch * d->nheads, nc, d->dstate, d->headdim,
-                                 io_bytes_of(d->io), impl.acc_bytes)
+                                 io_bytes_of(d->io), impl.acc_bytes, impl.fused)
         .total;
 }
 
@@ -108,7 +125,7 @@ extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B,
         if (!aligned4(p)) return M3_ERR_ALIGN;
     const ScanWorkspaceLayout wl = scan_workspace_layout(d->batch * d->nheads, nc, d->dstate,
                                                          d->headdim, io_bytes_of(d->io),
-                                                         impl.acc_bytes);
+                                                         impl.acc_bytes, impl.fused);
     if (nc > 0 && (workspace == nullptr || workspace_bytes < wl.total)) return M3_ERR_WORKSPACE;
 
     ScanArgs a;
@@ -117,9 +134,19 @@ extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B,
     a.init_state = init_state; a.init_cB = init_carryB; a.init_cX = init_carryX;
     a.y = y; a.final_state = final_state; a.cB = carryB; a.cX = carryX;
     char *ws = static_cast<char *>(workspace);
-    a.M = nc > 0 ? reinterpret_cast<float *>(ws + wl.off_M) : nullptr;
-    a.Sin = nc > 0 ? ws + wl.off_Sin : nullptr;
-    a.tot = nc > 0 ? ws + wl.off_tot : nullptr;
+    a.M = nullptr; a.Sin = nullptr; a.tot = nullptr;
+    a.ctl = nullptr; a.flags = nullptr; a.agg = nullptr; a.inc = nullptr;
+    if (nc > 0 && !impl.fused) {
+        a.M = reinterpret_cast<float *>(ws + wl.off_M);
+        a.Sin = ws + wl.off_Sin;
+        a.tot = ws + wl.off_tot;
+    } else if (nc > 0) {
+        a.ctl = reinterpret_cast<uint32_t *>(ws + wl.off_ctl);
+        a.flags = reinterpret_cast<uint32_t *>(ws + wl.off_flags);
+        a.tot = ws + wl.off_tot;
+        a.agg = reinterpret_cast<float *>(ws + wl.off_agg);
+        a.inc = reinterpret_cast<float *>(ws + wl.off_inc);
+    }
     a.batch = d->batch; a.L = d->seqlen; a.H = d->nheads; a.nchunks = nc;
     a.a_sb = d->a_stride_b; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
     const hipError_t e = impl.launch(a, static_cast<hipStream_t>(stream));

@@ -20,6 +20,11 @@ struct ScanArgs {
     float *M;        // [BH][nchunks][N][P] fp32  per-chunk state contributions
     void *Sin;       // [BH][nchunks][P][N] io    state entering each chunk
     void *tot;       // [BH][nchunks][1+N/2] acc  chunk log-decay and angle totals
+    // single-pass (look-back) scan only
+    uint32_t *ctl;   // [0] ticket counter, [1] look-back timeouts
+    uint32_t *flags; // [BH][nchunks] 0 / aggregate ready / inclusive state ready
+    float *agg;      // [BH][nchunks][N*P] chunk aggregates (owner's lane layout)
+    float *inc;      // [BH][nchunks][N*P] inclusive states (same layout)
     int64_t batch, L, H, nchunks;
     int64_t a_sb, a_st, a_sh;
 };
@@ -40,17 +45,21 @@ typedef hipError_t (*step_launch_fn)(const StepArgs &, hipStream_t);
 struct ScanImpl {
     scan_launch_fn launch;
     int acc_bytes;   // bytes of the prologue scalar type (4: fp32, 8: fp64)
+    bool fused;      // single-pass look-back kernel (else the three-kernel path)
 };
 
 // Kernel lookup by shape; null launch when no kernel is built for it.
 ScanImpl find_scan_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 step_launch_fn find_step_impl(int io, int64_t N, int64_t P, int64_t R);
+scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 
 // Byte offsets of the workspace regions for a scan.
 struct ScanWorkspaceLayout {
-    size_t off_M, off_Sin, off_tot, total;
+    size_t off_M, off_Sin, off_tot;                 // three-kernel path
+    size_t off_ctl, off_flags, off_agg, off_inc;    // single-pass path (off_tot shared)
+    size_t total;
 };
 ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N,
-                                          int64_t P, int io_bytes, int acc_bytes);
+                                          int64_t P, int io_bytes, int acc_bytes, bool fused);
 
 }  // namespace m3

@@ -1,0 +1,739 @@
+// Single-pass chunked prefill scan of the Mamba-3 SSM on gfx950 (N = 128,
+// P = 64): one workgroup per chunk, chunks of a (batch, head) slice linked by
+// a decoupled look-back over their N x P fp32 state maps.
+//
+// Math (Sec. 3.3 "Chunked Algorithm for MIMO SSMs", the two-band mask of
+// Sec. 3.1.2 eq. mamba3-mask, the rotary form of Sec. 3.2 Prop. "Rotary
+// Embedding Equivalence with Exponential-Trapezoidal Discretization"); for a
+// chunk of Q tokens with chunk-local prefix sums cum_t (of dt A) and psi_t
+// (of theta), C^_t = R(-psi_t) C_t, B^_j = R(-psi_j) B_j, gamma_t = lambda_t dt_t
+// and sigma_j = gamma_j + (1 - lambda_{j+1}) dt_{j+1} (sigma_{L-1} = gamma_{L-1}):
+//   y_t   = sum_{j<=t} w_tj (C^_t . B^_j) x_j + e^{cum_t} C^_t . S_in + D x_t,
+//           w_tt = gamma_t, w_tj = e^{cum_t - cum_j} sigma_j
+//   S_out = T_c S_in + A_c,  T_c = e^{cum_e} R(psi_e),
+//           A_c = R(psi_e) sum_j e^{cum_e - cum_j} sigma_j B^_j x_j^T
+// S is the physical-frame state with the next token's previous-input term
+// folded in.  Rows of every chunk operand are (token, rank) pairs.
+//
+// Work of one workgroup (NW waves; each wave owns TPW tiles of 16 rows):
+//   1. ticket -> (slice, chunk), chunk-major, so every predecessor of a chunk
+//      holds an earlier ticket and is already resident (forward progress);
+//   2. prologue: cum (wavefront scans), gamma, sigma, w; angle prefix sums and
+//      a cos/sin table in LDS;
+//   3. aggregate first: per 64-row block, (B^ W)^T and x^T staged in LDS and
+//      M += B^T W x (MFMA, K = rows); A_c published (flag AGG);
+//   4. decoupled look-back: predecessors' flags probed 16 at a time, their
+//      maps composed nearest first until an inclusive state (flag INC) or the
+//      sequence start; S_out published (flag INC) before any output work, so
+//      the chain across chunks advances at the speed of the look-back alone;
+//      the last chunk writes the final state and the carry;
+//   5. outputs: C^ rows rotated straight into MFMA fragments; y starts as
+//      e^{cum_t} C^ S_in (MFMA, K = N); per block at or below each owned tile
+//      G^T = B^ C^T (MFMA, K = N) masked by w_tj, y += (w o G) x (MFMA,
+//      K = rows); D x added; y stored.  A chunk of a single 64-row block
+//      stages B^ once for both uses; longer chunks restage it from cache.
+// A tiny reset kernel clears the ticket counter and the flags first.
+#include <type_traits>
+
+#include "m3_device.h"
+#include "m3_internal.h"
+
+namespace m3 {
+namespace {
+
+constexpr uint32_t kFlagAgg = 1, kFlagInc = 2;
+constexpr uint32_t kSpinMax = 1u << 22;   // bounded wait: ~seconds, then error exit
+
+struct alignas(4) h2 { _Float16 c, s; };
+template <typename T> struct CsOf { typedef h2 type; };          // bf16 path: fp16 cos/sin
+template <> struct CsOf<float> { typedef float2 type; };         // fp32 path: fp32 cos/sin
+__device__ __forceinline__ void cs_put(h2 *p, float c, float s) { *p = h2{(_Float16)c, (_Float16)s}; }
+__device__ __forceinline__ void cs_put(float2 *p, float c, float s) { *p = make_float2(c, s); }
+__device__ __forceinline__ void cs_get(const h2 &v, float &c, float &s) { c = (float)v.c; s = (float)v.s; }
+__device__ __forceinline__ void cs_get(const float2 &v, float &c, float &s) { c = v.x; s = v.y; }
+
+template <typename T> struct Vec16;            // 16-byte vector of T
+template <> struct Vec16<bf16> { typedef bf16x8 type; static constexpr int n = 8; };
+template <> struct Vec16<float> { typedef f32x4 type; static constexpr int n = 4; };
+
+__device__ __forceinline__ float fget(const bf16x8 &v, int e) { return (float)v[e]; }
+__device__ __forceinline__ void fset(bf16x8 &v, int e, float x) { v[e] = (bf16)x; }
+__device__ __forceinline__ float fget(const float &v, int) { return v; }
+__device__ __forceinline__ void fset(float &v, int, float x) { v = x; }
+__device__ __forceinline__ float fget(const f32x4 &v, int e) { return v[e]; }
+__device__ __forceinline__ void fset(f32x4 &v, int e, float x) { v[e] = x; }
+
+// Look-back traffic uses device-scope atomic accesses only (the sc1 scope
+// bit): they are coherent across the XCDs' L2 caches by themselves, so no
+// cache-wide write-back or invalidate is needed.  A publisher waits until its
+// stores are acknowledged (vmcnt(0)) before the flag store; a reader issues
+// its data loads only after it has seen the flag.
+__device__ __forceinline__ void wait_stores_done() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+__device__ __forceinline__ void st_coh(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coh(double *p, double v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coh(const float *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_coh(const double *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <typename T, int Q_, int R_>
+struct FShape {
+    static constexpr int N = 128, P = 64, NH = 64, Q = Q_, R = R_;
+    static constexpr int QR = Q * R;
+    static constexpr int RT = QR / 16;                    // 16-row tiles in a chunk
+    static constexpr int NW = RT / 4 > 4 ? RT / 4 : 4;    // waves per workgroup
+    static constexpr int NTHR = NW * kWave;
+    static constexpr int TPW = RT / NW;                   // row tiles per wave
+    static constexpr int PTW = 16 / NW;                   // state pair-tiles per wave
+    static constexpr int JB = 64, NJB = QR / JB;          // staged row blocks
+    static constexpr int PAD = 16 / (int)sizeof(T);
+    static constexpr int LDN = N + PAD;                   // [rows][N] and [P][N] tiles
+    static constexpr int LDJ = JB + PAD;                  // [N or P][rows] tiles
+    static constexpr int NSEG = NTHR / NH;                // angle-scan segments
+    static constexpr int TPS = (Q + NSEG - 1) / NSEG;     // tokens per segment
+    static constexpr int CE = Vec16<T>::n;                // elements per 16-byte vector
+    static constexpr int ST_ELEMS = PTW * 2 * 4;          // state floats owned per lane
+    typedef typename AccOf<T>::type Acc;
+    typedef typename CsOf<T>::type CS;
+    static_assert(QR % 64 == 0 && RT <= 32, "chunk*rank in {64, ..., 512}");
+    static_assert(16 % R == 0, "row tiles hold whole tokens");
+    static_assert(Q <= 256 && NTHR % NH == 0, "prologue mapping");
+    static_assert(TPW >= 1 && TPW <= 4 && (TPW == 1 || TPW % 2 == 0), "tile assignment");
+};
+
+// Row tile owned as the m-th tile of wave w: pairs of tiles from both ends
+// of the chunk so that every wave gets the same causal work.
+template <class S>
+__device__ __forceinline__ int owned_tile(int w, int m) {
+    const int base = (m / 2) * 2 * S::NW;
+    return (m % 2 == 0) ? base + w : base + 2 * S::NW - 1 - w;
+}
+
+__global__ void k_reset(uint32_t *ctl, uint32_t *flags, int64_t nflags) {
+    const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i0 < 2) ctl[i0] = 0u;
+    for (int64_t i = i0; i < nflags; i += (int64_t)gridDim.x * blockDim.x) flags[i] = 0u;
+}
+
+constexpr uint32_t kFlagInit = 3;   // probe result for "before the first chunk"
+constexpr int kProbe = 16;          // predecessors probed per look-back round
+
+template <typename T, int Q, int R>
+// Two waves per SIMD: two 4-wave workgroups (or one 8-wave one) per CU.
+__global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanArgs a) {
+    typedef FShape<T, Q, R> S;
+    typedef typename S::Acc Acc;
+    typedef typename S::CS CS;
+    typedef Mma<T> MM;
+    typedef typename MM::frag Frag;
+    typedef typename Vec16<T>::type V16;
+    constexpr int N = S::N, P = S::P, NH = S::NH, NW = S::NW, TPW = S::TPW, PTW = S::PTW;
+    constexpr int NK = N / MM::K;       // MFMA K-steps over the state axis
+    constexpr int JK = S::JB / MM::K;   // MFMA K-steps over a 64-row block
+    constexpr int PT = P / 16;
+    constexpr int LDC = Q + 1;          // cos/sin table [pair][token], padded
+
+    __shared__ Acc s_cum[Q];
+    __shared__ Acc s_wtot[NW];
+    __shared__ Acc s_psie[NH];
+    __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
+    __shared__ CS s_cs[NH * LDC];
+    __shared__ __attribute__((aligned(16))) T s_B[S::JB * S::LDN];   // B^ block [row][n]
+    __shared__ __attribute__((aligned(16))) T s_X[P * S::LDJ];       // x^T block [p][row]
+    constexpr int kBtS = (N * S::LDJ > P * S::LDN) ? N * S::LDJ : P * S::LDN;
+    __shared__ __attribute__((aligned(16))) T s_BtS[kBtS];   // (B^ W)^T block [n][row]; later S_in^T [p][n]
+    __shared__ int s_i[4];
+    Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
+    static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
+
+    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int g = lane >> 4, l16 = lane & 15;
+
+    // ---- 1. ticket -> (slice, chunk) ----
+    if (tid == 0) s_i[0] = (int)atomicAdd(a.ctl, 1u);
+    __syncthreads();
+    const int64_t nsl = a.batch * a.H;
+    const int64_t ticket = s_i[0];
+    const int64_t c = ticket / nsl, sl = ticket % nsl;
+    const int64_t b = sl / a.H, h = sl % a.H;
+    const int64_t t0 = c * Q;
+    const int nvalid = (int)min((int64_t)Q, a.L - t0);
+    const int64_t slot = sl * a.nchunks + c;
+    const int64_t tok0 = (b * a.L + t0) * a.H + h;       // (b, t0, h) flat token-head index
+    const int64_t tstr = a.H;                             // token stride in token-heads
+    const bool last = (c == a.nchunks - 1);
+
+    // ---- 2. prologue ----
+    {
+        Acc lg = 0;
+        if (tid < Q) {
+            float gam = 0.f, sig = 0.f;
+            if (tid < nvalid) {
+                const int64_t t = t0 + tid, k = tok0 + tid * tstr;
+                const float dtv = a.dt[k], lamv = a.lam[k];
+                lg = (Acc)dtv * (Acc)a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
+                gam = lamv * dtv;
+                sig = gam;
+                if (t + 1 < a.L) sig += (1.f - a.lam[k + tstr]) * a.dt[k + tstr];
+            }
+            s_gam[tid] = gam;
+            s_sig[tid] = sig;
+        }
+        Acc v = wave_incl_scan(lg, lane);
+        if (lane == kWave - 1) s_wtot[wave] = v;
+        // angles: thread (pair i, segment seg) keeps its segment's running sums
+        const int i = tid % NH, seg = tid / NH;
+        Acc ps[S::TPS];
+        Acc run = 0;
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            const int t = seg * S::TPS + k;
+            if (t < nvalid) run += (Acc)a.theta[(tok0 + t * tstr) * NH + i];
+            ps[k] = run;
+        }
+        s_segtot[seg * NH + i] = run;
+        __syncthreads();
+        if (tid < Q) {
+            Acc off = 0;
+            for (int w2 = 0; w2 < wave; ++w2) off += s_wtot[w2];
+            s_cum[tid] = v + off;
+        }
+        Acc off = 0;
+        for (int s2 = 0; s2 < seg; ++s2) off += s_segtot[s2 * NH + i];
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            const int t = seg * S::TPS + k;
+            if (t < Q) {
+                const Acc psi = ps[k] + off;
+                Acc sn, cs;
+                sincos_acc(psi, &sn, &cs);
+                cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
+                if (t == nvalid - 1) s_psie[i] = psi;
+            }
+        }
+        __syncthreads();
+        if (tid < Q) {
+            const Acc cum_e = s_cum[nvalid - 1];
+            s_w[tid] = (tid < nvalid) ? (float)(exp_acc(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
+        }
+        __syncthreads();
+    }
+
+    const T *Cg = static_cast<const T *>(a.C) + tok0 * (R * N);
+    const T *Bg = static_cast<const T *>(a.B) + tok0 * (R * N);
+    const T *Xg = static_cast<const T *>(a.x) + tok0 * (R * P);
+    const int64_t bstr = tstr * R * N, xstr = tstr * R * P;   // token strides of B/C and x
+
+    // Stage rows jb*64 .. of the chunk: B^ = R(-psi_t) B rotated, as the
+    // w-scaled transpose (kBt: operand of M) and/or row-major (kRow: operand
+    // of G^T), and x^T.  Consecutive lanes take consecutive rows, so the
+    // transposed LDS stores and the table reads are conflict-free.
+    auto stage = [&](int jb, auto kBt, auto kRow) {
+        for (int task = tid; task < S::JB * (NH / S::CE); task += S::NTHR) {
+            const int jr = task % S::JB, cp = task / S::JB;
+            const int row = jb * S::JB + jr, t = row / R, r = row % R;
+            V16 lo{}, hi{};
+            if (t < nvalid) {
+                const T *src = Bg + t * bstr + r * N + cp * S::CE;
+                lo = *reinterpret_cast<const V16 *>(src);
+                hi = *reinterpret_cast<const V16 *>(src + NH);
+            }
+            const float wt = s_w[t];
+#pragma unroll
+            for (int e = 0; e < S::CE; ++e) {
+                const int n = cp * S::CE + e;
+                float cs, sn;
+                cs_get(s_cs[n * LDC + t], cs, sn);
+                const float u = fget(lo, e), w = fget(hi, e);
+                const float re = cs * u + sn * w, im = cs * w - sn * u;
+                if constexpr (decltype(kRow)::value) {
+                    fset(lo, e, re);
+                    fset(hi, e, im);
+                }
+                if constexpr (decltype(kBt)::value) {
+                    s_BtS[n * S::LDJ + jr] = from_f32<T>(wt * re);
+                    s_BtS[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
+                }
+            }
+            if constexpr (decltype(kRow)::value) {
+                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + cp * S::CE]) = lo;
+                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + NH + cp * S::CE]) = hi;
+            }
+        }
+        for (int task = tid; task < S::JB * (P / S::CE); task += S::NTHR) {
+            const int jr = task % S::JB, pc = task / S::JB;
+            const int row = jb * S::JB + jr, t = row / R, r = row % R;
+            V16 xv{};
+            if (t < nvalid) xv = *reinterpret_cast<const V16 *>(Xg + t * xstr + r * P + pc * S::CE);
+#pragma unroll
+            for (int e = 0; e < S::CE; ++e) s_X[(pc * S::CE + e) * S::LDJ + jr] = xv[e];
+        }
+    };
+    using True = std::integral_constant<bool, true>;
+    using False = std::integral_constant<bool, false>;
+
+    // ---- 3. aggregate: M = B^T W x over the chunk (state pair-tiles) ----
+    f32x4 ms[PTW][2];
+#pragma unroll
+    for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int jb = 0; jb < S::NJB; ++jb) {
+        if constexpr (S::NJB == 1) stage(jb, True{}, True{});   // one block: keep B^ for the outputs
+        else stage(jb, True{}, False{});
+        __syncthreads();
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int nt = ntl + 4 * half;
+#pragma unroll
+                for (int ks = 0; ks < JK; ++ks) {
+                    const Frag af = MM::load(&s_BtS[(nt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    const Frag bf = MM::load(&s_X[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    ms[m2][half] = MM::mma(af, bf, ms[m2][half]);
+                }
+            }
+        }
+        __syncthreads();
+    }
+
+    // Owned state element (m2, half, v): row n = 16*(ntl + 4*half) + 4g + v,
+    // column p = 16*pt + l16; rows (i, i + N/2) of a pair sit in one lane.
+    const Acc cum_e = s_cum[nvalid - 1];
+    float Ast[PTW][2][4];   // A_c = R(psi_e) M
+#pragma unroll
+    for (int m2 = 0; m2 < PTW; ++m2) {
+        const int ntl = (wave + NW * m2) % 4;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            Acc sn, cs;
+            sincos_acc(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
+            const Acc re = ms[m2][0][v], im = ms[m2][1][v];
+            Ast[m2][0][v] = (float)(cs * re - sn * im);
+            Ast[m2][1][v] = (float)(sn * re + cs * im);
+        }
+    }
+    auto elem_index = [&](int m2, int half) -> int64_t {   // float4 slot of the owned layout
+        return ((int64_t)(m2 * 2 + half) * S::NTHR + tid) * 4;
+    };
+    const int64_t SZ = (int64_t)N * P;
+    Acc *totp = static_cast<Acc *>(a.tot);
+    if (c > 0 && !last) {   // publish the aggregate (only successors read it)
+        float *dst = a.agg + slot * SZ;
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) st_coh(dst + elem_index(m2, half) + v, Ast[m2][half][v]);
+        if (tid == 0) st_coh(totp + slot * (NH + 1), cum_e);
+        if (tid < NH) st_coh(totp + slot * (NH + 1) + 1 + tid, s_psie[tid]);
+        wait_stores_done();
+        __syncthreads();
+        if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagAgg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+
+    // ---- 4. look-back: S_in of this chunk ----
+    // S_init (owned): initial state plus the carried previous-input term of token 0
+    auto load_init = [&](float (&Si)[PTW][2][4]) {
+        const float *ist = a.init_state ? a.init_state + sl * SZ : nullptr;
+        float wb = 0.f;
+        if (a.init_cB) {
+            const int64_t k0 = (b * a.L) * a.H + h;
+            wb = (1.f - a.lam[k0]) * a.dt[k0];
+        }
+        const T *iB = a.init_cB ? static_cast<const T *>(a.init_cB) + sl * (R * N) : nullptr;
+        const T *iX = a.init_cX ? static_cast<const T *>(a.init_cX) + sl * (R * P) : nullptr;
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4, p = pt * 16 + l16;
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int n = 16 * (ntl + 4 * half) + 4 * g + v;
+                    float sv = ist ? ist[n * P + p] : 0.f;
+                    if (iB) {
+                        float u = 0.f;
+                        for (int r = 0; r < R; ++r) u += to_f32(iB[r * N + n]) * to_f32(iX[r * P + p]);
+                        sv += wb * u;
+                    }
+                    Si[m2][half][v] = sv;
+                }
+        }
+    };
+
+    float Sin[PTW][2][4];
+    if (c == 0) {
+        load_init(Sin);
+    } else {
+        // Decoupled look-back: compose predecessors' maps S -> T_j S + A_j
+        // (nearest first) until an inclusive state or the sequence start.
+        // All owned pair rows of a lane are 16*ntl + 4g + v (ntl = wave % 4),
+        // so the accumulated rotation needs one angle per v.
+        Acc ad = 1;                 // accumulated decay
+        Acc aps[4];                 // accumulated angle of pair rows 16*ntl + 4g + v
+        float aA[PTW][2][4];        // accumulated offset
+#pragma unroll
+        for (int v = 0; v < 4; ++v) aps[v] = 0;
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) aA[m2][0][v] = aA[m2][1][v] = 0.f;
+        auto finish = [&](const float (&X)[PTW][2][4]) {
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                Acc sn, cs;
+                sincos_acc(aps[v], &sn, &cs);
+                sn *= ad;
+                cs *= ad;
+#pragma unroll
+                for (int m2 = 0; m2 < PTW; ++m2) {
+                    const Acc re = X[m2][0][v], im = X[m2][1][v];
+                    Sin[m2][0][v] = (float)(cs * re - sn * im) + aA[m2][0][v];
+                    Sin[m2][1][v] = (float)(sn * re + cs * im) + aA[m2][1][v];
+                }
+            }
+        };
+        const int ntl_w = wave % 4;
+        struct Agg { float d[PTW][2][4]; Acc ps[4]; Acc cm; };
+        auto load_agg = [&](int64_t js, Agg &o) {
+            const float *src = a.agg + js * SZ;
+            const Acc *tp = totp + js * (NH + 1);
+            o.cm = ld_coh(tp);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) o.ps[v] = ld_coh(tp + 1 + ntl_w * 16 + 4 * g + v);
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    o.d[m2][0][v] = ld_coh(src + elem_index(m2, 0) + v);
+                    o.d[m2][1][v] = ld_coh(src + elem_index(m2, 1) + v);
+                }
+        };
+        int64_t j = c - 1;
+        const int64_t sbase = sl * a.nchunks;
+        while (true) {
+            // probe predecessors j, j-1, ..., j-15 at once (lanes of wave 0)
+            if (wave == 0) {
+                uint32_t f = 0;
+                if (lane < kProbe) {
+                    const int64_t jj = j - lane;
+                    f = (jj < 0) ? kFlagInit
+                                 : __hip_atomic_load(a.flags + sbase + jj, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+                }
+                const uint64_t mterm = __ballot(lane < kProbe && (f == kFlagInc || f == kFlagInit));
+                const uint64_t mzero = __ballot(lane < kProbe && f == 0u);
+                const int ft = mterm ? __ffsll((unsigned long long)mterm) - 1 : kProbe;
+                const int fz = mzero ? __ffsll((unsigned long long)mzero) - 1 : kProbe;
+                const uint32_t fterm = __shfl(f, ft < kProbe ? ft : 0, kWave);
+                if (lane == 0) {
+                    s_i[1] = (fz < ft) ? fz : ft;                        // aggregates to compose
+                    s_i[2] = (fz < ft || ft == kProbe) ? 0 : (int)fterm;  // terminal kind
+                    s_i[3] = (fz < ft) ? 1 : 0;                          // must wait on a chunk
+                }
+            }
+            __syncthreads();
+            const int ncomp = s_i[1], term = s_i[2], needwait = s_i[3];
+            __syncthreads();
+            for (int k = 0; k < ncomp; ++k) {
+                Agg cur;
+                load_agg(sbase + j - k, cur);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    Acc sn, cs;
+                    sincos_acc(aps[v], &sn, &cs);
+                    sn *= ad;
+                    cs *= ad;
+#pragma unroll
+                    for (int m2 = 0; m2 < PTW; ++m2) {
+                        const Acc re = cur.d[m2][0][v], im = cur.d[m2][1][v];
+                        aA[m2][0][v] += (float)(cs * re - sn * im);
+                        aA[m2][1][v] += (float)(sn * re + cs * im);
+                    }
+                    aps[v] += cur.ps[v];
+                }
+                ad *= exp_acc(cur.cm);
+            }
+            j -= ncomp;
+            if (term == (int)kFlagInc) {
+                const float *src = a.inc + (sbase + j) * SZ;
+                float X[PTW][2][4];
+#pragma unroll
+                for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                    for (int half = 0; half < 2; ++half)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) X[m2][half][v] = ld_coh(src + elem_index(m2, half) + v);
+                finish(X);
+                break;
+            }
+            if (term == (int)kFlagInit) {
+                float X[PTW][2][4];
+                load_init(X);
+                finish(X);
+                break;
+            }
+            if (needwait) {   // the nearest unfinished predecessor is j: wait for it
+                if (tid == 0) {
+                    uint32_t f = 0u;
+                    for (uint32_t spin = 0; spin < kSpinMax; ++spin) {
+                        f = __hip_atomic_load(a.flags + sbase + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                        if (f != 0u) break;
+                        __builtin_amdgcn_s_sleep(2);
+                    }
+                    if (f == 0u) atomicAdd(a.ctl + 1, 1u);   // timed out: report and stop waiting
+                    s_i[1] = (f == 0u) ? 1 : 0;
+                }
+                __syncthreads();
+                const int timed_out = s_i[1];
+                __syncthreads();
+                if (timed_out) {
+                    float X[PTW][2][4] = {};
+                    finish(X);
+                    break;
+                }
+            }
+        }
+    }
+
+    // S_out = e^{cum_e} R(psi_e) S_in + A_c
+    {
+        float Sout[PTW][2][4];
+        const Acc de = exp_acc(cum_e);
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int ntl = (wave + NW * m2) % 4;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                Acc sn, cs;
+                sincos_acc(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
+                const Acc re = Sin[m2][0][v], im = Sin[m2][1][v];
+                Sout[m2][0][v] = (float)(de * (cs * re - sn * im)) + Ast[m2][0][v];
+                Sout[m2][1][v] = (float)(de * (sn * re + cs * im)) + Ast[m2][1][v];
+            }
+        }
+        if (!last) {
+            float *dst = a.inc + slot * SZ;
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                for (int half = 0; half < 2; ++half)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) st_coh(dst + elem_index(m2, half) + v, Sout[m2][half][v]);
+            wait_stores_done();
+            __syncthreads();
+            if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagInc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            float *fs = a.final_state + sl * SZ;
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2) {
+                const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
+#pragma unroll
+                for (int half = 0; half < 2; ++half)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v)
+                        fs[(16 * (ntl + 4 * half) + 4 * g + v) * P + pt * 16 + l16] = Sout[m2][half][v];
+            }
+            T *cB = static_cast<T *>(a.cB) + sl * (R * N);
+            T *cX = static_cast<T *>(a.cX) + sl * (R * P);
+            const int64_t kl = (b * a.L + a.L - 1) * a.H + h;
+            const T *Bl = static_cast<const T *>(a.B) + kl * (R * N);
+            const T *Xl = static_cast<const T *>(a.x) + kl * (R * P);
+            for (int e = tid; e < R * N; e += S::NTHR) cB[e] = Bl[e];
+            for (int e = tid; e < R * P; e += S::NTHR) cX[e] = Xl[e];
+        }
+    }
+
+    // ---- 5. outputs ----
+    T *s_S = s_BtS;   // S_in^T [p][n] in the io dtype (the (B^ W)^T block is no longer read)
+#pragma unroll
+    for (int m2 = 0; m2 < PTW; ++m2) {
+        const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
+#pragma unroll
+        for (int half = 0; half < 2; ++half)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+                s_S[(pt * 16 + l16) * S::LDN + 16 * (ntl + 4 * half) + 4 * g + v] = from_f32<T>(Sin[m2][half][v]);
+    }
+    // C^ fragments of the owned row tiles, rotated by -psi_t
+    Frag cf[TPW][NK];
+#pragma unroll
+    for (int m = 0; m < TPW; ++m) {
+        const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
+        const T *src = Cg + t * bstr + r * N;
+#pragma unroll
+        for (int kk = 0; kk < NK; ++kk) {
+            if (t < nvalid) cf[m][kk] = MM::load(src + kk * MM::K + MM::KPL * g);
+            else cf[m][kk] = Frag{};
+        }
+#pragma unroll
+        for (int kk = 0; kk < NK / 2; ++kk) {
+#pragma unroll
+            for (int e = 0; e < MM::KPL; ++e) {
+                const int n = kk * MM::K + MM::KPL * g + e;
+                float cs, sn;
+                cs_get(s_cs[n * LDC + t], cs, sn);
+                const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
+                fset(cf[m][kk], e, cs * u + sn * w);
+                fset(cf[m][kk + NK / 2], e, cs * w - sn * u);
+            }
+        }
+    }
+    __syncthreads();   // s_S complete
+    // inter-chunk term e^{cum_t} C^_t . S_in starts the accumulators
+    f32x4 acc[TPW][PT];
+#pragma unroll
+    for (int m = 0; m < TPW; ++m) {
+        const int TT = owned_tile<S>(wave, m);
+#pragma unroll
+        for (int pt = 0; pt < PT; ++pt) {
+            f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kk = 0; kk < NK; ++kk)
+                tmp = MM::mma(cf[m][kk], MM::load(&s_S[(pt * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), tmp);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int t = (TT * 16 + 4 * g + v) / R;
+                tmp[v] *= (float)exp_acc(s_cum[t]);
+            }
+            acc[m][pt] = tmp;
+        }
+    }
+    // intra-chunk term over the row blocks at or below each owned tile
+    for (int jb = 0; jb < S::NJB; ++jb) {
+        if constexpr (S::NJB > 1) {
+            stage(jb, False{}, True{});
+            __syncthreads();
+        }
+#pragma unroll
+        for (int jp = 0; jp < S::JB / 32; ++jp) {
+            const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
+            Frag bfr[2][NK];
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk)
+                    bfr[q][kk] = MM::load(&s_B[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
+#pragma unroll
+            for (int m = 0; m < TPW; ++m) {
+                const int TT = owned_tile<S>(wave, m);
+                if (J0 > TT) continue;
+                f32x4 gt[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    if (J0 + q <= TT) {
+#pragma unroll
+                        for (int kk = 0; kk < NK; ++kk) gt[q] = MM::mma(bfr[q][kk], cf[m][kk], gt[q]);
+                    }
+                }
+                const int tt = (TT * 16 + l16) / R;
+                const Acc cum_t = s_cum[tt];
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        const int tj = ((J0 + q) * 16 + 4 * g + v) / R;
+                        float w = 0.f;
+                        if (tj < tt) w = (float)exp_acc(cum_t - s_cum[tj]) * s_sig[tj];
+                        else if (tj == tt) w = s_gam[tt];
+                        gt[q][v] *= w;
+                    }
+                if constexpr (MM::KPL == 8) {
+                    bf16x8 af;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        af[v] = (bf16)gt[0][v];
+                        af[4 + v] = (bf16)gt[1][v];
+                    }
+#pragma unroll
+                    for (int pt = 0; pt < PT; ++pt) {
+                        const T *xr = &s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
+                        const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
+                        const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
+                        bf16x8 xf;
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) { xf[v] = lo[v]; xf[4 + v] = hi[v]; }
+                        acc[m][pt] = MM::mma(af, xf, acc[m][pt]);
+                    }
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 2; ++q)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+#pragma unroll
+                            for (int pt = 0; pt < PT; ++pt) {
+                                const float xv = to_f32(s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
+                                acc[m][pt] = MM::mma(gt[q][v], xv, acc[m][pt]);
+                            }
+                }
+            }
+        }
+        if constexpr (S::NJB > 1) __syncthreads();
+    }
+    // skip term and store
+    const float Dh = a.D[h];
+    T *Yg = static_cast<T *>(a.y) + tok0 * (R * P);
+#pragma unroll
+    for (int m = 0; m < TPW; ++m) {
+        const int TT = owned_tile<S>(wave, m);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int row = TT * 16 + 4 * g + v, t = row / R, r = row % R;
+            if (t < nvalid) {
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) {
+                    const int p = pt * 16 + l16;
+                    const float yv = acc[m][pt][v] + Dh * to_f32(Xg[t * xstr + r * P + p]);
+                    Yg[t * xstr + r * P + p] = from_f32<T>(yv);
+                }
+            }
+        }
+    }
+}
+
+template <typename T, int Q, int R>
+hipError_t launch_fused(const ScanArgs &a, hipStream_t stream) {
+    typedef FShape<T, Q, R> S;
+    const int64_t nsl = a.batch * a.H;
+    const int64_t nflags = nsl * a.nchunks;
+    const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);
+    hipLaunchKernelGGL(k_reset, dim3(rblocks), dim3(256), 0, stream, a.ctl, a.flags, nflags);
+    hipLaunchKernelGGL((k_scan_fused<T, Q, R>), dim3((unsigned)(nsl * a.nchunks)), dim3(S::NTHR), 0,
+                       stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+#define M3_FUSED_SHAPES(X)   \
+    X(0, float, 2, 32)       \
+    X(0, float, 4, 16)       \
+    X(0, float, 4, 32)       \
+    X(1, bf16, 1, 64)        \
+    X(1, bf16, 1, 128)       \
+    X(1, bf16, 2, 32)        \
+    X(1, bf16, 2, 64)        \
+    X(1, bf16, 2, 128)       \
+    X(1, bf16, 4, 32)        \
+    X(1, bf16, 4, 64)        \
+    X(1, bf16, 4, 128)
+
+scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q) {
+    if (N != 128 || P != 64) return nullptr;
+#define M3_CASE(IO, T, R_, Q_) \
+    if (io == IO && R == R_ && Q == Q_) return &launch_fused<T, Q_, R_>;
+    M3_FUSED_SHAPES(M3_CASE)
+#undef M3_CASE
+    return nullptr;
+}
+
+}  // namespace m3

@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libm3.so")
 M3_OK, M3_ERR_NULL, M3_ERR_SHAPE, M3_ERR_DTYPE = 0, 1, 2, 3
 M3_ERR_UNSUPPORTED, M3_ERR_ALIGN, M3_ERR_WORKSPACE, M3_ERR_HIP = 4, 5, 6, 7
 M3_F32, M3_BF16 = 0, 1
+M3_SCAN_SPLIT = 1
 _IO = {torch.float32: M3_F32, torch.bfloat16: M3_BF16}
 
 
@@ -27,7 +28,7 @@ class M3Dims(ctypes.Structure):
                 ("nheads", ctypes.c_int64), ("headdim", ctypes.c_int64),
                 ("dstate", ctypes.c_int64), ("rank", ctypes.c_int64),
                 ("chunk", ctypes.c_int64), ("io", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("a_stride_b", ctypes.c_int64),
+                ("flags", ctypes.c_int32), ("a_stride_b", ctypes.c_int64),
                 ("a_stride_t", ctypes.c_int64), ("a_stride_h", ctypes.c_int64)]
 
 
@@ -97,12 +98,13 @@ def _a_strides(A: torch.Tensor, batch: int, seqlen: int, nheads: int):
     raise ValueError(f"A must be [H] or [B, L, H], got {tuple(A.shape)}")
 
 
-def scan_dims(x: torch.Tensor, Bm: torch.Tensor, chunk: int, A: Optional[torch.Tensor] = None) -> M3Dims:
+def scan_dims(x: torch.Tensor, Bm: torch.Tensor, chunk: int, A: Optional[torch.Tensor] = None,
+              split: bool = False) -> M3Dims:
     batch, seqlen, nheads, rank, headdim = x.shape
     dstate = Bm.shape[-1]
     sb, st, sh = _a_strides(A, batch, seqlen, nheads) if A is not None else (0, 0, 1)
     return M3Dims(batch, seqlen, nheads, headdim, dstate, rank, int(chunk),
-                  _IO[x.dtype], 0, sb, st, sh)
+                  _IO[x.dtype], M3_SCAN_SPLIT if split else 0, sb, st, sh)
 
 
 def workspace_bytes(dims: M3Dims) -> int:
@@ -111,11 +113,13 @@ def workspace_bytes(dims: M3Dims) -> int:
 
 def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
              init_state=None, init_carry=None, out=None, workspace=None,
-             stream=None) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
+             stream=None, split: bool = False
+             ) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
     """m3_scan_fwd: returns y [B,L,H,R,P], final_state [B,H,N,P] fp32 and the
     carry (B_{L-1} [B,H,R,N], X_{L-1} [B,H,R,P]).  `out` may supply
-    (y, final_state, carryB, carryX) to write into."""
-    d = scan_dims(x, Bm, chunk, A)
+    (y, final_state, carryB, carryX) to write into; `split` selects the
+    three-kernel scan (M3_SCAN_SPLIT)."""
+    d = scan_dims(x, Bm, chunk, A, split)
     batch, seqlen, nheads, rank, headdim = x.shape
     dstate = Bm.shape[-1]
     dev = x.device

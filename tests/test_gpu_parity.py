@@ -25,7 +25,7 @@ def say(msg):
     print(f"[gpu-case] {msg}", flush=True)
 
 
-def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True):
+def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, split=False):
     """Scan with every output pre-filled with NaN, so an unwritten element fails."""
     x = inp.x
     B_, L, H, R, P = x.shape
@@ -36,10 +36,17 @@ def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True):
                torch.full((B_, H, N, P), float("nan"), device=x.device),
                torch.full((B_, H, R, N), float("nan"), device=x.device, dtype=x.dtype),
                torch.full((B_, H, R, P), float("nan"), device=x.device, dtype=x.dtype))
+    nbytes = m3.workspace_bytes(m3.scan_dims(x, inp.Bm, chunk, inp.A, split))
+    # the single-pass kernel serves this shape iff its workspace differs from the split path's
+    single_pass = not split and nbytes != m3.workspace_bytes(m3.scan_dims(x, inp.Bm, chunk, inp.A, True))
+    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=x.device)
     y, fs, (cB, cX) = m3.scan_fwd(x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta, inp.D,
                                   chunk=chunk, init_state=init_state, init_carry=init_carry,
-                                  out=out)
+                                  out=out, split=split, workspace=ws)
     torch.cuda.synchronize()
+    if single_pass and L > 0:
+        # single-pass kernel: word 1 of the workspace counts look-back waits that timed out
+        assert int(ws[4:8].view(torch.int32).item()) == 0, "look-back wait timed out"
     return y, fs, cB, cX
 
 
@@ -169,13 +176,15 @@ SHAPES = [  # io, N, P, R, Q
 ]
 
 
+@pytest.mark.parametrize("split", [False, True])
 @pytest.mark.parametrize("io,N,P,R,Q", SHAPES)
-def test_shapes_ragged(io, N, P, R, Q):
-    """Several chunks plus a ragged tail, two batch rows and three heads."""
+def test_shapes_ragged(io, N, P, R, Q, split):
+    """Several chunks plus a ragged tail, two batch rows and three heads, on
+    the single-pass kernel and on the three-kernel path."""
     L = 3 * Q + Q // 2 + 3
-    say(f"shape io={io} N={N} P={P} R={R} Q={Q} L={L}")
+    say(f"shape io={io} N={N} P={P} R={R} Q={Q} L={L} split={split}")
     inp = make_scan_inputs(2, L, 3, P, N, R, io=io, seed=11 + N + R + Q, device=DEV, chunk=Q)
-    y, fs, cB, cX = run_scan(inp, Q)
+    y, fs, cB, cX = run_scan(inp, Q, split=split)
     check_slices(inp, y, fs, cB, cX, sample_slices(2, 3, 99, 5), TOL[io], label=f"{io}/{N}/{R}/{Q}")
 
 

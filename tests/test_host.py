@@ -47,7 +47,7 @@ FAKE = 0x100000  # 16-byte aligned fake device address; never dereferenced
 
 def dims(**kw):
     d = dict(batch=1, seqlen=256, nheads=2, headdim=16, dstate=16, rank=1, chunk=64,
-             io=m3.M3_F32, reserved=0, a_stride_b=0, a_stride_t=0, a_stride_h=1)
+             io=m3.M3_F32, flags=0, a_stride_b=0, a_stride_t=0, a_stride_h=1)
     d.update(kw)
     return m3.M3Dims(**d)
 
@@ -74,7 +74,7 @@ def test_scan_host_validation(L):
     assert scan_call(L, dims(batch=0)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(seqlen=-1)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(chunk=0)) == m3.M3_ERR_SHAPE
-    assert scan_call(L, dims(reserved=1)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(flags=2)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(dstate=64, headdim=64)) == m3.M3_ERR_UNSUPPORTED
     assert scan_call(L, dims(chunk=48)) == m3.M3_ERR_UNSUPPORTED
     assert scan_call(L, dims(io=m3.M3_BF16)) == m3.M3_ERR_UNSUPPORTED
@@ -97,6 +97,12 @@ def test_workspace_bytes(L):
              nheads=32)
     nb = L.m3_scan_workspace_bytes(ctypes.byref(d))
     per = 8 * 32 * 64
+    # single-pass: flags, chunk totals, aggregate and inclusive fp32 states
+    assert nb >= per * (4 + 65 * 4 + 2 * 128 * 64 * 4)
+    assert nb % 256 == 0
+    d.flags = m3.M3_SCAN_SPLIT
+    nb = L.m3_scan_workspace_bytes(ctypes.byref(d))
+    # three-kernel: per-chunk fp32 contributions, bf16 entering states, totals
     assert nb >= per * 128 * 64 * (4 + 2) + per * 65 * 4
     assert nb % 256 == 0
 
