@@ -62,6 +62,19 @@ __device__ __forceinline__ void sincos_acc(double x, double *s, double *c) { sin
 __device__ __forceinline__ float exp_acc(float x) { return expf(x); }
 __device__ __forceinline__ double exp_acc(double x) { return exp(x); }
 
+// Hardware transcendentals for the bf16 path (v_sin/v_cos/v_exp after an
+// explicit reduction of the angle to [-pi, pi]; errors ~1e-6 relative, far
+// below bf16 rounding), and accurate fp64 for the fp32 path.
+__device__ __forceinline__ float reduce_angle(float x) {
+    return x - 6.28318530717958647692f * rintf(x * 0.15915494309189533577f);
+}
+__device__ __forceinline__ void sincos_fast(float x, float *s, float *c) {
+    __sincosf(reduce_angle(x), s, c);
+}
+__device__ __forceinline__ void sincos_fast(double x, double *s, double *c) { sincos(x, s, c); }
+__device__ __forceinline__ float exp_fast(float x) { return __expf(x); }
+__device__ __forceinline__ double exp_fast(double x) { return exp(x); }
+
 // Inclusive prefix sum across the 64 lanes of a wavefront.
 template <typename A>
 __device__ __forceinline__ A wave_incl_scan(A v, int lane) {

@@ -70,6 +70,16 @@ __device__ __forceinline__ void fset(f32x4 &v, int e, float x) { v[e] = x; }
 // its data loads only after it has seen the flag.
 __device__ __forceinline__ void wait_stores_done() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
+__device__ __forceinline__ void st_coh2(unsigned long long *p, float x, float y) {
+    const unsigned long long w = (unsigned long long)__float_as_uint(x) |
+                                 ((unsigned long long)__float_as_uint(y) << 32);
+    __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void ld_coh2(const unsigned long long *p, float &x, float &y) {
+    const unsigned long long w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    x = __uint_as_float((unsigned)(w & 0xffffffffull));
+    y = __uint_as_float((unsigned)(w >> 32));
+}
 __device__ __forceinline__ void st_coh(float *p, float v) {
     __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
@@ -88,7 +98,7 @@ struct FShape {
     static constexpr int N = 128, P = 64, NH = 64, Q = Q_, R = R_;
     static constexpr int QR = Q * R;
     static constexpr int RT = QR / 16;                    // 16-row tiles in a chunk
-    static constexpr int NW = RT / 4 > 4 ? RT / 4 : 4;    // waves per workgroup
+    static constexpr int NW = RT >= 16 ? 8 : 4;           // waves per workgroup
     static constexpr int NTHR = NW * kWave;
     static constexpr int TPW = RT / NW;                   // row tiles per wave
     static constexpr int PTW = 16 / NW;                   // state pair-tiles per wave
@@ -126,8 +136,10 @@ constexpr uint32_t kFlagInit = 3;   // probe result for "before the first chunk"
 constexpr int kProbe = 16;          // predecessors probed per look-back round
 
 template <typename T, int Q, int R>
-// Two waves per SIMD: two 4-wave workgroups (or one 8-wave one) per CU.
-__global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanArgs a) {
+// Two waves per SIMD: two 4-wave workgroups or one 8-wave workgroup per CU
+// (more waves spill the tile registers of the output phase).
+__global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2)
+void k_scan_fused(ScanArgs a) {
     typedef FShape<T, Q, R> S;
     typedef typename S::Acc Acc;
     typedef typename S::CS CS;
@@ -152,8 +164,10 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
     __shared__ int s_i[4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
+    static_assert(NW * 16 * P <= S::JB * S::LDN, "y staging fits in the B^ block");
 
-    const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // uniform: scalar branches
     const int g = lane >> 4, l16 = lane & 15;
 
     // ---- 1. ticket -> (slice, chunk) ----
@@ -170,81 +184,49 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
     const int64_t tstr = a.H;                             // token stride in token-heads
     const bool last = (c == a.nchunks - 1);
 
-    // ---- 2. prologue ----
-    {
-        Acc lg = 0;
-        if (tid < Q) {
-            float gam = 0.f, sig = 0.f;
-            if (tid < nvalid) {
-                const int64_t t = t0 + tid, k = tok0 + tid * tstr;
-                const float dtv = a.dt[k], lamv = a.lam[k];
-                lg = (Acc)dtv * (Acc)a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
-                gam = lamv * dtv;
-                sig = gam;
-                if (t + 1 < a.L) sig += (1.f - a.lam[k + tstr]) * a.dt[k + tstr];
-            }
-            s_gam[tid] = gam;
-            s_sig[tid] = sig;
-        }
-        Acc v = wave_incl_scan(lg, lane);
-        if (lane == kWave - 1) s_wtot[wave] = v;
-        // angles: thread (pair i, segment seg) keeps its segment's running sums
-        const int i = tid % NH, seg = tid / NH;
-        Acc ps[S::TPS];
-        Acc run = 0;
-#pragma unroll
-        for (int k = 0; k < S::TPS; ++k) {
-            const int t = seg * S::TPS + k;
-            if (t < nvalid) run += (Acc)a.theta[(tok0 + t * tstr) * NH + i];
-            ps[k] = run;
-        }
-        s_segtot[seg * NH + i] = run;
-        __syncthreads();
-        if (tid < Q) {
-            Acc off = 0;
-            for (int w2 = 0; w2 < wave; ++w2) off += s_wtot[w2];
-            s_cum[tid] = v + off;
-        }
-        Acc off = 0;
-        for (int s2 = 0; s2 < seg; ++s2) off += s_segtot[s2 * NH + i];
-#pragma unroll
-        for (int k = 0; k < S::TPS; ++k) {
-            const int t = seg * S::TPS + k;
-            if (t < Q) {
-                const Acc psi = ps[k] + off;
-                Acc sn, cs;
-                sincos_acc(psi, &sn, &cs);
-                cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
-                if (t == nvalid - 1) s_psie[i] = psi;
-            }
-        }
-        __syncthreads();
-        if (tid < Q) {
-            const Acc cum_e = s_cum[nvalid - 1];
-            s_w[tid] = (tid < nvalid) ? (float)(exp_acc(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
-        }
-        __syncthreads();
-    }
-
     const T *Cg = static_cast<const T *>(a.C) + tok0 * (R * N);
     const T *Bg = static_cast<const T *>(a.B) + tok0 * (R * N);
     const T *Xg = static_cast<const T *>(a.x) + tok0 * (R * P);
     const int64_t bstr = tstr * R * N, xstr = tstr * R * P;   // token strides of B/C and x
 
-    // Stage rows jb*64 .. of the chunk: B^ = R(-psi_t) B rotated, as the
-    // w-scaled transpose (kBt: operand of M) and/or row-major (kRow: operand
-    // of G^T), and x^T.  Consecutive lanes take consecutive rows, so the
-    // transposed LDS stores and the table reads are conflict-free.
-    auto stage = [&](int jb, auto kBt, auto kRow) {
-        for (int task = tid; task < S::JB * (NH / S::CE); task += S::NTHR) {
-            const int jr = task % S::JB, cp = task / S::JB;
+    // Rows jb*64 .. of the chunk are staged in two steps so that the global
+    // loads of the next block overlap the MFMA work on this one: fetch()
+    // issues the loads into registers, commit() rotates B^ = R(-psi_t) B and
+    // writes it to LDS as the w-scaled transpose (kBt: operand of M) and/or
+    // row-major (kRow: operand of G^T), together with x^T.  Consecutive lanes
+    // take consecutive rows, so the transposed LDS stores and the cos/sin
+    // table reads are conflict-free.
+    constexpr int TB = S::JB * (NH / S::CE) / S::NTHR;   // B tasks per thread
+    constexpr int TX = S::JB * (P / S::CE) / S::NTHR;    // x tasks per thread
+    static_assert(TB * S::NTHR == S::JB * (NH / S::CE) && TX * S::NTHR == S::JB * (P / S::CE), "tasks");
+    struct Blk { V16 lo[TB], hi[TB], xv[TX]; };
+    auto fetch = [&](int jb, Blk &f) {
+#pragma unroll
+        for (int k = 0; k < TB; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            V16 lo{}, hi{};
+            f.lo[k] = V16{};
+            f.hi[k] = V16{};
             if (t < nvalid) {
                 const T *src = Bg + t * bstr + r * N + cp * S::CE;
-                lo = *reinterpret_cast<const V16 *>(src);
-                hi = *reinterpret_cast<const V16 *>(src + NH);
+                f.lo[k] = *reinterpret_cast<const V16 *>(src);
+                f.hi[k] = *reinterpret_cast<const V16 *>(src + NH);
             }
+        }
+#pragma unroll
+        for (int k = 0; k < TX; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
+            const int row = jb * S::JB + jr, t = row / R, r = row % R;
+            f.xv[k] = V16{};
+            if (t < nvalid) f.xv[k] = *reinterpret_cast<const V16 *>(Xg + t * xstr + r * P + pc * S::CE);
+        }
+    };
+    auto commit = [&](int jb, const Blk &f, auto kBt, auto kRow) {
+#pragma unroll
+        for (int k = 0; k < TB; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
+            const int row = jb * S::JB + jr, t = row / R;
+            V16 lo = f.lo[k], hi = f.hi[k];
             const float wt = s_w[t];
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
@@ -267,15 +249,87 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
                 *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + NH + cp * S::CE]) = hi;
             }
         }
-        for (int task = tid; task < S::JB * (P / S::CE); task += S::NTHR) {
-            const int jr = task % S::JB, pc = task / S::JB;
-            const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            V16 xv{};
-            if (t < nvalid) xv = *reinterpret_cast<const V16 *>(Xg + t * xstr + r * P + pc * S::CE);
 #pragma unroll
-            for (int e = 0; e < S::CE; ++e) s_X[(pc * S::CE + e) * S::LDJ + jr] = xv[e];
+        for (int k = 0; k < TX; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
+#pragma unroll
+            for (int e = 0; e < S::CE; ++e) s_X[(pc * S::CE + e) * S::LDJ + jr] = f.xv[k][e];
         }
     };
+    // Prefetch depth (blocks in flight, register ring): the aggregate phase
+    // has registers to spare; the output phase keeps C^ fragments and
+    // accumulators live, so wide-tile shapes prefetch less.
+    constexpr int DA = S::NJB < 4 ? S::NJB : 4;
+    constexpr int DC = S::NJB < 1 ? S::NJB : 1;
+    constexpr int DR = DA > DC ? DA : DC;
+    Blk ring[DR];
+
+    // ---- 2. prologue ----
+    {
+        // angles first (the largest prologue load): thread (pair i, segment seg)
+        const int i = tid % NH, seg = tid / NH;
+        Acc ps[S::TPS];
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            const int t = seg * S::TPS + k;
+            ps[k] = (t < nvalid) ? (Acc)a.theta[(tok0 + t * tstr) * NH + i] : (Acc)0;
+        }
+        Acc lg = 0;
+        float gam = 0.f, sig = 0.f;
+        if (tid < Q && tid < nvalid) {
+            const int64_t t = t0 + tid, k = tok0 + tid * tstr;
+            const float dtv = a.dt[k], lamv = a.lam[k];
+            lg = (Acc)dtv * (Acc)a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
+            gam = lamv * dtv;
+            sig = gam;
+            if (t + 1 < a.L) sig += (1.f - a.lam[k + tstr]) * a.dt[k + tstr];
+        }
+        // the first blocks' loads go out after the prologue's own loads (memory
+        // counters retire in order), so they overlap the prologue's arithmetic
+#pragma unroll
+        for (int d = 0; d < DA; ++d) fetch(d, ring[d]);
+        if (tid < Q) {
+            s_gam[tid] = gam;
+            s_sig[tid] = sig;
+        }
+        Acc v = wave_incl_scan(lg, lane);
+        if (lane == kWave - 1) s_wtot[wave] = v;
+        // running sums of the segment's angles
+        Acc run = 0;
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            run += ps[k];
+            ps[k] = run;
+        }
+        s_segtot[seg * NH + i] = run;
+        __syncthreads();
+        if (tid < Q) {
+            Acc off = 0;
+            for (int w2 = 0; w2 < wave; ++w2) off += s_wtot[w2];
+            s_cum[tid] = v + off;
+        }
+        Acc off = 0;
+        for (int s2 = 0; s2 < seg; ++s2) off += s_segtot[s2 * NH + i];
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            const int t = seg * S::TPS + k;
+            if (t < Q) {
+                const Acc psi = ps[k] + off;
+                Acc sn, cs;
+                sincos_fast(psi, &sn, &cs);
+                cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
+                if (t == nvalid - 1) s_psie[i] = psi;
+            }
+        }
+        __syncthreads();
+        if (tid < Q) {
+            const Acc cum_e = s_cum[nvalid - 1];
+            s_w[tid] = (tid < nvalid) ? (float)(exp_fast(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
+        }
+        __syncthreads();
+    }
+
+
     using True = std::integral_constant<bool, true>;
     using False = std::integral_constant<bool, false>;
 
@@ -283,10 +337,12 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
     f32x4 ms[PTW][2];
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
     for (int jb = 0; jb < S::NJB; ++jb) {
-        if constexpr (S::NJB == 1) stage(jb, True{}, True{});   // one block: keep B^ for the outputs
-        else stage(jb, True{}, False{});
+        if constexpr (S::NJB == 1) commit(jb, ring[jb % DA], True{}, True{});   // one block: keep B^ for the outputs
+        else commit(jb, ring[jb % DA], True{}, False{});
         __syncthreads();
+        if (jb + DA < S::NJB) fetch(jb + DA, ring[jb % DA]);
 #pragma unroll
         for (int m2 = 0; m2 < PTW; ++m2) {
             const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
@@ -304,6 +360,7 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
         __syncthreads();
     }
 
+
     // Owned state element (m2, half, v): row n = 16*(ntl + 4*half) + 4g + v,
     // column p = 16*pt + l16; rows (i, i + N/2) of a pair sit in one lane.
     const Acc cum_e = s_cum[nvalid - 1];
@@ -314,25 +371,28 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             Acc sn, cs;
-            sincos_acc(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
+            sincos_fast(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
             const Acc re = ms[m2][0][v], im = ms[m2][1][v];
             Ast[m2][0][v] = (float)(cs * re - sn * im);
             Ast[m2][1][v] = (float)(sn * re + cs * im);
         }
     }
-    auto elem_index = [&](int m2, int half) -> int64_t {   // float4 slot of the owned layout
-        return ((int64_t)(m2 * 2 + half) * S::NTHR + tid) * 4;
+    // Published maps: 8-byte words (v, v+1) of each owned (m2, half), laid out
+    // so that the lanes of a wave touch consecutive words (coalesced).
+    auto word_index = [&](int m2, int half, int vp) -> int64_t {
+        return (int64_t)((m2 * 2 + half) * 2 + vp) * S::NTHR + tid;
     };
     const int64_t SZ = (int64_t)N * P;
     Acc *totp = static_cast<Acc *>(a.tot);
     if (c > 0 && !last) {   // publish the aggregate (only successors read it)
-        float *dst = a.agg + slot * SZ;
+        unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.agg + slot * SZ);
 #pragma unroll
         for (int m2 = 0; m2 < PTW; ++m2)
 #pragma unroll
             for (int half = 0; half < 2; ++half)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) st_coh(dst + elem_index(m2, half) + v, Ast[m2][half][v]);
+                for (int vp = 0; vp < 2; ++vp)
+                    st_coh2(dst + word_index(m2, half, vp), Ast[m2][half][2 * vp], Ast[m2][half][2 * vp + 1]);
         if (tid == 0) st_coh(totp + slot * (NH + 1), cum_e);
         if (tid < NH) st_coh(totp + slot * (NH + 1) + 1 + tid, s_psie[tid]);
         wait_stores_done();
@@ -391,7 +451,7 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 Acc sn, cs;
-                sincos_acc(aps[v], &sn, &cs);
+                sincos_fast(aps[v], &sn, &cs);
                 sn *= ad;
                 cs *= ad;
 #pragma unroll
@@ -405,7 +465,7 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
         const int ntl_w = wave % 4;
         struct Agg { float d[PTW][2][4]; Acc ps[4]; Acc cm; };
         auto load_agg = [&](int64_t js, Agg &o) {
-            const float *src = a.agg + js * SZ;
+            const unsigned long long *src = reinterpret_cast<const unsigned long long *>(a.agg + js * SZ);
             const Acc *tp = totp + js * (NH + 1);
             o.cm = ld_coh(tp);
 #pragma unroll
@@ -413,10 +473,10 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    o.d[m2][0][v] = ld_coh(src + elem_index(m2, 0) + v);
-                    o.d[m2][1][v] = ld_coh(src + elem_index(m2, 1) + v);
-                }
+                for (int half = 0; half < 2; ++half)
+#pragma unroll
+                    for (int vp = 0; vp < 2; ++vp)
+                        ld_coh2(src + word_index(m2, half, vp), o.d[m2][half][2 * vp], o.d[m2][half][2 * vp + 1]);
         };
         int64_t j = c - 1;
         const int64_t sbase = sl * a.nchunks;
@@ -450,7 +510,7 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
 #pragma unroll
                 for (int v = 0; v < 4; ++v) {
                     Acc sn, cs;
-                    sincos_acc(aps[v], &sn, &cs);
+                    sincos_fast(aps[v], &sn, &cs);
                     sn *= ad;
                     cs *= ad;
 #pragma unroll
@@ -460,19 +520,21 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
                         aA[m2][1][v] += (float)(sn * re + cs * im);
                     }
                     aps[v] += cur.ps[v];
+                    if constexpr (sizeof(Acc) == 4) aps[v] = reduce_angle(aps[v]);
                 }
-                ad *= exp_acc(cur.cm);
+                ad *= exp_fast(cur.cm);
             }
             j -= ncomp;
             if (term == (int)kFlagInc) {
-                const float *src = a.inc + (sbase + j) * SZ;
+                const unsigned long long *src = reinterpret_cast<const unsigned long long *>(a.inc + (sbase + j) * SZ);
                 float X[PTW][2][4];
 #pragma unroll
                 for (int m2 = 0; m2 < PTW; ++m2)
 #pragma unroll
                     for (int half = 0; half < 2; ++half)
 #pragma unroll
-                        for (int v = 0; v < 4; ++v) X[m2][half][v] = ld_coh(src + elem_index(m2, half) + v);
+                        for (int vp = 0; vp < 2; ++vp)
+                            ld_coh2(src + word_index(m2, half, vp), X[m2][half][2 * vp], X[m2][half][2 * vp + 1]);
                 finish(X);
                 break;
             }
@@ -508,27 +570,28 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
     // S_out = e^{cum_e} R(psi_e) S_in + A_c
     {
         float Sout[PTW][2][4];
-        const Acc de = exp_acc(cum_e);
+        const Acc de = exp_fast(cum_e);
 #pragma unroll
         for (int m2 = 0; m2 < PTW; ++m2) {
             const int ntl = (wave + NW * m2) % 4;
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
                 Acc sn, cs;
-                sincos_acc(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
+                sincos_fast(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
                 const Acc re = Sin[m2][0][v], im = Sin[m2][1][v];
                 Sout[m2][0][v] = (float)(de * (cs * re - sn * im)) + Ast[m2][0][v];
                 Sout[m2][1][v] = (float)(de * (sn * re + cs * im)) + Ast[m2][1][v];
             }
         }
         if (!last) {
-            float *dst = a.inc + slot * SZ;
+            unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.inc + slot * SZ);
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2)
 #pragma unroll
                 for (int half = 0; half < 2; ++half)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) st_coh(dst + elem_index(m2, half) + v, Sout[m2][half][v]);
+                    for (int vp = 0; vp < 2; ++vp)
+                        st_coh2(dst + word_index(m2, half, vp), Sout[m2][half][2 * vp], Sout[m2][half][2 * vp + 1]);
             wait_stores_done();
             __syncthreads();
             if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagInc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -554,6 +617,12 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
     }
 
     // ---- 5. outputs ----
+    // Longer chunks restage their blocks: the first ones are fetched now (after
+    // the look-back and the publication, whose waits would drain them).
+    if constexpr (S::NJB > 1) {
+#pragma unroll
+        for (int d = 0; d < DC; ++d) fetch(d, ring[d]);
+    }
     T *s_S = s_BtS;   // S_in^T [p][n] in the io dtype (the (B^ W)^T block is no longer read)
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) {
@@ -594,6 +663,9 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int TT = owned_tile<S>(wave, m);
+        float ecum[4];   // e^{cum_t} of the lane's accumulator rows 4g+v
+#pragma unroll
+        for (int v = 0; v < 4; ++v) ecum[v] = (float)exp_fast(s_cum[(TT * 16 + 4 * g + v) / R]);
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
             f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
@@ -601,69 +673,85 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
             for (int kk = 0; kk < NK; ++kk)
                 tmp = MM::mma(cf[m][kk], MM::load(&s_S[(pt * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), tmp);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                const int t = (TT * 16 + 4 * g + v) / R;
-                tmp[v] *= (float)exp_acc(s_cum[t]);
-            }
+            for (int v = 0; v < 4; ++v) tmp[v] *= ecum[v];
             acc[m][pt] = tmp;
         }
     }
     // intra-chunk term over the row blocks at or below each owned tile
+    const float Dh = a.D[h];
+#pragma unroll
     for (int jb = 0; jb < S::NJB; ++jb) {
         if constexpr (S::NJB > 1) {
-            stage(jb, False{}, True{});
+            commit(jb, ring[jb % DC], False{}, True{});
             __syncthreads();
+            if (jb + DC < S::NJB) fetch(jb + DC, ring[jb % DC]);
         }
 #pragma unroll
         for (int jp = 0; jp < S::JB / 32; ++jp) {
             const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
-            Frag bfr[2][NK];
+            if (J0 > owned_tile<S>(wave, TPW - 1) && J0 > owned_tile<S>(wave, 0)) continue;
+            // x^T columns of the pair, shared by all owned tiles
+            bf16x8 xf[PT];
+            if constexpr (MM::KPL == 8) {
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) {
+                    const T *xr = &s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
+                    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
+                    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) { xf[pt][v] = lo[v]; xf[pt][4 + v] = hi[v]; }
+                }
+            }
+            // G^T tiles (K = N) for every owned tile at or below the pair; each
+            // B^ fragment is loaded once and used by all owned tiles
+            f32x4 gt[TPW][2];
+#pragma unroll
+            for (int m = 0; m < TPW; ++m) gt[m][0] = gt[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int q = 0; q < 2; ++q)
 #pragma unroll
-                for (int kk = 0; kk < NK; ++kk)
-                    bfr[q][kk] = MM::load(&s_B[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
+                for (int kk = 0; kk < NK; ++kk) {
+                    const Frag bf = MM::load(&s_B[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
+#pragma unroll
+                    for (int m = 0; m < TPW; ++m)
+                        if (J0 + q <= owned_tile<S>(wave, m)) gt[m][q] = MM::mma(bf, cf[m][kk], gt[m][q]);
+                }
+            // mask weights (branch-free): w_tj = e^{cum_t - cum_j} sigma_j (j < t),
+            // gamma_t (j = t), 0 (j > t); D x_t as D on the diagonal row = column
 #pragma unroll
             for (int m = 0; m < TPW; ++m) {
                 const int TT = owned_tile<S>(wave, m);
                 if (J0 > TT) continue;
-                f32x4 gt[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+                const int tt = (TT * 16 + l16) / R;
+                const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
+                // the lane's 4 rows 4g+v of a j-tile span NV tokens (one when R >= 4)
+                constexpr int NV = R >= 4 ? 1 : 4 / R;
 #pragma unroll
                 for (int q = 0; q < 2; ++q) {
-                    if (J0 + q <= TT) {
+                    float wv[NV];
 #pragma unroll
-                        for (int kk = 0; kk < NK; ++kk) gt[q] = MM::mma(bfr[q][kk], cf[m][kk], gt[q]);
+                    for (int u = 0; u < NV; ++u) {
+                        const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
+                        const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
+                        wv[u] = tj < tt ? e : (tj == tt ? gam_t : 0.f);
+                    }
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) gt[m][q][v] *= wv[(v * NV) / 4];
+                    if (J0 + q == TT) {   // diagonal tile (wave-uniform): the skip term
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
                     }
                 }
-                const int tt = (TT * 16 + l16) / R;
-                const Acc cum_t = s_cum[tt];
-#pragma unroll
-                for (int q = 0; q < 2; ++q)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int tj = ((J0 + q) * 16 + 4 * g + v) / R;
-                        float w = 0.f;
-                        if (tj < tt) w = (float)exp_acc(cum_t - s_cum[tj]) * s_sig[tj];
-                        else if (tj == tt) w = s_gam[tt];
-                        gt[q][v] *= w;
-                    }
+                // y += (w o G) x  (K = the pair's 32 rows)
                 if constexpr (MM::KPL == 8) {
                     bf16x8 af;
 #pragma unroll
                     for (int v = 0; v < 4; ++v) {
-                        af[v] = (bf16)gt[0][v];
-                        af[4 + v] = (bf16)gt[1][v];
+                        af[v] = (bf16)gt[m][0][v];
+                        af[4 + v] = (bf16)gt[m][1][v];
                     }
 #pragma unroll
-                    for (int pt = 0; pt < PT; ++pt) {
-                        const T *xr = &s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
-                        const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
-                        const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
-                        bf16x8 xf;
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) { xf[v] = lo[v]; xf[4 + v] = hi[v]; }
-                        acc[m][pt] = MM::mma(af, xf, acc[m][pt]);
-                    }
+                    for (int pt = 0; pt < PT; ++pt) acc[m][pt] = MM::mma(af, xf[pt], acc[m][pt]);
                 } else {
 #pragma unroll
                     for (int q = 0; q < 2; ++q)
@@ -672,31 +760,36 @@ __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2) void k_scan_fused(ScanA
 #pragma unroll
                             for (int pt = 0; pt < PT; ++pt) {
                                 const float xv = to_f32(s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
-                                acc[m][pt] = MM::mma(gt[q][v], xv, acc[m][pt]);
+                                acc[m][pt] = MM::mma(gt[m][q][v], xv, acc[m][pt]);
                             }
                 }
             }
         }
         if constexpr (S::NJB > 1) __syncthreads();
     }
-    // skip term and store
-    const float Dh = a.D[h];
+    // store: each wave stages one 16-row tile at a time in LDS (the B^ block
+    // is free now) and writes whole 16-byte pieces of the y rows
+    __syncthreads();
+    T *s_y = s_B + wave * (16 * P);
     T *Yg = static_cast<T *>(a.y) + tok0 * (R * P);
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int TT = owned_tile<S>(wave, m);
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const int row = TT * 16 + 4 * g + v, t = row / R, r = row % R;
-            if (t < nvalid) {
+        for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt) {
-                    const int p = pt * 16 + l16;
-                    const float yv = acc[m][pt][v] + Dh * to_f32(Xg[t * xstr + r * P + p]);
-                    Yg[t * xstr + r * P + p] = from_f32<T>(yv);
-                }
-            }
+            for (int v = 0; v < 4; ++v) s_y[(4 * g + v) * P + pt * 16 + l16] = from_f32<T>(acc[m][pt][v]);
+        __syncthreads();
+        constexpr int PIECES = 16 * P / S::CE;          // 16-byte pieces in the tile
+#pragma unroll
+        for (int k = lane; k < PIECES; k += kWave) {
+            const int rl = k / (P / S::CE), col = (k % (P / S::CE)) * S::CE;
+            const int row = TT * 16 + rl, t = row / R, r = row % R;
+            if (t < nvalid)
+                *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) =
+                    *reinterpret_cast<const V16 *>(&s_y[rl * P + col]);
         }
+        __syncthreads();
     }
 }
 
