@@ -32,6 +32,8 @@ def main():
     ap.add_argument("--steps", type=int, default=200)
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run 10 plain device copies of 1 GiB (reference for HBM byte counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); every (batch, head) "
@@ -47,6 +49,15 @@ def main():
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     stream = torch.cuda.current_stream()
+    if args.calibrate_copy:
+        # a plain copy kernel of known size: reads and writes 2^30 bytes per launch
+        src = torch.ones(1 << 28, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(10):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"calibrate_copy_bytes_each_way": 1 << 30, "launches": 10}), flush=True)
+        return
 
     # ---------------- prefill workload (SISO bf16) ----------------
     wp = WORKLOADS[1]
@@ -150,13 +161,14 @@ def main():
         "roofline": {
             "kernel": "k_step (m3_step, one launch per step)",
             "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": peak_gbs, "unit": "GB/s",
-            "frac": round(dec_gbs / peak_gbs, 4), "traffic": None,
+            "frac": round(dec_gbs / peak_gbs, 4), "traffic": measured_traffic("k_step"),
             "bytes_per_launch": dec_bytes,
         },
         "roofline_prefill": {
             "kernel": "m3_scan_fwd (all launches of one scan)",
             "bound": "hbm", "achieved": round(pre_gbs, 1), "peak": peak_gbs, "unit": "GB/s",
-            "frac": round(pre_gbs / peak_gbs, 4), "traffic": None, "bytes_per_launch": pre_bytes,
+            "frac": round(pre_gbs / peak_gbs, 4), "traffic": measured_traffic("k_scan_fused_siso"),
+            "bytes_per_launch": pre_bytes,
             "mfma_tflops": round(pre_tfs, 2),
             "mfma_frac": round(pre_tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
         },
@@ -165,6 +177,20 @@ def main():
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(base, layer, step_in, wp, wd)
     print(json.dumps(result), flush=True)
+
+
+def measured_traffic(key):
+    """HBM bytes per launch measured with rocprofv3 counters (profiles/traffic.json),
+    or None when the kernel source changed since the measurement."""
+    import hashlib
+    try:
+        rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[key]
+        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
+    except (OSError, KeyError, ValueError):
+        return None
+    if hashlib.sha256(src).hexdigest() != rec["src_sha256"]:
+        return None
+    return rec["read_bytes"] + rec["write_bytes"]
 
 
 class _LayerView:
