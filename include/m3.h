@@ -72,11 +72,17 @@ typedef enum {
 
 typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
 
-/* m3_dims.flags: run the prefill as three kernels (chunk states, a state
- * pass over chunks, chunk outputs) instead of the single-pass kernel with a
- * look-back across chunks.  Same results up to rounding; the single-pass
- * kernel is the default wherever it is built (dstate 128, headdim 64). */
+/* m3_dims.flags select the prefill kernels (same results up to rounding).
+ * Default (0), wherever built (dstate 128, headdim 64): the segmented
+ * single-pass kernel: each workgroup scans a segment of consecutive chunks of
+ * one (batch, head) slice and carries the state across them; segments of a
+ * slice are linked by a decoupled look-back over their state maps.
+ * M3_SCAN_SPLIT: three kernels (chunk states, a state pass over chunks,
+ * chunk outputs); the only path for other shapes.
+ * M3_SCAN_PER_CHUNK: the single-pass kernel with one chunk per workgroup
+ * (a look-back across every chunk).  Ignored together with M3_SCAN_SPLIT. */
 #define M3_SCAN_SPLIT 1
+#define M3_SCAN_PER_CHUNK 2
 
 typedef struct {
     int64_t batch;     /* >= 1                                              */
@@ -87,8 +93,12 @@ typedef struct {
     int64_t rank;      /* R >= 1 (MIMO rank)                                 */
     int64_t chunk;     /* Q: tokens per chunk of the prefill scan            */
     int32_t io;        /* m3_dtype of x, B, C, y and the carry               */
-    int32_t flags;     /* 0 or M3_SCAN_SPLIT; other bits must be 0           */
+    int32_t flags;     /* M3_SCAN_* bits; other bits must be 0               */
     int64_t a_stride_b, a_stride_t, a_stride_h; /* strides of A, in floats   */
+    int64_t seg_chunks; /* chunks per workgroup of the segmented kernel; 0 =
+                           enough that all workgroups are resident at once
+                           (results then depend on the device's CU count in
+                           the last bits); ignored by m3_step              */
 } m3_dims;
 
 /*

@@ -43,7 +43,7 @@ static int io_bytes_of(int32_t io) { return io == M3_F32 ? 4 : io == M3_BF16 ? 2
 static m3_status check_dims_common(const m3_dims *d) {
     if (!d) return M3_ERR_NULL;
     if (d->io != M3_F32 && d->io != M3_BF16) return M3_ERR_DTYPE;
-    if (d->flags & ~M3_SCAN_SPLIT) return M3_ERR_SHAPE;
+    if (d->flags & ~(M3_SCAN_SPLIT | M3_SCAN_PER_CHUNK)) return M3_ERR_SHAPE;
     if (d->batch < 1 || d->nheads < 1 || d->headdim < 1 || d->dstate < 2 || d->rank < 1)
         return M3_ERR_SHAPE;
     if (d->dstate % 2) return M3_ERR_SHAPE;
@@ -75,7 +75,7 @@ extern "C" int m3_last_hip_error(void) { return g_last_hip_error; }
 static m3_status check_scan_dims(const m3_dims *d, ScanImpl *impl, int64_t *nchunks) {
     m3_status s = check_dims_common(d);
     if (s != M3_OK) return s;
-    if (d->seqlen < 0 || d->chunk < 1) return M3_ERR_SHAPE;
+    if (d->seqlen < 0 || d->chunk < 1 || d->seg_chunks < 0) return M3_ERR_SHAPE;
     // element offsets of the largest tensors must fit in int64 comfortably
     const int64_t per_tok = d->nheads * d->rank * (d->dstate > d->headdim ? d->dstate : d->headdim);
     if (d->seqlen > (INT64_MAX / 4) / (d->batch * per_tok)) return M3_ERR_SHAPE;
@@ -83,10 +83,12 @@ static m3_status check_scan_dims(const m3_dims *d, ScanImpl *impl, int64_t *nchu
     if (d->batch * d->nheads * nc > (int64_t)INT_MAX) return M3_ERR_SHAPE;
     *impl = find_scan_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
     if (!impl->launch) return M3_ERR_UNSUPPORTED;
-    // the single-pass kernel serves every shape it is built for, except the
-    // empty sequence (handled by the three-kernel path's state kernel alone)
+    // the single-pass kernels serve every shape they are built for, except
+    // the empty sequence (handled by the three-kernel path's state kernel)
     if (nc > 0 && !(d->flags & M3_SCAN_SPLIT)) {
-        scan_launch_fn f = find_fused_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
+        scan_launch_fn f = nullptr;
+        if (!(d->flags & M3_SCAN_PER_CHUNK)) f = find_seg_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
+        if (!f) f = find_fused_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
         if (f) { impl->launch = f; impl->fused = true; }
     }
     *nchunks = nc;
@@ -149,6 +151,7 @@ extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B,
     }
     a.batch = d->batch; a.L = d->seqlen; a.H = d->nheads; a.nchunks = nc;
     a.a_sb = d->a_stride_b; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
+    a.G = d->seg_chunks; a.nseg = 0;
     const hipError_t e = impl.launch(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) {
         g_last_hip_error = (int)e;

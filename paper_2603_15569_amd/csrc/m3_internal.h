@@ -27,6 +27,9 @@ struct ScanArgs {
     float *inc;      // [BH][nchunks][N*P] inclusive states (same layout)
     int64_t batch, L, H, nchunks;
     int64_t a_sb, a_st, a_sh;
+    // segmented kernel: chunks per segment (0 = chosen at launch), segments
+    // per slice (set at launch)
+    int64_t G, nseg;
 };
 
 struct StepArgs {
@@ -45,13 +48,14 @@ typedef hipError_t (*step_launch_fn)(const StepArgs &, hipStream_t);
 struct ScanImpl {
     scan_launch_fn launch;
     int acc_bytes;   // bytes of the prologue scalar type (4: fp32, 8: fp64)
-    bool fused;      // single-pass look-back kernel (else the three-kernel path)
+    bool fused;      // a single-pass look-back kernel (else the three-kernel path)
 };
 
 // Kernel lookup by shape; null launch when no kernel is built for it.
 ScanImpl find_scan_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 step_launch_fn find_step_impl(int io, int64_t N, int64_t P, int64_t R);
 scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+scan_launch_fn find_seg_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 
 // Byte offsets of the workspace regions for a scan.
 struct ScanWorkspaceLayout {

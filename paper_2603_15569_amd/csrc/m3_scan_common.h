@@ -1,0 +1,108 @@
+// Pieces shared by the single-pass prefill kernels (one chunk per workgroup,
+// and G chunks per workgroup): shape traits of the N = 128, P = 64 tiling,
+// element helpers, coherent accesses of the look-back, the reset kernel.
+#pragma once
+#include "m3_device.h"
+
+namespace m3 {
+namespace scan {
+
+constexpr uint32_t kFlagAgg = 1, kFlagInc = 2;
+constexpr uint32_t kSpinMax = 1u << 22;   // bounded wait: ~seconds, then error exit
+
+struct alignas(4) h2 { _Float16 c, s; };
+template <typename T> struct CsOf { typedef h2 type; };          // bf16 path: fp16 cos/sin
+template <> struct CsOf<float> { typedef float2 type; };         // fp32 path: fp32 cos/sin
+__device__ __forceinline__ void cs_put(h2 *p, float c, float s) { *p = h2{(_Float16)c, (_Float16)s}; }
+__device__ __forceinline__ void cs_put(float2 *p, float c, float s) { *p = make_float2(c, s); }
+__device__ __forceinline__ void cs_get(const h2 &v, float &c, float &s) { c = (float)v.c; s = (float)v.s; }
+__device__ __forceinline__ void cs_get(const float2 &v, float &c, float &s) { c = v.x; s = v.y; }
+
+template <typename T> struct Vec16;            // 16-byte vector of T
+template <> struct Vec16<bf16> { typedef bf16x8 type; static constexpr int n = 8; };
+template <> struct Vec16<float> { typedef f32x4 type; static constexpr int n = 4; };
+
+__device__ __forceinline__ float fget(const bf16x8 &v, int e) { return (float)v[e]; }
+__device__ __forceinline__ void fset(bf16x8 &v, int e, float x) { v[e] = (bf16)x; }
+__device__ __forceinline__ float fget(const float &v, int) { return v; }
+__device__ __forceinline__ void fset(float &v, int, float x) { v = x; }
+__device__ __forceinline__ float fget(const f32x4 &v, int e) { return v[e]; }
+__device__ __forceinline__ void fset(f32x4 &v, int e, float x) { v[e] = x; }
+
+// Look-back traffic uses device-scope atomic accesses only (the sc1 scope
+// bit): they are coherent across the XCDs' L2 caches by themselves, so no
+// cache-wide write-back or invalidate is needed.  A publisher waits until its
+// stores are acknowledged (vmcnt(0)) before the flag store; a reader issues
+// its data loads only after it has seen the flag.
+__device__ __forceinline__ void wait_stores_done() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+__device__ __forceinline__ void st_coh2(unsigned long long *p, float x, float y) {
+    const unsigned long long w = (unsigned long long)__float_as_uint(x) |
+                                 ((unsigned long long)__float_as_uint(y) << 32);
+    __hip_atomic_store(p, w, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void ld_coh2(const unsigned long long *p, float &x, float &y) {
+    const unsigned long long w = __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    x = __uint_as_float((unsigned)(w & 0xffffffffull));
+    y = __uint_as_float((unsigned)(w >> 32));
+}
+__device__ __forceinline__ void st_coh(float *p, float v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ void st_coh(double *p, double v) {
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float ld_coh(const float *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ double ld_coh(const double *p) {
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+template <typename T, int Q_, int R_, int NW_ = 0>
+struct FShape {
+    static constexpr int N = 128, P = 64, NH = 64, Q = Q_, R = R_;
+    static constexpr int QR = Q * R;
+    static constexpr int RT = QR / 16;                    // 16-row tiles in a chunk
+    static constexpr int NW = NW_ ? NW_ : (RT >= 16 ? 8 : 4);   // waves per workgroup
+    static constexpr int NWO = NW < RT ? NW : RT;         // waves owning output row tiles
+    static constexpr int NTHR = NW * kWave;
+    static constexpr int TPW = RT / NWO;                  // row tiles per output wave
+    static constexpr int PTW = 16 / NW;                   // state pair-tiles per wave
+    static constexpr int JB = 64, NJB = QR / JB;          // staged row blocks
+    static constexpr int PAD = 16 / (int)sizeof(T);
+    static constexpr int LDN = N + PAD;                   // [rows][N] and [P][N] tiles
+    static constexpr int LDJ = JB + PAD;                  // [N or P][rows] tiles
+    static constexpr int NSEG = NTHR / NH;                // angle-scan segments
+    static constexpr int TPS = (Q + NSEG - 1) / NSEG;     // tokens per segment
+    static constexpr int CE = Vec16<T>::n;                // elements per 16-byte vector
+    static constexpr int ST_ELEMS = PTW * 2 * 4;          // state floats owned per lane
+    typedef typename AccOf<T>::type Acc;
+    typedef typename CsOf<T>::type CS;
+    static_assert(QR % 64 == 0 && RT <= 32, "chunk*rank in {64, ..., 512}");
+    static_assert(16 % R == 0, "row tiles hold whole tokens");
+    static_assert(Q <= 256 && NTHR % NH == 0, "prologue mapping");
+    static_assert(TPW >= 1 && TPW <= 4 && (TPW == 1 || TPW % 2 == 0), "tile assignment");
+};
+
+// Row tile owned as the m-th tile of output wave w: pairs of tiles from both
+// ends of the chunk so that every wave gets the same causal work.
+template <class S>
+__device__ __forceinline__ int owned_tile(int w, int m) {
+    const int base = (m / 2) * 2 * S::NWO;
+    return (m % 2 == 0) ? base + w : base + 2 * S::NWO - 1 - w;
+}
+
+// Clears the ticket counter, the timeout counter and the flags (one kernel
+// per translation unit: internal linkage).
+static __global__ void k_reset(uint32_t *ctl, uint32_t *flags, int64_t nflags) {
+    const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i0 < 2) ctl[i0] = 0u;
+    for (int64_t i = i0; i < nflags; i += (int64_t)gridDim.x * blockDim.x) flags[i] = 0u;
+}
+
+constexpr uint32_t kFlagInit = 3;   // probe result for "before the first chunk"
+constexpr int kProbe = 16;          // predecessors probed per look-back round
+
+}  // namespace scan
+}  // namespace m3

@@ -1,0 +1,919 @@
+// Segmented single-pass prefill scan of the Mamba-3 SSM on gfx950 (N = 128,
+// P = 64): each workgroup owns a segment of G consecutive chunks of one
+// (batch, head) slice and carries the state from chunk to chunk itself;
+// segments of a slice are linked by a decoupled look-back over their N x P
+// fp32 state maps.
+//
+// Chunk math as in the one-chunk-per-workgroup kernel (Sec. 3.3 chunked
+// algorithm, the two-band mask of Sec. 3.1.2 eq. mamba3-mask, the rotary form
+// of Sec. 3.2): with chunk-local prefix sums cum_t (of dt A) and psi_t (of
+// theta), C^_t = R(-psi_t) C_t, B^_j = R(-psi_j) B_j, w_tt = gamma_t,
+// w_tj = e^{cum_t - cum_j} sigma_j,
+//   y_t = sum_{j<=t} w_tj (C^_t . B^_j) x_j + e^{cum_t} C^_t . S + D x_t,
+//   S  <-  R(psi_e) (e^{cum_e} S + M),   M = sum_j e^{cum_e - cum_j} sigma_j B^_j x_j^T.
+// A segment composes its chunks' maps into one map S -> T S + A with
+// T = e^{sum cum_e} R(sum psi_e).
+//
+// Work of one workgroup:
+//   1. ticket -> (segment, slice), segment-major, so every predecessor of a
+//      segment holds an earlier ticket and is resident (forward progress);
+//      with one segment per slice there is no look-back and no ticket;
+//   2. (several segments) aggregate pass: per chunk the prologue (decay and
+//      angle prefix scans, cos/sin table, weights) and M from the row blocks
+//      (MFMA, K = rows); A <- R(psi_e)(e^{cum_e} A + M); the aggregate is
+//      published, the look-back yields the entering state, the segment's
+//      outgoing state is published (or written as the final state);
+//   3. output pass: per chunk the prologue again, C^ rotated into MFMA
+//      fragments, y = e^{cum_t} C^ S (MFMA, K = N), then per row block the
+//      masked G^T = B^ C^T (MFMA, K = N), y += (w o G) x (MFMA, K = rows) and,
+//      when the segment continues, M for the next chunk's state; y stored.
+// Loads run one chunk ahead: the next chunk's angles and scalars right after
+// this chunk's prologue, its first row blocks while this chunk's last blocks
+// are in use, its C rows after this chunk's last use of C^ (the last chunk of
+// a segment reloads its own rows instead, so that every iteration issues the
+// same loads).
+#include <type_traits>
+
+#include "m3_device.h"
+#include "m3_internal.h"
+#include "m3_scan_common.h"
+
+namespace m3 {
+namespace {
+
+using namespace scan;
+
+// Eight waves per workgroup: all of them stage row blocks and carry the
+// state; the first NWO of them own the output row tiles.
+template <typename T, int Q, int R>
+using SegShape = FShape<T, Q, R, 8>;
+
+template <typename T, int Q, int R>
+__global__ __launch_bounds__((SegShape<T, Q, R>::NTHR), 2)
+void k_scan_seg(ScanArgs a) {
+    typedef SegShape<T, Q, R> S;
+    typedef typename S::Acc Acc;
+    typedef typename S::CS CS;
+    typedef Mma<T> MM;
+    typedef typename MM::frag Frag;
+    typedef typename Vec16<T>::type V16;
+    constexpr int N = S::N, P = S::P, NH = S::NH, NW = S::NW, TPW = S::TPW, PTW = S::PTW;
+    constexpr int NK = N / MM::K;       // MFMA K-steps over the state axis
+    constexpr int JK = S::JB / MM::K;   // MFMA K-steps over a 64-row block
+    constexpr int PT = P / 16;
+    constexpr int LDC = Q + 1;          // cos/sin table [pair][token], padded
+    constexpr int NJB = S::NJB;
+    constexpr int kMaps = 2;            // look-back maps loaded per round trip
+
+    __shared__ Acc s_cum[Q];
+    __shared__ Acc s_wtot[NW];
+    __shared__ Acc s_psie[NH];
+    __shared__ Acc s_segps[NH];         // angle totals of the segment
+    __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
+    __shared__ CS s_cs[NH * LDC];
+    __shared__ __attribute__((aligned(16))) T s_B[S::JB * S::LDN];   // B^ block [row][n]; S^T [p][n]; y staging
+    __shared__ __attribute__((aligned(16))) T s_X[P * S::LDJ];       // x^T block [p][row]
+    __shared__ __attribute__((aligned(16))) T s_Bt[N * S::LDJ];      // (B^ W)^T block [n][row]
+    __shared__ int s_i[4];
+    Acc *s_segtot = reinterpret_cast<Acc *>(s_B);                    // prologue only
+    static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
+    static_assert(P == S::JB, "S^T [p][n] fits in the B^ block");
+    static_assert(NW * 16 * P <= S::JB * S::LDN, "y staging fits in the B^ block");
+
+    // Lane indices are re-derived from an opaque copy of the thread index at
+    // the top of every chunk iteration (relane), so that the compiler
+    // recomputes addresses instead of keeping them live across the loops.
+    int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // uniform: scalar branches
+    int g = lane >> 4, l16 = lane & 15;
+    const bool ow = wave < S::NWO;   // owns output row tiles (uniform)
+    auto relane = [&]() {
+        asm volatile("" : "+v"(tid));
+        lane = tid & (kWave - 1);
+        g = lane >> 4;
+        l16 = lane & 15;
+    };
+
+    // ---- 1. (segment, slice) ----
+    const int64_t nsl = a.batch * a.H;
+    int64_t ticket = blockIdx.x;
+    if (a.nseg > 1) {
+        if (tid == 0) s_i[0] = (int)atomicAdd(a.ctl, 1u);
+        __syncthreads();
+        ticket = s_i[0];
+    }
+    const int64_t sg = ticket / nsl, sl = ticket % nsl;
+    const int64_t b = sl / a.H, h = sl % a.H;
+    const int64_t cbeg = sg * a.G, cend = min(cbeg + a.G, a.nchunks);
+    const int64_t slot = sl * a.nseg + sg;
+    const bool last_seg = (sg == a.nseg - 1);
+    const bool run_agg = a.nseg > 1;     // segments are linked: aggregate pass + look-back
+    const int64_t tstr = a.H;            // token stride in token-heads
+    const int64_t bstr = tstr * R * N, xstr = tstr * R * P;
+    const T *Bs = static_cast<const T *>(a.B);
+    const T *Cs = static_cast<const T *>(a.C);
+    const T *Xs = static_cast<const T *>(a.x);
+    auto tok_of = [&](int64_t c) -> int64_t { return (b * a.L + c * Q) * a.H + h; };
+    auto nvalid_of = [&](int64_t c) -> int { return (int)min((int64_t)Q, a.L - c * Q); };
+    // The prefetch groups are issued in the same order before and inside the
+    // chunk loops, so that the compiler's count of loads in flight agrees on
+    // both paths into a loop and its waits stay exact.
+    auto sched_fence = []() { __builtin_amdgcn_sched_barrier(0); };
+
+    // Row blocks: fetch() issues the global loads of B and x rows into
+    // registers, commit() rotates B^ = R(-psi_t) B and writes it to LDS as the
+    // w-scaled transpose (operand of M) and row-major (operand of G^T),
+    // together with x^T.  Consecutive lanes take consecutive rows, so the
+    // transposed LDS stores and the cos/sin table reads are conflict-free.
+    constexpr int TB = S::JB * (NH / S::CE) / S::NTHR;   // B tasks per thread
+    constexpr int TX = S::JB * (P / S::CE) / S::NTHR;    // x tasks per thread
+    static_assert(TB * S::NTHR == S::JB * (NH / S::CE) && TX * S::NTHR == S::JB * (P / S::CE), "tasks");
+    struct Blk { V16 lo[TB], hi[TB], xv[TX]; };
+    // Every global load below is unconditional (rows past the end of the
+    // sequence read the last valid row and are zeroed afterwards), so the
+    // number of loads in flight is static and the waits the compiler inserts
+    // stop at exactly the loads a step needs, leaving later prefetches in
+    // flight.
+    auto fetch = [&](int64_t c, int jb, Blk &f) {
+        const int64_t tk = tok_of(c);
+        const int nv = nvalid_of(c);
+        const T *Bg = Bs + tk * (R * N);
+        const T *Xg = Xs + tk * (R * P);
+#pragma unroll
+        for (int k = 0; k < TB; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
+            const int row = jb * S::JB + jr, t = row / R, r = row % R;
+            const T *src = Bg + min(t, nv - 1) * bstr + r * N + cp * S::CE;
+            f.lo[k] = *reinterpret_cast<const V16 *>(src);
+            f.hi[k] = *reinterpret_cast<const V16 *>(src + NH);
+        }
+#pragma unroll
+        for (int k = 0; k < TX; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
+            const int row = jb * S::JB + jr, t = row / R, r = row % R;
+            f.xv[k] = *reinterpret_cast<const V16 *>(Xg + min(t, nv - 1) * xstr + r * P + pc * S::CE);
+        }
+    };
+    int cnv = 0;   // valid tokens of the chunk being committed
+    auto commit = [&](int jb, const Blk &f, auto kRow) {
+#pragma unroll
+        for (int k = 0; k < TB; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
+            const int row = jb * S::JB + jr, t = row / R;
+            V16 lo = f.lo[k], hi = f.hi[k];
+            const float wt = s_w[t];
+            const bool ok = t < cnv;
+#pragma unroll
+            for (int e = 0; e < S::CE; ++e) {
+                const int n = cp * S::CE + e;
+                float cs, sn;
+                cs_get(s_cs[n * LDC + t], cs, sn);
+                const float u = ok ? fget(lo, e) : 0.f, w = ok ? fget(hi, e) : 0.f;
+                const float re = cs * u + sn * w, im = cs * w - sn * u;
+                if constexpr (decltype(kRow)::value) {
+                    fset(lo, e, re);
+                    fset(hi, e, im);
+                }
+                s_Bt[n * S::LDJ + jr] = from_f32<T>(wt * re);
+                s_Bt[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
+            }
+            if constexpr (decltype(kRow)::value) {
+                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + cp * S::CE]) = lo;
+                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + NH + cp * S::CE]) = hi;
+            }
+        }
+#pragma unroll
+        for (int k = 0; k < TX; ++k) {
+            const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
+            const bool ok = (jb * S::JB + jr) / R < cnv;
+#pragma unroll
+            for (int e = 0; e < S::CE; ++e)
+                s_X[(pc * S::CE + e) * S::LDJ + jr] = ok ? f.xv[k][e] : from_f32<T>(0.f);
+        }
+    };
+    // M += (B^ W)^T x over one staged block (owned state pair-tiles)
+    auto m_block = [&](f32x4 (&ms)[PTW][2]) {
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+                const int nt = ntl + 4 * half;
+#pragma unroll
+                for (int ks = 0; ks < JK; ++ks) {
+                    const Frag af = MM::load(&s_Bt[(nt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    const Frag bf = MM::load(&s_X[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    ms[m2][half] = MM::mma(af, bf, ms[m2][half]);
+                }
+            }
+        }
+    };
+
+    // Prologue inputs of a chunk, loaded one chunk ahead (raw values only, so
+    // that nothing waits for them before the prologue itself).
+    struct Pro { float th[S::TPS]; float dtv, lamv, Av, dtn, lamn; };
+    auto load_pro = [&](int64_t c, Pro &p) {
+        const int64_t tk = tok_of(c);
+        const int nv = nvalid_of(c);
+        const int i = tid % NH, seg = tid / NH;
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            const int t = seg * S::TPS + k;
+            p.th[k] = a.theta[(tk + min(t, nv - 1) * tstr) * NH + i];
+        }
+        const int tt = min(tid, nv - 1);
+        const int64_t k = tk + tt * tstr, t = c * Q + tt;
+        const int64_t kn = (t + 1 < a.L) ? k + tstr : k;
+        p.dtv = a.dt[k];
+        p.lamv = a.lam[k];
+        p.Av = a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
+        p.dtn = a.dt[kn];
+        p.lamn = a.lam[kn];
+    };
+    // cum (wavefront scans), gamma, sigma, w; angle prefix sums, the cos/sin
+    // table and psi_e.  Ends with a barrier.
+    auto prologue = [&](int64_t c, const Pro &p) {
+        const int nv = nvalid_of(c);
+        const int i = tid % NH, seg = tid / NH;
+        // branch-free on the loaded values (a branch here would merge the
+        // compiler's load-counter state conservatively)
+        const bool ok = tid < nv;
+        const bool has_next = c * Q + tid + 1 < a.L;   // the next token's previous-input weight
+        const Acc lg = ok ? (Acc)p.dtv * (Acc)p.Av : (Acc)0;
+        const float gam = ok ? p.lamv * p.dtv : 0.f;
+        const float sig = ok ? gam + (has_next ? (1.f - p.lamn) * p.dtn : 0.f) : 0.f;
+        if (tid < Q) {
+            s_gam[tid] = gam;
+            s_sig[tid] = sig;
+        }
+        const Acc v = wave_incl_scan(lg, lane);
+        if (lane == kWave - 1) s_wtot[wave] = v;
+        Acc ps[S::TPS];
+        Acc run = 0;
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            run += (seg * S::TPS + k < nv) ? (Acc)p.th[k] : (Acc)0;
+            ps[k] = run;
+        }
+        s_segtot[seg * NH + i] = run;
+        __syncthreads();
+        if (tid < Q) {
+            Acc off = 0;
+            for (int w2 = 0; w2 < wave; ++w2) off += s_wtot[w2];
+            s_cum[tid] = v + off;
+        }
+        Acc off = 0;
+        for (int s2 = 0; s2 < seg; ++s2) off += s_segtot[s2 * NH + i];
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) {
+            const int t = seg * S::TPS + k;
+            if (t < Q) {
+                const Acc psi = ps[k] + off;
+                Acc sn, cs;
+                sincos_fast(psi, &sn, &cs);
+                cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
+                if (t == nv - 1) s_psie[i] = psi;
+            }
+        }
+        __syncthreads();
+        if (tid < Q) {
+            const Acc cum_e = s_cum[nv - 1];
+            s_w[tid] = (tid < nv) ? (float)(exp_fast(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
+        }
+        __syncthreads();
+    };
+    // Owned state element (m2, half, v): row n = 16*(ntl + 4*half) + 4g + v,
+    // column p = 16*pt + l16; rows (i, i + N/2) of a pair sit in one lane.
+    // X <- R(psi_e)(de X + M) with this chunk's psi_e.
+    auto chunk_update = [&](float (&X)[PTW][2][4], const f32x4 (&ms)[PTW][2], Acc de) {
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int ntl = (wave + NW * m2) % 4;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                Acc sn, cs;
+                sincos_fast(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
+                const Acc re = de * (Acc)X[m2][0][v] + (Acc)ms[m2][0][v];
+                const Acc im = de * (Acc)X[m2][1][v] + (Acc)ms[m2][1][v];
+                X[m2][0][v] = (float)(cs * re - sn * im);
+                X[m2][1][v] = (float)(sn * re + cs * im);
+            }
+        }
+    };
+    // X <- R(psi_e) M (the output pass's accumulator already holds e^{cum_e} S + M)
+    auto rotate_psie = [&](const f32x4 (&ms)[PTW][2], float (&X)[PTW][2][4]) {
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int ntl = (wave + NW * m2) % 4;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                Acc sn, cs;
+                sincos_fast(s_psie[ntl * 16 + 4 * g + v], &sn, &cs);
+                const Acc re = ms[m2][0][v], im = ms[m2][1][v];
+                X[m2][0][v] = (float)(cs * re - sn * im);
+                X[m2][1][v] = (float)(sn * re + cs * im);
+            }
+        }
+    };
+    const int64_t SZ = (int64_t)N * P;
+    auto write_final = [&](const float (&X)[PTW][2][4]) {
+        float *fs = a.final_state + sl * SZ;
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    fs[(16 * (ntl + 4 * half) + 4 * g + v) * P + pt * 16 + l16] = X[m2][half][v];
+        }
+        T *cB = static_cast<T *>(a.cB) + sl * (R * N);
+        T *cX = static_cast<T *>(a.cX) + sl * (R * P);
+        const int64_t kl = (b * a.L + a.L - 1) * a.H + h;
+        const T *Bl = Bs + kl * (R * N);
+        const T *Xl = Xs + kl * (R * P);
+        for (int e = tid; e < R * N; e += S::NTHR) cB[e] = Bl[e];
+        for (int e = tid; e < R * P; e += S::NTHR) cX[e] = Xl[e];
+    };
+    // Initial state plus the carried previous-input term of token 0 (owned)
+    auto load_init = [&](float (&Si)[PTW][2][4]) {
+        const float *ist = a.init_state ? a.init_state + sl * SZ : nullptr;
+        float wb = 0.f;
+        if (a.init_cB) {
+            const int64_t k0 = (b * a.L) * a.H + h;
+            wb = (1.f - a.lam[k0]) * a.dt[k0];
+        }
+        const T *iB = a.init_cB ? static_cast<const T *>(a.init_cB) + sl * (R * N) : nullptr;
+        const T *iX = a.init_cX ? static_cast<const T *>(a.init_cX) + sl * (R * P) : nullptr;
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4, p = pt * 16 + l16;
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    const int n = 16 * (ntl + 4 * half) + 4 * g + v;
+                    float sv = ist ? ist[n * P + p] : 0.f;
+                    if (iB) {
+                        float u = 0.f;
+                        for (int r = 0; r < R; ++r) u += to_f32(iB[r * N + n]) * to_f32(iX[r * P + p]);
+                        sv += wb * u;
+                    }
+                    Si[m2][half][v] = sv;
+                }
+        }
+    };
+
+    using True = std::integral_constant<bool, true>;
+    using False = std::integral_constant<bool, false>;
+    constexpr int DA = NJB < 4 ? NJB : 4;   // blocks in flight, aggregate pass
+    constexpr int DC = 1;                   // blocks in flight, output pass
+    Blk ring[DA];
+    Pro pro;
+    float Sst[PTW][2][4];                   // state entering the current chunk
+
+    // ---- 2. aggregate pass, look-back, segment state ----
+    if (run_agg) {
+        float Aseg[PTW][2][4];
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) Aseg[m2][0][v] = Aseg[m2][1][v] = 0.f;
+        Acc seg_lg = 0, segps = 0;
+        load_pro(cbeg, pro);
+        sched_fence();
+#pragma unroll
+        for (int d = 0; d < DA; ++d) fetch(cbeg, d, ring[d]);
+        sched_fence();
+        for (int64_t c = cbeg; c < cend; ++c) {
+            relane();
+            cnv = nvalid_of(c);
+            prologue(c, pro);
+            sched_fence();
+            load_pro(min(c + 1, cend - 1), pro);
+            sched_fence();
+            f32x4 ms[PTW][2];
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int jb = 0; jb < NJB; ++jb) {
+                commit(jb, ring[jb % DA], False{});
+                __syncthreads();
+                {
+                    const int jn = jb + DA;
+                    sched_fence();
+                    fetch(min(c + jn / NJB, cend - 1), jn % NJB, ring[jb % DA]);
+                    sched_fence();
+                }
+                m_block(ms);
+                __syncthreads();
+            }
+            const Acc cum_e = s_cum[nvalid_of(c) - 1];
+            chunk_update(Aseg, ms, exp_fast(cum_e));
+            seg_lg += cum_e;
+            if (tid < NH) {
+                segps += s_psie[tid];
+                if constexpr (sizeof(Acc) == 4) segps = reduce_angle(segps);
+            }
+            __syncthreads();   // s_cum, s_psie read before the next prologue
+        }
+        if (tid < NH) s_segps[tid] = segps;
+        __syncthreads();
+
+        auto word_index = [&](int m2, int half, int vp) -> int64_t {
+            return (int64_t)((m2 * 2 + half) * 2 + vp) * S::NTHR + tid;
+        };
+        Acc *totp = static_cast<Acc *>(a.tot);
+        if (sg > 0 && !last_seg) {   // publish the aggregate (only successors read it)
+            unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.agg + slot * SZ);
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                for (int half = 0; half < 2; ++half)
+#pragma unroll
+                    for (int vp = 0; vp < 2; ++vp)
+                        st_coh2(dst + word_index(m2, half, vp), Aseg[m2][half][2 * vp], Aseg[m2][half][2 * vp + 1]);
+            if (tid == 0) st_coh(totp + slot * (NH + 1), seg_lg);
+            if (tid < NH) st_coh(totp + slot * (NH + 1) + 1 + tid, s_segps[tid]);
+            wait_stores_done();
+            __syncthreads();
+            if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagAgg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+
+        if (sg == 0) {
+            load_init(Sst);
+        } else {
+            // Decoupled look-back over the preceding segments: compose their
+            // maps S -> T_j S + A_j (nearest first) until an inclusive state.
+            // All owned pair rows of a lane are 16*ntl + 4g + v (ntl = wave % 4),
+            // so the accumulated rotation needs one angle per v.
+            Acc ad = 1;
+            Acc aps[4];
+            float aA[PTW][2][4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) aps[v] = 0;
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                for (int v = 0; v < 4; ++v) aA[m2][0][v] = aA[m2][1][v] = 0.f;
+            auto finish = [&](const float (&X)[PTW][2][4]) {
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    Acc sn, cs;
+                    sincos_fast(aps[v], &sn, &cs);
+                    sn *= ad;
+                    cs *= ad;
+#pragma unroll
+                    for (int m2 = 0; m2 < PTW; ++m2) {
+                        const Acc re = X[m2][0][v], im = X[m2][1][v];
+                        Sst[m2][0][v] = (float)(cs * re - sn * im) + aA[m2][0][v];
+                        Sst[m2][1][v] = (float)(sn * re + cs * im) + aA[m2][1][v];
+                    }
+                }
+            };
+            const int ntl_w = wave % 4;
+            int64_t j = sg - 1;
+            const int64_t sbase = sl * a.nseg;
+            while (true) {
+                // probe predecessors j, j-1, ..., j-15 at once (lanes of wave 0)
+                if (wave == 0) {
+                    uint32_t f = 0;
+                    if (lane < kProbe) {
+                        const int64_t jj = j - lane;
+                        f = (jj < 0) ? kFlagInit
+                                     : __hip_atomic_load(a.flags + sbase + jj, __ATOMIC_RELAXED,
+                                                         __HIP_MEMORY_SCOPE_AGENT);
+                    }
+                    const uint64_t mterm = __ballot(lane < kProbe && (f == kFlagInc || f == kFlagInit));
+                    const uint64_t mzero = __ballot(lane < kProbe && f == 0u);
+                    const int ft = mterm ? __ffsll((unsigned long long)mterm) - 1 : kProbe;
+                    const int fz = mzero ? __ffsll((unsigned long long)mzero) - 1 : kProbe;
+                    const uint32_t fterm = __shfl(f, ft < kProbe ? ft : 0, kWave);
+                    if (lane == 0) {
+                        s_i[1] = (fz < ft) ? fz : ft;                        // aggregates to compose
+                        s_i[2] = (fz < ft || ft == kProbe) ? 0 : (int)fterm;  // terminal kind
+                        s_i[3] = (fz < ft) ? 1 : 0;                          // must wait on a segment
+                    }
+                }
+                __syncthreads();
+                const int ncomp = s_i[1], term = s_i[2], needwait = s_i[3];
+                __syncthreads();
+                // compose the ready aggregates, loading kMaps maps per round trip
+                for (int k = 0; k < ncomp; k += kMaps) {
+                    const int nk = (ncomp - k) < kMaps ? (ncomp - k) : kMaps;
+                    float d[kMaps][PTW][2][4];
+                    Acc cps[kMaps][4], ccm[kMaps];
+#pragma unroll
+                    for (int u = 0; u < kMaps; ++u) {
+                        if (u < nk) {
+                            const int64_t js = sbase + j - k - u;
+                            const unsigned long long *src =
+                                reinterpret_cast<const unsigned long long *>(a.agg + js * SZ);
+                            const Acc *tp = totp + js * (NH + 1);
+                            ccm[u] = ld_coh(tp);
+#pragma unroll
+                            for (int v = 0; v < 4; ++v) cps[u][v] = ld_coh(tp + 1 + ntl_w * 16 + 4 * g + v);
+#pragma unroll
+                            for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                                for (int half = 0; half < 2; ++half)
+#pragma unroll
+                                    for (int vp = 0; vp < 2; ++vp)
+                                        ld_coh2(src + word_index(m2, half, vp), d[u][m2][half][2 * vp],
+                                                d[u][m2][half][2 * vp + 1]);
+                        }
+                    }
+#pragma unroll
+                    for (int u = 0; u < kMaps; ++u) {
+                        if (u < nk) {
+#pragma unroll
+                            for (int v = 0; v < 4; ++v) {
+                                Acc sn, cs;
+                                sincos_fast(aps[v], &sn, &cs);
+                                sn *= ad;
+                                cs *= ad;
+#pragma unroll
+                                for (int m2 = 0; m2 < PTW; ++m2) {
+                                    const Acc re = d[u][m2][0][v], im = d[u][m2][1][v];
+                                    aA[m2][0][v] += (float)(cs * re - sn * im);
+                                    aA[m2][1][v] += (float)(sn * re + cs * im);
+                                }
+                                aps[v] += cps[u][v];
+                                if constexpr (sizeof(Acc) == 4) aps[v] = reduce_angle(aps[v]);
+                            }
+                            ad *= exp_fast(ccm[u]);
+                        }
+                    }
+                }
+                j -= ncomp;
+                if (term == (int)kFlagInc) {
+                    const unsigned long long *src =
+                        reinterpret_cast<const unsigned long long *>(a.inc + (sbase + j) * SZ);
+                    float X[PTW][2][4];
+#pragma unroll
+                    for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                        for (int half = 0; half < 2; ++half)
+#pragma unroll
+                            for (int vp = 0; vp < 2; ++vp)
+                                ld_coh2(src + word_index(m2, half, vp), X[m2][half][2 * vp], X[m2][half][2 * vp + 1]);
+                    finish(X);
+                    break;
+                }
+                if (term == (int)kFlagInit) {
+                    float X[PTW][2][4];
+                    load_init(X);
+                    finish(X);
+                    break;
+                }
+                if (needwait) {   // the nearest unfinished predecessor is j: wait for it
+                    if (tid == 0) {
+                        uint32_t f = 0u;
+                        for (uint32_t spin = 0; spin < kSpinMax; ++spin) {
+                            f = __hip_atomic_load(a.flags + sbase + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                            if (f != 0u) break;
+                            __builtin_amdgcn_s_sleep(2);
+                        }
+                        if (f == 0u) atomicAdd(a.ctl + 1, 1u);   // timed out: report and stop waiting
+                        s_i[1] = (f == 0u) ? 1 : 0;
+                    }
+                    __syncthreads();
+                    const int timed_out = s_i[1];
+                    __syncthreads();
+                    if (timed_out) {
+                        float X[PTW][2][4] = {};
+                        finish(X);
+                        break;
+                    }
+                }
+            }
+        }
+
+        // outgoing state of the segment: e^{seg_lg} R(segps) S + A
+        {
+            float Sout[PTW][2][4];
+            const Acc de = exp_fast(seg_lg);
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2) {
+                const int ntl = (wave + NW * m2) % 4;
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    Acc sn, cs;
+                    sincos_fast(s_segps[ntl * 16 + 4 * g + v], &sn, &cs);
+                    const Acc re = Sst[m2][0][v], im = Sst[m2][1][v];
+                    Sout[m2][0][v] = (float)(de * (cs * re - sn * im)) + Aseg[m2][0][v];
+                    Sout[m2][1][v] = (float)(de * (sn * re + cs * im)) + Aseg[m2][1][v];
+                }
+            }
+            if (!last_seg) {
+                unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.inc + slot * SZ);
+#pragma unroll
+                for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                    for (int half = 0; half < 2; ++half)
+#pragma unroll
+                        for (int vp = 0; vp < 2; ++vp)
+                            st_coh2(dst + word_index(m2, half, vp), Sout[m2][half][2 * vp], Sout[m2][half][2 * vp + 1]);
+                wait_stores_done();
+                __syncthreads();
+                if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagInc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            } else {
+                write_final(Sout);
+            }
+        }
+    } else {
+        load_init(Sst);
+    }
+
+    // ---- 3. output pass over the segment's chunks ----
+    Frag cf[TPW][NK];
+    auto load_cf = [&](int64_t c) {
+        if (!ow) return;
+        const int64_t tk = tok_of(c);
+        const int nv = nvalid_of(c);
+        const T *Cg = Cs + tk * (R * N);
+#pragma unroll
+        for (int m = 0; m < TPW; ++m) {
+            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
+            const T *src = Cg + min(t, nv - 1) * bstr + r * N;
+#pragma unroll
+            for (int kk = 0; kk < NK; ++kk) cf[m][kk] = MM::load(src + kk * MM::K + MM::KPL * g);
+        }
+    };
+    load_pro(cbeg, pro);
+    sched_fence();
+#pragma unroll
+    for (int d = 0; d < DC; ++d) fetch(cbeg, d, ring[d]);
+    sched_fence();
+    load_cf(cbeg);
+    sched_fence();
+    const float Dh = a.D[h];
+    for (int64_t c = cbeg; c < cend; ++c) {
+        relane();
+        const int nv = nvalid_of(c);
+        cnv = nv;
+        const int64_t tk = tok_of(c);
+        // the state leaving this chunk is needed inside the segment, or as the
+        // final state when no aggregate pass produced it
+        const bool chain = (c + 1 < cend) || (!run_agg && c == a.nchunks - 1);
+        prologue(c, pro);
+        sched_fence();
+        load_pro(min(c + 1, cend - 1), pro);
+        sched_fence();
+        // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
+        // end of the sequence zeroed)
+#pragma unroll
+        for (int m = 0; m < TPW; ++m) {
+            if (!ow) break;
+            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R;
+            const bool ok = t < nv;
+#pragma unroll
+            for (int kk = 0; kk < NK / 2; ++kk) {
+#pragma unroll
+                for (int e = 0; e < MM::KPL; ++e) {
+                    const int n = kk * MM::K + MM::KPL * g + e;
+                    float cs, sn;
+                    cs_get(s_cs[n * LDC + t], cs, sn);
+                    const float u = ok ? fget(cf[m][kk], e) : 0.f, w = ok ? fget(cf[m][kk + NK / 2], e) : 0.f;
+                    fset(cf[m][kk], e, cs * u + sn * w);
+                    fset(cf[m][kk + NK / 2], e, cs * w - sn * u);
+                }
+            }
+        }
+        // S^T in the io dtype (B^ block) for the inter-chunk term
+        T *s_S = s_B;
+#pragma unroll
+        for (int m2 = 0; m2 < PTW; ++m2) {
+            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
+#pragma unroll
+            for (int half = 0; half < 2; ++half)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    s_S[(pt * 16 + l16) * S::LDN + 16 * (ntl + 4 * half) + 4 * g + v] = from_f32<T>(Sst[m2][half][v]);
+        }
+        __syncthreads();
+        // inter-chunk term e^{cum_t} C^_t . S starts the accumulators
+        f32x4 acc[TPW][PT];
+#pragma unroll
+        for (int m = 0; m < TPW; ++m) {
+            if (!ow) break;
+            const int TT = owned_tile<S>(wave, m);
+            float ecum[4];
+#pragma unroll
+            for (int v = 0; v < 4; ++v) ecum[v] = (float)exp_fast(s_cum[(TT * 16 + 4 * g + v) / R]);
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) {
+                f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk)
+                    tmp = MM::mma(cf[m][kk], MM::load(&s_S[(pt * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), tmp);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) tmp[v] *= ecum[v];
+                acc[m][pt] = tmp;
+            }
+        }
+        __syncthreads();   // S^T read: the B^ block is rewritten below
+        // the state accumulator starts as e^{cum_e} S and collects M
+        f32x4 ms[PTW][2];
+        if (chain) {
+            const float de = (float)exp_fast(s_cum[nv - 1]);
+#pragma unroll
+            for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                for (int half = 0; half < 2; ++half)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) ms[m2][half][v] = de * Sst[m2][half][v];
+        }
+#pragma unroll
+        for (int jb = 0; jb < NJB; ++jb) {
+            commit(jb, ring[jb % DC], True{});
+            __syncthreads();
+            {
+                const int jn = jb + DC;
+                sched_fence();
+                fetch(min(c + jn / NJB, cend - 1), jn % NJB, ring[jb % DC]);
+                sched_fence();
+            }
+#pragma unroll
+            for (int jp = 0; jp < S::JB / 32; ++jp) {
+                const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
+                if (!ow) break;
+                if (J0 > owned_tile<S>(wave, TPW - 1) && J0 > owned_tile<S>(wave, 0)) continue;
+                // x^T columns of the pair, shared by all owned tiles
+                bf16x8 xf[PT];
+                if constexpr (MM::KPL == 8) {
+#pragma unroll
+                    for (int pt = 0; pt < PT; ++pt) {
+                        const T *xr = &s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
+                        const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
+                        const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) { xf[pt][v] = lo[v]; xf[pt][4 + v] = hi[v]; }
+                    }
+                }
+                // G^T tiles (K = N) for every owned tile at or below the pair
+                f32x4 gt[TPW][2];
+#pragma unroll
+                for (int m = 0; m < TPW; ++m) gt[m][0] = gt[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+#pragma unroll
+                    for (int kk = 0; kk < NK; ++kk) {
+                        const Frag bfr = MM::load(&s_B[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
+#pragma unroll
+                        for (int m = 0; m < TPW; ++m)
+                            if (J0 + q <= owned_tile<S>(wave, m)) gt[m][q] = MM::mma(bfr, cf[m][kk], gt[m][q]);
+                    }
+                // mask weights (branch-free): w_tj = e^{cum_t - cum_j} sigma_j (j < t),
+                // gamma_t (j = t), 0 (j > t); D x_t as D on the diagonal row = column
+#pragma unroll
+                for (int m = 0; m < TPW; ++m) {
+                    const int TT = owned_tile<S>(wave, m);
+                    if (J0 > TT) continue;
+                    const int tt = (TT * 16 + l16) / R;
+                    const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
+                    constexpr int NV = R >= 4 ? 1 : 4 / R;
+#pragma unroll
+                    for (int q = 0; q < 2; ++q) {
+                        float wv[NV];
+#pragma unroll
+                        for (int u = 0; u < NV; ++u) {
+                            const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
+                            const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
+                            wv[u] = tj < tt ? e : (tj == tt ? gam_t : 0.f);
+                        }
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) gt[m][q][v] *= wv[(v * NV) / 4];
+                        if (J0 + q == TT) {
+#pragma unroll
+                            for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
+                        }
+                    }
+                    // y += (w o G) x  (K = the pair's 32 rows)
+                    if constexpr (MM::KPL == 8) {
+                        bf16x8 af;
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) {
+                            af[v] = (bf16)gt[m][0][v];
+                            af[4 + v] = (bf16)gt[m][1][v];
+                        }
+#pragma unroll
+                        for (int pt = 0; pt < PT; ++pt) acc[m][pt] = MM::mma(af, xf[pt], acc[m][pt]);
+                    } else {
+#pragma unroll
+                        for (int q = 0; q < 2; ++q)
+#pragma unroll
+                            for (int v = 0; v < 4; ++v)
+#pragma unroll
+                                for (int pt = 0; pt < PT; ++pt) {
+                                    const float xv = to_f32(s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
+                                    acc[m][pt] = MM::mma(gt[m][q][v], xv, acc[m][pt]);
+                                }
+                    }
+                }
+            }
+            // M of this block for the state, once the G^T operands are dead
+            __builtin_amdgcn_sched_barrier(0);
+            if (chain) m_block(ms);
+            __syncthreads();   // staged block read: the next commit may overwrite it
+        }
+        sched_fence();
+        load_cf(min(c + 1, cend - 1));
+        sched_fence();
+        if (chain) {
+            rotate_psie(ms, Sst);
+            if (c == a.nchunks - 1) write_final(Sst);
+        }
+        // store: each wave stages one 16-row tile at a time in LDS and writes
+        // whole 16-byte pieces of the y rows
+        T *s_y = s_B + wave * (16 * P);
+        T *Yg = static_cast<T *>(a.y) + tk * (R * P);
+#pragma unroll
+        for (int m = 0; m < TPW; ++m) {
+            const int TT = owned_tile<S>(wave, m);
+            if (ow) {
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) s_y[(4 * g + v) * P + pt * 16 + l16] = from_f32<T>(acc[m][pt][v]);
+            }
+            __syncthreads();
+            constexpr int PIECES = 16 * P / S::CE;
+#pragma unroll
+            for (int k = lane; k < PIECES; k += kWave) {
+                if (!ow) break;
+                const int rl = k / (P / S::CE), col = (k % (P / S::CE)) * S::CE;
+                const int row = TT * 16 + rl, t = row / R, r = row % R;
+                if (t < nv)
+                    *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) =
+                        *reinterpret_cast<const V16 *>(&s_y[rl * P + col]);
+            }
+            __syncthreads();
+        }
+    }
+}
+
+// Workgroups of one kernel resident on the whole device at once (cached per
+// device).
+int resident_capacity(const void *fn, int nthr, int *cache) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    int v = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+    if (v > 0) return v;
+    int ncu = 0, per = 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, nthr, 0) != hipSuccess) return 0;
+    v = ncu * (per > 0 ? per : 1);
+    __atomic_store_n(&cache[dev], v, __ATOMIC_RELAXED);
+    return v;
+}
+
+template <typename T, int Q, int R>
+hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
+    typedef SegShape<T, Q, R> S;
+    static int cap_cache[64];
+    ScanArgs a = a0;
+    const int64_t nsl = a.batch * a.H;
+    int64_t G = a.G;
+    if (G <= 0) {   // one resident wave of workgroups covers the whole scan
+        const int cap = resident_capacity(reinterpret_cast<const void *>(&k_scan_seg<T, Q, R>), S::NTHR,
+                                          cap_cache);
+        if (cap <= 0) return hipErrorInvalidDevice;
+        G = (nsl * a.nchunks + cap - 1) / cap;
+    }
+    G = G < 1 ? 1 : (G > a.nchunks ? a.nchunks : G);
+    a.G = G;
+    a.nseg = (a.nchunks + G - 1) / G;
+    if (a.nseg > 1) {
+        const int64_t nflags = nsl * a.nseg;
+        const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);
+        hipLaunchKernelGGL(k_reset, dim3(rblocks), dim3(256), 0, stream, a.ctl, a.flags, nflags);
+    }
+    hipLaunchKernelGGL((k_scan_seg<T, Q, R>), dim3((unsigned)(nsl * a.nseg)), dim3(S::NTHR), 0, stream, a);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+#define M3_SEG_SHAPES(X)     \
+    X(0, float, 2, 32)       \
+    X(0, float, 4, 16)       \
+    X(0, float, 4, 32)       \
+    X(1, bf16, 1, 64)        \
+    X(1, bf16, 1, 128)       \
+    X(1, bf16, 2, 32)        \
+    X(1, bf16, 2, 64)        \
+    X(1, bf16, 2, 128)       \
+    X(1, bf16, 4, 32)        \
+    X(1, bf16, 4, 64)
+
+scan_launch_fn find_seg_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q) {
+    if (N != 128 || P != 64) return nullptr;
+#define M3_CASE(IO, T, R_, Q_) \
+    if (io == IO && R == R_ && Q == Q_) return &launch_seg<T, Q_, R_>;
+    M3_SEG_SHAPES(M3_CASE)
+#undef M3_CASE
+    return nullptr;
+}
+
+}  // namespace m3

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libm3.so")
 M3_OK, M3_ERR_NULL, M3_ERR_SHAPE, M3_ERR_DTYPE = 0, 1, 2, 3
 M3_ERR_UNSUPPORTED, M3_ERR_ALIGN, M3_ERR_WORKSPACE, M3_ERR_HIP = 4, 5, 6, 7
 M3_F32, M3_BF16 = 0, 1
-M3_SCAN_SPLIT = 1
+M3_SCAN_SPLIT, M3_SCAN_PER_CHUNK = 1, 2
 _IO = {torch.float32: M3_F32, torch.bfloat16: M3_BF16}
 
 
@@ -29,7 +29,8 @@ class M3Dims(ctypes.Structure):
                 ("dstate", ctypes.c_int64), ("rank", ctypes.c_int64),
                 ("chunk", ctypes.c_int64), ("io", ctypes.c_int32),
                 ("flags", ctypes.c_int32), ("a_stride_b", ctypes.c_int64),
-                ("a_stride_t", ctypes.c_int64), ("a_stride_h", ctypes.c_int64)]
+                ("a_stride_t", ctypes.c_int64), ("a_stride_h", ctypes.c_int64),
+                ("seg_chunks", ctypes.c_int64)]
 
 
 class M3Error(RuntimeError):
@@ -99,12 +100,13 @@ def _a_strides(A: torch.Tensor, batch: int, seqlen: int, nheads: int):
 
 
 def scan_dims(x: torch.Tensor, Bm: torch.Tensor, chunk: int, A: Optional[torch.Tensor] = None,
-              split: bool = False) -> M3Dims:
+              split: bool = False, per_chunk: bool = False, seg: int = 0) -> M3Dims:
     batch, seqlen, nheads, rank, headdim = x.shape
     dstate = Bm.shape[-1]
     sb, st, sh = _a_strides(A, batch, seqlen, nheads) if A is not None else (0, 0, 1)
+    flags = (M3_SCAN_SPLIT if split else 0) | (M3_SCAN_PER_CHUNK if per_chunk else 0)
     return M3Dims(batch, seqlen, nheads, headdim, dstate, rank, int(chunk),
-                  _IO[x.dtype], M3_SCAN_SPLIT if split else 0, sb, st, sh)
+                  _IO[x.dtype], flags, sb, st, sh, int(seg))
 
 
 def workspace_bytes(dims: M3Dims) -> int:
@@ -113,13 +115,15 @@ def workspace_bytes(dims: M3Dims) -> int:
 
 def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
              init_state=None, init_carry=None, out=None, workspace=None,
-             stream=None, split: bool = False
+             stream=None, split: bool = False, per_chunk: bool = False, seg: int = 0
              ) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
     """m3_scan_fwd: returns y [B,L,H,R,P], final_state [B,H,N,P] fp32 and the
     carry (B_{L-1} [B,H,R,N], X_{L-1} [B,H,R,P]).  `out` may supply
-    (y, final_state, carryB, carryX) to write into; `split` selects the
-    three-kernel scan (M3_SCAN_SPLIT)."""
-    d = scan_dims(x, Bm, chunk, A, split)
+    (y, final_state, carryB, carryX) to write into.  Kernel choice: `split`
+    (M3_SCAN_SPLIT, three kernels), `per_chunk` (M3_SCAN_PER_CHUNK, one chunk
+    per workgroup), else the segmented kernel with `seg` chunks per
+    workgroup (0: library choice)."""
+    d = scan_dims(x, Bm, chunk, A, split, per_chunk, seg)
     batch, seqlen, nheads, rank, headdim = x.shape
     dstate = Bm.shape[-1]
     dev = x.device
@@ -151,7 +155,7 @@ def step_dims(x_t: torch.Tensor, B_t: torch.Tensor, A: torch.Tensor) -> M3Dims:
         sb, sh = A.stride()
     else:
         raise ValueError(f"A must be [H] or [B, H], got {tuple(A.shape)}")
-    return M3Dims(batch, 1, nheads, headdim, dstate, rank, 1, _IO[x_t.dtype], 0, sb, 0, sh)
+    return M3Dims(batch, 1, nheads, headdim, dstate, rank, 1, _IO[x_t.dtype], 0, sb, 0, sh, 0)
 
 
 def step(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, y=None, stream=None):

@@ -25,7 +25,10 @@ def say(msg):
     print(f"[gpu-case] {msg}", flush=True)
 
 
-def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, split=False):
+MODES = ("seg", "per_chunk", "split")   # segmented single-pass (default), one chunk per WG, 3 kernels
+
+
+def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, mode="seg", seg=0):
     """Scan with every output pre-filled with NaN, so an unwritten element fails."""
     x = inp.x
     B_, L, H, R, P = x.shape
@@ -36,16 +39,18 @@ def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, split=
                torch.full((B_, H, N, P), float("nan"), device=x.device),
                torch.full((B_, H, R, N), float("nan"), device=x.device, dtype=x.dtype),
                torch.full((B_, H, R, P), float("nan"), device=x.device, dtype=x.dtype))
-    nbytes = m3.workspace_bytes(m3.scan_dims(x, inp.Bm, chunk, inp.A, split))
-    # the single-pass kernel serves this shape iff its workspace differs from the split path's
-    single_pass = not split and nbytes != m3.workspace_bytes(m3.scan_dims(x, inp.Bm, chunk, inp.A, True))
-    ws = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=x.device)
+    kw = dict(split=mode == "split", per_chunk=mode == "per_chunk", seg=seg)
+    nbytes = m3.workspace_bytes(m3.scan_dims(x, inp.Bm, chunk, inp.A, **kw))
+    # a single-pass kernel serves this shape iff its workspace differs from the split path's
+    single_pass = mode != "split" and nbytes != m3.workspace_bytes(
+        m3.scan_dims(x, inp.Bm, chunk, inp.A, split=True))
+    ws = torch.zeros(max(nbytes, 16), dtype=torch.uint8, device=x.device)
     y, fs, (cB, cX) = m3.scan_fwd(x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta, inp.D,
                                   chunk=chunk, init_state=init_state, init_carry=init_carry,
-                                  out=out, split=split, workspace=ws)
+                                  out=out, workspace=ws, **kw)
     torch.cuda.synchronize()
     if single_pass and L > 0:
-        # single-pass kernel: word 1 of the workspace counts look-back waits that timed out
+        # single-pass kernels: word 1 of the workspace counts look-back waits that timed out
         assert int(ws[4:8].view(torch.int32).item()) == 0, "look-back wait timed out"
     return y, fs, cB, cX
 
@@ -176,25 +181,26 @@ SHAPES = [  # io, N, P, R, Q
 ]
 
 
-@pytest.mark.parametrize("split", [False, True])
+@pytest.mark.parametrize("mode", MODES)
 @pytest.mark.parametrize("io,N,P,R,Q", SHAPES)
-def test_shapes_ragged(io, N, P, R, Q, split):
+def test_shapes_ragged(io, N, P, R, Q, mode):
     """Several chunks plus a ragged tail, two batch rows and three heads, on
-    the single-pass kernel and on the three-kernel path."""
+    each prefill kernel (shapes a kernel is not built for fall back)."""
     L = 3 * Q + Q // 2 + 3
-    say(f"shape io={io} N={N} P={P} R={R} Q={Q} L={L} split={split}")
+    say(f"shape io={io} N={N} P={P} R={R} Q={Q} L={L} mode={mode}")
     inp = make_scan_inputs(2, L, 3, P, N, R, io=io, seed=11 + N + R + Q, device=DEV, chunk=Q)
-    y, fs, cB, cX = run_scan(inp, Q, split=split)
+    y, fs, cB, cX = run_scan(inp, Q, mode=mode)
     check_slices(inp, y, fs, cB, cX, sample_slices(2, 3, 99, 5), TOL[io], label=f"{io}/{N}/{R}/{Q}")
 
 
+@pytest.mark.parametrize("mode", ["seg", "per_chunk"])
 @pytest.mark.parametrize("io", ["f32", "bf16"])
 @pytest.mark.parametrize("L", [1, 2, 63, 64, 65])
-def test_short_sequences(io, L):
-    N, P, R, Q = (16, 16, 1, 64) if io == "f32" else (128, 64, 4, 64)
-    say(f"short io={io} L={L}")
+def test_short_sequences(io, L, mode):
+    N, P, R, Q = (128, 64, 2, 32) if io == "f32" else (128, 64, 4, 64)
+    say(f"short io={io} L={L} mode={mode}")
     inp = make_scan_inputs(2, L, 2, P, N, R, io=io, seed=100 + L, device=DEV, chunk=Q)
-    y, fs, cB, cX = run_scan(inp, Q)
+    y, fs, cB, cX = run_scan(inp, Q, mode=mode)
     check_slices(inp, y, fs, cB, cX, sample_slices(2, 2, 99, 6), TOL[io], label=f"short{L}")
 
 
@@ -247,25 +253,59 @@ def test_segment_resume_and_decode_consistency(io):
             assert oracle.rel_err(fsl[b, h].cpu().numpy(), fsf[b, h].cpu().numpy()) <= tol
 
 
+@pytest.mark.parametrize("mode,seg", [("seg", 1), ("seg", 2), ("seg", 0), ("per_chunk", 0)])
 @pytest.mark.parametrize("io", ["f32", "bf16"])
-def test_chunk_boundary_impulse(io):
+def test_chunk_boundary_impulse(io, mode, seg):
     """Only x at the last token of a chunk is nonzero and lambda there is 0,
     so every later output flows through the cross-chunk previous-input term
-    (sigma of that token reads the next chunk's lambda and dt)."""
-    N, P, R, Q = (16, 16, 1, 64) if io == "f32" else (128, 64, 2, 64)
+    (sigma of that token reads the next chunk's lambda and dt); with one
+    chunk per segment the boundary is also a segment boundary."""
+    N, P, R, Q = (128, 64, 2, 32) if io == "f32" else (128, 64, 2, 64)
     L = 3 * Q
-    say(f"boundary impulse io={io}")
+    say(f"boundary impulse io={io} mode={mode} seg={seg}")
     inp = make_scan_inputs(1, L, 2, P, N, R, io=io, seed=9, device=DEV, chunk=Q)
     j = Q - 1
     keep = inp.x[:, j].clone()
     inp.x.zero_()
     inp.x[:, j] = keep
     inp.lam[:, j] = 0.0
-    y, fs, cB, cX = run_scan(inp, Q)
+    y, fs, cB, cX = run_scan(inp, Q, mode=mode, seg=seg)
     assert torch.count_nonzero(y[:, :j].float()) == 0
     check_slices(inp, y, fs, cB, cX, [(0, 0), (0, 1)], TOL[io], label="impulse")
     # beyond the boundary the output is large (not a trivially small residue)
     assert y[:, j + 1:].float().abs().max() > 1e-3
+
+
+SEG_SHAPES = [("f32", 128, 64, 2, 32), ("f32", 128, 64, 4, 16), ("bf16", 128, 64, 1, 64),
+              ("bf16", 128, 64, 1, 128), ("bf16", 128, 64, 4, 64), ("bf16", 128, 64, 2, 32)]
+
+
+@pytest.mark.parametrize("seg", [1, 2, 3, 8, 0])
+@pytest.mark.parametrize("io,N,P,R,Q", SEG_SHAPES)
+def test_segment_lengths(io, N, P, R, Q, seg):
+    """Segmented kernel: eight chunks (the last ragged) split into segments of
+    1, 2, 3 (uneven) or 8 chunks (no look-back), or the library's choice."""
+    L = 7 * Q + Q // 2 + 1
+    say(f"segments io={io} R={R} Q={Q} L={L} seg={seg}")
+    inp = make_scan_inputs(2, L, 3, P, N, R, io=io, seed=70 + R + Q + seg, device=DEV, chunk=Q)
+    y, fs, cB, cX = run_scan(inp, Q, seg=seg)
+    check_slices(inp, y, fs, cB, cX, sample_slices(2, 3, 99, 8), TOL[io],
+                 label=f"seg{seg}/{io}/{R}/{Q}")
+
+
+@pytest.mark.parametrize("seg", [1, 3, 0])
+def test_segment_lengths_with_initial_state(seg):
+    """A continued sequence (initial state and carry) through every segment split."""
+    N, P, R, Q = 128, 64, 4, 32
+    L = 9 * Q + 5
+    say(f"segments + init seg={seg}")
+    inp = make_scan_inputs(2, L, 2, P, N, R, io="bf16", seed=90 + seg, device=DEV, chunk=Q)
+    st0 = torch.randn(2, 2, N, P, device=DEV)
+    c0 = (torch.randn(2, 2, R, N, device=DEV).to(torch.bfloat16),
+          torch.randn(2, 2, R, P, device=DEV).to(torch.bfloat16))
+    y, fs, cB, cX = run_scan(inp, Q, init_state=st0, init_carry=c0, seg=seg)
+    check_slices(inp, y, fs, cB, cX, sample_slices(2, 2, 99, 9), TOL["bf16"], init_state=st0,
+                 init_carry=c0, label=f"seg{seg}+init")
 
 
 def test_chunk_size_invariance():
@@ -299,12 +339,13 @@ def test_per_token_A():
         assert oracle.rel_err(fs[b, h].cpu().numpy(), rs[k]) <= 1e-5
 
 
-def test_determinism():
+@pytest.mark.parametrize("mode,seg", [("seg", 0), ("seg", 2), ("per_chunk", 0)])
+def test_determinism(mode, seg):
     """Two runs give bitwise-identical outputs (no atomics in reductions)."""
-    say("determinism bf16 R=4")
+    say(f"determinism bf16 R=4 mode={mode} seg={seg}")
     inp = make_scan_inputs(2, 300, 4, 64, 128, 4, io="bf16", seed=8, device=DEV)
-    a = run_scan(inp, 64)
-    b = run_scan(inp, 64)
+    a = run_scan(inp, 64, mode=mode, seg=seg)
+    b = run_scan(inp, 64, mode=mode, seg=seg)
     for u, v in zip(a, b):
         assert torch.equal(u, v)
 

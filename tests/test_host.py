@@ -47,7 +47,7 @@ FAKE = 0x100000  # 16-byte aligned fake device address; never dereferenced
 
 def dims(**kw):
     d = dict(batch=1, seqlen=256, nheads=2, headdim=16, dstate=16, rank=1, chunk=64,
-             io=m3.M3_F32, flags=0, a_stride_b=0, a_stride_t=0, a_stride_h=1)
+             io=m3.M3_F32, flags=0, a_stride_b=0, a_stride_t=0, a_stride_h=1, seg_chunks=0)
     d.update(kw)
     return m3.M3Dims(**d)
 
@@ -74,7 +74,8 @@ def test_scan_host_validation(L):
     assert scan_call(L, dims(batch=0)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(seqlen=-1)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(chunk=0)) == m3.M3_ERR_SHAPE
-    assert scan_call(L, dims(flags=2)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(flags=4)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(seg_chunks=-1)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(dstate=64, headdim=64)) == m3.M3_ERR_UNSUPPORTED
     assert scan_call(L, dims(chunk=48)) == m3.M3_ERR_UNSUPPORTED
     assert scan_call(L, dims(io=m3.M3_BF16)) == m3.M3_ERR_UNSUPPORTED
