@@ -76,7 +76,10 @@ typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
  * Default (0), wherever built (dstate 128, headdim 64): the segmented
  * single-pass kernel: each workgroup scans a segment of consecutive chunks of
  * one (batch, head) slice and carries the state across them; segments of a
- * slice are linked by a decoupled look-back over their state maps.
+ * slice are linked by a decoupled look-back over their state maps.  When
+ * seg_chunks is 0 and chunks of fewer than 128 rows (chunk * rank) would need
+ * several segments per slice, the one-chunk-per-workgroup kernel runs
+ * instead (it is faster there).
  * M3_SCAN_SPLIT: three kernels (chunk states, a state pass over chunks,
  * chunk outputs); the only path for other shapes.
  * M3_SCAN_PER_CHUNK: the single-pass kernel with one chunk per workgroup

@@ -87,9 +87,10 @@ static m3_status check_scan_dims(const m3_dims *d, ScanImpl *impl, int64_t *nchu
     // the empty sequence (handled by the three-kernel path's state kernel)
     if (nc > 0 && !(d->flags & M3_SCAN_SPLIT)) {
         scan_launch_fn f = nullptr;
+        scan_launch_fn pc = find_fused_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
         if (!(d->flags & M3_SCAN_PER_CHUNK)) f = find_seg_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
-        if (!f) f = find_fused_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
-        if (f) { impl->launch = f; impl->fused = true; }
+        if (!f) f = pc;
+        if (f) { impl->launch = f; impl->fused = true; impl->per_chunk = pc; }
     }
     *nchunks = nc;
     return M3_OK;
@@ -151,7 +152,7 @@ extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B,
     }
     a.batch = d->batch; a.L = d->seqlen; a.H = d->nheads; a.nchunks = nc;
     a.a_sb = d->a_stride_b; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
-    a.G = d->seg_chunks; a.nseg = 0;
+    a.G = d->seg_chunks; a.nseg = 0; a.per_chunk = impl.per_chunk;
     const hipError_t e = impl.launch(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) {
         g_last_hip_error = (int)e;

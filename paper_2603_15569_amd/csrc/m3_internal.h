@@ -28,8 +28,11 @@ struct ScanArgs {
     int64_t batch, L, H, nchunks;
     int64_t a_sb, a_st, a_sh;
     // segmented kernel: chunks per segment (0 = chosen at launch), segments
-    // per slice (set at launch)
+    // per slice (set at launch), and the one-chunk-per-workgroup kernel it
+    // hands over to when its own choice would give short chunks several
+    // segments per slice (null: none)
     int64_t G, nseg;
+    hipError_t (*per_chunk)(const ScanArgs &, hipStream_t);
 };
 
 struct StepArgs {
@@ -49,6 +52,7 @@ struct ScanImpl {
     scan_launch_fn launch;
     int acc_bytes;   // bytes of the prologue scalar type (4: fp32, 8: fp64)
     bool fused;      // a single-pass look-back kernel (else the three-kernel path)
+    scan_launch_fn per_chunk;   // one-chunk-per-workgroup kernel for the shape, if built
 };
 
 // Kernel lookup by shape; null launch when no kernel is built for it.

@@ -523,10 +523,10 @@ hipError_t launch_scan(const ScanArgs &a, hipStream_t stream) {
 ScanImpl find_scan_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q) {
 #define M3_CASE(IO, T, N_, P_, R_, Q_)                                      \
     if (io == IO && N == N_ && P == P_ && R == R_ && Q == Q_)               \
-        return ScanImpl{&launch_scan<T, N_, P_, R_, Q_>, (int)sizeof(typename AccOf<T>::type), false};
+        return ScanImpl{&launch_scan<T, N_, P_, R_, Q_>, (int)sizeof(typename AccOf<T>::type), false, nullptr};
     M3_SCAN_SHAPES(M3_CASE)
 #undef M3_CASE
-    return ScanImpl{nullptr, 0, false};
+    return ScanImpl{nullptr, 0, false, nullptr};
 }
 
 }  // namespace m3

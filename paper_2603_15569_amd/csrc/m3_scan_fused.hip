@@ -66,10 +66,14 @@ void k_scan_fused(ScanArgs a) {
     __shared__ Acc s_psie[NH];
     __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
     __shared__ CS s_cs[NH * LDC];
-    __shared__ __attribute__((aligned(16))) T s_B[S::JB * S::LDN];   // B^ block [row][n]
-    __shared__ __attribute__((aligned(16))) T s_X[P * S::LDJ];       // x^T block [p][row]
+    // Chunks of several row blocks double-buffer the staged blocks: block
+    // jb + 1 is committed while the MFMAs read block jb (one barrier a block).
+    constexpr int NBUF = (S::NJB > 1 && sizeof(T) == 2) ? 2 : 1;   // (fp32 blocks: LDS too small)
+    constexpr int kSB = S::JB * S::LDN, kSX = P * S::LDJ;
     constexpr int kBtS = (N * S::LDJ > P * S::LDN) ? N * S::LDJ : P * S::LDN;
-    __shared__ __attribute__((aligned(16))) T s_BtS[kBtS];   // (B^ W)^T block [n][row]; later S_in^T [p][n]
+    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];      // B^ block [row][n]
+    __shared__ __attribute__((aligned(16))) T s_X[NBUF * kSX];      // x^T block [p][row]
+    __shared__ __attribute__((aligned(16))) T s_BtS[NBUF * kBtS];   // (B^ W)^T block [n][row]; later S_in^T [p][n]
     __shared__ int s_i[4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
@@ -109,60 +113,63 @@ void k_scan_fused(ScanArgs a) {
     constexpr int TX = S::JB * (P / S::CE) / S::NTHR;    // x tasks per thread
     static_assert(TB * S::NTHR == S::JB * (NH / S::CE) && TX * S::NTHR == S::JB * (P / S::CE), "tasks");
     struct Blk { V16 lo[TB], hi[TB], xv[TX]; };
+    // The global loads are unconditional (rows past the end of the sequence
+    // read the last valid row and are zeroed in commit()), so the number of
+    // loads in flight is static and the compiler's waits stop at exactly the
+    // loads a step needs, leaving later prefetches in flight.
     auto fetch = [&](int jb, Blk &f) {
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            f.lo[k] = V16{};
-            f.hi[k] = V16{};
-            if (t < nvalid) {
-                const T *src = Bg + t * bstr + r * N + cp * S::CE;
-                f.lo[k] = *reinterpret_cast<const V16 *>(src);
-                f.hi[k] = *reinterpret_cast<const V16 *>(src + NH);
-            }
+            const T *src = Bg + min(t, nvalid - 1) * bstr + r * N + cp * S::CE;
+            f.lo[k] = *reinterpret_cast<const V16 *>(src);
+            f.hi[k] = *reinterpret_cast<const V16 *>(src + NH);
         }
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            f.xv[k] = V16{};
-            if (t < nvalid) f.xv[k] = *reinterpret_cast<const V16 *>(Xg + t * xstr + r * P + pc * S::CE);
+            f.xv[k] = *reinterpret_cast<const V16 *>(Xg + min(t, nvalid - 1) * xstr + r * P + pc * S::CE);
         }
     };
     auto commit = [&](int jb, const Blk &f, auto kBt, auto kRow) {
+        T *sB = s_B + (jb % NBUF) * kSB, *sX = s_X + (jb % NBUF) * kSX, *sBt = s_BtS + (jb % NBUF) * kBtS;
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R;
             V16 lo = f.lo[k], hi = f.hi[k];
             const float wt = s_w[t];
+            const bool ok = t < nvalid;
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
                 const int n = cp * S::CE + e;
                 float cs, sn;
                 cs_get(s_cs[n * LDC + t], cs, sn);
-                const float u = fget(lo, e), w = fget(hi, e);
+                const float u = ok ? fget(lo, e) : 0.f, w = ok ? fget(hi, e) : 0.f;
                 const float re = cs * u + sn * w, im = cs * w - sn * u;
                 if constexpr (decltype(kRow)::value) {
                     fset(lo, e, re);
                     fset(hi, e, im);
                 }
                 if constexpr (decltype(kBt)::value) {
-                    s_BtS[n * S::LDJ + jr] = from_f32<T>(wt * re);
-                    s_BtS[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
+                    sBt[n * S::LDJ + jr] = from_f32<T>(wt * re);
+                    sBt[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
                 }
             }
             if constexpr (decltype(kRow)::value) {
-                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + cp * S::CE]) = lo;
-                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + NH + cp * S::CE]) = hi;
+                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
+                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
             }
         }
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
+            const bool ok = (jb * S::JB + jr) / R < nvalid;
 #pragma unroll
-            for (int e = 0; e < S::CE; ++e) s_X[(pc * S::CE + e) * S::LDJ + jr] = f.xv[k][e];
+            for (int e = 0; e < S::CE; ++e)
+                sX[(pc * S::CE + e) * S::LDJ + jr] = ok ? f.xv[k][e] : from_f32<T>(0.f);
         }
     };
     // Prefetch depth (blocks in flight, register ring): the aggregate phase
@@ -177,26 +184,32 @@ void k_scan_fused(ScanArgs a) {
     {
         // angles first (the largest prologue load): thread (pair i, segment seg)
         const int i = tid % NH, seg = tid / NH;
-        Acc ps[S::TPS];
+        float th[S::TPS];
 #pragma unroll
         for (int k = 0; k < S::TPS; ++k) {
             const int t = seg * S::TPS + k;
-            ps[k] = (t < nvalid) ? (Acc)a.theta[(tok0 + t * tstr) * NH + i] : (Acc)0;
+            th[k] = a.theta[(tok0 + min(t, nvalid - 1) * tstr) * NH + i];
         }
-        Acc lg = 0;
-        float gam = 0.f, sig = 0.f;
-        if (tid < Q && tid < nvalid) {
-            const int64_t t = t0 + tid, k = tok0 + tid * tstr;
-            const float dtv = a.dt[k], lamv = a.lam[k];
-            lg = (Acc)dtv * (Acc)a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
-            gam = lamv * dtv;
-            sig = gam;
-            if (t + 1 < a.L) sig += (1.f - a.lam[k + tstr]) * a.dt[k + tstr];
-        }
+        const int tq = min(tid, nvalid - 1);
+        const int64_t kq = tok0 + tq * tstr, tg = t0 + tq;
+        const int64_t kn = (tg + 1 < a.L) ? kq + tstr : kq;
+        const float dtv = a.dt[kq], lamv = a.lam[kq];
+        const float Av = a.A[b * a.a_sb + tg * a.a_st + h * a.a_sh];
+        const float dtn = a.dt[kn], lamn = a.lam[kn];
         // the first blocks' loads go out after the prologue's own loads (memory
         // counters retire in order), so they overlap the prologue's arithmetic
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int d = 0; d < DA; ++d) fetch(d, ring[d]);
+        __builtin_amdgcn_sched_barrier(0);
+        const bool ok = tid < Q && tid < nvalid;
+        const bool has_next = t0 + tid + 1 < a.L;
+        const Acc lg = ok ? (Acc)dtv * (Acc)Av : (Acc)0;
+        const float gam = ok ? lamv * dtv : 0.f;
+        const float sig = ok ? gam + (has_next ? (1.f - lamn) * dtn : 0.f) : 0.f;
+        Acc ps[S::TPS];
+#pragma unroll
+        for (int k = 0; k < S::TPS; ++k) ps[k] = (seg * S::TPS + k < nvalid) ? (Acc)th[k] : (Acc)0;
         if (tid < Q) {
             s_gam[tid] = gam;
             s_sig[tid] = sig;
@@ -246,12 +259,25 @@ void k_scan_fused(ScanArgs a) {
     f32x4 ms[PTW][2];
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (NBUF == 2) {
+        commit(0, ring[0], True{}, False{});
+        __syncthreads();
+        if (DA < S::NJB) fetch(DA, ring[0]);
+    }
 #pragma unroll
     for (int jb = 0; jb < S::NJB; ++jb) {
-        if constexpr (S::NJB == 1) commit(jb, ring[jb % DA], True{}, True{});   // one block: keep B^ for the outputs
-        else commit(jb, ring[jb % DA], True{}, False{});
-        __syncthreads();
-        if (jb + DA < S::NJB) fetch(jb + DA, ring[jb % DA]);
+        if constexpr (NBUF == 2) {
+            if (jb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
+                commit(jb + 1, ring[(jb + 1) % DA], True{}, False{});
+                if (jb + 1 + DA < S::NJB) fetch(jb + 1 + DA, ring[(jb + 1) % DA]);
+            }
+        } else {
+            if constexpr (S::NJB == 1) commit(jb, ring[0], True{}, True{});   // one block: keep B^ for the outputs
+            else commit(jb, ring[jb % DA], True{}, False{});
+            __syncthreads();
+            if (jb + DA < S::NJB) fetch(jb + DA, ring[jb % DA]);
+        }
+        const T *sBt = s_BtS + (jb % NBUF) * kBtS, *sX = s_X + (jb % NBUF) * kSX;
 #pragma unroll
         for (int m2 = 0; m2 < PTW; ++m2) {
             const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
@@ -260,8 +286,8 @@ void k_scan_fused(ScanArgs a) {
                 const int nt = ntl + 4 * half;
 #pragma unroll
                 for (int ks = 0; ks < JK; ++ks) {
-                    const Frag af = MM::load(&s_BtS[(nt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
-                    const Frag bf = MM::load(&s_X[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    const Frag af = MM::load(&sBt[(nt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    const Frag bf = MM::load(&sX[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
                     ms[m2][half] = MM::mma(af, bf, ms[m2][half]);
                 }
             }
@@ -547,12 +573,10 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
-        const T *src = Cg + t * bstr + r * N;
+        const T *src = Cg + min(t, nvalid - 1) * bstr + r * N;
+        const bool ok = t < nvalid;   // rows past the end of the sequence are zeroed
 #pragma unroll
-        for (int kk = 0; kk < NK; ++kk) {
-            if (t < nvalid) cf[m][kk] = MM::load(src + kk * MM::K + MM::KPL * g);
-            else cf[m][kk] = Frag{};
-        }
+        for (int kk = 0; kk < NK; ++kk) cf[m][kk] = MM::load(src + kk * MM::K + MM::KPL * g);
 #pragma unroll
         for (int kk = 0; kk < NK / 2; ++kk) {
 #pragma unroll
@@ -560,13 +584,19 @@ void k_scan_fused(ScanArgs a) {
                 const int n = kk * MM::K + MM::KPL * g + e;
                 float cs, sn;
                 cs_get(s_cs[n * LDC + t], cs, sn);
-                const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
+                const float u = ok ? fget(cf[m][kk], e) : 0.f, w = ok ? fget(cf[m][kk + NK / 2], e) : 0.f;
                 fset(cf[m][kk], e, cs * u + sn * w);
                 fset(cf[m][kk + NK / 2], e, cs * w - sn * u);
             }
         }
     }
-    __syncthreads();   // s_S complete
+    // longer chunks restage their blocks: the first one now (double-buffered
+    // with the (B^ W)^T area, which holds S_in^T and is not written here)
+    if constexpr (NBUF == 2) {
+        commit(0, ring[0], False{}, True{});
+        if (DC < S::NJB) fetch(DC, ring[0]);
+    }
+    __syncthreads();   // s_S and the first block complete
     // inter-chunk term e^{cum_t} C^_t . S_in starts the accumulators
     f32x4 acc[TPW][PT];
 #pragma unroll
@@ -590,11 +620,17 @@ void k_scan_fused(ScanArgs a) {
     const float Dh = a.D[h];
 #pragma unroll
     for (int jb = 0; jb < S::NJB; ++jb) {
-        if constexpr (S::NJB > 1) {
+        if constexpr (NBUF == 2) {
+            if (jb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
+                commit(jb + 1, ring[(jb + 1) % DC], False{}, True{});
+                if (jb + 1 + DC < S::NJB) fetch(jb + 1 + DC, ring[(jb + 1) % DC]);
+            }
+        } else if constexpr (S::NJB > 1) {
             commit(jb, ring[jb % DC], False{}, True{});
             __syncthreads();
             if (jb + DC < S::NJB) fetch(jb + DC, ring[jb % DC]);
         }
+        const T *sB = s_B + (jb % NBUF) * kSB, *sX = s_X + (jb % NBUF) * kSX;
 #pragma unroll
         for (int jp = 0; jp < S::JB / 32; ++jp) {
             const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
@@ -604,7 +640,7 @@ void k_scan_fused(ScanArgs a) {
             if constexpr (MM::KPL == 8) {
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) {
-                    const T *xr = &s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
+                    const T *xr = &sX[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
                     const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
                     const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
 #pragma unroll
@@ -620,7 +656,7 @@ void k_scan_fused(ScanArgs a) {
             for (int q = 0; q < 2; ++q)
 #pragma unroll
                 for (int kk = 0; kk < NK; ++kk) {
-                    const Frag bf = MM::load(&s_B[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
+                    const Frag bf = MM::load(&sB[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
 #pragma unroll
                     for (int m = 0; m < TPW; ++m)
                         if (J0 + q <= owned_tile<S>(wave, m)) gt[m][q] = MM::mma(bf, cf[m][kk], gt[m][q]);
@@ -668,7 +704,7 @@ void k_scan_fused(ScanArgs a) {
                         for (int v = 0; v < 4; ++v)
 #pragma unroll
                             for (int pt = 0; pt < PT; ++pt) {
-                                const float xv = to_f32(s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
+                                const float xv = to_f32(sX[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
                                 acc[m][pt] = MM::mma(gt[m][q][v], xv, acc[m][pt]);
                             }
                 }

@@ -44,7 +44,8 @@ namespace {
 using namespace scan;
 
 // Eight waves per workgroup: all of them stage row blocks and carry the
-// state; the first NWO of them own the output row tiles.
+// state; output row tiles are owned by NWO waves each, or, when a chunk has
+// fewer row tiles than waves, by NSP waves each (one share of the columns).
 template <typename T, int Q, int R>
 using SegShape = FShape<T, Q, R, 8>;
 
@@ -63,6 +64,9 @@ void k_scan_seg(ScanArgs a) {
     constexpr int PT = P / 16;
     constexpr int LDC = Q + 1;          // cos/sin table [pair][token], padded
     constexpr int NJB = S::NJB;
+    constexpr int NSP = S::NW / S::NWO;  // waves sharing a row tile (column split)
+    constexpr int PTS = PT / NSP;       // 16-column tiles of y per wave
+    static_assert(NSP * S::NWO == S::NW && PTS * NSP == PT, "column split");
     constexpr int kMaps = 2;            // look-back maps loaded per round trip
 
     __shared__ Acc s_cum[Q];
@@ -86,7 +90,9 @@ void k_scan_seg(ScanArgs a) {
     int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // uniform: scalar branches
     int g = lane >> 4, l16 = lane & 15;
-    const bool ow = wave < S::NWO;   // owns output row tiles (uniform)
+    const bool ow = true;                      // every wave owns output tiles
+    const int wt = wave % S::NWO;              // row-tile owner index (uniform)
+    const int pofs = (wave / S::NWO) * PTS;    // first owned column tile (uniform)
     auto relane = [&]() {
         asm volatile("" : "+v"(tid));
         lane = tid & (kWave - 1);
@@ -634,7 +640,7 @@ void k_scan_seg(ScanArgs a) {
         const T *Cg = Cs + tk * (R * N);
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
-            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
+            const int row = owned_tile<S>(wt, m) * 16 + l16, t = row / R, r = row % R;
             const T *src = Cg + min(t, nv - 1) * bstr + r * N;
 #pragma unroll
             for (int kk = 0; kk < NK; ++kk) cf[m][kk] = MM::load(src + kk * MM::K + MM::KPL * g);
@@ -665,7 +671,7 @@ void k_scan_seg(ScanArgs a) {
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
             if (!ow) break;
-            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R;
+            const int row = owned_tile<S>(wt, m) * 16 + l16, t = row / R;
             const bool ok = t < nv;
 #pragma unroll
             for (int kk = 0; kk < NK / 2; ++kk) {
@@ -693,20 +699,20 @@ void k_scan_seg(ScanArgs a) {
         }
         __syncthreads();
         // inter-chunk term e^{cum_t} C^_t . S starts the accumulators
-        f32x4 acc[TPW][PT];
+        f32x4 acc[TPW][PTS];
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
             if (!ow) break;
-            const int TT = owned_tile<S>(wave, m);
+            const int TT = owned_tile<S>(wt, m);
             float ecum[4];
 #pragma unroll
             for (int v = 0; v < 4; ++v) ecum[v] = (float)exp_fast(s_cum[(TT * 16 + 4 * g + v) / R]);
 #pragma unroll
-            for (int pt = 0; pt < PT; ++pt) {
+            for (int pt = 0; pt < PTS; ++pt) {
                 f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kk = 0; kk < NK; ++kk)
-                    tmp = MM::mma(cf[m][kk], MM::load(&s_S[(pt * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), tmp);
+                    tmp = MM::mma(cf[m][kk], MM::load(&s_S[((pofs + pt) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), tmp);
 #pragma unroll
                 for (int v = 0; v < 4; ++v) tmp[v] *= ecum[v];
                 acc[m][pt] = tmp;
@@ -738,13 +744,13 @@ void k_scan_seg(ScanArgs a) {
             for (int jp = 0; jp < S::JB / 32; ++jp) {
                 const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
                 if (!ow) break;
-                if (J0 > owned_tile<S>(wave, TPW - 1) && J0 > owned_tile<S>(wave, 0)) continue;
+                if (J0 > owned_tile<S>(wt, TPW - 1) && J0 > owned_tile<S>(wt, 0)) continue;
                 // x^T columns of the pair, shared by all owned tiles
-                bf16x8 xf[PT];
+                bf16x8 xf[PTS];
                 if constexpr (MM::KPL == 8) {
 #pragma unroll
-                    for (int pt = 0; pt < PT; ++pt) {
-                        const T *xr = &s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
+                    for (int pt = 0; pt < PTS; ++pt) {
+                        const T *xr = &s_X[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
                         const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
                         const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
 #pragma unroll
@@ -762,13 +768,13 @@ void k_scan_seg(ScanArgs a) {
                         const Frag bfr = MM::load(&s_B[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
 #pragma unroll
                         for (int m = 0; m < TPW; ++m)
-                            if (J0 + q <= owned_tile<S>(wave, m)) gt[m][q] = MM::mma(bfr, cf[m][kk], gt[m][q]);
+                            if (J0 + q <= owned_tile<S>(wt, m)) gt[m][q] = MM::mma(bfr, cf[m][kk], gt[m][q]);
                     }
                 // mask weights (branch-free): w_tj = e^{cum_t - cum_j} sigma_j (j < t),
                 // gamma_t (j = t), 0 (j > t); D x_t as D on the diagonal row = column
 #pragma unroll
                 for (int m = 0; m < TPW; ++m) {
-                    const int TT = owned_tile<S>(wave, m);
+                    const int TT = owned_tile<S>(wt, m);
                     if (J0 > TT) continue;
                     const int tt = (TT * 16 + l16) / R;
                     const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
@@ -798,15 +804,15 @@ void k_scan_seg(ScanArgs a) {
                             af[4 + v] = (bf16)gt[m][1][v];
                         }
 #pragma unroll
-                        for (int pt = 0; pt < PT; ++pt) acc[m][pt] = MM::mma(af, xf[pt], acc[m][pt]);
+                        for (int pt = 0; pt < PTS; ++pt) acc[m][pt] = MM::mma(af, xf[pt], acc[m][pt]);
                     } else {
 #pragma unroll
                         for (int q = 0; q < 2; ++q)
 #pragma unroll
                             for (int v = 0; v < 4; ++v)
 #pragma unroll
-                                for (int pt = 0; pt < PT; ++pt) {
-                                    const float xv = to_f32(s_X[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
+                                for (int pt = 0; pt < PTS; ++pt) {
+                                    const float xv = to_f32(s_X[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
                                     acc[m][pt] = MM::mma(gt[m][q][v], xv, acc[m][pt]);
                                 }
                     }
@@ -824,23 +830,24 @@ void k_scan_seg(ScanArgs a) {
             rotate_psie(ms, Sst);
             if (c == a.nchunks - 1) write_final(Sst);
         }
-        // store: each wave stages one 16-row tile at a time in LDS and writes
-        // whole 16-byte pieces of the y rows
-        T *s_y = s_B + wave * (16 * P);
+        // store: the waves of a row tile stage their columns of it in LDS, then
+        // write whole 16-byte pieces of the y rows
+        T *s_y = s_B + wt * (16 * P);
         T *Yg = static_cast<T *>(a.y) + tk * (R * P);
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
-            const int TT = owned_tile<S>(wave, m);
+            const int TT = owned_tile<S>(wt, m);
             if (ow) {
 #pragma unroll
-                for (int pt = 0; pt < PT; ++pt)
+                for (int pt = 0; pt < PTS; ++pt)
 #pragma unroll
-                    for (int v = 0; v < 4; ++v) s_y[(4 * g + v) * P + pt * 16 + l16] = from_f32<T>(acc[m][pt][v]);
+                    for (int v = 0; v < 4; ++v)
+                        s_y[(4 * g + v) * P + (pofs + pt) * 16 + l16] = from_f32<T>(acc[m][pt][v]);
             }
             __syncthreads();
             constexpr int PIECES = 16 * P / S::CE;
 #pragma unroll
-            for (int k = lane; k < PIECES; k += kWave) {
+            for (int k = lane + (wave / S::NWO) * kWave; k < PIECES; k += NSP * kWave) {
                 if (!ow) break;
                 const int rl = k / (P / S::CE), col = (k % (P / S::CE)) * S::CE;
                 const int row = TT * 16 + rl, t = row / R, r = row % R;
@@ -880,6 +887,10 @@ hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
                                           cap_cache);
         if (cap <= 0) return hipErrorInvalidDevice;
         G = (nsl * a.nchunks + cap - 1) / cap;
+        // Short chunks (fewer than 128 rows) split over several segments run
+        // faster one chunk per workgroup: the aggregate pass and the per-chunk
+        // fixed costs of a segment then outweigh what it saves.
+        if (G < a.nchunks && S::QR < 128 && a.per_chunk) return a.per_chunk(a0, stream);
     }
     G = G < 1 ? 1 : (G > a.nchunks ? a.nchunks : G);
     a.G = G;
