@@ -18,16 +18,27 @@
 namespace m3 {
 namespace {
 
-template <typename T, int N, int P, int R>
-__global__ __launch_bounds__(kBlock) void k_step(StepArgs a) {
+// 16-byte piece of the io dtype
+template <typename T> struct Vec8;
+template <> struct Vec8<bf16> { typedef bf16x8 type; static constexpr int n = 8; };
+template <> struct Vec8<float> { typedef f32x4 type; static constexpr int n = 4; };
+
+template <typename T, int N, int P, int R, int NT>
+__global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     constexpr int NH = N / 2;
     constexpr int TX = P / 4;                   // threads across columns (float4 each)
-    constexpr int TY = kBlock / TX;             // thread rows
+    constexpr int TY = NT / TX;                 // thread rows
     constexpr int NPT = (NH + TY - 1) / TY;     // row pairs per thread
-    constexpr int NW = kBlock / kWave;
-    static_assert(P % 4 == 0 && kBlock % TX == 0 && kWave % TX == 0, "column split");
+    constexpr int NW = NT / kWave;
+    static_assert(P % 4 == 0 && NT % TX == 0 && kWave % TX == 0 && NT % kWave == 0, "column split");
+    static_assert(NH <= NT, "one thread per rotation angle");
 
-    __shared__ float s_B[R * N], s_Bp[R * N], s_C[R * N];
+    // Per-slice vectors in LDS (fp32), rank innermost so that one 16-byte read
+    // fetches all ranks of a state row; the step's scalars are folded in:
+    // s_Bp = beta' B_{t-1}, s_B = gamma B_t, s_cs = alpha (cos, sin).
+    constexpr int RV = R == 1 ? 1 : (R == 2 ? 2 : 4);   // ranks per vector read
+    static_assert(R % RV == 0, "rank vectors");
+    __shared__ __attribute__((aligned(16))) float s_B[N * R], s_Bp[N * R], s_C[N * R];
     __shared__ float s_X[R * P], s_Xp[R * P];
     __shared__ float s_cs[NH], s_sn[NH];
     __shared__ float s_red[NW * R * P];
@@ -37,7 +48,39 @@ __global__ __launch_bounds__(kBlock) void k_step(StepArgs a) {
     const int tid = threadIdx.x, tx = tid % TX, ty = tid / TX;
     const int lane = tid & (kWave - 1), wave = tid / kWave;
 
-    // 1. issue the state loads first: they are the bytes that matter
+    // per-slice vectors into LDS
+    const T *Bt = static_cast<const T *>(a.B) + bh * (R * N);
+    const T *Ct = static_cast<const T *>(a.C) + bh * (R * N);
+    const T *Xt = static_cast<const T *>(a.x) + bh * (R * P);
+    T *cB = static_cast<T *>(a.cB) + bh * (R * N);
+    T *cX = static_cast<T *>(a.cX) + bh * (R * P);
+    const float dtv = a.dt[bh], lamv = a.lam[bh], Av = a.A[b * a.a_sb + h * a.a_sh];
+    // B_t, C_t, the carry and X in 16-byte pieces; the loaded B_t and X_t
+    // pieces are also the new carry (written after the barrier below)
+    typedef typename Vec8<T>::type V8;
+    constexpr int VE = Vec8<T>::n;                      // elements per piece
+    constexpr int PB = R * N / VE, PX = R * P / VE;     // pieces per vector
+    constexpr int TPB = (PB + NT - 1) / NT, TPX = (PX + NT - 1) / NT;
+    // The small per-slice loads go out before the state loads (memory
+    // counters retire in order), so their LDS staging overlaps the state's
+    // flight time.
+    V8 vb[TPB], vc[TPB], vbp[TPB], vx[TPX], vxp[TPX];
+#pragma unroll
+    for (int k = 0; k < TPB; ++k) {
+        const int pc = min(tid + k * NT, PB - 1);
+        vb[k] = *reinterpret_cast<const V8 *>(Bt + pc * VE);
+        vc[k] = *reinterpret_cast<const V8 *>(Ct + pc * VE);
+        vbp[k] = *reinterpret_cast<const V8 *>(cB + pc * VE);
+    }
+#pragma unroll
+    for (int k = 0; k < TPX; ++k) {
+        const int pc = min(tid + k * NT, PX - 1);
+        vx[k] = *reinterpret_cast<const V8 *>(Xt + pc * VE);
+        vxp[k] = *reinterpret_cast<const V8 *>(cX + pc * VE);
+    }
+    const float *th = a.theta + bh * NH;
+    const float thv = th[min(tid, NH - 1)];
+    // 1. the state: the bytes that matter
     float *st = a.state + bh * (int64_t)(N * P);
     float4 re[NPT], im[NPT];
 #pragma unroll
@@ -48,37 +91,49 @@ __global__ __launch_bounds__(kBlock) void k_step(StepArgs a) {
             im[k] = *reinterpret_cast<const float4 *>(&st[(i + NH) * P + 4 * tx]);
         }
     }
-    // 2. per-slice vectors into LDS (fp32)
-    const T *Bt = static_cast<const T *>(a.B) + bh * (R * N);
-    const T *Ct = static_cast<const T *>(a.C) + bh * (R * N);
-    const T *Xt = static_cast<const T *>(a.x) + bh * (R * P);
-    T *cB = static_cast<T *>(a.cB) + bh * (R * N);
-    T *cX = static_cast<T *>(a.cX) + bh * (R * P);
-    for (int e = tid; e < R * N; e += kBlock) {
-        s_B[e] = to_f32(Bt[e]);
-        s_C[e] = to_f32(Ct[e]);
-        s_Bp[e] = to_f32(cB[e]);
-    }
-    for (int e = tid; e < R * P; e += kBlock) {
-        s_X[e] = to_f32(Xt[e]);
-        s_Xp[e] = to_f32(cX[e]);
-    }
-    const float *th = a.theta + bh * NH;
-    for (int i = tid; i < NH; i += kBlock) {
-        float sn, cs;
-        sincosf(th[i], &sn, &cs);
-        s_cs[i] = cs;
-        s_sn[i] = sn;
-    }
-    const float dtv = a.dt[bh], lamv = a.lam[bh];
-    const float alpha = expf(dtv * a.A[b * a.a_sb + h * a.a_sh]);
+    const float alpha = (float)exp_fast((typename AccOf<T>::type)dtv * Av);
     const float bprev = (1.f - lamv) * dtv, gam = lamv * dtv;
+#pragma unroll
+    for (int k = 0; k < TPB; ++k) {
+        const int pc = tid + k * NT;
+        if (pc < PB) {
+#pragma unroll
+            for (int e = 0; e < VE; ++e) {   // element pc*VE + e = r*N + n  ->  [n][r]
+                const int r = (pc * VE + e) / N, n = (pc * VE + e) % N;
+                s_B[n * R + r] = gam * to_f32(vb[k][e]);
+                s_C[n * R + r] = to_f32(vc[k][e]);
+                s_Bp[n * R + r] = bprev * to_f32(vbp[k][e]);
+            }
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < TPX; ++k) {
+        const int pc = tid + k * NT;
+        if (pc < PX) {
+#pragma unroll
+            for (int e = 0; e < VE; ++e) {
+                s_X[pc * VE + e] = to_f32(vx[k][e]);
+                s_Xp[pc * VE + e] = to_f32(vxp[k][e]);
+            }
+        }
+    }
+    if (tid < NH) {
+        typename AccOf<T>::type sn, cs;   // hardware sin/cos for the bf16 build, accurate for fp32
+        sincos_fast((typename AccOf<T>::type)thv, &sn, &cs);
+        s_cs[tid] = alpha * (float)cs;
+        s_sn[tid] = alpha * (float)sn;
+    }
     __syncthreads();
     // 3. the carry becomes (B_t, X_t)
-    for (int e = tid; e < R * N; e += kBlock) cB[e] = Bt[e];
-    for (int e = tid; e < R * P; e += kBlock) cX[e] = Xt[e];
+#pragma unroll
+    for (int k = 0; k < TPB; ++k)
+        if (tid + k * NT < PB) *reinterpret_cast<V8 *>(cB + (tid + k * NT) * VE) = vb[k];
+#pragma unroll
+    for (int k = 0; k < TPX; ++k)
+        if (tid + k * NT < PX) *reinterpret_cast<V8 *>(cX + (tid + k * NT) * VE) = vx[k];
 
-    // 4. update the owned state elements and accumulate Y partials
+    // 4. update the owned state elements and accumulate Y partials:
+    //    u = h + beta' B_{t-1} X_{t-1}^T,  h' = alpha R(theta) u + gamma B_t X_t^T
     float yp[R][4];
 #pragma unroll
     for (int r = 0; r < R; ++r)
@@ -92,11 +147,32 @@ __global__ __launch_bounds__(kBlock) void k_step(StepArgs a) {
             xp[r][q] = s_Xp[r * P + 4 * tx + q];
             xc[r][q] = s_X[r * P + 4 * tx + q];
         }
+    auto rank_vec = [&](const float *base, float (&v)[R]) {
+#pragma unroll
+        for (int r0 = 0; r0 < R; r0 += RV) {
+            if constexpr (RV == 4) {
+                const float4 t = *reinterpret_cast<const float4 *>(base + r0);
+                v[r0] = t.x; v[r0 + 1] = t.y; v[r0 + 2] = t.z; v[r0 + 3] = t.w;
+            } else if constexpr (RV == 2) {
+                const float2 t = *reinterpret_cast<const float2 *>(base + r0);
+                v[r0] = t.x; v[r0 + 1] = t.y;
+            } else {
+                v[r0] = base[r0];
+            }
+        }
+    };
 #pragma unroll
     for (int k = 0; k < NPT; ++k) {
         const int i = ty + TY * k;
         if (i < NH) {
             const float cs = s_cs[i], sn = s_sn[i];
+            float bp0[R], bp1[R], bc0[R], bc1[R], c0[R], c1[R];
+            rank_vec(&s_Bp[i * R], bp0);
+            rank_vec(&s_Bp[(i + NH) * R], bp1);
+            rank_vec(&s_B[i * R], bc0);
+            rank_vec(&s_B[(i + NH) * R], bc1);
+            rank_vec(&s_C[i * R], c0);
+            rank_vec(&s_C[(i + NH) * R], c1);
             float hr[4] = {re[k].x, re[k].y, re[k].z, re[k].w};
             float hi[4] = {im[k].x, im[k].y, im[k].z, im[k].w};
 #pragma unroll
@@ -104,16 +180,15 @@ __global__ __launch_bounds__(kBlock) void k_step(StepArgs a) {
                 float ur = hr[q], ui = hi[q], vr = 0.f, vi = 0.f;
 #pragma unroll
                 for (int r = 0; r < R; ++r) {
-                    ur += bprev * s_Bp[r * N + i] * xp[r][q];
-                    ui += bprev * s_Bp[r * N + i + NH] * xp[r][q];
-                    vr += s_B[r * N + i] * xc[r][q];
-                    vi += s_B[r * N + i + NH] * xc[r][q];
+                    ur = fmaf(bp0[r], xp[r][q], ur);
+                    ui = fmaf(bp1[r], xp[r][q], ui);
+                    vr = fmaf(bc0[r], xc[r][q], vr);
+                    vi = fmaf(bc1[r], xc[r][q], vi);
                 }
-                hr[q] = alpha * (cs * ur - sn * ui) + gam * vr;
-                hi[q] = alpha * (sn * ur + cs * ui) + gam * vi;
+                hr[q] = fmaf(cs, ur, fmaf(-sn, ui, vr));
+                hi[q] = fmaf(sn, ur, fmaf(cs, ui, vi));
 #pragma unroll
-                for (int r = 0; r < R; ++r)
-                    yp[r][q] += hr[q] * s_C[r * N + i] + hi[q] * s_C[r * N + i + NH];
+                for (int r = 0; r < R; ++r) yp[r][q] = fmaf(hr[q], c0[r], fmaf(hi[q], c1[r], yp[r][q]));
             }
             *reinterpret_cast<float4 *>(&st[i * P + 4 * tx]) = make_float4(hr[0], hr[1], hr[2], hr[3]);
             *reinterpret_cast<float4 *>(&st[(i + NH) * P + 4 * tx]) = make_float4(hi[0], hi[1], hi[2], hi[3]);
@@ -138,7 +213,7 @@ __global__ __launch_bounds__(kBlock) void k_step(StepArgs a) {
     __syncthreads();
     T *yt = static_cast<T *>(a.y) + bh * (R * P);
     const float Dh = a.D[h];
-    for (int e = tid; e < R * P; e += kBlock) {
+    for (int e = tid; e < R * P; e += NT) {
         float v = 0.f;
 #pragma unroll
         for (int w = 0; w < NW; ++w) v += s_red[w * R * P + e];
@@ -146,9 +221,14 @@ __global__ __launch_bounds__(kBlock) void k_step(StepArgs a) {
     }
 }
 
+// Threads per (batch, head): four waves for the 128 x 64 state (fewer
+// threads per slice measured slower: longer per-thread update chains).
+template <int N, int P> struct StepThreads { static constexpr int value = N * P >= 8192 ? 256 : 64; };
+
 template <typename T, int N, int P, int R>
 hipError_t launch_step(const StepArgs &a, hipStream_t stream) {
-    hipLaunchKernelGGL((k_step<T, N, P, R>), dim3((unsigned)(a.batch * a.H)), dim3(kBlock), 0,
+    constexpr int NT = StepThreads<N, P>::value;
+    hipLaunchKernelGGL((k_step<T, N, P, R, NT>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
                        stream, a);
     return hipGetLastError();
 }
