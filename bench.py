@@ -185,10 +185,11 @@ def measured_traffic(key):
     import hashlib
     try:
         rec = json.load(open(os.path.join(ROOT, "profiles", "traffic.json")))[key]
-        src = open(os.path.join(ROOT, rec["source"]), "rb").read()
-    except (OSError, KeyError, ValueError):
+        srcs = rec["sources"]
+        blob = b"".join(open(os.path.join(ROOT, f), "rb").read() for f in srcs)
+    except (OSError, KeyError, ValueError, TypeError):
         return None
-    if hashlib.sha256(src).hexdigest() != rec["src_sha256"]:
+    if hashlib.sha256(blob).hexdigest() != rec["src_sha256"]:
         return None
     return rec["read_bytes"] + rec["write_bytes"]
 

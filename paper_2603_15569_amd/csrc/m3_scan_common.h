@@ -104,5 +104,20 @@ static __global__ void k_reset(uint32_t *ctl, uint32_t *flags, int64_t nflags) {
 constexpr uint32_t kFlagInit = 3;   // probe result for "before the first chunk"
 constexpr int kProbe = 16;          // predecessors probed per look-back round
 
+// Workgroups of one kernel resident on the whole device at once (cached per
+// device in `cache`; 0 on error).
+inline int resident_capacity(const void *fn, int nthr, int *cache) {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
+    int v = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
+    if (v > 0) return v;
+    int ncu = 0, per = 0;
+    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, nthr, 0) != hipSuccess) return 0;
+    v = ncu * (per > 0 ? per : 1);
+    __atomic_store_n(&cache[dev], v, __ATOMIC_RELAXED);
+    return v;
+}
+
 }  // namespace scan
 }  // namespace m3

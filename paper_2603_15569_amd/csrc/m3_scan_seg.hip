@@ -860,21 +860,6 @@ void k_scan_seg(ScanArgs a) {
     }
 }
 
-// Workgroups of one kernel resident on the whole device at once (cached per
-// device).
-int resident_capacity(const void *fn, int nthr, int *cache) {
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 0;
-    int v = __atomic_load_n(&cache[dev], __ATOMIC_RELAXED);
-    if (v > 0) return v;
-    int ncu = 0, per = 0;
-    if (hipDeviceGetAttribute(&ncu, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per, fn, nthr, 0) != hipSuccess) return 0;
-    v = ncu * (per > 0 ? per : 1);
-    __atomic_store_n(&cache[dev], v, __ATOMIC_RELAXED);
-    return v;
-}
-
 template <typename T, int Q, int R>
 hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
     typedef SegShape<T, Q, R> S;
