@@ -75,9 +75,13 @@ void k_scan_seg(ScanArgs a) {
     __shared__ Acc s_segps[NH];         // angle totals of the segment
     __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
     __shared__ CS s_cs[NH * LDC];
-    __shared__ __attribute__((aligned(16))) T s_B[S::JB * S::LDN];   // B^ block [row][n]; S^T [p][n]; y staging
-    __shared__ __attribute__((aligned(16))) T s_X[P * S::LDJ];       // x^T block [p][row]
-    __shared__ __attribute__((aligned(16))) T s_Bt[N * S::LDJ];      // (B^ W)^T block [n][row]
+    // Chunks of several row blocks double-buffer the staged blocks: in the
+    // output pass block jb + 1 is committed while block jb feeds the MFMAs.
+    constexpr int NBUF = (NJB > 1 && sizeof(T) == 2) ? 2 : 1;
+    constexpr int kSB = S::JB * S::LDN, kSX = P * S::LDJ, kSBt = N * S::LDJ;
+    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];    // B^ blocks [row][n]; S^T [p][n]; y staging
+    __shared__ __attribute__((aligned(16))) T s_X[NBUF * kSX];    // x^T blocks [p][row]
+    __shared__ __attribute__((aligned(16))) T s_Bt[NBUF * kSBt];  // (B^ W)^T blocks [n][row]
     __shared__ int s_i[4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);                    // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
@@ -162,6 +166,7 @@ void k_scan_seg(ScanArgs a) {
     };
     int cnv = 0;   // valid tokens of the chunk being committed
     auto commit = [&](int jb, const Blk &f, auto kRow) {
+        T *sB = s_B + (jb % NBUF) * kSB, *sX = s_X + (jb % NBUF) * kSX, *sBt = s_Bt + (jb % NBUF) * kSBt;
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
@@ -180,12 +185,12 @@ void k_scan_seg(ScanArgs a) {
                     fset(lo, e, re);
                     fset(hi, e, im);
                 }
-                s_Bt[n * S::LDJ + jr] = from_f32<T>(wt * re);
-                s_Bt[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
+                sBt[n * S::LDJ + jr] = from_f32<T>(wt * re);
+                sBt[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
             }
             if constexpr (decltype(kRow)::value) {
-                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + cp * S::CE]) = lo;
-                *reinterpret_cast<V16 *>(&s_B[jr * S::LDN + NH + cp * S::CE]) = hi;
+                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
+                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
             }
         }
 #pragma unroll
@@ -194,11 +199,12 @@ void k_scan_seg(ScanArgs a) {
             const bool ok = (jb * S::JB + jr) / R < cnv;
 #pragma unroll
             for (int e = 0; e < S::CE; ++e)
-                s_X[(pc * S::CE + e) * S::LDJ + jr] = ok ? f.xv[k][e] : from_f32<T>(0.f);
+                sX[(pc * S::CE + e) * S::LDJ + jr] = ok ? f.xv[k][e] : from_f32<T>(0.f);
         }
     };
     // M += (B^ W)^T x over one staged block (owned state pair-tiles)
-    auto m_block = [&](f32x4 (&ms)[PTW][2]) {
+    auto m_block = [&](f32x4 (&ms)[PTW][2], int jb) {
+        const T *sBt = s_Bt + (jb % NBUF) * kSBt, *sX = s_X + (jb % NBUF) * kSX;
 #pragma unroll
         for (int m2 = 0; m2 < PTW; ++m2) {
             const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
@@ -207,8 +213,8 @@ void k_scan_seg(ScanArgs a) {
                 const int nt = ntl + 4 * half;
 #pragma unroll
                 for (int ks = 0; ks < JK; ++ks) {
-                    const Frag af = MM::load(&s_Bt[(nt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
-                    const Frag bf = MM::load(&s_X[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    const Frag af = MM::load(&sBt[(nt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                    const Frag bf = MM::load(&sX[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
                     ms[m2][half] = MM::mma(af, bf, ms[m2][half]);
                 }
             }
@@ -411,7 +417,7 @@ void k_scan_seg(ScanArgs a) {
                     fetch(min(c + jn / NJB, cend - 1), jn % NJB, ring[jb % DA]);
                     sched_fence();
                 }
-                m_block(ms);
+                m_block(ms, jb);
                 __syncthreads();
             }
             const Acc cum_e = s_cum[nvalid_of(c) - 1];
@@ -686,8 +692,8 @@ void k_scan_seg(ScanArgs a) {
                 }
             }
         }
-        // S^T in the io dtype (B^ block) for the inter-chunk term
-        T *s_S = s_B;
+        // S^T in the io dtype (the last B^ buffer) for the inter-chunk term
+        T *s_S = s_B + (NBUF - 1) * kSB;
 #pragma unroll
         for (int m2 = 0; m2 < PTW; ++m2) {
             const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
@@ -696,6 +702,12 @@ void k_scan_seg(ScanArgs a) {
 #pragma unroll
                 for (int v = 0; v < 4; ++v)
                     s_S[(pt * 16 + l16) * S::LDN + 16 * (ntl + 4 * half) + 4 * g + v] = from_f32<T>(Sst[m2][half][v]);
+        }
+        if constexpr (NBUF == 2) {   // the first block stages beside S^T
+            commit(0, ring[0], True{});
+            sched_fence();
+            fetch(min(c + 1 / NJB, cend - 1), 1 % NJB, ring[0]);
+            sched_fence();
         }
         __syncthreads();
         // inter-chunk term e^{cum_t} C^_t . S starts the accumulators
@@ -732,14 +744,23 @@ void k_scan_seg(ScanArgs a) {
         }
 #pragma unroll
         for (int jb = 0; jb < NJB; ++jb) {
-            commit(jb, ring[jb % DC], True{});
-            __syncthreads();
-            {
+            if constexpr (NBUF == 2) {   // stage the next block while this one feeds the MFMAs
+                if (jb + 1 < NJB) {
+                    commit(jb + 1, ring[0], True{});
+                    const int jn = jb + 2;
+                    sched_fence();
+                    fetch(min(c + jn / NJB, cend - 1), jn % NJB, ring[0]);
+                    sched_fence();
+                }
+            } else {
+                commit(jb, ring[jb % DC], True{});
+                __syncthreads();
                 const int jn = jb + DC;
                 sched_fence();
                 fetch(min(c + jn / NJB, cend - 1), jn % NJB, ring[jb % DC]);
                 sched_fence();
             }
+            const T *sBc = s_B + (jb % NBUF) * kSB, *sXc = s_X + (jb % NBUF) * kSX;
 #pragma unroll
             for (int jp = 0; jp < S::JB / 32; ++jp) {
                 const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
@@ -750,7 +771,7 @@ void k_scan_seg(ScanArgs a) {
                 if constexpr (MM::KPL == 8) {
 #pragma unroll
                     for (int pt = 0; pt < PTS; ++pt) {
-                        const T *xr = &s_X[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
+                        const T *xr = &sXc[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
                         const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
                         const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
 #pragma unroll
@@ -765,7 +786,7 @@ void k_scan_seg(ScanArgs a) {
                 for (int q = 0; q < 2; ++q)
 #pragma unroll
                     for (int kk = 0; kk < NK; ++kk) {
-                        const Frag bfr = MM::load(&s_B[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
+                        const Frag bfr = MM::load(&sBc[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
 #pragma unroll
                         for (int m = 0; m < TPW; ++m)
                             if (J0 + q <= owned_tile<S>(wt, m)) gt[m][q] = MM::mma(bfr, cf[m][kk], gt[m][q]);
@@ -812,7 +833,7 @@ void k_scan_seg(ScanArgs a) {
                             for (int v = 0; v < 4; ++v)
 #pragma unroll
                                 for (int pt = 0; pt < PTS; ++pt) {
-                                    const float xv = to_f32(s_X[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
+                                    const float xv = to_f32(sXc[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
                                     acc[m][pt] = MM::mma(gt[m][q][v], xv, acc[m][pt]);
                                 }
                     }
@@ -820,7 +841,7 @@ void k_scan_seg(ScanArgs a) {
             }
             // M of this block for the state, once the G^T operands are dead
             __builtin_amdgcn_sched_barrier(0);
-            if (chain) m_block(ms);
+            if (chain) m_block(ms, jb);
             __syncthreads();   // staged block read: the next commit may overwrite it
         }
         sched_fence();
