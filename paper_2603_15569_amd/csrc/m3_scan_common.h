@@ -34,6 +34,16 @@ __device__ __forceinline__ void fset(f32x4 &v, int e, float x) { v[e] = x; }
 // cache-wide write-back or invalidate is needed.  A publisher waits until its
 // stores are acknowledged (vmcnt(0)) before the flag store; a reader issues
 // its data loads only after it has seen the flag.
+// Four consecutive output columns of one row, held by one lane of a
+// transposed MFMA tile (the lane's four accumulator rows are y columns).
+__device__ __forceinline__ void store4(bf16 *dst, const f32x4 &v) {
+    bf16x4 o;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) o[e] = (bf16)v[e];
+    *reinterpret_cast<bf16x4 *>(dst) = o;
+}
+__device__ __forceinline__ void store4(float *dst, const f32x4 &v) { *reinterpret_cast<f32x4 *>(dst) = v; }
+
 __device__ __forceinline__ void wait_stores_done() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 __device__ __forceinline__ void st_coh2(unsigned long long *p, float x, float y) {

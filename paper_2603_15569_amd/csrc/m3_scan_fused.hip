@@ -30,7 +30,8 @@
 //   5. outputs: C^ rows rotated straight into MFMA fragments; y starts as
 //      e^{cum_t} C^ S_in (MFMA, K = N); per block at or below each owned tile
 //      G^T = B^ C^T (MFMA, K = N) masked by w_tj, y += (w o G) x (MFMA,
-//      K = rows); D x added; y stored.  A chunk of a single 64-row block
+//      K = rows); D x added; y staged per wave from the (transposed)
+//      accumulator tiles and stored.  A chunk of a single 64-row block
 //      stages B^ once for both uses; longer chunks restage it from cache.
 // A tiny reset kernel clears the ticket counter and the flags first.
 #include <type_traits>
@@ -77,7 +78,7 @@ void k_scan_fused(ScanArgs a) {
     __shared__ int s_i[4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
-    static_assert(NW * 16 * P <= S::JB * S::LDN, "y staging fits in the B^ block");
+    static_assert(P <= S::JB && NW * 16 <= N, "y staging fits in the (B^ W)^T buffer");
 
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // uniform: scalar branches
@@ -597,22 +598,22 @@ void k_scan_fused(ScanArgs a) {
         if (DC < S::NJB) fetch(DC, ring[0]);
     }
     __syncthreads();   // s_S and the first block complete
-    // inter-chunk term e^{cum_t} C^_t . S_in starts the accumulators
+    // inter-chunk term e^{cum_t} C^_t . S_in starts the accumulators.  The
+    // output tiles are transposed (y^T = S^T C^T, y^T += x^T (w o G)^T): lane
+    // l holds row l % 16 of a tile and four consecutive columns.
     f32x4 acc[TPW][PT];
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int TT = owned_tile<S>(wave, m);
-        float ecum[4];   // e^{cum_t} of the lane's accumulator rows 4g+v
-#pragma unroll
-        for (int v = 0; v < 4; ++v) ecum[v] = (float)exp_fast(s_cum[(TT * 16 + 4 * g + v) / R]);
+        const float ecum = (float)exp_fast(s_cum[(TT * 16 + l16) / R]);
 #pragma unroll
         for (int pt = 0; pt < PT; ++pt) {
             f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
             for (int kk = 0; kk < NK; ++kk)
-                tmp = MM::mma(cf[m][kk], MM::load(&s_S[(pt * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), tmp);
+                tmp = MM::mma(MM::load(&s_S[(pt * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), cf[m][kk], tmp);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) tmp[v] *= ecum[v];
+            for (int v = 0; v < 4; ++v) tmp[v] *= ecum;
             acc[m][pt] = tmp;
         }
     }
@@ -687,7 +688,7 @@ void k_scan_fused(ScanArgs a) {
                         for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
                     }
                 }
-                // y += (w o G) x  (K = the pair's 32 rows)
+                // y^T += x^T (w o G)^T  (K = the pair's 32 rows)
                 if constexpr (MM::KPL == 8) {
                     bf16x8 af;
 #pragma unroll
@@ -696,7 +697,7 @@ void k_scan_fused(ScanArgs a) {
                         af[4 + v] = (bf16)gt[m][1][v];
                     }
 #pragma unroll
-                    for (int pt = 0; pt < PT; ++pt) acc[m][pt] = MM::mma(af, xf[pt], acc[m][pt]);
+                    for (int pt = 0; pt < PT; ++pt) acc[m][pt] = MM::mma(xf[pt], af, acc[m][pt]);
                 } else {
 #pragma unroll
                     for (int q = 0; q < 2; ++q)
@@ -705,36 +706,36 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
                             for (int pt = 0; pt < PT; ++pt) {
                                 const float xv = to_f32(sX[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
-                                acc[m][pt] = MM::mma(gt[m][q][v], xv, acc[m][pt]);
+                                acc[m][pt] = MM::mma(xv, gt[m][q][v], acc[m][pt]);
                             }
                 }
             }
         }
         if constexpr (S::NJB > 1) __syncthreads();
     }
-    // store: each wave stages one 16-row tile at a time in LDS (the B^ block
-    // is free now) and writes whole 16-byte pieces of the y rows
+    // store: once every wave is past its last LDS read, each wave stages its
+    // tiles in its own part of the (B^ W)^T buffer (a wave's LDS accesses
+    // execute in order: no further barrier) and writes whole 16-byte pieces
+    // of the y rows
     __syncthreads();
-    T *s_y = s_B + wave * (16 * P);
+    T *s_y = s_BtS + wave * (16 * S::LDJ);
     T *Yg = static_cast<T *>(a.y) + tok0 * (R * P);
+    constexpr int RP = P / S::CE;                   // 16-byte pieces of a row
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int TT = owned_tile<S>(wave, m);
 #pragma unroll
-        for (int pt = 0; pt < PT; ++pt)
+        for (int pt = 0; pt < PT; ++pt) store4(&s_y[l16 * S::LDJ + pt * 16 + 4 * g], acc[m][pt]);
+        asm volatile("" ::: "memory");
 #pragma unroll
-            for (int v = 0; v < 4; ++v) s_y[(4 * g + v) * P + pt * 16 + l16] = from_f32<T>(acc[m][pt][v]);
-        __syncthreads();
-        constexpr int PIECES = 16 * P / S::CE;          // 16-byte pieces in the tile
-#pragma unroll
-        for (int k = lane; k < PIECES; k += kWave) {
-            const int rl = k / (P / S::CE), col = (k % (P / S::CE)) * S::CE;
+        for (int k = lane; k < 16 * RP; k += kWave) {
+            const int rl = k / RP, col = (k % RP) * S::CE;
             const int row = TT * 16 + rl, t = row / R, r = row % R;
             if (t < nvalid)
                 *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) =
-                    *reinterpret_cast<const V16 *>(&s_y[rl * P + col]);
+                    *reinterpret_cast<const V16 *>(&s_y[rl * S::LDJ + col]);
         }
-        __syncthreads();
+        asm volatile("" ::: "memory");
     }
 }
 

@@ -79,14 +79,14 @@ void k_scan_seg(ScanArgs a) {
     // output pass block jb + 1 is committed while block jb feeds the MFMAs.
     constexpr int NBUF = (NJB > 1 && sizeof(T) == 2) ? 2 : 1;
     constexpr int kSB = S::JB * S::LDN, kSX = P * S::LDJ, kSBt = N * S::LDJ;
-    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];    // B^ blocks [row][n]; S^T [p][n]; y staging
+    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];    // B^ blocks [row][n]; S^T [p][n]
     __shared__ __attribute__((aligned(16))) T s_X[NBUF * kSX];    // x^T blocks [p][row]
     __shared__ __attribute__((aligned(16))) T s_Bt[NBUF * kSBt];  // (B^ W)^T blocks [n][row]
     __shared__ int s_i[4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);                    // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
     static_assert(P == S::JB, "S^T [p][n] fits in the B^ block");
-    static_assert(NW * 16 * P <= S::JB * S::LDN, "y staging fits in the B^ block");
+    static_assert(NW * 16 <= NBUF * N, "y staging fits in the (B^ W)^T buffer");
 
     // Lane indices are re-derived from an opaque copy of the thread index at
     // the top of every chunk iteration (relane), so that the compiler
@@ -710,23 +710,23 @@ void k_scan_seg(ScanArgs a) {
             sched_fence();
         }
         __syncthreads();
-        // inter-chunk term e^{cum_t} C^_t . S starts the accumulators
+        // inter-chunk term e^{cum_t} C^_t . S starts the accumulators.  The
+        // output tiles are transposed (y^T = S^T C^T, y^T += x^T (w o G)^T):
+        // lane l holds row l % 16 of a tile and four consecutive columns.
         f32x4 acc[TPW][PTS];
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
             if (!ow) break;
             const int TT = owned_tile<S>(wt, m);
-            float ecum[4];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) ecum[v] = (float)exp_fast(s_cum[(TT * 16 + 4 * g + v) / R]);
+            const float ecum = (float)exp_fast(s_cum[(TT * 16 + l16) / R]);
 #pragma unroll
             for (int pt = 0; pt < PTS; ++pt) {
                 f32x4 tmp = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                 for (int kk = 0; kk < NK; ++kk)
-                    tmp = MM::mma(cf[m][kk], MM::load(&s_S[((pofs + pt) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), tmp);
+                    tmp = MM::mma(MM::load(&s_S[((pofs + pt) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), cf[m][kk], tmp);
 #pragma unroll
-                for (int v = 0; v < 4; ++v) tmp[v] *= ecum[v];
+                for (int v = 0; v < 4; ++v) tmp[v] *= ecum;
                 acc[m][pt] = tmp;
             }
         }
@@ -816,7 +816,7 @@ void k_scan_seg(ScanArgs a) {
                             for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
                         }
                     }
-                    // y += (w o G) x  (K = the pair's 32 rows)
+                    // y^T += x^T (w o G)^T  (K = the pair's 32 rows)
                     if constexpr (MM::KPL == 8) {
                         bf16x8 af;
 #pragma unroll
@@ -825,7 +825,7 @@ void k_scan_seg(ScanArgs a) {
                             af[4 + v] = (bf16)gt[m][1][v];
                         }
 #pragma unroll
-                        for (int pt = 0; pt < PTS; ++pt) acc[m][pt] = MM::mma(af, xf[pt], acc[m][pt]);
+                        for (int pt = 0; pt < PTS; ++pt) acc[m][pt] = MM::mma(xf[pt], af, acc[m][pt]);
                     } else {
 #pragma unroll
                         for (int q = 0; q < 2; ++q)
@@ -834,7 +834,7 @@ void k_scan_seg(ScanArgs a) {
 #pragma unroll
                                 for (int pt = 0; pt < PTS; ++pt) {
                                     const float xv = to_f32(sXc[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
-                                    acc[m][pt] = MM::mma(gt[m][q][v], xv, acc[m][pt]);
+                                    acc[m][pt] = MM::mma(xv, gt[m][q][v], acc[m][pt]);
                                 }
                     }
                 }
@@ -851,32 +851,29 @@ void k_scan_seg(ScanArgs a) {
             rotate_psie(ms, Sst);
             if (c == a.nchunks - 1) write_final(Sst);
         }
-        // store: the waves of a row tile stage their columns of it in LDS, then
-        // write whole 16-byte pieces of the y rows
-        T *s_y = s_B + wt * (16 * P);
+        // store: each wave stages its tiles in its own part of the (B^ W)^T
+        // buffer, free after the last block's barrier (a wave's LDS accesses
+        // execute in order: no barrier), and writes whole 16-byte pieces of
+        // its columns of the y rows
+        T *s_y = s_Bt + wave * (16 * S::LDJ);
         T *Yg = static_cast<T *>(a.y) + tk * (R * P);
+        constexpr int RP = PTS * 16 / S::CE;        // 16-byte pieces of a row per wave
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
+            if (!ow) break;
             const int TT = owned_tile<S>(wt, m);
-            if (ow) {
 #pragma unroll
-                for (int pt = 0; pt < PTS; ++pt)
+            for (int pt = 0; pt < PTS; ++pt) store4(&s_y[l16 * S::LDJ + pt * 16 + 4 * g], acc[m][pt]);
+            asm volatile("" ::: "memory");
 #pragma unroll
-                    for (int v = 0; v < 4; ++v)
-                        s_y[(4 * g + v) * P + (pofs + pt) * 16 + l16] = from_f32<T>(acc[m][pt][v]);
-            }
-            __syncthreads();
-            constexpr int PIECES = 16 * P / S::CE;
-#pragma unroll
-            for (int k = lane + (wave / S::NWO) * kWave; k < PIECES; k += NSP * kWave) {
-                if (!ow) break;
-                const int rl = k / (P / S::CE), col = (k % (P / S::CE)) * S::CE;
+            for (int k = lane; k < 16 * RP; k += kWave) {
+                const int rl = k / RP, col = (k % RP) * S::CE;
                 const int row = TT * 16 + rl, t = row / R, r = row % R;
                 if (t < nv)
-                    *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) =
-                        *reinterpret_cast<const V16 *>(&s_y[rl * P + col]);
+                    *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + pofs * 16 + col) =
+                        *reinterpret_cast<const V16 *>(&s_y[rl * S::LDJ + col]);
             }
-            __syncthreads();
+            asm volatile("" ::: "memory");
         }
     }
 }
