@@ -81,7 +81,10 @@ typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
  * several segments per slice, the one-chunk-per-workgroup kernel runs
  * instead (it is faster there).
  * M3_SCAN_SPLIT: three kernels (chunk states, a state pass over chunks,
- * chunk outputs); the only path for other shapes.
+ * chunk outputs); the only path for other shapes, and for tokens wider than
+ * the single-pass kernels' 32-bit row offsets allow (nheads * rank *
+ * max(dstate, headdim) elements of at least 16 MiB, or a chunk of such
+ * tokens of at least 2 GiB).
  * M3_SCAN_PER_CHUNK: the single-pass kernel with one chunk per workgroup
  * (a look-back across every chunk).  Ignored together with M3_SCAN_SPLIT. */
 #define M3_SCAN_SPLIT 1

@@ -85,7 +85,11 @@ static m3_status check_scan_dims(const m3_dims *d, ScanImpl *impl, int64_t *nchu
     if (!impl->launch) return M3_ERR_UNSUPPORTED;
     // the single-pass kernels serve every shape they are built for, except
     // the empty sequence (handled by the three-kernel path's state kernel)
-    if (nc > 0 && !(d->flags & M3_SCAN_SPLIT)) {
+    // and per-token strides too wide for their 32-bit row offsets (24-bit
+    // stride multiplies, a chunk's rows within 2 GiB)
+    const int64_t tok_bytes = per_tok * (int64_t)io_bytes_of(d->io);
+    const bool narrow = tok_bytes < (INT64_C(1) << 24) && d->chunk * tok_bytes < (INT64_C(1) << 31);
+    if (nc > 0 && !(d->flags & M3_SCAN_SPLIT) && narrow) {
         scan_launch_fn f = nullptr;
         scan_launch_fn pc = find_fused_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
         if (!(d->flags & M3_SCAN_PER_CHUNK)) f = find_seg_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);

@@ -34,6 +34,29 @@ __device__ __forceinline__ void fset(f32x4 &v, int e, float x) { v[e] = x; }
 // cache-wide write-back or invalidate is needed.  A publisher waits until its
 // stores are acknowledged (vmcnt(0)) before the flag store; a reader issues
 // its data loads only after it has seen the flag.
+// Raw buffer resource (stride 0) over `bytes` bytes from `base`: a load at
+// an offset at or past `bytes` returns zeros, so rows past the end of a
+// sequence read as zero without address clamping or masks, and addresses are
+// a scalar base plus a 32-bit per-lane offset.
+typedef __amdgpu_buffer_rsrc_t Rsrc;
+__device__ __forceinline__ Rsrc make_rsrc(const void *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, 0x00020000);
+}
+template <typename V> __device__ __forceinline__ V buf_load(Rsrc r, uint32_t off) {
+    if constexpr (sizeof(V) == 16) {
+        typedef int i32x4 __attribute__((ext_vector_type(4)));
+        return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, 0));
+    } else {
+        static_assert(sizeof(V) == 4, "16- or 4-byte loads");
+        return __builtin_bit_cast(V, __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0));
+    }
+}
+// Offset of token t at a per-token stride below 2^24 bytes (full-rate 24-bit
+// multiply; the library routes larger strides to the three-kernel path).
+__device__ __forceinline__ uint32_t tok_off(int t, uint32_t stride_bytes) {
+    return __umul24((uint32_t)t, stride_bytes);
+}
+
 // Four consecutive output columns of one row, held by one lane of a
 // transposed MFMA tile (the lane's four accumulator rows are y columns).
 __device__ __forceinline__ void store4(bf16 *dst, const f32x4 &v) {

@@ -139,32 +139,33 @@ void k_scan_seg(ScanArgs a) {
     constexpr int TX = S::JB * (P / S::CE) / S::NTHR;    // x tasks per thread
     static_assert(TB * S::NTHR == S::JB * (NH / S::CE) && TX * S::NTHR == S::JB * (P / S::CE), "tasks");
     struct Blk { V16 lo[TB], hi[TB], xv[TX]; };
-    // Every global load below is unconditional (rows past the end of the
-    // sequence read the last valid row and are zeroed afterwards), so the
-    // number of loads in flight is static and the waits the compiler inserts
-    // stop at exactly the loads a step needs, leaving later prefetches in
-    // flight.
-    auto fetch = [&](int64_t c, int jb, Blk &f) {
-        const int64_t tk = tok_of(c);
+    // Every load below is unconditional and goes through a buffer resource
+    // that ends at the chunk's last valid token (rows past the end of the
+    // sequence read as zeros), so the number of loads in flight is static and
+    // the waits the compiler inserts stop at exactly the loads a step needs,
+    // leaving later prefetches in flight.
+    const uint32_t bstr_b = (uint32_t)(bstr * sizeof(T)), xstr_b = (uint32_t)(xstr * sizeof(T));
+    auto rows_rsrc = [&](const T *base, int64_t c, int64_t str, int width) {
         const int nv = nvalid_of(c);
-        const T *Bg = Bs + tk * (R * N);
-        const T *Xg = Xs + tk * (R * P);
+        return make_rsrc(base + tok_of(c) * width, (uint32_t)(((nv - 1) * str + width) * (int64_t)sizeof(T)));
+    };
+    auto fetch = [&](int64_t c, int jb, Blk &f) {
+        const Rsrc rb = rows_rsrc(Bs, c, bstr, R * N), rx = rows_rsrc(Xs, c, xstr, R * P);
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            const T *src = Bg + min(t, nv - 1) * bstr + r * N + cp * S::CE;
-            f.lo[k] = *reinterpret_cast<const V16 *>(src);
-            f.hi[k] = *reinterpret_cast<const V16 *>(src + NH);
+            const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + cp * S::CE) * sizeof(T));
+            f.lo[k] = buf_load<V16>(rb, off);
+            f.hi[k] = buf_load<V16>(rb, off + NH * sizeof(T));
         }
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            f.xv[k] = *reinterpret_cast<const V16 *>(Xg + min(t, nv - 1) * xstr + r * P + pc * S::CE);
+            f.xv[k] = buf_load<V16>(rx, tok_off(t, xstr_b) + (uint32_t)((r * P + pc * S::CE) * sizeof(T)));
         }
     };
-    int cnv = 0;   // valid tokens of the chunk being committed
     auto commit = [&](int jb, const Blk &f, auto kRow) {
         T *sB = s_B + (jb % NBUF) * kSB, *sX = s_X + (jb % NBUF) * kSX, *sBt = s_Bt + (jb % NBUF) * kSBt;
 #pragma unroll
@@ -173,13 +174,12 @@ void k_scan_seg(ScanArgs a) {
             const int row = jb * S::JB + jr, t = row / R;
             V16 lo = f.lo[k], hi = f.hi[k];
             const float wt = s_w[t];
-            const bool ok = t < cnv;
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
                 const int n = cp * S::CE + e;
                 float cs, sn;
                 cs_get(s_cs[n * LDC + t], cs, sn);
-                const float u = ok ? fget(lo, e) : 0.f, w = ok ? fget(hi, e) : 0.f;
+                const float u = fget(lo, e), w = fget(hi, e);
                 const float re = cs * u + sn * w, im = cs * w - sn * u;
                 if constexpr (decltype(kRow)::value) {
                     fset(lo, e, re);
@@ -196,10 +196,8 @@ void k_scan_seg(ScanArgs a) {
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
-            const bool ok = (jb * S::JB + jr) / R < cnv;
 #pragma unroll
-            for (int e = 0; e < S::CE; ++e)
-                sX[(pc * S::CE + e) * S::LDJ + jr] = ok ? f.xv[k][e] : from_f32<T>(0.f);
+            for (int e = 0; e < S::CE; ++e) sX[(pc * S::CE + e) * S::LDJ + jr] = f.xv[k][e];
         }
     };
     // M += (B^ W)^T x over one staged block (owned state pair-tiles)
@@ -224,23 +222,27 @@ void k_scan_seg(ScanArgs a) {
     // Prologue inputs of a chunk, loaded one chunk ahead (raw values only, so
     // that nothing waits for them before the prologue itself).
     struct Pro { float th[S::TPS]; float dtv, lamv, Av, dtn, lamn; };
+    // Tokens past the end of the sequence read as zeros; the dt and lambda
+    // ranges extend to the next chunk's first token when there is one.
     auto load_pro = [&](int64_t c, Pro &p) {
         const int64_t tk = tok_of(c);
         const int nv = nvalid_of(c);
+        const int nvn = nv + (c * Q + nv < a.L ? 1 : 0);
         const int i = tid % NH, seg = tid / NH;
+        const Rsrc rth = make_rsrc(a.theta + tk * NH, (uint32_t)(((nv - 1) * tstr + 1) * NH * 4));
+        const uint32_t thstr_b = (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
 #pragma unroll
-        for (int k = 0; k < S::TPS; ++k) {
-            const int t = seg * S::TPS + k;
-            p.th[k] = a.theta[(tk + min(t, nv - 1) * tstr) * NH + i];
-        }
-        const int tt = min(tid, nv - 1);
-        const int64_t k = tk + tt * tstr, t = c * Q + tt;
-        const int64_t kn = (t + 1 < a.L) ? k + tstr : k;
-        p.dtv = a.dt[k];
-        p.lamv = a.lam[k];
+        for (int k = 0; k < S::TPS; ++k)
+            p.th[k] = buf_load<float>(rth, tok_off(seg * S::TPS + k, thstr_b) + i * 4);
+        const Rsrc rdt = make_rsrc(a.dt + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
+        const Rsrc rlam = make_rsrc(a.lam + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
+        const uint32_t o = tok_off(tid, tstr_b);
+        p.dtv = buf_load<float>(rdt, o);
+        p.lamv = buf_load<float>(rlam, o);
+        p.dtn = buf_load<float>(rdt, o + tstr_b);
+        p.lamn = buf_load<float>(rlam, o + tstr_b);
+        const int64_t t = c * Q + min(tid, nv - 1);
         p.Av = a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
-        p.dtn = a.dt[kn];
-        p.lamn = a.lam[kn];
     };
     // cum (wavefront scans), gamma, sigma, w; angle prefix sums, the cos/sin
     // table and psi_e.  Ends with a barrier.
@@ -249,11 +251,11 @@ void k_scan_seg(ScanArgs a) {
         const int i = tid % NH, seg = tid / NH;
         // branch-free on the loaded values (a branch here would merge the
         // compiler's load-counter state conservatively)
-        const bool ok = tid < nv;
-        const bool has_next = c * Q + tid + 1 < a.L;   // the next token's previous-input weight
-        const Acc lg = ok ? (Acc)p.dtv * (Acc)p.Av : (Acc)0;
-        const float gam = ok ? p.lamv * p.dtv : 0.f;
-        const float sig = ok ? gam + (has_next ? (1.f - p.lamn) * p.dtn : 0.f) : 0.f;
+        // dt and lambda read as zero past the end of the sequence, so
+        // sigma_{L-1} = gamma_{L-1} and rows past the end carry zeros
+        const Acc lg = (Acc)p.dtv * (Acc)p.Av;
+        const float gam = p.lamv * p.dtv;
+        const float sig = gam + (1.f - p.lamn) * p.dtn;
         if (tid < Q) {
             s_gam[tid] = gam;
             s_sig[tid] = sig;
@@ -264,7 +266,7 @@ void k_scan_seg(ScanArgs a) {
         Acc run = 0;
 #pragma unroll
         for (int k = 0; k < S::TPS; ++k) {
-            run += (seg * S::TPS + k < nv) ? (Acc)p.th[k] : (Acc)0;
+            run += (Acc)p.th[k];   // zero past the end of the sequence
             ps[k] = run;
         }
         s_segtot[seg * NH + i] = run;
@@ -399,7 +401,6 @@ void k_scan_seg(ScanArgs a) {
         sched_fence();
         for (int64_t c = cbeg; c < cend; ++c) {
             relane();
-            cnv = nvalid_of(c);
             prologue(c, pro);
             sched_fence();
             load_pro(min(c + 1, cend - 1), pro);
@@ -641,15 +642,13 @@ void k_scan_seg(ScanArgs a) {
     Frag cf[TPW][NK];
     auto load_cf = [&](int64_t c) {
         if (!ow) return;
-        const int64_t tk = tok_of(c);
-        const int nv = nvalid_of(c);
-        const T *Cg = Cs + tk * (R * N);
+        const Rsrc rc = rows_rsrc(Cs, c, bstr, R * N);
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
             const int row = owned_tile<S>(wt, m) * 16 + l16, t = row / R, r = row % R;
-            const T *src = Cg + min(t, nv - 1) * bstr + r * N;
+            const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + MM::KPL * g) * sizeof(T));
 #pragma unroll
-            for (int kk = 0; kk < NK; ++kk) cf[m][kk] = MM::load(src + kk * MM::K + MM::KPL * g);
+            for (int kk = 0; kk < NK; ++kk) cf[m][kk] = buf_load<Frag>(rc, off + kk * MM::K * sizeof(T));
         }
     };
     load_pro(cbeg, pro);
@@ -663,7 +662,6 @@ void k_scan_seg(ScanArgs a) {
     for (int64_t c = cbeg; c < cend; ++c) {
         relane();
         const int nv = nvalid_of(c);
-        cnv = nv;
         const int64_t tk = tok_of(c);
         // the state leaving this chunk is needed inside the segment, or as the
         // final state when no aggregate pass produced it
@@ -673,12 +671,11 @@ void k_scan_seg(ScanArgs a) {
         load_pro(min(c + 1, cend - 1), pro);
         sched_fence();
         // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
-        // end of the sequence zeroed)
+        // end of the sequence were loaded as zeros)
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
             if (!ow) break;
             const int row = owned_tile<S>(wt, m) * 16 + l16, t = row / R;
-            const bool ok = t < nv;
 #pragma unroll
             for (int kk = 0; kk < NK / 2; ++kk) {
 #pragma unroll
@@ -686,7 +683,7 @@ void k_scan_seg(ScanArgs a) {
                     const int n = kk * MM::K + MM::KPL * g + e;
                     float cs, sn;
                     cs_get(s_cs[n * LDC + t], cs, sn);
-                    const float u = ok ? fget(cf[m][kk], e) : 0.f, w = ok ? fget(cf[m][kk + NK / 2], e) : 0.f;
+                    const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
                     fset(cf[m][kk], e, cs * u + sn * w);
                     fset(cf[m][kk + NK / 2], e, cs * w - sn * u);
                 }
