@@ -114,24 +114,29 @@ void k_scan_fused(ScanArgs a) {
     constexpr int TX = S::JB * (P / S::CE) / S::NTHR;    // x tasks per thread
     static_assert(TB * S::NTHR == S::JB * (NH / S::CE) && TX * S::NTHR == S::JB * (P / S::CE), "tasks");
     struct Blk { V16 lo[TB], hi[TB], xv[TX]; };
-    // The global loads are unconditional (rows past the end of the sequence
-    // read the last valid row and are zeroed in commit()), so the number of
-    // loads in flight is static and the compiler's waits stop at exactly the
-    // loads a step needs, leaving later prefetches in flight.
+    // The loads are unconditional and go through buffer resources that end
+    // at the chunk's last valid token (rows past the end of the sequence read
+    // as zeros), so the number of loads in flight is static and the
+    // compiler's waits stop at exactly the loads a step needs, leaving later
+    // prefetches in flight.
+    const uint32_t bstr_b = (uint32_t)(bstr * sizeof(T)), xstr_b = (uint32_t)(xstr * sizeof(T));
+    const Rsrc rb = make_rsrc(Bg, (uint32_t)(((nvalid - 1) * bstr + R * N) * (int64_t)sizeof(T)));
+    const Rsrc rc = make_rsrc(Cg, (uint32_t)(((nvalid - 1) * bstr + R * N) * (int64_t)sizeof(T)));
+    const Rsrc rx = make_rsrc(Xg, (uint32_t)(((nvalid - 1) * xstr + R * P) * (int64_t)sizeof(T)));
     auto fetch = [&](int jb, Blk &f) {
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            const T *src = Bg + min(t, nvalid - 1) * bstr + r * N + cp * S::CE;
-            f.lo[k] = *reinterpret_cast<const V16 *>(src);
-            f.hi[k] = *reinterpret_cast<const V16 *>(src + NH);
+            const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + cp * S::CE) * sizeof(T));
+            f.lo[k] = buf_load<V16>(rb, off);
+            f.hi[k] = buf_load<V16>(rb, off + NH * sizeof(T));
         }
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            f.xv[k] = *reinterpret_cast<const V16 *>(Xg + min(t, nvalid - 1) * xstr + r * P + pc * S::CE);
+            f.xv[k] = buf_load<V16>(rx, tok_off(t, xstr_b) + (uint32_t)((r * P + pc * S::CE) * sizeof(T)));
         }
     };
     auto commit = [&](int jb, const Blk &f, auto kBt, auto kRow) {
@@ -142,13 +147,12 @@ void k_scan_fused(ScanArgs a) {
             const int row = jb * S::JB + jr, t = row / R;
             V16 lo = f.lo[k], hi = f.hi[k];
             const float wt = s_w[t];
-            const bool ok = t < nvalid;
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
                 const int n = cp * S::CE + e;
                 float cs, sn;
                 cs_get(s_cs[n * LDC + t], cs, sn);
-                const float u = ok ? fget(lo, e) : 0.f, w = ok ? fget(hi, e) : 0.f;
+                const float u = fget(lo, e), w = fget(hi, e);
                 const float re = cs * u + sn * w, im = cs * w - sn * u;
                 if constexpr (decltype(kRow)::value) {
                     fset(lo, e, re);
@@ -167,10 +171,8 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
-            const bool ok = (jb * S::JB + jr) / R < nvalid;
 #pragma unroll
-            for (int e = 0; e < S::CE; ++e)
-                sX[(pc * S::CE + e) * S::LDJ + jr] = ok ? f.xv[k][e] : from_f32<T>(0.f);
+            for (int e = 0; e < S::CE; ++e) sX[(pc * S::CE + e) * S::LDJ + jr] = f.xv[k][e];
         }
     };
     // Prefetch depth (blocks in flight, register ring): the aggregate phase
@@ -185,32 +187,36 @@ void k_scan_fused(ScanArgs a) {
     {
         // angles first (the largest prologue load): thread (pair i, segment seg)
         const int i = tid % NH, seg = tid / NH;
+        // (tokens past the end of the sequence read as zeros; the dt and
+        // lambda ranges extend to the next chunk's first token if there is one)
+        const Rsrc rth = make_rsrc(a.theta + tok0 * NH, (uint32_t)(((nvalid - 1) * tstr + 1) * NH * 4));
+        const uint32_t thstr_b = (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
         float th[S::TPS];
 #pragma unroll
-        for (int k = 0; k < S::TPS; ++k) {
-            const int t = seg * S::TPS + k;
-            th[k] = a.theta[(tok0 + min(t, nvalid - 1) * tstr) * NH + i];
-        }
-        const int tq = min(tid, nvalid - 1);
-        const int64_t kq = tok0 + tq * tstr, tg = t0 + tq;
-        const int64_t kn = (tg + 1 < a.L) ? kq + tstr : kq;
-        const float dtv = a.dt[kq], lamv = a.lam[kq];
+        for (int k = 0; k < S::TPS; ++k) th[k] = buf_load<float>(rth, tok_off(seg * S::TPS + k, thstr_b) + i * 4);
+        const int nvn = nvalid + (t0 + nvalid < a.L ? 1 : 0);
+        const Rsrc rdt = make_rsrc(a.dt + tok0, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
+        const Rsrc rlam = make_rsrc(a.lam + tok0, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
+        const uint32_t o = tok_off(tid, tstr_b);
+        const float dtv = buf_load<float>(rdt, o), lamv = buf_load<float>(rlam, o);
+        const float dtn = buf_load<float>(rdt, o + tstr_b), lamn = buf_load<float>(rlam, o + tstr_b);
+        const int64_t tg = t0 + min(tid, nvalid - 1);
         const float Av = a.A[b * a.a_sb + tg * a.a_st + h * a.a_sh];
-        const float dtn = a.dt[kn], lamn = a.lam[kn];
         // the first blocks' loads go out after the prologue's own loads (memory
         // counters retire in order), so they overlap the prologue's arithmetic
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int d = 0; d < DA; ++d) fetch(d, ring[d]);
         __builtin_amdgcn_sched_barrier(0);
-        const bool ok = tid < Q && tid < nvalid;
-        const bool has_next = t0 + tid + 1 < a.L;
+        // dt and lambda are zero past the end of the sequence, so
+        // sigma_{L-1} = gamma_{L-1} and rows past the end carry zeros
+        const bool ok = tid < Q;
         const Acc lg = ok ? (Acc)dtv * (Acc)Av : (Acc)0;
-        const float gam = ok ? lamv * dtv : 0.f;
-        const float sig = ok ? gam + (has_next ? (1.f - lamn) * dtn : 0.f) : 0.f;
+        const float gam = lamv * dtv;
+        const float sig = gam + (1.f - lamn) * dtn;
         Acc ps[S::TPS];
 #pragma unroll
-        for (int k = 0; k < S::TPS; ++k) ps[k] = (seg * S::TPS + k < nvalid) ? (Acc)th[k] : (Acc)0;
+        for (int k = 0; k < S::TPS; ++k) ps[k] = (Acc)th[k];
         if (tid < Q) {
             s_gam[tid] = gam;
             s_sig[tid] = sig;
@@ -569,15 +575,15 @@ void k_scan_fused(ScanArgs a) {
             for (int v = 0; v < 4; ++v)
                 s_S[(pt * 16 + l16) * S::LDN + 16 * (ntl + 4 * half) + 4 * g + v] = from_f32<T>(Sin[m2][half][v]);
     }
-    // C^ fragments of the owned row tiles, rotated by -psi_t
+    // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
+    // end of the sequence were loaded as zeros)
     Frag cf[TPW][NK];
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
-        const T *src = Cg + min(t, nvalid - 1) * bstr + r * N;
-        const bool ok = t < nvalid;   // rows past the end of the sequence are zeroed
+        const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + MM::KPL * g) * sizeof(T));
 #pragma unroll
-        for (int kk = 0; kk < NK; ++kk) cf[m][kk] = MM::load(src + kk * MM::K + MM::KPL * g);
+        for (int kk = 0; kk < NK; ++kk) cf[m][kk] = buf_load<Frag>(rc, off + kk * MM::K * sizeof(T));
 #pragma unroll
         for (int kk = 0; kk < NK / 2; ++kk) {
 #pragma unroll
@@ -585,7 +591,7 @@ void k_scan_fused(ScanArgs a) {
                 const int n = kk * MM::K + MM::KPL * g + e;
                 float cs, sn;
                 cs_get(s_cs[n * LDC + t], cs, sn);
-                const float u = ok ? fget(cf[m][kk], e) : 0.f, w = ok ? fget(cf[m][kk + NK / 2], e) : 0.f;
+                const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
                 fset(cf[m][kk], e, cs * u + sn * w);
                 fset(cf[m][kk + NK / 2], e, cs * w - sn * u);
             }
