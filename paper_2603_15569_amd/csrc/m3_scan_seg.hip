@@ -201,20 +201,25 @@ void k_scan_seg(ScanArgs a) {
         }
     };
     // M += (B^ W)^T x over one staged block (owned state pair-tiles)
+    // (a wave's state tiles share their row tiles, wave % 4 and wave % 4 + 4:
+    // each (B^ W)^T fragment is loaded once for all of them, each x^T
+    // fragment once for both halves)
+    static_assert(NW % 4 == 0, "state row tiles shared across a wave's tiles");
     auto m_block = [&](f32x4 (&ms)[PTW][2], int jb) {
         const T *sBt = s_Bt + (jb % NBUF) * kSBt, *sX = s_X + (jb % NBUF) * kSX;
+        const int ntl = wave % 4;
 #pragma unroll
-        for (int m2 = 0; m2 < PTW; ++m2) {
-            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
+        for (int ks = 0; ks < JK; ++ks) {
+            Frag af[2];
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
-                const int nt = ntl + 4 * half;
+            for (int half = 0; half < 2; ++half)
+                af[half] = MM::load(&sBt[((ntl + 4 * half) * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
 #pragma unroll
-                for (int ks = 0; ks < JK; ++ks) {
-                    const Frag af = MM::load(&sBt[(nt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
-                    const Frag bf = MM::load(&sX[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
-                    ms[m2][half] = MM::mma(af, bf, ms[m2][half]);
-                }
+            for (int m2 = 0; m2 < PTW; ++m2) {
+                const int pt = (wave + NW * m2) / 4;
+                const Frag bf = MM::load(&sX[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+#pragma unroll
+                for (int half = 0; half < 2; ++half) ms[m2][half] = MM::mma(af[half], bf, ms[m2][half]);
             }
         }
     };
