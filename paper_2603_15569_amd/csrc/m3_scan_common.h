@@ -57,6 +57,35 @@ __device__ __forceinline__ uint32_t tok_off(int t, uint32_t stride_bytes) {
     return __umul24((uint32_t)t, stride_bytes);
 }
 
+// Inclusive prefix sum over the 64 lanes of a wavefront.  fp32: six DPP
+// adds on the VALU (row shifts by 1, 2, 4, 8 within each 16-lane row, then
+// the last lane of a row broadcast into the next rows); fp64 (the fp32
+// build's prologue): lane shuffles.
+template <int CTRL, int ROWS>
+__device__ __forceinline__ float dpp_src(float v) {
+    // lanes with no source in the pattern, or outside ROWS, read 0
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROWS, 0xf, false));
+}
+__device__ __forceinline__ float lane_scan(float v) {
+    v += dpp_src<0x111, 0xf>(v);   // row_shr:1
+    v += dpp_src<0x112, 0xf>(v);   // row_shr:2
+    v += dpp_src<0x114, 0xf>(v);   // row_shr:4
+    v += dpp_src<0x118, 0xf>(v);   // row_shr:8
+    v += dpp_src<0x142, 0xa>(v);   // row_bcast:15 into rows 1 and 3
+    v += dpp_src<0x143, 0xc>(v);   // row_bcast:31 into rows 2 and 3
+    return v;
+}
+__device__ __forceinline__ double lane_scan(double v) { return wave_incl_scan(v, (int)(threadIdx.x % kWave)); }
+// Value of lane l (uniform l) in every lane.
+__device__ __forceinline__ float lane_bcast(float v, int l) {
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), l));
+}
+__device__ __forceinline__ double lane_bcast(double v, int l) {
+    const long long b = __double_as_longlong(v);
+    const int lo = __builtin_amdgcn_readlane((int)(b & 0xffffffff), l), hi = __builtin_amdgcn_readlane((int)(b >> 32), l);
+    return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
+}
+
 // Four consecutive output columns of one row, held by one lane of a
 // transposed MFMA tile (the lane's four accumulator rows are y columns).
 __device__ __forceinline__ void store4(bf16 *dst, const f32x4 &v) {

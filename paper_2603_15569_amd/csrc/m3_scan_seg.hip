@@ -69,9 +69,12 @@ void k_scan_seg(ScanArgs a) {
     static_assert(NSP * S::NWO == S::NW && PTS * NSP == PT, "column split");
     constexpr int kMaps = 2;            // look-back maps loaded per round trip
 
-    __shared__ Acc s_cum[Q];
-    __shared__ Acc s_wtot[NW];
-    __shared__ Acc s_psie[NH];
+    // chunk-parity double buffers: the tail of a chunk (state rotation by
+    // psi_e, the aggregate's cum_e) may still read them while faster waves
+    // run the next chunk's prologue
+    __shared__ Acc s_cumb[2][Q];
+    __shared__ Acc s_psieb[2][NH];
+    Acc *s_cum = s_cumb[0], *s_psie = s_psieb[0];
     __shared__ Acc s_segps[NH];         // angle totals of the segment
     __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
     __shared__ CS s_cs[NH * LDC];
@@ -83,8 +86,6 @@ void k_scan_seg(ScanArgs a) {
     __shared__ __attribute__((aligned(16))) T s_X[NBUF * kSX];    // x^T blocks [p][row]
     __shared__ __attribute__((aligned(16))) T s_Bt[NBUF * kSBt];  // (B^ W)^T blocks [n][row]
     __shared__ int s_i[4];
-    Acc *s_segtot = reinterpret_cast<Acc *>(s_B);                    // prologue only
-    static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
     static_assert(P == S::JB, "S^T [p][n] fits in the B^ block");
     static_assert(NW * 16 <= NBUF * N, "y staging fits in the (B^ W)^T buffer");
 
@@ -225,79 +226,99 @@ void k_scan_seg(ScanArgs a) {
     };
 
     // Prologue inputs of a chunk, loaded one chunk ahead (raw values only, so
-    // that nothing waits for them before the prologue itself).
-    struct Pro { float th[S::TPS]; float dtv, lamv, Av, dtn, lamn; };
+    // that nothing waits for them before the prologue itself).  Lanes are
+    // tokens (TPL consecutive tokens per lane); wave w owns angle pairs
+    // w*PPW .. w*PPW + PPW-1.
+    constexpr int TPL = Q > kWave ? Q / kWave : 1;   // tokens per lane
+    constexpr int PPW = NH / NW;                     // angle pairs per wave
+    static_assert(TPL * kWave >= Q && PPW % 4 == 0, "prologue layout");
+    struct Pro { f32x4 th[TPL][PPW / 4]; float dtv[TPL], lamv[TPL], Av[TPL], dtn[TPL], lamn[TPL]; };
     // Tokens past the end of the sequence read as zeros; the dt and lambda
     // ranges extend to the next chunk's first token when there is one.
     auto load_pro = [&](int64_t c, Pro &p) {
         const int64_t tk = tok_of(c);
         const int nv = nvalid_of(c);
         const int nvn = nv + (c * Q + nv < a.L ? 1 : 0);
-        const int i = tid % NH, seg = tid / NH;
         const Rsrc rth = make_rsrc(a.theta + tk * NH, (uint32_t)(((nv - 1) * tstr + 1) * NH * 4));
-        const uint32_t thstr_b = (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
-#pragma unroll
-        for (int k = 0; k < S::TPS; ++k)
-            p.th[k] = buf_load<float>(rth, tok_off(seg * S::TPS + k, thstr_b) + i * 4);
         const Rsrc rdt = make_rsrc(a.dt + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
         const Rsrc rlam = make_rsrc(a.lam + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
-        const uint32_t o = tok_off(tid, tstr_b);
-        p.dtv = buf_load<float>(rdt, o);
-        p.lamv = buf_load<float>(rlam, o);
-        p.dtn = buf_load<float>(rdt, o + tstr_b);
-        p.lamn = buf_load<float>(rlam, o + tstr_b);
-        const int64_t t = c * Q + min(tid, nv - 1);
-        p.Av = a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
+        const uint32_t thstr_b = (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
+#pragma unroll
+        for (int u = 0; u < TPL; ++u) {
+            const int t = lane * TPL + u;
+            const uint32_t oth = tok_off(t, thstr_b) + wave * PPW * 4;
+#pragma unroll
+            for (int q = 0; q < PPW / 4; ++q) p.th[u][q] = buf_load<f32x4>(rth, oth + 16 * q);
+            const uint32_t o = tok_off(t, tstr_b);
+            p.dtv[u] = buf_load<float>(rdt, o);
+            p.lamv[u] = buf_load<float>(rlam, o);
+            p.dtn[u] = buf_load<float>(rdt, o + tstr_b);
+            p.lamn[u] = buf_load<float>(rlam, o + tstr_b);
+            p.Av[u] = a.A[b * a.a_sb + (c * Q + min(t, nv - 1)) * a.a_st + h * a.a_sh];
+        }
     };
-    // cum (wavefront scans), gamma, sigma, w; angle prefix sums, the cos/sin
-    // table and psi_e.  Ends with a barrier.
+    // cum, gamma, sigma, w (wave 0 publishes them) and the angle prefix sums,
+    // the cos/sin table and psi_e of each wave's pairs: lane prefix sums over
+    // tokens (wavefront scans), no LDS round trip.  Ends with the one barrier.
     auto prologue = [&](int64_t c, const Pro &p) {
         const int nv = nvalid_of(c);
-        const int i = tid % NH, seg = tid / NH;
-        // branch-free on the loaded values (a branch here would merge the
-        // compiler's load-counter state conservatively)
+        s_cum = s_cumb[c & 1];
+        s_psie = s_psieb[c & 1];
         // dt and lambda read as zero past the end of the sequence, so
         // sigma_{L-1} = gamma_{L-1} and rows past the end carry zeros
-        const Acc lg = (Acc)p.dtv * (Acc)p.Av;
-        const float gam = p.lamv * p.dtv;
-        const float sig = gam + (1.f - p.lamn) * p.dtn;
-        if (tid < Q) {
-            s_gam[tid] = gam;
-            s_sig[tid] = sig;
-        }
-        const Acc v = wave_incl_scan(lg, lane);
-        if (lane == kWave - 1) s_wtot[wave] = v;
-        Acc ps[S::TPS];
-        Acc run = 0;
+        if (wave == 0) {
+            Acc lg[TPL], loc = 0;
 #pragma unroll
-        for (int k = 0; k < S::TPS; ++k) {
-            run += (Acc)p.th[k];   // zero past the end of the sequence
-            ps[k] = run;
-        }
-        s_segtot[seg * NH + i] = run;
-        __syncthreads();
-        if (tid < Q) {
-            Acc off = 0;
-            for (int w2 = 0; w2 < wave; ++w2) off += s_wtot[w2];
-            s_cum[tid] = v + off;
-        }
-        Acc off = 0;
-        for (int s2 = 0; s2 < seg; ++s2) off += s_segtot[s2 * NH + i];
+            for (int u = 0; u < TPL; ++u) {
+                lg[u] = (Acc)p.dtv[u] * (Acc)p.Av[u];
+                loc += lg[u];
+            }
+            Acc cum = lane_scan(loc) - loc;   // exclusive over lanes
+            Acc cumv[TPL];
 #pragma unroll
-        for (int k = 0; k < S::TPS; ++k) {
-            const int t = seg * S::TPS + k;
-            if (t < Q) {
-                const Acc psi = ps[k] + off;
-                Acc sn, cs;
-                sincos_fast(psi, &sn, &cs);
-                cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
-                if (t == nv - 1) s_psie[i] = psi;
+            for (int u = 0; u < TPL; ++u) {
+                cum += lg[u];
+                cumv[u] = cum;
+            }
+            // cum_e = cum of token nv - 1
+            Acc cum_e = cumv[0];
+#pragma unroll
+            for (int u = 1; u < TPL; ++u) cum_e = ((nv - 1) % TPL == u) ? cumv[u] : cum_e;
+            cum_e = lane_bcast(cum_e, (nv - 1) / TPL);
+#pragma unroll
+            for (int u = 0; u < TPL; ++u) {
+                const int t = lane * TPL + u;
+                const float gam = p.lamv[u] * p.dtv[u];
+                const float sig = gam + (1.f - p.lamn[u]) * p.dtn[u];
+                if (t < Q) {
+                    s_cum[t] = cumv[u];
+                    s_gam[t] = gam;
+                    s_sig[t] = sig;
+                    s_w[t] = (t < nv) ? (float)(exp_fast(cum_e - cumv[u]) * (Acc)sig) : 0.f;
+                }
             }
         }
-        __syncthreads();
-        if (tid < Q) {
-            const Acc cum_e = s_cum[nv - 1];
-            s_w[tid] = (tid < nv) ? (float)(exp_fast(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
+#pragma unroll
+        for (int k = 0; k < PPW; ++k) {
+            const int i = wave * PPW + k;
+            Acc th[TPL], loc = 0;
+#pragma unroll
+            for (int u = 0; u < TPL; ++u) {
+                th[u] = (Acc)p.th[u][k / 4][k % 4];   // zero past the end of the sequence
+                loc += th[u];
+            }
+            Acc psi = lane_scan(loc) - loc;
+#pragma unroll
+            for (int u = 0; u < TPL; ++u) {
+                const int t = lane * TPL + u;
+                psi += th[u];
+                if (t < Q) {
+                    Acc sn, cs;
+                    sincos_fast(psi, &sn, &cs);
+                    cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
+                    if (t == nv - 1) s_psie[i] = psi;
+                }
+            }
         }
         __syncthreads();
     };
@@ -433,7 +454,6 @@ void k_scan_seg(ScanArgs a) {
                 segps += s_psie[tid];
                 if constexpr (sizeof(Acc) == 4) segps = reduce_angle(segps);
             }
-            __syncthreads();   // s_cum, s_psie read before the next prologue
         }
         if (tid < NH) s_segps[tid] = segps;
         __syncthreads();
