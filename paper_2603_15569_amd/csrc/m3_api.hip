@@ -24,7 +24,7 @@ ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N
         w.total = align_up(w.off_tot + tot_bytes, 256);
     } else {
         w.off_ctl = 0;
-        w.off_flags = 256;
+        w.off_flags = align_up(kCtlWords * sizeof(uint32_t), 256);
         w.off_tot = align_up(w.off_flags + per * sizeof(uint32_t), 256);
         w.off_agg = align_up(w.off_tot + tot_bytes, 256);
         w.off_inc = align_up(w.off_agg + state_bytes, 256);

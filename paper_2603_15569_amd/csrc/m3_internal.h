@@ -61,6 +61,14 @@ step_launch_fn find_step_impl(int io, int64_t N, int64_t P, int64_t R);
 scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 scan_launch_fn find_seg_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 
+// Control words of the single-pass scans (start of their workspace): ctl[0]
+// the ticket counter, ctl[1] the count of look-back waits that timed out, and
+// one ticket counter per slice group at ctl[kGroupStride * (y + 1)] (128
+// bytes apart, so that the groups' atomics do not share a cache line).
+constexpr int kGroups = 8;           // slice groups (one per XCD)
+constexpr int kGroupStride = 32;     // words
+constexpr int kCtlWords = kGroupStride * (kGroups + 1);
+
 // Byte offsets of the workspace regions for a scan.
 struct ScanWorkspaceLayout {
     size_t off_M, off_Sin, off_tot;                 // three-kernel path

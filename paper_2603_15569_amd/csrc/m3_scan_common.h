@@ -3,6 +3,7 @@
 // element helpers, coherent accesses of the look-back, the reset kernel.
 #pragma once
 #include "m3_device.h"
+#include "m3_internal.h"
 
 namespace m3 {
 namespace scan {
@@ -155,12 +156,40 @@ __device__ __forceinline__ int owned_tile(int w, int m) {
     return (m % 2 == 0) ? base + w : base + 2 * S::NWO - 1 - w;
 }
 
-// Clears the ticket counter, the timeout counter and the flags (one kernel
+// Clears the ticket counters, the timeout counter and the flags (one kernel
 // per translation unit: internal linkage).
 static __global__ void k_reset(uint32_t *ctl, uint32_t *flags, int64_t nflags) {
     const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i0 < 2) ctl[i0] = 0u;
+    if (i0 < kGroups) ctl[kGroupStride * (i0 + 1)] = 0u;
     for (int64_t i = i0; i < nflags; i += (int64_t)gridDim.x * blockDim.x) flags[i] = 0u;
+}
+
+// Work item of a one-item-per-workgroup launch (grid = nsl * nchunks) whose
+// chunks chain within a slice: slices are split into kGroups groups (slice %
+// kGroups) and each group hands out its (chunk, slice) items chunk-major from
+// its own counter, so every predecessor of an item holds an earlier ticket of
+// the same counter and is resident or done (forward progress).  A workgroup
+// asks the group of the XCD it runs on first (workgroups are spread over the
+// XCDs, so the eight counters share the traffic), then the others; since the
+// grid has exactly one workgroup per item, every workgroup finds one.
+// Called by one thread.
+__device__ __forceinline__ void take_item(uint32_t *ctl, int64_t nsl, int64_t nchunks, int64_t *c,
+                                          int64_t *sl) {
+    const int x = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & (kGroups - 1));   // XCC id
+    for (int tries = 0; tries < kGroups; ++tries) {
+        const int y = (x + tries) & (kGroups - 1);
+        const int64_t ny = (nsl - y + kGroups - 1) / kGroups;   // slices of group y
+        if (ny <= 0) continue;
+        const int64_t k = atomicAdd(ctl + kGroupStride * (y + 1), 1u);
+        if (k < ny * nchunks) {
+            *c = k / ny;
+            *sl = y + kGroups * (k % ny);
+            return;
+        }
+    }
+    *c = -1;   // unreachable with one workgroup per item
+    *sl = -1;
 }
 
 constexpr uint32_t kFlagInit = 3;   // probe result for "before the first chunk"

@@ -16,8 +16,9 @@
 // folded in.  Rows of every chunk operand are (token, rank) pairs.
 //
 // Work of one workgroup (NW waves; each wave owns TPW tiles of 16 rows):
-//   1. ticket -> (slice, chunk), chunk-major, so every predecessor of a chunk
-//      holds an earlier ticket and is already resident (forward progress);
+//   1. ticket -> (slice, chunk), chunk-major within a slice group, so every
+//      predecessor of a chunk holds an earlier ticket of the same counter and
+//      is already resident (forward progress);
 //   2. prologue: cum (wavefront scans), gamma, sigma, w; angle prefix sums and
 //      a cos/sin table in LDS;
 //   3. aggregate first: per 64-row block, (B^ W)^T and x^T staged in LDS and
@@ -33,7 +34,7 @@
 //      K = rows); D x added; y staged per wave from the (transposed)
 //      accumulator tiles and stored.  A chunk of a single 64-row block
 //      stages B^ once for both uses; longer chunks restage it from cache.
-// A tiny reset kernel clears the ticket counter and the flags first.
+// A tiny reset kernel clears the ticket counters and the flags first.
 #include <type_traits>
 
 #include "m3_device.h"
@@ -85,11 +86,16 @@ void k_scan_fused(ScanArgs a) {
     const int g = lane >> 4, l16 = lane & 15;
 
     // ---- 1. ticket -> (slice, chunk) ----
-    if (tid == 0) s_i[0] = (int)atomicAdd(a.ctl, 1u);
-    __syncthreads();
     const int64_t nsl = a.batch * a.H;
-    const int64_t ticket = s_i[0];
-    const int64_t c = ticket / nsl, sl = ticket % nsl;
+    if (tid == 0) {
+        int64_t ci, si;
+        take_item(a.ctl, nsl, a.nchunks, &ci, &si);
+        s_i[0] = (int)ci;
+        s_i[1] = (int)si;
+    }
+    __syncthreads();
+    const int64_t c = s_i[0], sl = s_i[1];
+    if (c < 0) return;   // (cannot happen: one workgroup per item)
     const int64_t b = sl / a.H, h = sl % a.H;
     const int64_t t0 = c * Q;
     const int nvalid = (int)min((int64_t)Q, a.L - t0);

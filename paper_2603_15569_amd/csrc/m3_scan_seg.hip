@@ -15,8 +15,9 @@
 // T = e^{sum cum_e} R(sum psi_e).
 //
 // Work of one workgroup:
-//   1. ticket -> (segment, slice), segment-major, so every predecessor of a
-//      segment holds an earlier ticket and is resident (forward progress);
+//   1. ticket -> (segment, slice), segment-major within a slice group, so
+//      every predecessor of a segment holds an earlier ticket of the same
+//      counter and is resident (forward progress);
 //      with one segment per slice there is no look-back and no ticket;
 //   2. (several segments) aggregate pass: per chunk the prologue (decay and
 //      angle prefix scans, cos/sin table, weights) and M from the row blocks
@@ -107,13 +108,22 @@ void k_scan_seg(ScanArgs a) {
 
     // ---- 1. (segment, slice) ----
     const int64_t nsl = a.batch * a.H;
-    int64_t ticket = blockIdx.x;
+    // linked segments take (segment, slice) items from the slice groups'
+    // counters (segment-major within a group: every predecessor segment holds
+    // an earlier ticket); independent slices take their block index
+    int64_t sg = 0, sl = blockIdx.x;
     if (a.nseg > 1) {
-        if (tid == 0) s_i[0] = (int)atomicAdd(a.ctl, 1u);
+        if (tid == 0) {
+            int64_t si, sli;
+            take_item(a.ctl, nsl, a.nseg, &si, &sli);
+            s_i[0] = (int)si;
+            s_i[1] = (int)sli;
+        }
         __syncthreads();
-        ticket = s_i[0];
+        sg = s_i[0];
+        sl = s_i[1];
+        if (sg < 0) return;   // (cannot happen: one workgroup per item)
     }
-    const int64_t sg = ticket / nsl, sl = ticket % nsl;
     const int64_t b = sl / a.H, h = sl % a.H;
     const int64_t cbeg = sg * a.G, cend = min(cbeg + a.G, a.nchunks);
     const int64_t slot = sl * a.nseg + sg;
