@@ -189,6 +189,17 @@ void k_scan_fused(ScanArgs a) {
     constexpr int DR = DA > DC ? DA : DC;
     Blk ring[DR];
 
+    Frag cf[TPW][NK];   // C rows of the owned output tiles (rotated in the output phase)
+    constexpr bool kEarlyC = S::NJB > 1;
+    auto load_c = [&]() {
+#pragma unroll
+        for (int m = 0; m < TPW; ++m) {
+            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
+            const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + MM::KPL * g) * sizeof(T));
+#pragma unroll
+            for (int kk = 0; kk < NK; ++kk) cf[m][kk] = buf_load<Frag>(rc, off + kk * MM::K * sizeof(T));
+        }
+    };
     // ---- 2. prologue ----
     {
         // angles first (the largest prologue load): thread (pair i, segment seg)
@@ -213,6 +224,11 @@ void k_scan_fused(ScanArgs a) {
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int d = 0; d < DA; ++d) fetch(d, ring[d]);
+        __builtin_amdgcn_sched_barrier(0);
+        // chunks of several row blocks load the C rows of their output tiles
+        // now too: the round trip overlaps the aggregate and the look-back
+        // (single-block chunks have no registers to spare for them)
+        if constexpr (kEarlyC) load_c();
         __builtin_amdgcn_sched_barrier(0);
         // dt and lambda are zero past the end of the sequence, so
         // sigma_{L-1} = gamma_{L-1} and rows past the end carry zeros
@@ -588,13 +604,10 @@ void k_scan_fused(ScanArgs a) {
     }
     // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
     // end of the sequence were loaded as zeros)
-    Frag cf[TPW][NK];
+    if constexpr (!kEarlyC) load_c();
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
-        const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
-        const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + MM::KPL * g) * sizeof(T));
-#pragma unroll
-        for (int kk = 0; kk < NK; ++kk) cf[m][kk] = buf_load<Frag>(rc, off + kk * MM::K * sizeof(T));
+        const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
 #pragma unroll
         for (int kk = 0; kk < NK / 2; ++kk) {
 #pragma unroll
