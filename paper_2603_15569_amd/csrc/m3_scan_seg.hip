@@ -78,6 +78,11 @@ void k_scan_seg(ScanArgs a) {
     Acc *s_cum = s_cumb[0], *s_psie = s_psieb[0];
     __shared__ Acc s_segps[NH];         // angle totals of the segment
     __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
+    // Chunks of up to 64 tokens tabulate the causal weights of the chunk:
+    // s_W[t][j] = e^{cum_t - cum_j} sigma_j (j < t), gamma_t (j = t), 0 (j > t)
+    constexpr bool kWTab = Q <= 64;
+    constexpr int LDW = Q + 4;
+    __shared__ float s_W[kWTab ? Q * LDW : 1];
     __shared__ CS s_cs[NH * LDC];
     // Chunks of several row blocks double-buffer the staged blocks: in the
     // output pass block jb + 1 is committed while block jb feeds the MFMAs.
@@ -276,20 +281,25 @@ void k_scan_seg(ScanArgs a) {
         s_psie = s_psieb[c & 1];
         // dt and lambda read as zero past the end of the sequence, so
         // sigma_{L-1} = gamma_{L-1} and rows past the end carry zeros
-        if (wave == 0) {
+        Acc cumv[TPL];
+        float gamv[TPL], sigv[TPL];
+        {
             Acc lg[TPL], loc = 0;
 #pragma unroll
             for (int u = 0; u < TPL; ++u) {
                 lg[u] = (Acc)p.dtv[u] * (Acc)p.Av[u];
                 loc += lg[u];
+                gamv[u] = p.lamv[u] * p.dtv[u];
+                sigv[u] = gamv[u] + (1.f - p.lamn[u]) * p.dtn[u];
             }
             Acc cum = lane_scan(loc) - loc;   // exclusive over lanes
-            Acc cumv[TPL];
 #pragma unroll
             for (int u = 0; u < TPL; ++u) {
                 cum += lg[u];
                 cumv[u] = cum;
             }
+        }
+        if (wave == 0) {
             // cum_e = cum of token nv - 1
             Acc cum_e = cumv[0];
 #pragma unroll
@@ -298,14 +308,23 @@ void k_scan_seg(ScanArgs a) {
 #pragma unroll
             for (int u = 0; u < TPL; ++u) {
                 const int t = lane * TPL + u;
-                const float gam = p.lamv[u] * p.dtv[u];
-                const float sig = gam + (1.f - p.lamn[u]) * p.dtn[u];
                 if (t < Q) {
                     s_cum[t] = cumv[u];
-                    s_gam[t] = gam;
-                    s_sig[t] = sig;
-                    s_w[t] = (t < nv) ? (float)(exp_fast(cum_e - cumv[u]) * (Acc)sig) : 0.f;
+                    s_gam[t] = gamv[u];
+                    s_sig[t] = sigv[u];
+                    s_w[t] = (t < nv) ? (float)(exp_fast(cum_e - cumv[u]) * (Acc)sigv[u]) : 0.f;
                 }
+            }
+        }
+        if constexpr (kWTab) {   // wave w fills rows w*Q/NW ..; lane j is column j
+            static_assert(TPL == 1 && Q % NW == 0, "weight table layout");
+            const float cum_j = (float)cumv[0], sig_j = sigv[0];
+#pragma unroll
+            for (int k = 0; k < Q / NW; ++k) {
+                const int t = wave * (Q / NW) + k;
+                const float cum_t = (float)lane_bcast(cumv[0], t), gam_t = lane_bcast(gamv[0], t);
+                const float e = exp_fast(fminf(cum_t - cum_j, 0.f)) * sig_j;
+                if (lane < Q) s_W[t * LDW + lane] = lane < t ? e : (lane == t ? gam_t : 0.f);
             }
         }
 #pragma unroll
@@ -830,7 +849,6 @@ void k_scan_seg(ScanArgs a) {
                     const int TT = owned_tile<S>(wt, m);
                     if (J0 > TT) continue;
                     const int tt = (TT * 16 + l16) / R;
-                    const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
                     constexpr int NV = R >= 4 ? 1 : 4 / R;
 #pragma unroll
                     for (int q = 0; q < 2; ++q) {
@@ -838,8 +856,13 @@ void k_scan_seg(ScanArgs a) {
 #pragma unroll
                         for (int u = 0; u < NV; ++u) {
                             const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
-                            const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
-                            wv[u] = tj < tt ? e : (tj == tt ? gam_t : 0.f);
+                            if constexpr (kWTab) {
+                                wv[u] = s_W[tt * LDW + tj];
+                            } else {
+                                const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
+                                const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
+                                wv[u] = tj < tt ? e : (tj == tt ? gam_t : 0.f);
+                            }
                         }
 #pragma unroll
                         for (int v = 0; v < 4; ++v) gt[m][q][v] *= wv[(v * NV) / 4];
