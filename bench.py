@@ -34,6 +34,10 @@ def main():
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 10 plain device copies of 1 GiB (reference for HBM byte counters)")
+    ap.add_argument("--scan-workload", type=int, default=None, metavar="K",
+                    help="only run --steps m3_scan_fwd calls (after one warm-up call) on prefill "
+                         "workload K (1-4; the scan of workload 4 is its decode-state prefill) and "
+                         "print their mean time, for hardware-counter runs")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); every (batch, head) "
@@ -57,6 +61,33 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes_each_way": 1 << 30, "launches": 10}), flush=True)
+        return
+
+    if args.scan_workload is not None:
+        k = args.scan_workload
+        if k not in (1, 2, 3, 4):
+            print("--scan-workload takes 1, 2, 3 or 4", file=sys.stderr)
+            sys.exit(2)
+        w = WORKLOADS[k]
+        inp = workload_inputs(k, device=dev)
+        Bk, Lk, Hk, Rk, Pk = inp.x.shape
+        Nk = inp.Bm.shape[-1]
+        dims = m3.scan_dims(inp.x, inp.Bm, w["chunk"], inp.A)
+        ws = torch.zeros(m3.workspace_bytes(dims), dtype=torch.uint8, device=dev)
+        args_k = (inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta, inp.D)
+        m3.scan_fwd(*args_k, chunk=w["chunk"], workspace=ws)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            m3.scan_fwd(*args_k, chunk=w["chunk"], workspace=ws)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / max(1, args.steps)
+        fl = Bk * Hk * roofline.chunked_flops(Lk, Nk, Pk, Rk, w["chunk"])
+        print(json.dumps({"scan_workload": k, "shape": [Bk, Lk, Hk, Rk, Pk, Nk], "chunk": w["chunk"],
+                          "calls": args.steps, "ms_per_call": round(ms, 5),
+                          "alg_tflops": round(fl / ms / 1e9, 2)}), flush=True)
         return
 
     # ---------------- prefill workload (SISO bf16) ----------------
