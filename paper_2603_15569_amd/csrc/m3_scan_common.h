@@ -87,6 +87,15 @@ __device__ __forceinline__ double lane_bcast(double v, int l) {
     return __longlong_as_double(((long long)hi << 32) | (unsigned)lo);
 }
 
+// LDS transposing read (gfx950 ds_read_b64_tr_b16) of a 4 x 16 bf16 block of
+// a row-major LDS array: lane s of each 16-lane group addresses row s / 4,
+// columns 4 (s % 4) .. +3 of the block (here `p`), and lane i of the group
+// receives the block's column i, rows 0 .. 3.
+__device__ __forceinline__ bf16x4 lds_tr4(const bf16 *p) {
+    typedef __attribute__((address_space(3))) bf16x4 lds_bf16x4;
+    return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(p));
+}
+
 // Four consecutive output columns of one row, held by one lane of a
 // transposed MFMA tile (the lane's four accumulator rows are y columns).
 __device__ __forceinline__ void store4(bf16 *dst, const f32x4 &v) {

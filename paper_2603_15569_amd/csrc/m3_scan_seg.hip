@@ -87,13 +87,16 @@ void k_scan_seg(ScanArgs a) {
     // Chunks of several row blocks double-buffer the staged blocks: in the
     // output pass block jb + 1 is committed while block jb feeds the MFMAs.
     constexpr int NBUF = (NJB > 1 && sizeof(T) == 2) ? 2 : 1;
-    constexpr int kSB = S::JB * S::LDN, kSX = P * S::LDJ, kSBt = N * S::LDJ;
-    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];    // B^ blocks [row][n]; S^T [p][n]
-    __shared__ __attribute__((aligned(16))) T s_X[NBUF * kSX];    // x^T blocks [p][row]
-    __shared__ __attribute__((aligned(16))) T s_Bt[NBUF * kSBt];  // (B^ W)^T blocks [n][row]
+    // Row blocks are staged row-major (16-byte writes): B^ [row][n], x and
+    // W x [row][p].  MFMA operands whose K axis runs along the rows (x^T for
+    // y, B^T and (W x)^T for M) are read with the LDS transposing reads.
+    constexpr int LDP = P + S::PAD;
+    constexpr int kSB = S::JB * S::LDN, kSXr = S::JB * LDP;
+    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];        // B^ blocks [row][n]; S^T [p][n]
+    __shared__ __attribute__((aligned(16))) T s_XW[2 * NBUF * kSXr];  // x blocks, then W x blocks [row][p]
     __shared__ int s_i[4];
     static_assert(P == S::JB, "S^T [p][n] fits in the B^ block");
-    static_assert(NW * 16 <= NBUF * N, "y staging fits in the (B^ W)^T buffer");
+    static_assert(NW * 16 <= 2 * NBUF * S::JB, "y staging fits in the x / W x buffers");
 
     // Lane indices are re-derived from an opaque copy of the thread index at
     // the top of every chunk iteration (relane), so that the compiler
@@ -182,58 +185,69 @@ void k_scan_seg(ScanArgs a) {
             f.xv[k] = buf_load<V16>(rx, tok_off(t, xstr_b) + (uint32_t)((r * P + pc * S::CE) * sizeof(T)));
         }
     };
-    auto commit = [&](int jb, const Blk &f, auto kRow) {
-        T *sB = s_B + (jb % NBUF) * kSB, *sX = s_X + (jb % NBUF) * kSX, *sBt = s_Bt + (jb % NBUF) * kSBt;
+    // kX: also stage x itself (the output pass's operand of y)
+    auto commit = [&](int jb, const Blk &f, auto kX) {
+        T *sB = s_B + (jb % NBUF) * kSB, *sX = s_XW + (jb % NBUF) * kSXr, *sWX = s_XW + (NBUF + jb % NBUF) * kSXr;
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
-            const int row = jb * S::JB + jr, t = row / R;
+            const int t = (jb * S::JB + jr) / R;
             V16 lo = f.lo[k], hi = f.hi[k];
-            const float wt = s_w[t];
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
                 const int n = cp * S::CE + e;
                 float cs, sn;
                 cs_get(s_cs[n * LDC + t], cs, sn);
                 const float u = fget(lo, e), w = fget(hi, e);
-                const float re = cs * u + sn * w, im = cs * w - sn * u;
-                if constexpr (decltype(kRow)::value) {
-                    fset(lo, e, re);
-                    fset(hi, e, im);
-                }
-                sBt[n * S::LDJ + jr] = from_f32<T>(wt * re);
-                sBt[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
+                fset(lo, e, cs * u + sn * w);
+                fset(hi, e, cs * w - sn * u);
             }
-            if constexpr (decltype(kRow)::value) {
-                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
-                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
-            }
+            *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
+            *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
         }
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
+            const float wt = s_w[(jb * S::JB + jr) / R];
+            if constexpr (decltype(kX)::value) *reinterpret_cast<V16 *>(&sX[jr * LDP + pc * S::CE]) = f.xv[k];
+            V16 wx;
 #pragma unroll
-            for (int e = 0; e < S::CE; ++e) sX[(pc * S::CE + e) * S::LDJ + jr] = f.xv[k][e];
+            for (int e = 0; e < S::CE; ++e) fset(wx, e, wt * fget(f.xv[k], e));
+            *reinterpret_cast<V16 *>(&sWX[jr * LDP + pc * S::CE]) = wx;
         }
     };
-    // M += (B^ W)^T x over one staged block (owned state pair-tiles)
+    // MFMA operand whose K axis runs down the rows of a row-major LDS block M
+    // (leading dimension ld): lane (g, l16) receives M[r0 + k][c0 + l16] for
+    // its K elements k — 8g .. 8g+7 (bf16, two transposing reads) or g (fp32)
+    auto load_kt = [&](const T *M, int ld, int r0, int c0) -> Frag {
+        if constexpr (MM::KPL == 8) {
+            const T *p0 = M + (r0 + 8 * g + l16 / 4) * ld + c0 + 4 * (l16 % 4);
+            const bf16x4 lo = lds_tr4(p0), hi = lds_tr4(p0 + 4 * ld);
+            Frag fr;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) { fr[v] = lo[v]; fr[4 + v] = hi[v]; }
+            return fr;
+        } else {
+            return M[(r0 + g) * ld + c0 + l16];
+        }
+    };
+    // M += B^T (W x) over one staged block (owned state pair-tiles)
     // (a wave's state tiles share their row tiles, wave % 4 and wave % 4 + 4:
-    // each (B^ W)^T fragment is loaded once for all of them, each x^T
+    // each B^T fragment is loaded once for all of them, each (W x)^T
     // fragment once for both halves)
     static_assert(NW % 4 == 0, "state row tiles shared across a wave's tiles");
     auto m_block = [&](f32x4 (&ms)[PTW][2], int jb) {
-        const T *sBt = s_Bt + (jb % NBUF) * kSBt, *sX = s_X + (jb % NBUF) * kSX;
+        const T *sB = s_B + (jb % NBUF) * kSB, *sWX = s_XW + (NBUF + jb % NBUF) * kSXr;
         const int ntl = wave % 4;
 #pragma unroll
         for (int ks = 0; ks < JK; ++ks) {
-            Frag af[2];
+            Frag af[2];   // B^T
 #pragma unroll
-            for (int half = 0; half < 2; ++half)
-                af[half] = MM::load(&sBt[((ntl + 4 * half) * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+            for (int half = 0; half < 2; ++half) af[half] = load_kt(sB, S::LDN, ks * MM::K, (ntl + 4 * half) * 16);
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2) {
                 const int pt = (wave + NW * m2) / 4;
-                const Frag bf = MM::load(&sX[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                const Frag bf = load_kt(sWX, LDP, ks * MM::K, pt * 16);   // (W x)^T
 #pragma unroll
                 for (int half = 0; half < 2; ++half) ms[m2][half] = MM::mma(af[half], bf, ms[m2][half]);
             }
@@ -811,7 +825,7 @@ void k_scan_seg(ScanArgs a) {
                 fetch(min(c + jn / NJB, cend - 1), jn % NJB, ring[jb % DC]);
                 sched_fence();
             }
-            const T *sBc = s_B + (jb % NBUF) * kSB, *sXc = s_X + (jb % NBUF) * kSX;
+            const T *sBc = s_B + (jb % NBUF) * kSB, *sXc = s_XW + (jb % NBUF) * kSXr;
 #pragma unroll
             for (int jp = 0; jp < S::JB / 32; ++jp) {
                 const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
@@ -822,9 +836,9 @@ void k_scan_seg(ScanArgs a) {
                 if constexpr (MM::KPL == 8) {
 #pragma unroll
                     for (int pt = 0; pt < PTS; ++pt) {
-                        const T *xr = &sXc[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
-                        const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
-                        const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
+                        // rows 32 jp + 4g .. +3 and 32 jp + 16 + 4g .. +3 of x, column l16
+                        const T *xr = &sXc[(32 * jp + 4 * g + l16 / 4) * LDP + (pofs + pt) * 16 + 4 * (l16 % 4)];
+                        const bf16x4 lo = lds_tr4(xr), hi = lds_tr4(xr + 16 * LDP);
 #pragma unroll
                         for (int v = 0; v < 4; ++v) { xf[pt][v] = lo[v]; xf[pt][4 + v] = hi[v]; }
                     }
@@ -888,7 +902,7 @@ void k_scan_seg(ScanArgs a) {
                             for (int v = 0; v < 4; ++v)
 #pragma unroll
                                 for (int pt = 0; pt < PTS; ++pt) {
-                                    const float xv = to_f32(sXc[((pofs + pt) * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
+                                    const float xv = to_f32(sXc[(32 * jp + 16 * q + 4 * g + v) * LDP + (pofs + pt) * 16 + l16]);
                                     acc[m][pt] = MM::mma(xv, gt[m][q][v], acc[m][pt]);
                                 }
                     }
@@ -906,11 +920,11 @@ void k_scan_seg(ScanArgs a) {
             rotate_psie(ms, Sst);
             if (c == a.nchunks - 1) write_final(Sst);
         }
-        // store: each wave stages its tiles in its own part of the (B^ W)^T
-        // buffer, free after the last block's barrier (a wave's LDS accesses
+        // store: each wave stages its tiles in its own part of the x / W x
+        // buffers, free after the last block's barrier (a wave's LDS accesses
         // execute in order: no barrier), and writes whole 16-byte pieces of
         // its columns of the y rows
-        T *s_y = s_Bt + wave * (16 * S::LDJ);
+        T *s_y = s_XW + wave * (16 * LDP);
         T *Yg = static_cast<T *>(a.y) + tk * (R * P);
         constexpr int RP = PTS * 16 / S::CE;        // 16-byte pieces of a row per wave
 #pragma unroll
@@ -918,7 +932,7 @@ void k_scan_seg(ScanArgs a) {
             if (!ow) break;
             const int TT = owned_tile<S>(wt, m);
 #pragma unroll
-            for (int pt = 0; pt < PTS; ++pt) store4(&s_y[l16 * S::LDJ + pt * 16 + 4 * g], acc[m][pt]);
+            for (int pt = 0; pt < PTS; ++pt) store4(&s_y[l16 * LDP + pt * 16 + 4 * g], acc[m][pt]);
             asm volatile("" ::: "memory");
 #pragma unroll
             for (int k = lane; k < 16 * RP; k += kWave) {
@@ -926,7 +940,7 @@ void k_scan_seg(ScanArgs a) {
                 const int row = TT * 16 + rl, t = row / R, r = row % R;
                 if (t < nv)
                     *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + pofs * 16 + col) =
-                        *reinterpret_cast<const V16 *>(&s_y[rl * S::LDJ + col]);
+                        *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
             }
             asm volatile("" ::: "memory");
         }
