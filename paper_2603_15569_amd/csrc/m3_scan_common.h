@@ -96,6 +96,24 @@ __device__ __forceinline__ bf16x4 lds_tr4(const bf16 *p) {
     return __builtin_amdgcn_ds_read_tr16_b64_v4bf16((lds_bf16x4 *)(p));
 }
 
+// MFMA operand whose K axis runs down the rows of a row-major LDS block M
+// (leading dimension ld): lane (g, l16) receives M[r0 + k][c0 + l16] for its
+// K elements k — 8g .. 8g+7 (bf16: two transposing reads) or g (fp32).
+__device__ __forceinline__ bf16x8 load_kt(const bf16 *M, int ld, int r0, int c0, int g, int l16) {
+    const bf16 *p0 = M + (r0 + 8 * g + l16 / 4) * ld + c0 + 4 * (l16 % 4);
+    const bf16x4 lo = lds_tr4(p0), hi = lds_tr4(p0 + 4 * ld);
+    bf16x8 fr;
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+        fr[v] = lo[v];
+        fr[4 + v] = hi[v];
+    }
+    return fr;
+}
+__device__ __forceinline__ float load_kt(const float *M, int ld, int r0, int c0, int g, int l16) {
+    return M[(r0 + g) * ld + c0 + l16];
+}
+
 // Four consecutive output columns of one row, held by one lane of a
 // transposed MFMA tile (the lane's four accumulator rows are y columns).
 __device__ __forceinline__ void store4(bf16 *dst, const f32x4 &v) {

@@ -21,8 +21,9 @@
 //      is already resident (forward progress);
 //   2. prologue: cum (wavefront scans), gamma, sigma, w; angle prefix sums and
 //      a cos/sin table in LDS;
-//   3. aggregate first: per 64-row block, (B^ W)^T and x^T staged in LDS and
-//      M += B^T W x (MFMA, K = rows); A_c published (flag AGG);
+//   3. aggregate first: per 64-row block, B^ and W x staged row-major in LDS
+//      and M += B^T W x (MFMA, K = rows, operands read with transposing LDS
+//      reads); A_c published (flag AGG);
 //   4. decoupled look-back: predecessors' flags probed 16 at a time, their
 //      maps composed nearest first until an inclusive state (flag INC) or the
 //      sequence start; S_out published (flag INC) before any output work, so
@@ -71,15 +72,18 @@ void k_scan_fused(ScanArgs a) {
     // Chunks of several row blocks double-buffer the staged blocks: block
     // jb + 1 is committed while the MFMAs read block jb (one barrier a block).
     constexpr int NBUF = (S::NJB > 1 && sizeof(T) == 2) ? 2 : 1;   // (fp32 blocks: LDS too small)
-    constexpr int kSB = S::JB * S::LDN, kSX = P * S::LDJ;
-    constexpr int kBtS = (N * S::LDJ > P * S::LDN) ? N * S::LDJ : P * S::LDN;
-    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];      // B^ block [row][n]
-    __shared__ __attribute__((aligned(16))) T s_X[NBUF * kSX];      // x^T block [p][row]
-    __shared__ __attribute__((aligned(16))) T s_BtS[NBUF * kBtS];   // (B^ W)^T block [n][row]; later S_in^T [p][n]
+    // Row blocks are staged row-major (16-byte writes): B^ [row][n], x and
+    // W x [row][p]; MFMA operands whose K axis runs along the rows (B^T and
+    // (W x)^T for M, x^T for y) are read with the LDS transposing reads.
+    constexpr int LDP = P + S::PAD;
+    constexpr int kSB = S::JB * S::LDN, kSXr = S::JB * LDP;
+    __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];        // B^ blocks [row][n]
+    __shared__ __attribute__((aligned(16))) T s_XW[2 * NBUF * kSXr];  // x blocks, then W x blocks [row][p]
+    __shared__ __attribute__((aligned(16))) T s_S[P * S::LDN];        // S_in^T [p][n] (io dtype)
     __shared__ int s_i[4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
-    static_assert(P <= S::JB && NW * 16 <= N, "y staging fits in the (B^ W)^T buffer");
+    static_assert(P <= S::JB && NW * 16 <= 2 * NBUF * S::JB, "y staging fits in the x / W x buffers");
 
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
     const int wave = __builtin_amdgcn_readfirstlane(tid / kWave);   // uniform: scalar branches
@@ -112,10 +116,9 @@ void k_scan_fused(ScanArgs a) {
     // Rows jb*64 .. of the chunk are staged in two steps so that the global
     // loads of the next block overlap the MFMA work on this one: fetch()
     // issues the loads into registers, commit() rotates B^ = R(-psi_t) B and
-    // writes it to LDS as the w-scaled transpose (kBt: operand of M) and/or
-    // row-major (kRow: operand of G^T), together with x^T.  Consecutive lanes
-    // take consecutive rows, so the transposed LDS stores and the cos/sin
-    // table reads are conflict-free.
+    // writes it to LDS row-major, together with W x (aggregate: operand of M)
+    // and/or x (outputs: operand of y).  Consecutive lanes take consecutive
+    // rows, so the cos/sin table reads are conflict-free.
     constexpr int TB = S::JB * (NH / S::CE) / S::NTHR;   // B tasks per thread
     constexpr int TX = S::JB * (P / S::CE) / S::NTHR;    // x tasks per thread
     static_assert(TB * S::NTHR == S::JB * (NH / S::CE) && TX * S::NTHR == S::JB * (P / S::CE), "tasks");
@@ -145,40 +148,37 @@ void k_scan_fused(ScanArgs a) {
             f.xv[k] = buf_load<V16>(rx, tok_off(t, xstr_b) + (uint32_t)((r * P + pc * S::CE) * sizeof(T)));
         }
     };
-    auto commit = [&](int jb, const Blk &f, auto kBt, auto kRow) {
-        T *sB = s_B + (jb % NBUF) * kSB, *sX = s_X + (jb % NBUF) * kSX, *sBt = s_BtS + (jb % NBUF) * kBtS;
+    // kAgg: stage W x too (operand of M); kOut: stage x too (operand of y)
+    auto commit = [&](int jb, const Blk &f, auto kAgg, auto kOut) {
+        T *sB = s_B + (jb % NBUF) * kSB, *sX = s_XW + (jb % NBUF) * kSXr, *sWX = s_XW + (NBUF + jb % NBUF) * kSXr;
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
-            const int row = jb * S::JB + jr, t = row / R;
+            const int t = (jb * S::JB + jr) / R;
             V16 lo = f.lo[k], hi = f.hi[k];
-            const float wt = s_w[t];
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
                 const int n = cp * S::CE + e;
                 float cs, sn;
                 cs_get(s_cs[n * LDC + t], cs, sn);
                 const float u = fget(lo, e), w = fget(hi, e);
-                const float re = cs * u + sn * w, im = cs * w - sn * u;
-                if constexpr (decltype(kRow)::value) {
-                    fset(lo, e, re);
-                    fset(hi, e, im);
-                }
-                if constexpr (decltype(kBt)::value) {
-                    sBt[n * S::LDJ + jr] = from_f32<T>(wt * re);
-                    sBt[(n + NH) * S::LDJ + jr] = from_f32<T>(wt * im);
-                }
+                fset(lo, e, cs * u + sn * w);
+                fset(hi, e, cs * w - sn * u);
             }
-            if constexpr (decltype(kRow)::value) {
-                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
-                *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
-            }
+            *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
+            *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
         }
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
+            if constexpr (decltype(kOut)::value) *reinterpret_cast<V16 *>(&sX[jr * LDP + pc * S::CE]) = f.xv[k];
+            if constexpr (decltype(kAgg)::value) {
+                const float wt = s_w[(jb * S::JB + jr) / R];
+                V16 wx;
 #pragma unroll
-            for (int e = 0; e < S::CE; ++e) sX[(pc * S::CE + e) * S::LDJ + jr] = f.xv[k][e];
+                for (int e = 0; e < S::CE; ++e) fset(wx, e, wt * fget(f.xv[k], e));
+                *reinterpret_cast<V16 *>(&sWX[jr * LDP + pc * S::CE]) = wx;
+            }
         }
     };
     // Prefetch depth (blocks in flight, register ring): the aggregate phase
@@ -306,22 +306,22 @@ void k_scan_fused(ScanArgs a) {
             __syncthreads();
             if (jb + DA < S::NJB) fetch(jb + DA, ring[jb % DA]);
         }
-        // (a wave's state tiles share their row tiles, wave % 4 and
-        // wave % 4 + 4: each (B^ W)^T fragment is loaded once for all of
-        // them, each x^T fragment once for both halves)
+        // M += B^T (W x) (a wave's state tiles share their row tiles,
+        // wave % 4 and wave % 4 + 4: each B^T fragment is loaded once for all
+        // of them, each (W x)^T fragment once for both halves)
         static_assert(NW % 4 == 0, "state row tiles shared across a wave's tiles");
-        const T *sBt = s_BtS + (jb % NBUF) * kBtS, *sX = s_X + (jb % NBUF) * kSX;
+        const T *sB = s_B + (jb % NBUF) * kSB, *sWX = s_XW + (NBUF + jb % NBUF) * kSXr;
         const int ntl = wave % 4;
 #pragma unroll
         for (int ks = 0; ks < JK; ++ks) {
             Frag af[2];
 #pragma unroll
             for (int half = 0; half < 2; ++half)
-                af[half] = MM::load(&sBt[((ntl + 4 * half) * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                af[half] = load_kt(sB, S::LDN, ks * MM::K, (ntl + 4 * half) * 16, g, l16);
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2) {
                 const int pt = (wave + NW * m2) / 4;
-                const Frag bf = MM::load(&sX[(pt * 16 + l16) * S::LDJ + ks * MM::K + MM::KPL * g]);
+                const Frag bf = load_kt(sWX, LDP, ks * MM::K, pt * 16, g, l16);
 #pragma unroll
                 for (int half = 0; half < 2; ++half) ms[m2][half] = MM::mma(af[half], bf, ms[m2][half]);
             }
@@ -592,7 +592,6 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
         for (int d = 0; d < DC; ++d) fetch(d, ring[d]);
     }
-    T *s_S = s_BtS;   // S_in^T [p][n] in the io dtype (the (B^ W)^T block is no longer read)
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) {
         const int k = wave + NW * m2, ntl = k % 4, pt = k / 4;
@@ -621,8 +620,7 @@ void k_scan_fused(ScanArgs a) {
             }
         }
     }
-    // longer chunks restage their blocks: the first one now (double-buffered
-    // with the (B^ W)^T area, which holds S_in^T and is not written here)
+    // longer chunks restage their blocks: the first one now
     if constexpr (NBUF == 2) {
         commit(0, ring[0], False{}, True{});
         if (DC < S::NJB) fetch(DC, ring[0]);
@@ -661,7 +659,7 @@ void k_scan_fused(ScanArgs a) {
             __syncthreads();
             if (jb + DC < S::NJB) fetch(jb + DC, ring[jb % DC]);
         }
-        const T *sB = s_B + (jb % NBUF) * kSB, *sX = s_X + (jb % NBUF) * kSX;
+        const T *sB = s_B + (jb % NBUF) * kSB, *sX = s_XW + (jb % NBUF) * kSXr;
 #pragma unroll
         for (int jp = 0; jp < S::JB / 32; ++jp) {
             const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
@@ -671,9 +669,9 @@ void k_scan_fused(ScanArgs a) {
             if constexpr (MM::KPL == 8) {
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) {
-                    const T *xr = &sX[(pt * 16 + l16) * S::LDJ + 32 * jp + 4 * g];
-                    const bf16x4 lo = *reinterpret_cast<const bf16x4 *>(xr);
-                    const bf16x4 hi = *reinterpret_cast<const bf16x4 *>(xr + 16);
+                    // rows 32 jp + 4g .. +3 and 32 jp + 16 + 4g .. +3 of x, column l16
+                    const T *xr = &sX[(32 * jp + 4 * g + l16 / 4) * LDP + pt * 16 + 4 * (l16 % 4)];
+                    const bf16x4 lo = lds_tr4(xr), hi = lds_tr4(xr + 16 * LDP);
 #pragma unroll
                     for (int v = 0; v < 4; ++v) { xf[pt][v] = lo[v]; xf[pt][4 + v] = hi[v]; }
                 }
@@ -735,7 +733,7 @@ void k_scan_fused(ScanArgs a) {
                         for (int v = 0; v < 4; ++v)
 #pragma unroll
                             for (int pt = 0; pt < PT; ++pt) {
-                                const float xv = to_f32(sX[(pt * 16 + l16) * S::LDJ + 32 * jp + 16 * q + 4 * g + v]);
+                                const float xv = to_f32(sX[(32 * jp + 16 * q + 4 * g + v) * LDP + pt * 16 + l16]);
                                 acc[m][pt] = MM::mma(xv, gt[m][q][v], acc[m][pt]);
                             }
                 }
@@ -744,18 +742,18 @@ void k_scan_fused(ScanArgs a) {
         if constexpr (S::NJB > 1) __syncthreads();
     }
     // store: once every wave is past its last LDS read, each wave stages its
-    // tiles in its own part of the (B^ W)^T buffer (a wave's LDS accesses
+    // tiles in its own part of the x / W x buffers (a wave's LDS accesses
     // execute in order: no further barrier) and writes whole 16-byte pieces
     // of the y rows
     __syncthreads();
-    T *s_y = s_BtS + wave * (16 * S::LDJ);
+    T *s_y = s_XW + wave * (16 * LDP);
     T *Yg = static_cast<T *>(a.y) + tok0 * (R * P);
     constexpr int RP = P / S::CE;                   // 16-byte pieces of a row
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int TT = owned_tile<S>(wave, m);
 #pragma unroll
-        for (int pt = 0; pt < PT; ++pt) store4(&s_y[l16 * S::LDJ + pt * 16 + 4 * g], acc[m][pt]);
+        for (int pt = 0; pt < PT; ++pt) store4(&s_y[l16 * LDP + pt * 16 + 4 * g], acc[m][pt]);
         asm volatile("" ::: "memory");
 #pragma unroll
         for (int k = lane; k < 16 * RP; k += kWave) {
@@ -763,7 +761,7 @@ void k_scan_fused(ScanArgs a) {
             const int row = TT * 16 + rl, t = row / R, r = row % R;
             if (t < nvalid)
                 *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) =
-                    *reinterpret_cast<const V16 *>(&s_y[rl * S::LDJ + col]);
+                    *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
         }
         asm volatile("" ::: "memory");
     }

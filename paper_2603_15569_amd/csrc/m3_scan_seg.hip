@@ -150,10 +150,10 @@ void k_scan_seg(ScanArgs a) {
     auto sched_fence = []() { __builtin_amdgcn_sched_barrier(0); };
 
     // Row blocks: fetch() issues the global loads of B and x rows into
-    // registers, commit() rotates B^ = R(-psi_t) B and writes it to LDS as the
-    // w-scaled transpose (operand of M) and row-major (operand of G^T),
-    // together with x^T.  Consecutive lanes take consecutive rows, so the
-    // transposed LDS stores and the cos/sin table reads are conflict-free.
+    // registers, commit() rotates B^ = R(-psi_t) B and writes it to LDS
+    // row-major (operand of G^T and, read transposed, of M), together with
+    // W x (operand of M) and, in the output pass, x.  Consecutive lanes take
+    // consecutive rows, so the cos/sin table reads are conflict-free.
     constexpr int TB = S::JB * (NH / S::CE) / S::NTHR;   // B tasks per thread
     constexpr int TX = S::JB * (P / S::CE) / S::NTHR;    // x tasks per thread
     static_assert(TB * S::NTHR == S::JB * (NH / S::CE) && TX * S::NTHR == S::JB * (P / S::CE), "tasks");
@@ -216,21 +216,7 @@ void k_scan_seg(ScanArgs a) {
             *reinterpret_cast<V16 *>(&sWX[jr * LDP + pc * S::CE]) = wx;
         }
     };
-    // MFMA operand whose K axis runs down the rows of a row-major LDS block M
-    // (leading dimension ld): lane (g, l16) receives M[r0 + k][c0 + l16] for
-    // its K elements k — 8g .. 8g+7 (bf16, two transposing reads) or g (fp32)
-    auto load_kt = [&](const T *M, int ld, int r0, int c0) -> Frag {
-        if constexpr (MM::KPL == 8) {
-            const T *p0 = M + (r0 + 8 * g + l16 / 4) * ld + c0 + 4 * (l16 % 4);
-            const bf16x4 lo = lds_tr4(p0), hi = lds_tr4(p0 + 4 * ld);
-            Frag fr;
-#pragma unroll
-            for (int v = 0; v < 4; ++v) { fr[v] = lo[v]; fr[4 + v] = hi[v]; }
-            return fr;
-        } else {
-            return M[(r0 + g) * ld + c0 + l16];
-        }
-    };
+    auto load_kt = [&](const T *M, int ld, int r0, int c0) -> Frag { return scan::load_kt(M, ld, r0, c0, g, l16); };
     // M += B^T (W x) over one staged block (owned state pair-tiles)
     // (a wave's state tiles share their row tiles, wave % 4 and wave % 4 + 4:
     // each B^T fragment is loaded once for all of them, each (W x)^T
