@@ -833,14 +833,21 @@ void k_scan_seg(ScanArgs a) {
                 f32x4 gt[TPW][2];
 #pragma unroll
                 for (int m = 0; m < TPW; ++m) gt[m][0] = gt[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+                // (the pair's B^ fragments are loaded before the MFMAs, whose
+                // per-tile conditions split the code into small blocks)
+                Frag bfr[2][NK];
+#pragma unroll
+                for (int q = 0; q < 2; ++q)
+#pragma unroll
+                    for (int kk = 0; kk < NK; ++kk)
+                        bfr[q][kk] = MM::load(&sBc[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
 #pragma unroll
                 for (int q = 0; q < 2; ++q)
 #pragma unroll
                     for (int kk = 0; kk < NK; ++kk) {
-                        const Frag bfr = MM::load(&sBc[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
 #pragma unroll
                         for (int m = 0; m < TPW; ++m)
-                            if (J0 + q <= owned_tile<S>(wt, m)) gt[m][q] = MM::mma(bfr, cf[m][kk], gt[m][q]);
+                            if (J0 + q <= owned_tile<S>(wt, m)) gt[m][q] = MM::mma(bfr[q][kk], cf[m][kk], gt[m][q]);
                     }
                 // mask weights (branch-free): w_tj = e^{cum_t - cum_j} sigma_j (j < t),
                 // gamma_t (j = t), 0 (j > t); D x_t as D on the diagonal row = column
