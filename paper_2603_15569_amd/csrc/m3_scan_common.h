@@ -18,6 +18,61 @@ __device__ __forceinline__ void cs_put(h2 *p, float c, float s) { *p = h2{(_Floa
 __device__ __forceinline__ void cs_put(float2 *p, float c, float s) { *p = make_float2(c, s); }
 __device__ __forceinline__ void cs_get(const h2 &v, float &c, float &s) { c = (float)v.c; s = (float)v.s; }
 __device__ __forceinline__ void cs_get(const float2 &v, float &c, float &s) { c = v.x; s = v.y; }
+// K consecutive (cos, sin) entries of a row of the table (16-byte LDS reads
+// when K fills them; p is then 16-byte aligned)
+struct alignas(16) h2x4 { h2 v[4]; };
+struct alignas(16) f2x2 { float2 v[2]; };
+template <int K>
+__device__ __forceinline__ void cs_getn(const h2 *p, float (&c)[K], float (&s)[K]) {
+    if constexpr (K % 4 == 0) {
+#pragma unroll
+        for (int q = 0; q < K / 4; ++q) {
+            const h2x4 w = *reinterpret_cast<const h2x4 *>(p + 4 * q);
+#pragma unroll
+            for (int j = 0; j < 4; ++j) cs_get(w.v[j], c[4 * q + j], s[4 * q + j]);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < K; ++j) cs_get(p[j], c[j], s[j]);
+    }
+}
+template <int K>
+__device__ __forceinline__ void cs_getn(const float2 *p, float (&c)[K], float (&s)[K]) {
+    if constexpr (K % 2 == 0) {
+#pragma unroll
+        for (int q = 0; q < K / 2; ++q) {
+            const f2x2 w = *reinterpret_cast<const f2x2 *>(p + 2 * q);
+#pragma unroll
+            for (int j = 0; j < 2; ++j) cs_get(w.v[j], c[2 * q + j], s[2 * q + j]);
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < K; ++j) cs_get(p[j], c[j], s[j]);
+    }
+}
+// K consecutive entries written from registers (16-byte LDS writes)
+template <int K>
+__device__ __forceinline__ void cs_putn(h2 *p, const float (&c)[K], const float (&s)[K]) {
+    static_assert(K % 4 == 0, "16-byte pieces");
+#pragma unroll
+    for (int q = 0; q < K / 4; ++q) {
+        h2x4 w;
+#pragma unroll
+        for (int j = 0; j < 4; ++j) w.v[j] = h2{(_Float16)c[4 * q + j], (_Float16)s[4 * q + j]};
+        *reinterpret_cast<h2x4 *>(p + 4 * q) = w;
+    }
+}
+template <int K>
+__device__ __forceinline__ void cs_putn(float2 *p, const float (&c)[K], const float (&s)[K]) {
+    static_assert(K % 2 == 0, "16-byte pieces");
+#pragma unroll
+    for (int q = 0; q < K / 2; ++q) {
+        f2x2 w;
+#pragma unroll
+        for (int j = 0; j < 2; ++j) w.v[j] = make_float2(c[2 * q + j], s[2 * q + j]);
+        *reinterpret_cast<f2x2 *>(p + 2 * q) = w;
+    }
+}
 
 template <typename T> struct Vec16;            // 16-byte vector of T
 template <> struct Vec16<bf16> { typedef bf16x8 type; static constexpr int n = 8; };

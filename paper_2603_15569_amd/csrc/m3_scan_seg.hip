@@ -63,7 +63,9 @@ void k_scan_seg(ScanArgs a) {
     constexpr int NK = N / MM::K;       // MFMA K-steps over the state axis
     constexpr int JK = S::JB / MM::K;   // MFMA K-steps over a 64-row block
     constexpr int PT = P / 16;
-    constexpr int LDC = Q + 1;          // cos/sin table [pair][token], padded
+    // cos/sin table [token][pair]: a thread's consecutive pairs are 16-byte
+    // LDS pieces; rows 32 bytes longer than the pairs (bank spread)
+    constexpr int LDT = NH + 32 / (int)sizeof(typename S::CS);
     constexpr int NJB = S::NJB;
     constexpr int NSP = S::NW / S::NWO;  // waves sharing a row tile (column split)
     constexpr int PTS = PT / NSP;       // 16-column tiles of y per wave
@@ -83,7 +85,7 @@ void k_scan_seg(ScanArgs a) {
     constexpr bool kWTab = Q <= 64;
     constexpr int LDW = Q + 4;
     __shared__ float s_W[kWTab ? Q * LDW : 1];
-    __shared__ CS s_cs[NH * LDC];
+    __shared__ __attribute__((aligned(16))) CS s_cs[Q * LDT];
     // Chunks of several row blocks double-buffer the staged blocks: in the
     // output pass block jb + 1 is committed while block jb feeds the MFMAs.
     constexpr int NBUF = (NJB > 1 && sizeof(T) == 2) ? 2 : 1;
@@ -193,14 +195,13 @@ void k_scan_seg(ScanArgs a) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
             const int t = (jb * S::JB + jr) / R;
             V16 lo = f.lo[k], hi = f.hi[k];
+            float csv[S::CE], snv[S::CE];
+            cs_getn<S::CE>(&s_cs[t * LDT + cp * S::CE], csv, snv);
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
-                const int n = cp * S::CE + e;
-                float cs, sn;
-                cs_get(s_cs[n * LDC + t], cs, sn);
                 const float u = fget(lo, e), w = fget(hi, e);
-                fset(lo, e, cs * u + sn * w);
-                fset(hi, e, cs * w - sn * u);
+                fset(lo, e, csv[e] * u + snv[e] * w);
+                fset(hi, e, csv[e] * w - snv[e] * u);
             }
             *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
             *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
@@ -327,6 +328,7 @@ void k_scan_seg(ScanArgs a) {
                 if (lane < Q) s_W[t * LDW + lane] = lane < t ? e : (lane == t ? gam_t : 0.f);
             }
         }
+        float csv[TPL][PPW], snv[TPL][PPW];
 #pragma unroll
         for (int k = 0; k < PPW; ++k) {
             const int i = wave * PPW + k;
@@ -341,13 +343,17 @@ void k_scan_seg(ScanArgs a) {
             for (int u = 0; u < TPL; ++u) {
                 const int t = lane * TPL + u;
                 psi += th[u];
-                if (t < Q) {
-                    Acc sn, cs;
-                    sincos_fast(psi, &sn, &cs);
-                    cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
-                    if (t == nv - 1) s_psie[i] = psi;
-                }
+                Acc sn, cs;
+                sincos_fast(psi, &sn, &cs);
+                csv[u][k] = (float)cs;
+                snv[u][k] = (float)sn;
+                if (t == nv - 1) s_psie[i] = psi;
             }
+        }
+#pragma unroll
+        for (int u = 0; u < TPL; ++u) {
+            const int t = lane * TPL + u;
+            if (t < Q) cs_putn<PPW>(&s_cs[t * LDT + wave * PPW], csv[u], snv[u]);
         }
         __syncthreads();
     };
@@ -732,14 +738,13 @@ void k_scan_seg(ScanArgs a) {
             const int row = owned_tile<S>(wt, m) * 16 + l16, t = row / R;
 #pragma unroll
             for (int kk = 0; kk < NK / 2; ++kk) {
+                float csv[MM::KPL], snv[MM::KPL];
+                cs_getn<MM::KPL>(&s_cs[t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
 #pragma unroll
                 for (int e = 0; e < MM::KPL; ++e) {
-                    const int n = kk * MM::K + MM::KPL * g + e;
-                    float cs, sn;
-                    cs_get(s_cs[n * LDC + t], cs, sn);
                     const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
-                    fset(cf[m][kk], e, cs * u + sn * w);
-                    fset(cf[m][kk + NK / 2], e, cs * w - sn * u);
+                    fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
+                    fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
                 }
             }
         }
