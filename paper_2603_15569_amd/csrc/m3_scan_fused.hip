@@ -62,13 +62,15 @@ void k_scan_fused(ScanArgs a) {
     constexpr int NK = N / MM::K;       // MFMA K-steps over the state axis
     constexpr int JK = S::JB / MM::K;   // MFMA K-steps over a 64-row block
     constexpr int PT = P / 16;
-    constexpr int LDC = Q + 1;          // cos/sin table [pair][token], padded
+    // cos/sin table [token][pair]: a thread's consecutive pairs are 16-byte
+    // LDS pieces; rows 32 bytes longer than the pairs (bank spread)
+    constexpr int LDT = NH + 32 / (int)sizeof(typename S::CS);
 
     __shared__ Acc s_cum[Q];
     __shared__ Acc s_wtot[NW];
     __shared__ Acc s_psie[NH];
     __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
-    __shared__ CS s_cs[NH * LDC];
+    __shared__ __attribute__((aligned(16))) CS s_cs[Q * LDT];
     // Chunks of several row blocks double-buffer the staged blocks: block
     // jb + 1 is committed while the MFMAs read block jb (one barrier a block).
     constexpr int NBUF = (S::NJB > 1 && sizeof(T) == 2) ? 2 : 1;   // (fp32 blocks: LDS too small)
@@ -156,14 +158,13 @@ void k_scan_fused(ScanArgs a) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
             const int t = (jb * S::JB + jr) / R;
             V16 lo = f.lo[k], hi = f.hi[k];
+            float csv[S::CE], snv[S::CE];
+            cs_getn<S::CE>(&s_cs[t * LDT + cp * S::CE], csv, snv);
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
-                const int n = cp * S::CE + e;
-                float cs, sn;
-                cs_get(s_cs[n * LDC + t], cs, sn);
                 const float u = fget(lo, e), w = fget(hi, e);
-                fset(lo, e, cs * u + sn * w);
-                fset(hi, e, cs * w - sn * u);
+                fset(lo, e, csv[e] * u + snv[e] * w);
+                fset(hi, e, csv[e] * w - snv[e] * u);
             }
             *reinterpret_cast<V16 *>(&sB[jr * S::LDN + cp * S::CE]) = lo;
             *reinterpret_cast<V16 *>(&sB[jr * S::LDN + NH + cp * S::CE]) = hi;
@@ -268,7 +269,7 @@ void k_scan_fused(ScanArgs a) {
                 const Acc psi = ps[k] + off;
                 Acc sn, cs;
                 sincos_fast(psi, &sn, &cs);
-                cs_put(&s_cs[i * LDC + t], (float)cs, (float)sn);
+                cs_put(&s_cs[t * LDT + i], (float)cs, (float)sn);
                 if (t == nvalid - 1) s_psie[i] = psi;
             }
         }
@@ -609,14 +610,13 @@ void k_scan_fused(ScanArgs a) {
         const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
 #pragma unroll
         for (int kk = 0; kk < NK / 2; ++kk) {
+            float csv[MM::KPL], snv[MM::KPL];
+            cs_getn<MM::KPL>(&s_cs[t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
 #pragma unroll
             for (int e = 0; e < MM::KPL; ++e) {
-                const int n = kk * MM::K + MM::KPL * g + e;
-                float cs, sn;
-                cs_get(s_cs[n * LDC + t], cs, sn);
                 const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
-                fset(cf[m][kk], e, cs * u + sn * w);
-                fset(cf[m][kk + NK / 2], e, cs * w - sn * u);
+                fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
+                fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
             }
         }
     }
