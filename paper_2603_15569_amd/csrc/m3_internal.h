@@ -60,6 +60,8 @@ ScanImpl find_scan_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 step_launch_fn find_step_impl(int io, int64_t N, int64_t P, int64_t R);
 scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 scan_launch_fn find_seg_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+// warp-specialised kernel for one segment per slice (null: none for the shape)
+scan_launch_fn find_ws_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 
 // Control words of the single-pass scans (start of their workspace): ctl[0]
 // the ticket counter, ctl[1] the count of look-back waits that timed out, and

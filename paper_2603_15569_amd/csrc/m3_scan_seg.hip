@@ -965,6 +965,10 @@ hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
     G = G < 1 ? 1 : (G > a.nchunks ? a.nchunks : G);
     a.G = G;
     a.nseg = (a.nchunks + G - 1) / G;
+    // one segment per slice: the warp-specialised kernel, where built
+    if (a.nseg == 1 && std::is_same<T, bf16>::value) {
+        if (scan_launch_fn f = find_ws_impl(1, S::N, S::P, R, Q)) return f(a, stream);
+    }
     if (a.nseg > 1) {
         const int64_t nflags = nsl * a.nseg;
         const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);

@@ -308,6 +308,26 @@ def test_segment_lengths_with_initial_state(seg):
                  init_carry=c0, label=f"seg{seg}+init")
 
 
+@pytest.mark.parametrize("L", [1, 37, 64, 64 * 5 + 17, 64 * 12])
+def test_one_segment_per_slice(L):
+    """Each slice scanned whole by one workgroup (R=4, chunk 64: the
+    warp-specialised kernel): one token, one partial chunk, one full chunk,
+    a ragged tail and whole chunks, continuing from an initial state and
+    carry."""
+    N, P, R, Q = 128, 64, 4, 64
+    say(f"one segment per slice bf16 R={R} Q={Q} L={L}")
+    inp = make_scan_inputs(2, L, 3, P, N, R, io="bf16", seed=400 + L, device=DEV, chunk=Q)
+    st0 = torch.randn(2, 3, N, P, device=DEV)
+    c0 = (torch.randn(2, 3, R, N, device=DEV).to(torch.bfloat16),
+          torch.randn(2, 3, R, P, device=DEV).to(torch.bfloat16))
+    y, fs, cB, cX = run_scan(inp, Q, init_state=st0, init_carry=c0, seg=1 << 20)
+    check_slices(inp, y, fs, cB, cX, sample_slices(2, 3, 99, 3), TOL["bf16"], init_state=st0,
+                 init_carry=c0, label=f"one segment L={L}")
+    y0, fs0, _, _ = run_scan(inp, Q, seg=1 << 20)
+    check_slices(inp, y0, fs0, cB, cX, sample_slices(2, 3, 99, 4), TOL["bf16"],
+                 label=f"one segment L={L} zero state")
+
+
 def test_chunk_size_invariance():
     """Results do not depend on the chunk length (Sec. 3.3)."""
     say("chunk invariance bf16 R=4 Q in {32, 64, 128}")
