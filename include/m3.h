@@ -79,7 +79,9 @@ typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
  * slice are linked by a decoupled look-back over their state maps.  When
  * seg_chunks is 0 and chunks of fewer than 128 rows (chunk * rank) would need
  * several segments per slice, the one-chunk-per-workgroup kernel runs
- * instead (it is faster there).
+ * instead (it is faster there).  When a slice is one segment and io is bf16
+ * with rank 4 and chunk 64, a warp-specialised variant runs (half of its
+ * waves form the outputs, half stage the inputs and carry the state).
  * M3_SCAN_SPLIT: three kernels (chunk states, a state pass over chunks,
  * chunk outputs); the only path for other shapes, and for tokens wider than
  * the single-pass kernels' 32-bit row offsets allow (nheads * rank *
