@@ -359,7 +359,30 @@ def test_per_token_A():
         assert oracle.rel_err(fs[b, h].cpu().numpy(), rs[k]) <= 1e-5
 
 
-@pytest.mark.parametrize("mode,seg", [("seg", 0), ("seg", 2), ("per_chunk", 0)])
+@pytest.mark.parametrize("mode,seg", [("seg", 1 << 20), ("seg", 2), ("per_chunk", 0)])
+def test_per_token_A_bf16_mimo(mode, seg):
+    """Per-token A_t through the bf16 rank-4 kernels: one segment per slice
+    (the warp-specialised kernel), two-chunk segments and one chunk per
+    workgroup."""
+    say(f"per-token A bf16 R=4 mode={mode} seg={seg}")
+    L = 3 * 64 + 29
+    inp = make_scan_inputs(2, L, 2, 64, 128, 4, io="bf16", seed=23, device=DEV, chunk=64)
+    A_t = -torch.rand(2, L, 2, device=DEV) * 4 - 0.1
+    kw = dict(per_chunk=mode == "per_chunk", seg=seg)
+    y, fs, (cB, cX) = m3.scan_fwd(inp.x, inp.Bm, inp.Cm, inp.dt, A_t, inp.lam, inp.theta, inp.D,
+                                  chunk=64, **kw)
+    torch.cuda.synchronize()
+    sl = [(0, 0), (1, 1)]
+    ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                inp.D, sl)
+    ref["A"] = np.stack([A_t[b, :, h].double().cpu().numpy() for b, h in sl])
+    ry, rs, _, _ = oracle.scan(**ref)
+    for k, (b, h) in enumerate(sl):
+        assert oracle.rel_err(y[b, :, h].double().cpu().numpy(), ry[k]) <= TOL["bf16"]
+        assert oracle.rel_err(fs[b, h].cpu().numpy(), rs[k]) <= TOL["bf16"]
+
+
+@pytest.mark.parametrize("mode,seg", [("seg", 0), ("seg", 1 << 20), ("seg", 2), ("per_chunk", 0)])
 def test_determinism(mode, seg):
     """Two runs give bitwise-identical outputs (no atomics in reductions)."""
     say(f"determinism bf16 R=4 mode={mode} seg={seg}")
