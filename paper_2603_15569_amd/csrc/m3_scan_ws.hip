@@ -186,8 +186,11 @@ void k_scan_ws(ScanArgs a) {
                 const T *sBc = s_B[jb & 1], *sXc = s_X[jb & 1];
 #pragma unroll
                 for (int jp = 0; jp < S::JB / 32; ++jp) {
+                    // Owned tile m lies in block m (rows 64 m .. 64 m + 63): tiles
+                    // m < jb are above this block (no work), tiles m > jb below
+                    // it (every pair unmasked); only tile jb needs the row test.
                     const int J0 = jb * 4 + 2 * jp;   // first j-tile of the pair (chunk-global)
-                    if (J0 > TT[TPW - 1]) continue;   // the last owned tile is the lowest one
+                    if (jb == NJB - 1 && J0 > TT[TPW - 1]) continue;
                     // x^T columns of the pair: rows 32 jp + 4g .. +3 and +16, column l16
                     bf16x8 xf[PT];
 #pragma unroll
@@ -218,13 +221,14 @@ void k_scan_ws(ScanArgs a) {
                         for (int kk = 0; kk < NK; ++kk)
 #pragma unroll
                             for (int m = 0; m < TPW; ++m)
-                                if (J0 + q <= TT[m]) gt[m][q] = MM::mma(bfr[kk], cf[m][kk], gt[m][q]);
+                                if (m > jb || (m == jb && J0 + q <= TT[m]))
+                                    gt[m][q] = MM::mma(bfr[kk], cf[m][kk], gt[m][q]);
                     }
                     // mask weights: w_tj = e^{cum_t - cum_j} sigma_j (j < t),
                     // gamma_t (j = t), 0 (j > t); D x_t on the diagonal
 #pragma unroll
                     for (int m = 0; m < TPW; ++m) {
-                        if (J0 > TT[m]) continue;
+                        if (m < jb || (m == jb && J0 > TT[m])) continue;
                         const int tt = (TT[m] * 16 + l16) / R;
 #pragma unroll
                         for (int q = 0; q < 2; ++q) {
@@ -232,7 +236,7 @@ void k_scan_ws(ScanArgs a) {
 #pragma unroll
                             for (int u = 0; u < NV; ++u) {
                                 const float e = exp_fast(fminf(cum_t[m] - cj[q][u], 0.f)) * sj[q][u];
-                                if (J0 + q < TT[m]) {
+                                if (m > jb || J0 + q < TT[m]) {
                                     wv[u] = e;
                                 } else {
                                     const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
@@ -241,7 +245,7 @@ void k_scan_ws(ScanArgs a) {
                             }
 #pragma unroll
                             for (int v = 0; v < 4; ++v) gt[m][q][v] *= wv[(v * NV) / 4];
-                            if (J0 + q == TT[m]) {
+                            if (m == jb && J0 + q == TT[m]) {
 #pragma unroll
                                 for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
                             }
