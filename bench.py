@@ -112,8 +112,25 @@ def main():
     # ---------------- decode workload (B=256, MIMO R=4) ----------------
     wd = WORKLOADS[4]
     layer = workload_inputs(4, device=dev)
-    _, dstate, (dcB, dcX) = m3.scan_fwd(layer.x, layer.Bm, layer.Cm, layer.dt, layer.A,
-                                        layer.lam, layer.theta, layer.D, chunk=wd["chunk"])
+    pre_args = (layer.x, layer.Bm, layer.Cm, layer.dt, layer.A, layer.lam, layer.theta, layer.D)
+    _, dstate, (dcB, dcX) = m3.scan_fwd(*pre_args, chunk=wd["chunk"])
+    # The same MIMO prefill (rank 4, 8192 slices), timed: a few more calls
+    # writing the same state (the decode steps start from it).
+    mimo_out = (torch.empty_like(layer.x), dstate, dcB, dcX)
+    mimo_ws = torch.empty(max(m3.workspace_bytes(m3.scan_dims(layer.x, layer.Bm, wd["chunk"], layer.A)), 1),
+                          dtype=torch.uint8, device=dev)
+    n_mimo = 3
+    mimo_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_mimo + 1)]
+    torch.cuda.synchronize()
+    mimo_ev[0].record(stream)
+    for i in range(n_mimo):
+        m3.scan_fwd(*pre_args, chunk=wd["chunk"], out=mimo_out, workspace=mimo_ws)
+        mimo_ev[i + 1].record(stream)
+    torch.cuda.synchronize()
+    mimo_ms = float(np.mean([mimo_ev[i].elapsed_time(mimo_ev[i + 1]) for i in range(n_mimo)]))
+    Bm_, Lm_, Hm_, Rm_, Pm_ = layer.x.shape
+    Nm_ = layer.Bm.shape[-1]
+    del mimo_out, mimo_ws, pre_args
     del layer.x, layer.Bm, layer.Cm, layer.theta, layer.lam, layer.dt  # free the prefill inputs
     torch.cuda.synchronize()
     n_step_inputs = max(1, min(args.steps + args.warmup, wd["steps"]))
@@ -203,11 +220,31 @@ def main():
             "mfma_tflops": round(pre_tfs, 2),
             "mfma_frac": round(pre_tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
         },
+        "roofline_prefill_mimo": mimo_roofline(Bm_, Lm_, Hm_, Nm_, Pm_, Rm_, wd["chunk"], mimo_ms,
+                                               roofline, peak_gbs),
         "wall_s_timed_loop": round(wall, 3),
     }
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(base, layer, step_in, wp, wd)
     print(json.dumps(result), flush=True)
+
+
+def mimo_roofline(B, L, H, N, P, R, Q, ms, roofline, peak_gbs):
+    """HBM and MFMA rates of the rank-4 prefill that builds the decode state
+    (mean over a few calls; not part of the timed step)."""
+    nbytes = roofline.prefill_bytes(B, L, H, N, P, R, 2)
+    flops = B * H * roofline.chunked_flops(L, N, P, R, Q)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    tfs = flops / (ms * 1e-3) / 1e12
+    return {
+        "kernel": "m3_scan_fwd (warp-specialised kernel, one workgroup per slice)",
+        "workload": f"prefill B={B} L={L} H={H} P={P} N={N} R={R} chunk={Q} bf16",
+        "ms": round(ms, 4), "tokens_per_s": round(B * L / (ms * 1e-3), 1),
+        "bound": "hbm", "achieved": round(gbs, 1), "peak": peak_gbs, "unit": "GB/s",
+        "frac": round(gbs / peak_gbs, 4), "traffic": measured_traffic("k_scan_ws_mimo"),
+        "bytes_per_launch": nbytes,
+        "mfma_tflops": round(tfs, 2), "mfma_frac": round(tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
+    }
 
 
 def measured_traffic(key):
