@@ -354,7 +354,18 @@ void k_scan_fused(ScanArgs a) {
     };
     const int64_t SZ = (int64_t)N * P;
     Acc *totp = static_cast<Acc *>(a.tot);
-    if (c > 0 && !last) {   // publish the aggregate (only successors read it)
+    // publish the aggregate (only successors read it), unless (chunks of
+    // several row blocks) the predecessor's inclusive state is already there:
+    // this chunk's own then follows at once, and successors that find no flag
+    // wait for it.  (Single-block chunks measured faster always publishing.)
+    bool publish_agg = c > 0 && !last;
+    if (S::NJB > 1 && publish_agg) {
+        if (tid == 0)
+            s_i[0] = __hip_atomic_load(a.flags + slot - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != kFlagInc;
+        __syncthreads();
+        publish_agg = s_i[0] != 0;
+    }
+    if (publish_agg) {
         unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.agg + slot * SZ);
 #pragma unroll
         for (int m2 = 0; m2 < PTW; ++m2)
