@@ -10,8 +10,8 @@
 //   S  <-  R(psi_e) (e^{cum_e} S + M),   M = sum_j e^{cum_e - cum_j} sigma_j B^_j x_j^T.
 //
 // The eight waves take two roles, one wave of each on every SIMD (waves w and
-// w + 4 share a SIMD), so that one role's vector arithmetic issues while the
-// other role's matrix instructions run:
+// w + 4 share a SIMD), so that the two roles' work can overlap there (the
+// outputs are MFMA-heavy, the staging and prologue VALU-heavy):
 //   output waves (0-3) own 16-row output tiles: they rotate their C rows,
 //     form y = e^{cum_t} C^ S and, per staged row block, the masked
 //     G^T = B^ C^T, y += (w o G) x, and store y;
