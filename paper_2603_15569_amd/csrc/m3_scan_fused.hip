@@ -289,8 +289,14 @@ void k_scan_fused(ScanArgs a) {
     f32x4 ms[PTW][2];
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    // With two LDS buffers the last two blocks also stage x: the output pass
+    // starts from them (blocks in reverse order) without reloading them.
+    auto commit_agg = [&](int jb, const Blk &f) {
+        if (NBUF == 2 && jb >= S::NJB - 2) commit(jb, f, True{}, True{});
+        else commit(jb, f, True{}, False{});
+    };
     if constexpr (NBUF == 2) {
-        commit(0, ring[0], True{}, False{});
+        commit_agg(0, ring[0]);
         __syncthreads();
         if (DA < S::NJB) fetch(DA, ring[0]);
     }
@@ -298,7 +304,7 @@ void k_scan_fused(ScanArgs a) {
     for (int jb = 0; jb < S::NJB; ++jb) {
         if constexpr (NBUF == 2) {
             if (jb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
-                commit(jb + 1, ring[(jb + 1) % DA], True{}, False{});
+                commit_agg(jb + 1, ring[(jb + 1) % DA]);
                 if (jb + 1 + DA < S::NJB) fetch(jb + 1 + DA, ring[(jb + 1) % DA]);
             }
         } else {
@@ -599,8 +605,12 @@ void k_scan_fused(ScanArgs a) {
 
     // ---- 5. outputs ----
     // Longer chunks restage their blocks: the first ones are fetched now (after
-    // the look-back and the publication, whose waits would drain them).
-    if constexpr (S::NJB > 1) {
+    // the look-back and the publication, whose waits would drain them).  With
+    // two LDS buffers the blocks run in reverse order, the last two still
+    // staged from the aggregate, so the first block to reload is NJB - 3.
+    if constexpr (NBUF == 2) {
+        if (S::NJB >= 3) fetch(S::NJB - 3, ring[0]);
+    } else if constexpr (S::NJB > 1) {
 #pragma unroll
         for (int d = 0; d < DC; ++d) fetch(d, ring[d]);
     }
@@ -631,12 +641,7 @@ void k_scan_fused(ScanArgs a) {
             }
         }
     }
-    // longer chunks restage their blocks: the first one now
-    if constexpr (NBUF == 2) {
-        commit(0, ring[0], False{}, True{});
-        if (DC < S::NJB) fetch(DC, ring[0]);
-    }
-    __syncthreads();   // s_S and the first block complete
+    __syncthreads();   // s_S complete
     // inter-chunk term e^{cum_t} C^_t . S_in starts the accumulators.  The
     // output tiles are transposed (y^T = S^T C^T, y^T += x^T (w o G)^T): lane
     // l holds row l % 16 of a tile and four consecutive columns.
@@ -659,11 +664,12 @@ void k_scan_fused(ScanArgs a) {
     // intra-chunk term over the row blocks at or below each owned tile
     const float Dh = a.D[h];
 #pragma unroll
-    for (int jb = 0; jb < S::NJB; ++jb) {
+    for (int pi = 0; pi < S::NJB; ++pi) {
+        const int jb = NBUF == 2 ? S::NJB - 1 - pi : pi;   // block of this step
         if constexpr (NBUF == 2) {
-            if (jb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
-                commit(jb + 1, ring[(jb + 1) % DC], False{}, True{});
-                if (jb + 1 + DC < S::NJB) fetch(jb + 1 + DC, ring[(jb + 1) % DC]);
+            if (pi >= 1 && jb >= 1) {   // stage the next block (jb - 1) while this one feeds the MFMAs
+                commit(jb - 1, ring[0], False{}, True{});
+                if (jb >= 2) fetch(jb - 2, ring[0]);
             }
         } else if constexpr (S::NJB > 1) {
             commit(jb, ring[jb % DC], False{}, True{});
