@@ -817,6 +817,12 @@ void k_scan_seg(ScanArgs a) {
                 sched_fence();
             }
             const T *sBc = s_B + (jb % NBUF) * kSB, *sXc = s_XW + (jb % NBUF) * kSXr;
+            // Owned tile m lies in rows 16 m NWO .. 16 (m + 1) NWO - 1: tiles
+            // whose blocks all come before block jb have no work in it, tiles
+            // whose blocks all come after it take every pair unmasked; only
+            // the others compare rows.
+            auto tile_above = [&](int m) { return ((m + 1) * S::NWO - 1) / 4 < jb; };
+            auto tile_below = [&](int m) { return (m * S::NWO) / 4 > jb; };
 #pragma unroll
             for (int jp = 0; jp < S::JB / 32; ++jp) {
                 const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
@@ -852,14 +858,15 @@ void k_scan_seg(ScanArgs a) {
                     for (int kk = 0; kk < NK; ++kk) {
 #pragma unroll
                         for (int m = 0; m < TPW; ++m)
-                            if (J0 + q <= owned_tile<S>(wt, m)) gt[m][q] = MM::mma(bfr[q][kk], cf[m][kk], gt[m][q]);
+                            if (!tile_above(m) && (tile_below(m) || J0 + q <= owned_tile<S>(wt, m)))
+                                gt[m][q] = MM::mma(bfr[q][kk], cf[m][kk], gt[m][q]);
                     }
                 // mask weights (branch-free): w_tj = e^{cum_t - cum_j} sigma_j (j < t),
                 // gamma_t (j = t), 0 (j > t); D x_t as D on the diagonal row = column
 #pragma unroll
                 for (int m = 0; m < TPW; ++m) {
                     const int TT = owned_tile<S>(wt, m);
-                    if (J0 > TT) continue;
+                    if (tile_above(m) || (!tile_below(m) && J0 > TT)) continue;
                     const int tt = (TT * 16 + l16) / R;
                     constexpr int NV = R >= 4 ? 1 : 4 / R;
 #pragma unroll
@@ -873,12 +880,12 @@ void k_scan_seg(ScanArgs a) {
                             } else {
                                 const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
                                 const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
-                                wv[u] = tj < tt ? e : (tj == tt ? gam_t : 0.f);
+                                wv[u] = (tile_below(m) || tj < tt) ? e : (tj == tt ? gam_t : 0.f);
                             }
                         }
 #pragma unroll
                         for (int v = 0; v < 4; ++v) gt[m][q][v] *= wv[(v * NV) / 4];
-                        if (J0 + q == TT) {
+                        if (!tile_below(m) && J0 + q == TT) {
 #pragma unroll
                             for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
                         }
