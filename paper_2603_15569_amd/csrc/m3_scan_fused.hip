@@ -74,6 +74,10 @@ void k_scan_fused(ScanArgs a) {
     // Chunks of several row blocks double-buffer the staged blocks: block
     // jb + 1 is committed while the MFMAs read block jb (one barrier a block).
     constexpr int NBUF = (S::NJB > 1 && sizeof(T) == 2) ? 2 : 1;   // (fp32 blocks: LDS too small)
+    // With two buffers the intra-chunk outputs are formed in the aggregate
+    // pass itself, from the same staged blocks (B^, x and W x): one pass over
+    // the chunk's rows; only e^{cum_t} C^ S_in waits for the look-back.
+    constexpr bool kMerged = NBUF == 2;
     // Row blocks are staged row-major (16-byte writes): B^ [row][n], x and
     // W x [row][p]; MFMA operands whose K axis runs along the rows (B^T and
     // (W x)^T for M, x^T for y) are read with the LDS transposing reads.
@@ -185,7 +189,7 @@ void k_scan_fused(ScanArgs a) {
     // Prefetch depth (blocks in flight, register ring): the aggregate phase
     // has registers to spare; the output phase keeps C^ fragments and
     // accumulators live, so wide-tile shapes prefetch less.
-    constexpr int DA = S::NJB < 4 ? S::NJB : 4;
+    constexpr int DA = kMerged ? 1 : (S::NJB < 4 ? S::NJB : 4);
     constexpr int DC = S::NJB < 1 ? S::NJB : 1;
     constexpr int DR = DA > DC ? DA : DC;
     Blk ring[DR];
@@ -285,18 +289,132 @@ void k_scan_fused(ScanArgs a) {
     using True = std::integral_constant<bool, true>;
     using False = std::integral_constant<bool, false>;
 
+    // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
+    // end of the sequence were loaded as zeros)
+    auto rotate_cf = [&]() {
+#pragma unroll
+        for (int m = 0; m < TPW; ++m) {
+            const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
+#pragma unroll
+            for (int kk = 0; kk < NK / 2; ++kk) {
+                float csv[MM::KPL], snv[MM::KPL];
+                cs_getn<MM::KPL>(&s_cs[t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
+#pragma unroll
+                for (int e = 0; e < MM::KPL; ++e) {
+                    const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
+                    fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
+                    fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
+                }
+            }
+        }
+    };
+    // Output tiles are transposed (y^T = S^T C^T, y^T += x^T (w o G)^T):
+    // lane l holds row l % 16 of a tile and four consecutive columns.
+    f32x4 acc[TPW][PT];
+    const float Dh = a.D[h];
+    // Intra-chunk outputs of staged block jb: per pair of 16-row j-tiles, the
+    // masked G^T tiles of every owned tile at or below it and y += (w o G) x.
+    auto out_block = [&](int jb) {
+        const T *sB = s_B + (jb % NBUF) * kSB, *sX = s_XW + (jb % NBUF) * kSXr;
+        // Owned tile m of any wave lies in rows 16 m NWO .. 16 (m + 1) NWO - 1,
+        // i.e. in blocks m NWO / 4 .. ((m + 1) NWO - 1) / 4: tiles whose blocks
+        // all come before block jb have no work in it, tiles whose blocks all
+        // come after it take every pair unmasked; only the others compare rows.
+        auto tile_above = [&](int m) { return ((m + 1) * S::NWO - 1) / 4 < jb; };
+        auto tile_below = [&](int m) { return (m * S::NWO) / 4 > jb; };
+#pragma unroll
+        for (int jp = 0; jp < S::JB / 32; ++jp) {
+            const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
+            if (J0 > owned_tile<S>(wave, TPW - 1) && J0 > owned_tile<S>(wave, 0)) continue;
+            // x^T columns of the pair, shared by all owned tiles
+            bf16x8 xf[PT];
+            if constexpr (MM::KPL == 8) {
+#pragma unroll
+                for (int pt = 0; pt < PT; ++pt) {
+                    // rows 32 jp + 4g .. +3 and 32 jp + 16 + 4g .. +3 of x, column l16
+                    const T *xr = &sX[(32 * jp + 4 * g + l16 / 4) * LDP + pt * 16 + 4 * (l16 % 4)];
+                    const bf16x4 lo = lds_tr4(xr), hi = lds_tr4(xr + 16 * LDP);
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) { xf[pt][v] = lo[v]; xf[pt][4 + v] = hi[v]; }
+                }
+            }
+            // G^T tiles (K = N) for every owned tile at or below the pair; each
+            // B^ fragment is loaded once and used by all owned tiles
+            f32x4 gt[TPW][2];
+#pragma unroll
+            for (int m = 0; m < TPW; ++m) gt[m][0] = gt[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int q = 0; q < 2; ++q)
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk) {
+                    const Frag bf = MM::load(&sB[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
+#pragma unroll
+                    for (int m = 0; m < TPW; ++m)
+                        if (!tile_above(m) && (tile_below(m) || J0 + q <= owned_tile<S>(wave, m)))
+                            gt[m][q] = MM::mma(bf, cf[m][kk], gt[m][q]);
+                }
+            // mask weights (branch-free): w_tj = e^{cum_t - cum_j} sigma_j (j < t),
+            // gamma_t (j = t), 0 (j > t); D x_t as D on the diagonal row = column
+#pragma unroll
+            for (int m = 0; m < TPW; ++m) {
+                const int TT = owned_tile<S>(wave, m);
+                if (tile_above(m) || (!tile_below(m) && J0 > TT)) continue;
+                const int tt = (TT * 16 + l16) / R;
+                const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
+                // the lane's 4 rows 4g+v of a j-tile span NV tokens (one when R >= 4)
+                constexpr int NV = R >= 4 ? 1 : 4 / R;
+#pragma unroll
+                for (int q = 0; q < 2; ++q) {
+                    float wv[NV];
+#pragma unroll
+                    for (int u = 0; u < NV; ++u) {
+                        const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
+                        const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
+                        wv[u] = (tile_below(m) || tj < tt) ? e : (tj == tt ? gam_t : 0.f);
+                    }
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) gt[m][q][v] *= wv[(v * NV) / 4];
+                    if (!tile_below(m) && J0 + q == TT) {   // diagonal tile (wave-uniform): the skip term
+#pragma unroll
+                        for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
+                    }
+                }
+                // y^T += x^T (w o G)^T  (K = the pair's 32 rows)
+                if constexpr (MM::KPL == 8) {
+                    bf16x8 af;
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) {
+                        af[v] = (bf16)gt[m][0][v];
+                        af[4 + v] = (bf16)gt[m][1][v];
+                    }
+#pragma unroll
+                    for (int pt = 0; pt < PT; ++pt) acc[m][pt] = MM::mma(xf[pt], af, acc[m][pt]);
+                } else {
+#pragma unroll
+                    for (int q = 0; q < 2; ++q)
+#pragma unroll
+                        for (int v = 0; v < 4; ++v)
+#pragma unroll
+                            for (int pt = 0; pt < PT; ++pt) {
+                                const float xv = to_f32(sX[(32 * jp + 16 * q + 4 * g + v) * LDP + pt * 16 + l16]);
+                                acc[m][pt] = MM::mma(xv, gt[m][q][v], acc[m][pt]);
+                            }
+                }
+            }
+        }
+    };
+
     // ---- 3. aggregate: M = B^T W x over the chunk (state pair-tiles) ----
     f32x4 ms[PTW][2];
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-    // With two LDS buffers the last two blocks also stage x: the output pass
-    // starts from them (blocks in reverse order) without reloading them.
-    auto commit_agg = [&](int jb, const Blk &f) {
-        if (NBUF == 2 && jb >= S::NJB - 2) commit(jb, f, True{}, True{});
-        else commit(jb, f, True{}, False{});
-    };
-    if constexpr (NBUF == 2) {
-        commit_agg(0, ring[0]);
+    if constexpr (kMerged) {
+        rotate_cf();
+#pragma unroll
+        for (int m = 0; m < TPW; ++m)
+#pragma unroll
+            for (int pt = 0; pt < PT; ++pt) acc[m][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
+        commit(0, ring[0], True{}, True{});
         __syncthreads();
         if (DA < S::NJB) fetch(DA, ring[0]);
     }
@@ -304,7 +422,7 @@ void k_scan_fused(ScanArgs a) {
     for (int jb = 0; jb < S::NJB; ++jb) {
         if constexpr (NBUF == 2) {
             if (jb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
-                commit_agg(jb + 1, ring[(jb + 1) % DA]);
+                commit(jb + 1, ring[(jb + 1) % DA], True{}, True{});
                 if (jb + 1 + DA < S::NJB) fetch(jb + 1 + DA, ring[(jb + 1) % DA]);
             }
         } else {
@@ -333,6 +451,7 @@ void k_scan_fused(ScanArgs a) {
                 for (int half = 0; half < 2; ++half) ms[m2][half] = MM::mma(af[half], bf, ms[m2][half]);
             }
         }
+        if constexpr (kMerged) out_block(jb);
         __syncthreads();
     }
 
@@ -604,13 +723,11 @@ void k_scan_fused(ScanArgs a) {
     }
 
     // ---- 5. outputs ----
-    // Longer chunks restage their blocks: the first ones are fetched now (after
-    // the look-back and the publication, whose waits would drain them).  With
-    // two LDS buffers the blocks run in reverse order, the last two still
-    // staged from the aggregate, so the first block to reload is NJB - 3.
-    if constexpr (NBUF == 2) {
-        if (S::NJB >= 3) fetch(S::NJB - 3, ring[0]);
-    } else if constexpr (S::NJB > 1) {
+    // Single-pass chunks (two buffers) only add e^{cum_t} C^ S_in to the
+    // accumulators; the others restage their blocks (the first ones fetched
+    // now, after the look-back and the publication, whose waits would drain
+    // them) and form the intra-chunk term here.
+    if constexpr (!kMerged && S::NJB > 1) {
 #pragma unroll
         for (int d = 0; d < DC; ++d) fetch(d, ring[d]);
     }
@@ -623,29 +740,12 @@ void k_scan_fused(ScanArgs a) {
             for (int v = 0; v < 4; ++v)
                 s_S[(pt * 16 + l16) * S::LDN + 16 * (ntl + 4 * half) + 4 * g + v] = from_f32<T>(Sin[m2][half][v]);
     }
-    // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
-    // end of the sequence were loaded as zeros)
-    if constexpr (!kEarlyC) load_c();
-#pragma unroll
-    for (int m = 0; m < TPW; ++m) {
-        const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
-#pragma unroll
-        for (int kk = 0; kk < NK / 2; ++kk) {
-            float csv[MM::KPL], snv[MM::KPL];
-            cs_getn<MM::KPL>(&s_cs[t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
-#pragma unroll
-            for (int e = 0; e < MM::KPL; ++e) {
-                const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
-                fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
-                fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
-            }
-        }
+    if constexpr (!kMerged) {
+        if constexpr (!kEarlyC) load_c();
+        rotate_cf();
     }
     __syncthreads();   // s_S complete
-    // inter-chunk term e^{cum_t} C^_t . S_in starts the accumulators.  The
-    // output tiles are transposed (y^T = S^T C^T, y^T += x^T (w o G)^T): lane
-    // l holds row l % 16 of a tile and four consecutive columns.
-    f32x4 acc[TPW][PT];
+    // inter-chunk term e^{cum_t} C^_t . S_in
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int TT = owned_tile<S>(wave, m);
@@ -657,113 +757,24 @@ void k_scan_fused(ScanArgs a) {
             for (int kk = 0; kk < NK; ++kk)
                 tmp = MM::mma(MM::load(&s_S[(pt * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]), cf[m][kk], tmp);
 #pragma unroll
-            for (int v = 0; v < 4; ++v) tmp[v] *= ecum;
-            acc[m][pt] = tmp;
+            for (int v = 0; v < 4; ++v) {
+                if constexpr (kMerged) acc[m][pt][v] += ecum * tmp[v];
+                else acc[m][pt][v] = ecum * tmp[v];
+            }
         }
     }
-    // intra-chunk term over the row blocks at or below each owned tile
-    const float Dh = a.D[h];
+    if constexpr (!kMerged) {
+        // intra-chunk term over the row blocks at or below each owned tile
 #pragma unroll
-    for (int pi = 0; pi < S::NJB; ++pi) {
-        const int jb = NBUF == 2 ? S::NJB - 1 - pi : pi;   // block of this step
-        if constexpr (NBUF == 2) {
-            if (pi >= 1 && jb >= 1) {   // stage the next block (jb - 1) while this one feeds the MFMAs
-                commit(jb - 1, ring[0], False{}, True{});
-                if (jb >= 2) fetch(jb - 2, ring[0]);
+        for (int jb = 0; jb < S::NJB; ++jb) {
+            if constexpr (S::NJB > 1) {
+                commit(jb, ring[jb % DC], False{}, True{});
+                __syncthreads();
+                if (jb + DC < S::NJB) fetch(jb + DC, ring[jb % DC]);
             }
-        } else if constexpr (S::NJB > 1) {
-            commit(jb, ring[jb % DC], False{}, True{});
-            __syncthreads();
-            if (jb + DC < S::NJB) fetch(jb + DC, ring[jb % DC]);
+            out_block(jb);
+            if constexpr (S::NJB > 1) __syncthreads();
         }
-        const T *sB = s_B + (jb % NBUF) * kSB, *sX = s_XW + (jb % NBUF) * kSXr;
-        // Owned tile m of any wave lies in rows 16 m NWO .. 16 (m + 1) NWO - 1,
-        // i.e. in blocks m NWO / 4 .. ((m + 1) NWO - 1) / 4: tiles whose blocks
-        // all come before block jb have no work in it, tiles whose blocks all
-        // come after it take every pair unmasked; only the others compare rows.
-        auto tile_above = [&](int m) { return ((m + 1) * S::NWO - 1) / 4 < jb; };
-        auto tile_below = [&](int m) { return (m * S::NWO) / 4 > jb; };
-#pragma unroll
-        for (int jp = 0; jp < S::JB / 32; ++jp) {
-            const int J0 = jb * 4 + 2 * jp;        // first j-tile of the pair (chunk-global)
-            if (J0 > owned_tile<S>(wave, TPW - 1) && J0 > owned_tile<S>(wave, 0)) continue;
-            // x^T columns of the pair, shared by all owned tiles
-            bf16x8 xf[PT];
-            if constexpr (MM::KPL == 8) {
-#pragma unroll
-                for (int pt = 0; pt < PT; ++pt) {
-                    // rows 32 jp + 4g .. +3 and 32 jp + 16 + 4g .. +3 of x, column l16
-                    const T *xr = &sX[(32 * jp + 4 * g + l16 / 4) * LDP + pt * 16 + 4 * (l16 % 4)];
-                    const bf16x4 lo = lds_tr4(xr), hi = lds_tr4(xr + 16 * LDP);
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) { xf[pt][v] = lo[v]; xf[pt][4 + v] = hi[v]; }
-                }
-            }
-            // G^T tiles (K = N) for every owned tile at or below the pair; each
-            // B^ fragment is loaded once and used by all owned tiles
-            f32x4 gt[TPW][2];
-#pragma unroll
-            for (int m = 0; m < TPW; ++m) gt[m][0] = gt[m][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-            for (int q = 0; q < 2; ++q)
-#pragma unroll
-                for (int kk = 0; kk < NK; ++kk) {
-                    const Frag bf = MM::load(&sB[((2 * jp + q) * 16 + l16) * S::LDN + kk * MM::K + MM::KPL * g]);
-#pragma unroll
-                    for (int m = 0; m < TPW; ++m)
-                        if (!tile_above(m) && (tile_below(m) || J0 + q <= owned_tile<S>(wave, m)))
-                            gt[m][q] = MM::mma(bf, cf[m][kk], gt[m][q]);
-                }
-            // mask weights (branch-free): w_tj = e^{cum_t - cum_j} sigma_j (j < t),
-            // gamma_t (j = t), 0 (j > t); D x_t as D on the diagonal row = column
-#pragma unroll
-            for (int m = 0; m < TPW; ++m) {
-                const int TT = owned_tile<S>(wave, m);
-                if (tile_above(m) || (!tile_below(m) && J0 > TT)) continue;
-                const int tt = (TT * 16 + l16) / R;
-                const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
-                // the lane's 4 rows 4g+v of a j-tile span NV tokens (one when R >= 4)
-                constexpr int NV = R >= 4 ? 1 : 4 / R;
-#pragma unroll
-                for (int q = 0; q < 2; ++q) {
-                    float wv[NV];
-#pragma unroll
-                    for (int u = 0; u < NV; ++u) {
-                        const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
-                        const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
-                        wv[u] = (tile_below(m) || tj < tt) ? e : (tj == tt ? gam_t : 0.f);
-                    }
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) gt[m][q][v] *= wv[(v * NV) / 4];
-                    if (!tile_below(m) && J0 + q == TT) {   // diagonal tile (wave-uniform): the skip term
-#pragma unroll
-                        for (int v = 0; v < 4; ++v) gt[m][q][v] += (4 * g + v == l16) ? Dh : 0.f;
-                    }
-                }
-                // y^T += x^T (w o G)^T  (K = the pair's 32 rows)
-                if constexpr (MM::KPL == 8) {
-                    bf16x8 af;
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        af[v] = (bf16)gt[m][0][v];
-                        af[4 + v] = (bf16)gt[m][1][v];
-                    }
-#pragma unroll
-                    for (int pt = 0; pt < PT; ++pt) acc[m][pt] = MM::mma(xf[pt], af, acc[m][pt]);
-                } else {
-#pragma unroll
-                    for (int q = 0; q < 2; ++q)
-#pragma unroll
-                        for (int v = 0; v < 4; ++v)
-#pragma unroll
-                            for (int pt = 0; pt < PT; ++pt) {
-                                const float xv = to_f32(sX[(32 * jp + 16 * q + 4 * g + v) * LDP + pt * 16 + l16]);
-                                acc[m][pt] = MM::mma(xv, gt[m][q][v], acc[m][pt]);
-                            }
-                }
-            }
-        }
-        if constexpr (S::NJB > 1) __syncthreads();
     }
     // store: once every wave is past its last LDS read, each wave stages its
     // tiles in its own part of the x / W x buffers (a wave's LDS accesses
