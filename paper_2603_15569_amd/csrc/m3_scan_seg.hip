@@ -966,8 +966,12 @@ hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
         G = (nsl * a.nchunks + cap - 1) / cap;
         // Short chunks (fewer than 128 rows) split over several segments run
         // faster one chunk per workgroup: the aggregate pass and the per-chunk
-        // fixed costs of a segment then outweigh what it saves.
-        if (G < a.nchunks && S::QR < 128 && a.per_chunk) return a.per_chunk(a0, stream);
+        // fixed costs of a segment then outweigh what it saves.  So do chunks
+        // of 64 or more tokens in scans of at least 16384 chunk items, where
+        // the per-chunk kernel's single pass over each chunk pays off.
+        if (G < a.nchunks && a.per_chunk &&
+            (S::QR < 128 || (Q >= 64 && nsl * a.nchunks >= 16384)))
+            return a.per_chunk(a0, stream);
     }
     G = G < 1 ? 1 : (G > a.nchunks ? a.nchunks : G);
     a.G = G;
