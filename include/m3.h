@@ -77,9 +77,11 @@ typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
  * single-pass kernel: each workgroup scans a segment of consecutive chunks of
  * one (batch, head) slice and carries the state across them; segments of a
  * slice are linked by a decoupled look-back over their state maps.  When
- * seg_chunks is 0 and chunks of fewer than 128 rows (chunk * rank) would need
- * several segments per slice, the one-chunk-per-workgroup kernel runs
- * instead (it is faster there).  When a slice is one segment and io is bf16
+ * seg_chunks is 0 and several segments per slice would be needed, the
+ * one-chunk-per-workgroup kernel runs instead for chunks of fewer than 128
+ * rows (chunk * rank), and for chunks of 64 or more tokens when the scan has
+ * at least 16384 chunks in all (batch * nheads * chunks per slice): it is
+ * faster there.  When a slice is one segment and io is bf16
  * with rank 4 and chunk 64, a warp-specialised variant runs (half of its
  * waves form the outputs, half stage the inputs and carry the state).
  * M3_SCAN_SPLIT: three kernels (chunk states, a state pass over chunks,
