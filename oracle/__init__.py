@@ -105,6 +105,25 @@ def step(state, carryB, carryX, x, B, C, dt, A, lam, theta, D, nthreads=0):
 
 
 # ---------------------------------------------------------------------------
+# Output gate (App. "MIMO for Mamba-3", paragraph "Mamba with MIMO": the
+# block's residual function phi(Y, Z) = Y o SiLU(Z), Z shaped like X).
+# ---------------------------------------------------------------------------
+
+def silu(z):
+    """SiLU(z) = z / (1 + e^{-z}), elementwise, fp64 (exp overflow for very
+    negative z gives the correct limit -0)."""
+    z = _f64(z)
+    with np.errstate(over="ignore"):
+        return z / (1.0 + np.exp(-z))
+
+
+def gate(y, z):
+    """phi(Y, Z) = Y o SiLU(Z): the SSM output (D skip included, the Mamba
+    order) times SiLU of the gate input, elementwise, fp64."""
+    return _f64(y) * silu(z)
+
+
+# ---------------------------------------------------------------------------
 # Slice extraction from tensors in the library layout.
 # ---------------------------------------------------------------------------
 

@@ -253,3 +253,34 @@ def test_empty_sequence_returns_initial_state(oracle_lib):
     y, st, cb, cx = run1(s, init_state=st0, init_B=cb0, init_X=cx0)
     assert y.shape == (0, 2, 2)
     assert np.array_equal(st, st0[0]) and np.array_equal(cb, cb0[0]) and np.array_equal(cx, cx0[0])
+
+
+def test_gate_silu_closed_forms():
+    """SiLU against textbook values of the logistic function: sigma(1) =
+    1 / (1 + 1/e), sigma(-1) = 1 - sigma(1); SiLU(0) = 0; the odd-part
+    identity SiLU(z) - SiLU(-z) = z; and the limits (identity for large z,
+    zero for very negative z, where exp overflows)."""
+    s1 = 0.7310585786300049          # logistic(1) = e / (1 + e)
+    assert math.isclose(s1, math.e / (1.0 + math.e), rel_tol=0, abs_tol=1e-16)
+    got = oracle.silu(np.array([0.0, 1.0, -1.0, 2.0, 40.0, -800.0]))
+    assert got[0] == 0.0
+    assert math.isclose(got[1], s1, rel_tol=1e-15)
+    assert math.isclose(got[2], -(1.0 - s1), rel_tol=1e-15)
+    assert math.isclose(got[3], 2.0 * math.e ** 2 / (1.0 + math.e ** 2), rel_tol=1e-15)
+    assert got[4] == 40.0            # 1 + e^-40 rounds to 1
+    assert got[5] == 0.0 and np.isfinite(got).all()
+    z = np.random.default_rng(7).normal(scale=4.0, size=1000)
+    assert np.max(np.abs(oracle.silu(z) - oracle.silu(-z) - z)) <= 1e-13
+
+
+def test_gate_is_elementwise_product():
+    """phi(Y, Z) = Y o SiLU(Z), elementwise: y z for a large gate (sigma = 1),
+    zero for a zero gate, and for a gate pair z, -z the sum
+    y (SiLU(z) + SiLU(-z)) = y z tanh(z / 2)."""
+    rng = np.random.default_rng(8)
+    y = rng.normal(size=(3, 5, 2, 4))
+    np.testing.assert_array_equal(oracle.gate(y, np.full_like(y, 40.0)), y * 40.0)
+    np.testing.assert_array_equal(oracle.gate(y, np.zeros_like(y)), np.zeros_like(y))
+    z = rng.normal(size=y.shape)
+    lhs = oracle.gate(y, z) + oracle.gate(y, -z)
+    np.testing.assert_allclose(lhs, y * z * np.tanh(z / 2.0), rtol=1e-13, atol=1e-15)
