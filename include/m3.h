@@ -149,6 +149,28 @@ m3_status m3_scan_fwd(const m3_dims *dims,
                       void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * m3_scan_fwd with the block's output gate fused into the y store (App.
+ * "MIMO for Mamba-3", paragraph "Mamba with MIMO": Y' = Y o SiLU(Z), the
+ * residual function phi, with Z computed like X).  z has the layout, dtype
+ * and alignment of x ([batch][seqlen][nheads][rank][headdim], io dtype,
+ * 16-byte aligned) and may be NULL only when seqlen == 0; it must not
+ * overlap y.  y receives (SSM output + D x) o SiLU(z), SiLU(u) = u / (1 +
+ * e^{-u}), evaluated in fp32; with io bf16 the single-pass kernels gate the
+ * bf16-rounded y and round again (the three-kernel path and m3_step gate
+ * before their one rounding).  The final state and the carry are those of
+ * m3_scan_fwd (the gate acts on the output only).  Everything else,
+ * including the errors, as m3_scan_fwd.
+ */
+m3_status m3_scan_fwd_gated(const m3_dims *dims,
+                            const void *x, const void *B, const void *C,
+                            const float *dt, const float *A, const float *lambda,
+                            const float *theta, const float *D, const void *z,
+                            const float *init_state, const void *init_carryB,
+                            const void *init_carryX,
+                            void *y, float *final_state, void *carryB, void *carryX,
+                            void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * One decode step (one iteration of the recurrence) for every (b, h):
  * state <- h_t, carry <- (B_t, X_t) in place, y_t written.  dims->seqlen
  * and dims->chunk are ignored; A is read at t = 0 (a_stride_t unused).
@@ -164,6 +186,19 @@ m3_status m3_step(const m3_dims *dims,
                   const float *dt_t, const float *A, const float *lambda_t,
                   const float *theta_t, const float *D,
                   void *y_t, void *stream);
+
+/*
+ * m3_step with the output gate (as m3_scan_fwd_gated): y_t = (S'^T C_t +
+ * D X_t) o SiLU(z_t), z_t [batch][nheads][rank][headdim] in the io dtype,
+ * 16-byte aligned, not NULL (M3_ERR_NULL), gated in fp32 before the one
+ * rounding.  State and carry updates as m3_step.
+ */
+m3_status m3_step_gated(const m3_dims *dims,
+                        float *state, void *carryB, void *carryX,
+                        const void *x_t, const void *B_t, const void *C_t,
+                        const float *dt_t, const float *A, const float *lambda_t,
+                        const float *theta_t, const float *D, const void *z_t,
+                        void *y_t, void *stream);
 
 /* Static description of a status code. */
 const char *m3_status_string(m3_status status);

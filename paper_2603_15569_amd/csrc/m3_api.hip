@@ -109,21 +109,23 @@ extern "C" size_t m3_scan_workspace_bytes(const m3_dims *d) {
         .total;
 }
 
-extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B, const void *C,
-                                 const float *dt, const float *A, const float *lambda,
-                                 const float *theta, const float *D, const float *init_state,
-                                 const void *init_carryB, const void *init_carryX, void *y,
-                                 float *final_state, void *carryB, void *carryX, void *workspace,
-                                 size_t workspace_bytes, void *stream) {
+// Both scan entry points; `gated` requires z (a token array like x).
+static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const void *C,
+                          const float *dt, const float *A, const float *lambda,
+                          const float *theta, const float *D, bool gated, const void *z,
+                          const float *init_state, const void *init_carryB,
+                          const void *init_carryX, void *y, float *final_state, void *carryB,
+                          void *carryX, void *workspace, size_t workspace_bytes, void *stream) {
     ScanImpl impl;
     int64_t nc = 0;
     m3_status s = check_scan_dims(d, &impl, &nc);
     if (s != M3_OK) return s;
     // token arrays may be NULL only for an empty sequence (empty tensors)
-    const bool tok_ok = d->seqlen == 0 || (x && B && C && dt && lambda && theta && y);
+    const bool tok_ok = d->seqlen == 0 || (x && B && C && dt && lambda && theta && y && (z || !gated));
     if (!tok_ok || !A || !D || !final_state || !carryB || !carryX) return M3_ERR_NULL;
     if ((init_carryB == nullptr) != (init_carryX == nullptr)) return M3_ERR_NULL;
-    const void *vec[] = {x, B, C, theta, init_state, init_carryB, init_carryX,
+    if (!gated || d->seqlen == 0) z = nullptr;
+    const void *vec[] = {x, B, C, theta, z, init_state, init_carryB, init_carryX,
                          y, final_state, carryB, carryX, workspace};
     for (const void *p : vec)
         if (!aligned16(p)) return M3_ERR_ALIGN;
@@ -139,7 +141,7 @@ extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B,
     a.x = x; a.B = B; a.C = C;
     a.dt = dt; a.A = A; a.lam = lambda; a.theta = theta; a.D = D;
     a.init_state = init_state; a.init_cB = init_carryB; a.init_cX = init_carryX;
-    a.y = y; a.final_state = final_state; a.cB = carryB; a.cX = carryX;
+    a.y = y; a.z = z; a.final_state = final_state; a.cB = carryB; a.cX = carryX;
     char *ws = static_cast<char *>(workspace);
     a.M = nullptr; a.Sin = nullptr; a.tot = nullptr;
     a.ctl = nullptr; a.flags = nullptr; a.agg = nullptr; a.inc = nullptr;
@@ -165,18 +167,40 @@ extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B,
     return M3_OK;
 }
 
-extern "C" m3_status m3_step(const m3_dims *d, float *state, void *carryB, void *carryX,
-                             const void *x_t, const void *B_t, const void *C_t,
-                             const float *dt_t, const float *A, const float *lambda_t,
-                             const float *theta_t, const float *D, void *y_t, void *stream) {
+extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B, const void *C,
+                                 const float *dt, const float *A, const float *lambda,
+                                 const float *theta, const float *D, const float *init_state,
+                                 const void *init_carryB, const void *init_carryX, void *y,
+                                 float *final_state, void *carryB, void *carryX, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    return scan_fwd(d, x, B, C, dt, A, lambda, theta, D, false, nullptr, init_state, init_carryB,
+                    init_carryX, y, final_state, carryB, carryX, workspace, workspace_bytes, stream);
+}
+
+extern "C" m3_status m3_scan_fwd_gated(const m3_dims *d, const void *x, const void *B,
+                                       const void *C, const float *dt, const float *A,
+                                       const float *lambda, const float *theta, const float *D,
+                                       const void *z, const float *init_state,
+                                       const void *init_carryB, const void *init_carryX, void *y,
+                                       float *final_state, void *carryB, void *carryX,
+                                       void *workspace, size_t workspace_bytes, void *stream) {
+    return scan_fwd(d, x, B, C, dt, A, lambda, theta, D, true, z, init_state, init_carryB,
+                    init_carryX, y, final_state, carryB, carryX, workspace, workspace_bytes, stream);
+}
+
+static m3_status step(const m3_dims *d, float *state, void *carryB, void *carryX,
+                      const void *x_t, const void *B_t, const void *C_t, const float *dt_t,
+                      const float *A, const float *lambda_t, const float *theta_t, const float *D,
+                      bool gated, const void *z_t, void *y_t, void *stream) {
     m3_status s = check_dims_common(d);
     if (s != M3_OK) return s;
     step_launch_fn fn = find_step_impl(d->io, d->dstate, d->headdim, d->rank);
     if (!fn) return M3_ERR_UNSUPPORTED;
     if (!state || !carryB || !carryX || !x_t || !B_t || !C_t || !dt_t || !A || !lambda_t ||
-        !theta_t || !D || !y_t)
+        !theta_t || !D || !y_t || (gated && !z_t))
         return M3_ERR_NULL;
-    const void *vec[] = {state, carryB, carryX, x_t, B_t, C_t, theta_t, y_t};
+    if (!gated) z_t = nullptr;
+    const void *vec[] = {state, carryB, carryX, x_t, B_t, C_t, theta_t, z_t, y_t};
     for (const void *p : vec)
         if (!aligned16(p)) return M3_ERR_ALIGN;
     const void *scal[] = {dt_t, A, lambda_t, D};
@@ -186,7 +210,7 @@ extern "C" m3_status m3_step(const m3_dims *d, float *state, void *carryB, void 
     a.state = state; a.cB = carryB; a.cX = carryX;
     a.x = x_t; a.B = B_t; a.C = C_t;
     a.dt = dt_t; a.A = A; a.lam = lambda_t; a.theta = theta_t; a.D = D;
-    a.y = y_t;
+    a.y = y_t; a.z = z_t;
     a.batch = d->batch; a.H = d->nheads;
     a.a_sb = d->a_stride_b; a.a_sh = d->a_stride_h;
     const hipError_t e = fn(a, static_cast<hipStream_t>(stream));
@@ -195,4 +219,21 @@ extern "C" m3_status m3_step(const m3_dims *d, float *state, void *carryB, void 
         return M3_ERR_HIP;
     }
     return M3_OK;
+}
+
+extern "C" m3_status m3_step(const m3_dims *d, float *state, void *carryB, void *carryX,
+                             const void *x_t, const void *B_t, const void *C_t,
+                             const float *dt_t, const float *A, const float *lambda_t,
+                             const float *theta_t, const float *D, void *y_t, void *stream) {
+    return step(d, state, carryB, carryX, x_t, B_t, C_t, dt_t, A, lambda_t, theta_t, D, false,
+                nullptr, y_t, stream);
+}
+
+extern "C" m3_status m3_step_gated(const m3_dims *d, float *state, void *carryB, void *carryX,
+                                   const void *x_t, const void *B_t, const void *C_t,
+                                   const float *dt_t, const float *A, const float *lambda_t,
+                                   const float *theta_t, const float *D, const void *z_t,
+                                   void *y_t, void *stream) {
+    return step(d, state, carryB, carryX, x_t, B_t, C_t, dt_t, A, lambda_t, theta_t, D, true, z_t,
+                y_t, stream);
 }

@@ -23,7 +23,7 @@ template <typename T> struct Vec8;
 template <> struct Vec8<bf16> { typedef bf16x8 type; static constexpr int n = 8; };
 template <> struct Vec8<float> { typedef f32x4 type; static constexpr int n = 4; };
 
-template <typename T, int N, int P, int R, int NT>
+template <typename T, int N, int P, int R, int NT, bool kGate>
 __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     constexpr int NH = N / 2;
     constexpr int TX = P / 4;                   // threads across columns (float4 each)
@@ -80,6 +80,14 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     }
     const float *th = a.theta + bh * NH;
     const float thv = th[min(tid, NH - 1)];
+    // gate inputs of this thread's outputs (y_t o SiLU(z_t))
+    constexpr int TZ = (R * P + NT - 1) / NT;
+    float zv[TZ];
+    if constexpr (kGate) {
+        const T *Zt = static_cast<const T *>(a.z) + bh * (R * P);
+#pragma unroll
+        for (int k = 0; k < TZ; ++k) zv[k] = to_f32(Zt[min(tid + k * NT, R * P - 1)]);
+    }
     // 1. the state: the bytes that matter
     float *st = a.state + bh * (int64_t)(N * P);
     float4 re[NPT], im[NPT];
@@ -213,11 +221,17 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     __syncthreads();
     T *yt = static_cast<T *>(a.y) + bh * (R * P);
     const float Dh = a.D[h];
-    for (int e = tid; e < R * P; e += NT) {
-        float v = 0.f;
 #pragma unroll
-        for (int w = 0; w < NW; ++w) v += s_red[w * R * P + e];
-        yt[e] = from_f32<T>(v + Dh * s_X[e]);
+    for (int k = 0; k < TZ; ++k) {
+        const int e = tid + k * NT;
+        if (e < R * P) {
+            float v = 0.f;
+#pragma unroll
+            for (int w = 0; w < NW; ++w) v += s_red[w * R * P + e];
+            v += Dh * s_X[e];
+            if constexpr (kGate) v *= silu(zv[k]);
+            yt[e] = from_f32<T>(v);
+        }
     }
 }
 
@@ -228,8 +242,12 @@ template <int N, int P> struct StepThreads { static constexpr int value = N * P 
 template <typename T, int N, int P, int R>
 hipError_t launch_step(const StepArgs &a, hipStream_t stream) {
     constexpr int NT = StepThreads<N, P>::value;
-    hipLaunchKernelGGL((k_step<T, N, P, R, NT>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
-                       stream, a);
+    if (a.z)
+        hipLaunchKernelGGL((k_step<T, N, P, R, NT, true>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((k_step<T, N, P, R, NT, false>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
+                           stream, a);
     return hipGetLastError();
 }
 

@@ -75,6 +75,13 @@ __device__ __forceinline__ void sincos_fast(double x, double *s, double *c) { si
 __device__ __forceinline__ float exp_fast(float x) { return __expf(x); }
 __device__ __forceinline__ double exp_fast(double x) { return exp(x); }
 
+// SiLU(u) = u / (1 + e^{-u}), the output gate's activation (App. "MIMO for
+// Mamba-3": Y' = Y o SiLU(Z)).  Hardware exp and reciprocal (~1e-7 relative);
+// e^{-u} overflowing to +inf for very negative u gives the limit -0.
+__device__ __forceinline__ float silu(float u) {
+    return u * __builtin_amdgcn_rcpf(1.f + __expf(-u));
+}
+
 // Inclusive prefix sum across the 64 lanes of a wavefront.
 template <typename A>
 __device__ __forceinline__ A wave_incl_scan(A v, int lane) {

@@ -14,6 +14,7 @@ struct ScanArgs {
     const float *init_state;
     const void *init_cB, *init_cX;      // both null or both set
     void *y;
+    const void *z;                      // output gate [B,L,H,R,P] (io), or null
     float *final_state;
     void *cB, *cX;
     // workspace regions (see scan_workspace_layout)
@@ -41,6 +42,7 @@ struct StepArgs {
     const void *x, *B, *C;
     const float *dt, *A, *lam, *theta, *D;
     void *y;
+    const void *z;                      // output gate [B,H,R,P] (io), or null
     int64_t batch, H;
     int64_t a_sb, a_sh;
 };

@@ -368,6 +368,7 @@ __global__ __launch_bounds__(kBlock) void k_chunk_out(ScanArgs a) {
     const T *Bsrc = static_cast<const T *>(a.B) + tok_bc * (R * N);
     const T *Xsrc = static_cast<const T *>(a.x) + tok_bc * (R * P);
     T *Ydst = static_cast<T *>(a.y) + tok_bc * (R * P);
+    const T *Zsrc = a.z ? static_cast<const T *>(a.z) + tok_bc * (R * P) : nullptr;   // output gate
     const int64_t bstride = a.H * R * N, xstride = a.H * R * P;
     constexpr int PT = P / 16;
 
@@ -472,7 +473,8 @@ __global__ __launch_bounds__(kBlock) void k_chunk_out(ScanArgs a) {
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt) {
                     const int p = pt * 16 + l16;
-                    const float yv = acc[pt][v] + Dh * to_f32(s_Xt[p * S::LDB + rl]);
+                    float yv = acc[pt][v] + Dh * to_f32(s_Xt[p * S::LDB + rl]);
+                    if (Zsrc) yv *= silu(to_f32(Zsrc[t * xstride + r * P + p]));
                     Ydst[t * xstride + r * P + p] = from_f32<T>(yv);
                 }
             }

@@ -179,6 +179,15 @@ __device__ __forceinline__ void store4(bf16 *dst, const f32x4 &v) {
 }
 __device__ __forceinline__ void store4(float *dst, const f32x4 &v) { *reinterpret_cast<f32x4 *>(dst) = v; }
 
+// Output gate on one 16-byte piece of y: y o SiLU(z), elementwise in fp32.
+template <typename T>
+__device__ __forceinline__ typename Vec16<T>::type gate_piece(typename Vec16<T>::type y,
+                                                            const typename Vec16<T>::type &z) {
+#pragma unroll
+    for (int e = 0; e < Vec16<T>::n; ++e) fset(y, e, fget(y, e) * silu(fget(z, e)));
+    return y;
+}
+
 __device__ __forceinline__ void wait_stores_done() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 __device__ __forceinline__ void st_coh2(unsigned long long *p, float x, float y) {

@@ -47,9 +47,10 @@ namespace {
 
 using namespace scan;
 
-template <typename T, int Q, int R>
+template <typename T, int Q, int R, bool kGate>
 // Two waves per SIMD: two 4-wave workgroups or one 8-wave workgroup per CU
-// (more waves spill the tile registers of the output phase).
+// (more waves spill the tile registers of the output phase).  kGate: the
+// stored y is multiplied by SiLU(z) (the block's output gate).
 __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2)
 void k_scan_fused(ScanArgs a) {
     typedef FShape<T, Q, R> S;
@@ -740,6 +741,25 @@ void k_scan_fused(ScanArgs a) {
             for (int v = 0; v < 4; ++v)
                 s_S[(pt * 16 + l16) * S::LDN + 16 * (ntl + 4 * half) + 4 * g + v] = from_f32<T>(Sin[m2][half][v]);
     }
+    // y leaves in 16-byte pieces of its rows (NPC per lane and owned tile);
+    // with the gate, the matching pieces of z are loaded now and arrive
+    // during the inter-chunk products
+    constexpr int RP = P / S::CE;                   // 16-byte pieces of a row
+    constexpr int NPC = 16 * RP / kWave;
+    static_assert(NPC * kWave == 16 * RP, "store pieces");
+    V16 zp[kGate ? TPW : 1][NPC];
+    if constexpr (kGate) {
+        const Rsrc rz = make_rsrc(static_cast<const T *>(a.z) + tok0 * (R * P),
+                                  (uint32_t)(((nvalid - 1) * xstr + R * P) * (int64_t)sizeof(T)));
+#pragma unroll
+        for (int m = 0; m < TPW; ++m)
+#pragma unroll
+            for (int i = 0; i < NPC; ++i) {
+                const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * S::CE;
+                const int row = owned_tile<S>(wave, m) * 16 + rl, t = row / R, r = row % R;
+                zp[m][i] = buf_load<V16>(rz, tok_off(t, xstr_b) + (uint32_t)((r * P + col) * sizeof(T)));
+            }
+    }
     if constexpr (!kMerged) {
         if constexpr (!kEarlyC) load_c();
         rotate_cf();
@@ -783,7 +803,6 @@ void k_scan_fused(ScanArgs a) {
     __syncthreads();
     T *s_y = s_XW + wave * (16 * LDP);
     T *Yg = static_cast<T *>(a.y) + tok0 * (R * P);
-    constexpr int RP = P / S::CE;                   // 16-byte pieces of a row
 #pragma unroll
     for (int m = 0; m < TPW; ++m) {
         const int TT = owned_tile<S>(wave, m);
@@ -791,12 +810,14 @@ void k_scan_fused(ScanArgs a) {
         for (int pt = 0; pt < PT; ++pt) store4(&s_y[l16 * LDP + pt * 16 + 4 * g], acc[m][pt]);
         asm volatile("" ::: "memory");
 #pragma unroll
-        for (int k = lane; k < 16 * RP; k += kWave) {
-            const int rl = k / RP, col = (k % RP) * S::CE;
+        for (int i = 0; i < NPC; ++i) {
+            const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * S::CE;
             const int row = TT * 16 + rl, t = row / R, r = row % R;
-            if (t < nvalid)
-                *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) =
-                    *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
+            if (t < nvalid) {
+                V16 yv = *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
+                if constexpr (kGate) yv = gate_piece<T>(yv, zp[m][i]);
+                *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) = yv;
+            }
         }
         asm volatile("" ::: "memory");
     }
@@ -809,8 +830,12 @@ hipError_t launch_fused(const ScanArgs &a, hipStream_t stream) {
     const int64_t nflags = nsl * a.nchunks;
     const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);
     hipLaunchKernelGGL(k_reset, dim3(rblocks), dim3(256), 0, stream, a.ctl, a.flags, nflags);
-    hipLaunchKernelGGL((k_scan_fused<T, Q, R>), dim3((unsigned)(nsl * a.nchunks)), dim3(S::NTHR), 0,
-                       stream, a);
+    if (a.z)
+        hipLaunchKernelGGL((k_scan_fused<T, Q, R, true>), dim3((unsigned)(nsl * a.nchunks)), dim3(S::NTHR), 0,
+                           stream, a);
+    else
+        hipLaunchKernelGGL((k_scan_fused<T, Q, R, false>), dim3((unsigned)(nsl * a.nchunks)), dim3(S::NTHR), 0,
+                           stream, a);
     return hipGetLastError();
 }
 

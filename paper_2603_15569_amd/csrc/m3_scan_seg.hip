@@ -50,7 +50,8 @@ using namespace scan;
 template <typename T, int Q, int R>
 using SegShape = FShape<T, Q, R, 8>;
 
-template <typename T, int Q, int R>
+// kGate: the stored y is multiplied by SiLU(z) (the block's output gate).
+template <typename T, int Q, int R, bool kGate>
 __global__ __launch_bounds__((SegShape<T, Q, R>::NTHR), 2)
 void k_scan_seg(ScanArgs a) {
     typedef SegShape<T, Q, R> S;
@@ -787,6 +788,23 @@ void k_scan_seg(ScanArgs a) {
             }
         }
         __syncthreads();   // S^T read: the B^ block is rewritten below
+        // y leaves in 16-byte pieces of the wave's columns of its rows (NPC
+        // per lane and owned tile); with the gate, the matching pieces of z
+        // are loaded now and arrive during the intra-chunk products
+        constexpr int RP = PTS * 16 / S::CE;        // 16-byte pieces of a row per wave
+        constexpr int NPC = (16 * RP + kWave - 1) / kWave;
+        V16 zp[kGate ? TPW : 1][NPC];
+        if constexpr (kGate) {
+            const Rsrc rz = rows_rsrc(static_cast<const T *>(a.z), c, xstr, R * P);
+#pragma unroll
+            for (int m = 0; m < TPW; ++m)
+#pragma unroll
+                for (int i = 0; i < NPC; ++i) {
+                    const int k = min(lane + i * kWave, 16 * RP - 1), rl = k / RP, col = (k % RP) * S::CE;
+                    const int row = owned_tile<S>(wt, m) * 16 + rl, t = row / R, r = row % R;
+                    zp[m][i] = buf_load<V16>(rz, tok_off(t, xstr_b) + (uint32_t)((r * P + pofs * 16 + col) * sizeof(T)));
+                }
+        }
         // the state accumulator starts as e^{cum_e} S and collects M
         f32x4 ms[PTW][2];
         if (chain) {
@@ -931,7 +949,6 @@ void k_scan_seg(ScanArgs a) {
         // its columns of the y rows
         T *s_y = s_XW + wave * (16 * LDP);
         T *Yg = static_cast<T *>(a.y) + tk * (R * P);
-        constexpr int RP = PTS * 16 / S::CE;        // 16-byte pieces of a row per wave
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
             if (!ow) break;
@@ -940,12 +957,14 @@ void k_scan_seg(ScanArgs a) {
             for (int pt = 0; pt < PTS; ++pt) store4(&s_y[l16 * LDP + pt * 16 + 4 * g], acc[m][pt]);
             asm volatile("" ::: "memory");
 #pragma unroll
-            for (int k = lane; k < 16 * RP; k += kWave) {
-                const int rl = k / RP, col = (k % RP) * S::CE;
+            for (int i = 0; i < NPC; ++i) {
+                const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * S::CE;
                 const int row = TT * 16 + rl, t = row / R, r = row % R;
-                if (t < nv)
-                    *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + pofs * 16 + col) =
-                        *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
+                if (k < 16 * RP && t < nv) {
+                    V16 yv = *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
+                    if constexpr (kGate) yv = gate_piece<T>(yv, zp[m][i]);
+                    *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + pofs * 16 + col) = yv;
+                }
             }
             asm volatile("" ::: "memory");
         }
@@ -955,13 +974,15 @@ void k_scan_seg(ScanArgs a) {
 template <typename T, int Q, int R>
 hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
     typedef SegShape<T, Q, R> S;
-    static int cap_cache[64];
+    static int cap_cache[2][64];
     ScanArgs a = a0;
+    const bool gate = a.z != nullptr;
+    const void *kfn = gate ? reinterpret_cast<const void *>(&k_scan_seg<T, Q, R, true>)
+                           : reinterpret_cast<const void *>(&k_scan_seg<T, Q, R, false>);
     const int64_t nsl = a.batch * a.H;
     int64_t G = a.G;
     if (G <= 0) {   // one resident wave of workgroups covers the whole scan
-        const int cap = resident_capacity(reinterpret_cast<const void *>(&k_scan_seg<T, Q, R>), S::NTHR,
-                                          cap_cache);
+        const int cap = resident_capacity(kfn, S::NTHR, cap_cache[gate ? 1 : 0]);
         if (cap <= 0) return hipErrorInvalidDevice;
         G = (nsl * a.nchunks + cap - 1) / cap;
         // Short chunks (fewer than 128 rows) split over several segments run
@@ -985,7 +1006,10 @@ hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
         const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);
         hipLaunchKernelGGL(k_reset, dim3(rblocks), dim3(256), 0, stream, a.ctl, a.flags, nflags);
     }
-    hipLaunchKernelGGL((k_scan_seg<T, Q, R>), dim3((unsigned)(nsl * a.nseg)), dim3(S::NTHR), 0, stream, a);
+    if (gate)
+        hipLaunchKernelGGL((k_scan_seg<T, Q, R, true>), dim3((unsigned)(nsl * a.nseg)), dim3(S::NTHR), 0, stream, a);
+    else
+        hipLaunchKernelGGL((k_scan_seg<T, Q, R, false>), dim3((unsigned)(nsl * a.nseg)), dim3(S::NTHR), 0, stream, a);
     return hipGetLastError();
 }
 

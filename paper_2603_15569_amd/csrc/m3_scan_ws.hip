@@ -52,7 +52,8 @@ struct WsShape {
     static_assert(PPW == 16, "prologue parts");
 };
 
-template <int Q, int R>
+// kGate: the stored y is multiplied by SiLU(z) (the block's output gate).
+template <int Q, int R, bool kGate>
 __global__ __launch_bounds__(512, 1)
 void k_scan_ws(ScanArgs a) {
     typedef bf16 T;
@@ -181,9 +182,29 @@ void k_scan_ws(ScanArgs a) {
 #pragma unroll
                     for (int v = 0; v < 4; ++v) acc[m][pt][v] *= ec;
             }
+            // y leaves in 16-byte pieces of its rows (NPC per lane and owned
+            // tile); with the gate, the matching pieces of z are loaded at the
+            // start of the last step and arrive during its products
+            constexpr int RP = P / CE;   // 16-byte pieces of a row
+            constexpr int NPC = 16 * RP / kWave;
+            static_assert(NPC * kWave == 16 * RP, "store pieces");
+            V16 zp[kGate ? TPW : 1][NPC];
 #pragma unroll
             for (int jb = 0; jb < NJB; ++jb) {
                 const T *sBc = s_B[jb & 1], *sXc = s_X[jb & 1];
+                if constexpr (kGate) {
+                    if (jb == NJB - 1) {
+                        const Rsrc rz = rows_rsrc(static_cast<const T *>(a.z), c, xstr, R * P);
+#pragma unroll
+                        for (int m = 0; m < TPW; ++m)
+#pragma unroll
+                            for (int i = 0; i < NPC; ++i) {
+                                const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * CE;
+                                const int row = TT[m] * 16 + rl, t = row / R, r = row % R;
+                                zp[m][i] = buf_load<V16>(rz, tok_off(t, xstr_b) + (uint32_t)((r * P + col) * sizeof(T)));
+                            }
+                    }
+                }
 #pragma unroll
                 for (int jp = 0; jp < S::JB / 32; ++jp) {
                     // Owned tile m lies in block m (rows 64 m .. 64 m + 63): tiles
@@ -272,19 +293,20 @@ void k_scan_ws(ScanArgs a) {
                     // 16-byte pieces of the rows
                     T *sy = s_Y[ow];
                     T *Yg = static_cast<T *>(a.y) + tok_of(c) * (R * P);
-                    constexpr int RP = P / CE;   // 16-byte pieces of a row
 #pragma unroll
                     for (int m = 0; m < TPW; ++m) {
 #pragma unroll
                         for (int pt = 0; pt < PT; ++pt) store4(&sy[l16 * LDP + pt * 16 + 4 * g], acc[m][pt]);
                         asm volatile("" ::: "memory");
 #pragma unroll
-                        for (int k = lane; k < 16 * RP; k += kWave) {
-                            const int rl = k / RP, col = (k % RP) * CE;
+                        for (int i = 0; i < NPC; ++i) {
+                            const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * CE;
                             const int row = TT[m] * 16 + rl, t = row / R, r = row % R;
-                            if (t < nv)
-                                *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) =
-                                    *reinterpret_cast<const V16 *>(&sy[rl * LDP + col]);
+                            if (t < nv) {
+                                V16 yv = *reinterpret_cast<const V16 *>(&sy[rl * LDP + col]);
+                                if constexpr (kGate) yv = gate_piece<T>(yv, zp[m][i]);
+                                *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) = yv;
+                            }
                         }
                         asm volatile("" ::: "memory");
                     }
@@ -568,7 +590,10 @@ template <int Q, int R>
 hipError_t launch_ws(const ScanArgs &a, hipStream_t stream) {
     typedef WsShape<Q, R> S;
     const int64_t nsl = a.batch * a.H;
-    hipLaunchKernelGGL((k_scan_ws<Q, R>), dim3((unsigned)nsl), dim3(S::NTHR), 0, stream, a);
+    if (a.z)
+        hipLaunchKernelGGL((k_scan_ws<Q, R, true>), dim3((unsigned)nsl), dim3(S::NTHR), 0, stream, a);
+    else
+        hipLaunchKernelGGL((k_scan_ws<Q, R, false>), dim3((unsigned)nsl), dim3(S::NTHR), 0, stream, a);
     return hipGetLastError();
 }
 

@@ -152,3 +152,12 @@ def workload_inputs(k: int, device="cpu", **override) -> ScanInputs:
                             w["dstate"], w["rank"], io=w["io"],
                             seed=w.get("seed", 1000 + k), device=device,
                             chunk=w["chunk"])
+
+
+def make_gate_input(like: torch.Tensor, seed: int) -> torch.Tensor:
+    """Output-gate input z shaped and typed like `like` (x of a scan, or x_t
+    of a step): N(0, 1) pre-activations, own seed 5000 + seed."""
+    g = torch.Generator(device=like.device)
+    g.manual_seed(5000 + int(seed))
+    z = torch.randn(tuple(like.shape), device=like.device, dtype=torch.float32, generator=g)
+    return z.to(like.dtype).contiguous()

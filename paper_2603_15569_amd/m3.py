@@ -39,8 +39,8 @@ class M3Error(RuntimeError):
         self.status = status
 
 
-EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_step", "m3_status_string",
-           "m3_last_hip_error")
+EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_step",
+           "m3_step_gated", "m3_status_string", "m3_last_hip_error")
 _lib = None
 
 
@@ -57,8 +57,12 @@ def lib() -> ctypes.CDLL:
         L.m3_scan_workspace_bytes.restype = ctypes.c_size_t
         L.m3_scan_fwd.argtypes = [dims_p] + [vp] * 15 + [vp, ctypes.c_size_t, vp]
         L.m3_scan_fwd.restype = ctypes.c_int
+        L.m3_scan_fwd_gated.argtypes = [dims_p] + [vp] * 16 + [vp, ctypes.c_size_t, vp]
+        L.m3_scan_fwd_gated.restype = ctypes.c_int
         L.m3_step.argtypes = [dims_p] + [vp] * 12 + [vp]
         L.m3_step.restype = ctypes.c_int
+        L.m3_step_gated.argtypes = [dims_p] + [vp] * 13 + [vp]
+        L.m3_step_gated.restype = ctypes.c_int
         L.m3_status_string.argtypes = [ctypes.c_int]
         L.m3_status_string.restype = ctypes.c_char_p
         L.m3_last_hip_error.argtypes = []
@@ -115,10 +119,11 @@ def workspace_bytes(dims: M3Dims) -> int:
 
 def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
              init_state=None, init_carry=None, out=None, workspace=None,
-             stream=None, split: bool = False, per_chunk: bool = False, seg: int = 0
-             ) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
-    """m3_scan_fwd: returns y [B,L,H,R,P], final_state [B,H,N,P] fp32 and the
-    carry (B_{L-1} [B,H,R,N], X_{L-1} [B,H,R,P]).  `out` may supply
+             stream=None, split: bool = False, per_chunk: bool = False, seg: int = 0,
+             z=None) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
+    """m3_scan_fwd (m3_scan_fwd_gated when the gate input `z`, shaped like x,
+    is given: y o SiLU(z)): returns y [B,L,H,R,P], final_state [B,H,N,P] fp32
+    and the carry (B_{L-1} [B,H,R,N], X_{L-1} [B,H,R,P]).  `out` may supply
     (y, final_state, carryB, carryX) to write into.  Kernel choice: `split`
     (M3_SCAN_SPLIT, three kernels), `per_chunk` (M3_SCAN_PER_CHUNK, one chunk
     per workgroup), else the segmented kernel with `seg` chunks per
@@ -138,11 +143,18 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
     if workspace is None and nbytes > 0:
         workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
     icB, icX = (None, None) if init_carry is None else init_carry
-    _check(lib().m3_scan_fwd(ctypes.byref(d), _p(x), _p(Bm), _p(Cm), _p(dt), _p(A), _p(lam),
-                             _p(theta), _p(D), _p(init_state), _p(icB), _p(icX), _p(y), _p(fs),
-                             _p(cB), _p(cX), _p(workspace),
-                             workspace.numel() if workspace is not None else 0,
-                             _stream(stream)))
+    wsb = workspace.numel() if workspace is not None else 0
+    if z is None:
+        _check(lib().m3_scan_fwd(ctypes.byref(d), _p(x), _p(Bm), _p(Cm), _p(dt), _p(A), _p(lam),
+                                 _p(theta), _p(D), _p(init_state), _p(icB), _p(icX), _p(y),
+                                 _p(fs), _p(cB), _p(cX), _p(workspace), wsb, _stream(stream)))
+    else:
+        if z.shape != x.shape or z.dtype != x.dtype:
+            raise ValueError("z must have the shape and dtype of x")
+        _check(lib().m3_scan_fwd_gated(ctypes.byref(d), _p(x), _p(Bm), _p(Cm), _p(dt), _p(A),
+                                       _p(lam), _p(theta), _p(D), _p(z), _p(init_state), _p(icB),
+                                       _p(icX), _p(y), _p(fs), _p(cB), _p(cX), _p(workspace), wsb,
+                                       _stream(stream)))
     return y, fs, (cB, cX)
 
 
@@ -158,13 +170,22 @@ def step_dims(x_t: torch.Tensor, B_t: torch.Tensor, A: torch.Tensor) -> M3Dims:
     return M3Dims(batch, 1, nheads, headdim, dstate, rank, 1, _IO[x_t.dtype], 0, sb, 0, sh, 0)
 
 
-def step(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, y=None, stream=None):
-    """m3_step: advances `state` [B,H,N,P] and `carry` (B [B,H,R,N],
-    X [B,H,R,P]) in place by one token; returns y_t [B,H,R,P]."""
+def step(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, y=None, stream=None, z=None):
+    """m3_step (m3_step_gated when the gate input `z`, shaped like x_t, is
+    given: y_t o SiLU(z_t)): advances `state` [B,H,N,P] and `carry`
+    (B [B,H,R,N], X [B,H,R,P]) in place by one token; returns y_t [B,H,R,P]."""
     d = step_dims(x_t, B_t, A)
     if y is None:
         y = torch.empty_like(x_t)
     cB, cX = carry
-    _check(lib().m3_step(ctypes.byref(d), _p(state), _p(cB), _p(cX), _p(x_t), _p(B_t), _p(C_t),
-                         _p(dt_t), _p(A), _p(lam_t), _p(theta_t), _p(D), _p(y), _stream(stream)))
+    if z is None:
+        _check(lib().m3_step(ctypes.byref(d), _p(state), _p(cB), _p(cX), _p(x_t), _p(B_t),
+                             _p(C_t), _p(dt_t), _p(A), _p(lam_t), _p(theta_t), _p(D), _p(y),
+                             _stream(stream)))
+    else:
+        if z.shape != x_t.shape or z.dtype != x_t.dtype:
+            raise ValueError("z must have the shape and dtype of x_t")
+        _check(lib().m3_step_gated(ctypes.byref(d), _p(state), _p(cB), _p(cX), _p(x_t), _p(B_t),
+                                   _p(C_t), _p(dt_t), _p(A), _p(lam_t), _p(theta_t), _p(D), _p(z),
+                                   _p(y), _stream(stream)))
     return y

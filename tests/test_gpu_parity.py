@@ -12,8 +12,8 @@ import torch
 
 import oracle
 from paper_2603_15569_amd import m3
-from paper_2603_15569_amd.inputs import (WORKLOADS, make_scan_inputs, make_step_inputs,
-                                         workload_inputs)
+from paper_2603_15569_amd.inputs import (WORKLOADS, make_gate_input, make_scan_inputs,
+                                         make_step_inputs, workload_inputs)
 
 pytestmark = pytest.mark.gpu
 
@@ -28,7 +28,8 @@ def say(msg):
 MODES = ("seg", "per_chunk", "split")   # segmented single-pass (default), one chunk per WG, 3 kernels
 
 
-def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, mode="seg", seg=0):
+def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, mode="seg", seg=0,
+             z=None):
     """Scan with every output pre-filled with NaN, so an unwritten element fails."""
     x = inp.x
     B_, L, H, R, P = x.shape
@@ -47,7 +48,7 @@ def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, mode="
     ws = torch.zeros(max(nbytes, 16), dtype=torch.uint8, device=x.device)
     y, fs, (cB, cX) = m3.scan_fwd(x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta, inp.D,
                                   chunk=chunk, init_state=init_state, init_carry=init_carry,
-                                  out=out, workspace=ws, **kw)
+                                  out=out, workspace=ws, z=z, **kw)
     torch.cuda.synchronize()
     if single_pass and L > 0:
         # single-pass kernels: word 1 of the workspace counts look-back waits that timed out
@@ -55,7 +56,8 @@ def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, mode="
     return y, fs, cB, cX
 
 
-def check_slices(inp, y, fs, cB, cX, slices, tol, init_state=None, init_carry=None, label=""):
+def check_slices(inp, y, fs, cB, cX, slices, tol, init_state=None, init_carry=None, label="",
+                 z=None):
     ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
                                 inp.D, slices)
     kw = {}
@@ -65,6 +67,8 @@ def check_slices(inp, y, fs, cB, cX, slices, tol, init_state=None, init_carry=No
         kw["init_B"] = oracle.slices_of_state(init_carry[0], slices)
         kw["init_X"] = oracle.slices_of_state(init_carry[1], slices)
     ry, rs, rb, rx = oracle.scan(**ref, **kw)
+    if z is not None:   # the output gate y o SiLU(z)
+        ry = oracle.gate(ry, np.stack([oracle._np(z[b, :, h]) for b, h in slices]))
     worst = 0.0
     for k, (b, h) in enumerate(slices):
         gy = y[b, :, h].double().cpu().numpy()
@@ -421,3 +425,83 @@ def test_decode_steps_small(io, N, P, R):
             assert oracle.rel_err(y[b, h].double().cpu().numpy(), ry[k]) <= tol
             assert oracle.rel_err(state[b, h].cpu().numpy(), rs[k]) <= tol
         assert np.array_equal(oracle.slices_of_state(cB, sl), rb)
+
+
+# ---------------------------------------------------------------------------
+# Output gate y o SiLU(z) (m3_scan_fwd_gated, m3_step_gated)
+# ---------------------------------------------------------------------------
+
+GATE_CASES = [  # io, N, P, R, Q, mode, seg
+    ("f32", 16, 16, 1, 64, "seg", 0), ("f32", 16, 16, 1, 64, "per_chunk", 0),
+    ("f32", 16, 16, 1, 64, "split", 0), ("f32", 128, 64, 4, 32, "seg", 2),
+    ("bf16", 128, 64, 1, 64, "seg", 0), ("bf16", 128, 64, 1, 64, "seg", 1 << 20),
+    ("bf16", 128, 64, 1, 64, "per_chunk", 0), ("bf16", 128, 64, 1, 64, "split", 0),
+    ("bf16", 128, 64, 2, 32, "per_chunk", 0),
+    ("bf16", 128, 64, 4, 64, "seg", 1 << 20), ("bf16", 128, 64, 4, 64, "seg", 2),
+    ("bf16", 128, 64, 4, 64, "per_chunk", 0), ("bf16", 128, 64, 4, 128, "per_chunk", 0),
+    ("bf16", 128, 64, 4, 128, "seg", 2),
+]
+
+
+@pytest.mark.parametrize("io,N,P,R,Q,mode,seg", GATE_CASES)
+def test_gated_scan(io, N, P, R, Q, mode, seg):
+    """Gated prefill on every kernel (several chunks and a ragged tail) against
+    the oracle's y o SiLU(z); the final state and the carry are those of the
+    ungated call, bit for bit (the gate acts on the output only)."""
+    L = 3 * Q + Q // 2 + 3
+    say(f"gated scan io={io} N={N} R={R} Q={Q} L={L} mode={mode} seg={seg}")
+    inp = make_scan_inputs(2, L, 3, P, N, R, io=io, seed=71 + R + Q, device=DEV, chunk=Q)
+    z = make_gate_input(inp.x, R + Q)
+    y, fs, cB, cX = run_scan(inp, Q, mode=mode, seg=seg, z=z)
+    check_slices(inp, y, fs, cB, cX, sample_slices(2, 3, 99, 6), TOL[io],
+                 label=f"gated {io}/{R}/{Q}/{mode}", z=z)
+    y0, fs0, cB0, cX0 = run_scan(inp, Q, mode=mode, seg=seg)
+    assert torch.equal(fs, fs0) and torch.equal(cB, cB0) and torch.equal(cX, cX0)
+    # the gate itself, against the ungated output of the same kernel
+    ref = y0.double() * torch.nn.functional.silu(z.double())
+    scale = ref.abs().max().item()
+    assert (y.double() - ref).abs().max().item() <= (1e-6 if io == "f32" else 8e-3) * scale
+
+
+def test_gated_workload1_siso():
+    """Workload 1 (SISO bf16 prefill) gated, all 64 slices."""
+    say("gated workload 1: all 64 slices")
+    w = WORKLOADS[1]
+    inp = workload_inputs(1, device=DEV)
+    z = make_gate_input(inp.x, 1)
+    y, fs, cB, cX = run_scan(inp, w["chunk"], z=z)
+    check_slices(inp, y, fs, cB, cX, sample_slices(w["batch"], w["nheads"], 10**6, 1),
+                 TOL["bf16"], label="gated w1", z=z)
+
+
+@pytest.mark.parametrize("io,N,P,R", [("f32", 16, 16, 1), ("f32", 128, 64, 4),
+                                      ("bf16", 128, 64, 1), ("bf16", 128, 64, 4)])
+def test_gated_decode_steps(io, N, P, R):
+    """Gated decode steps: y_t o SiLU(z_t) against the oracle, state and
+    carry advanced as by the ungated step."""
+    say(f"gated decode io={io} N={N} R={R}")
+    dt = torch.float32 if io == "f32" else torch.bfloat16
+    inp = make_scan_inputs(3, 4, 5, P, N, R, io=io, seed=37, device=DEV)
+    state = torch.randn(3, 5, N, P, device=DEV)
+    cB = torch.randn(3, 5, R, N, device=DEV).to(dt)
+    cX = torch.randn(3, 5, R, P, device=DEV).to(dt)
+    state0, cB0, cX0 = state.clone(), cB.clone(), cX.clone()
+    sl = [(b, h) for b in range(3) for h in range(5)]
+    rs = oracle.slices_of_state(state, sl)
+    rb, rx = oracle.slices_of_state(cB, sl), oracle.slices_of_state(cX, sl)
+    A_s = np.array([float(inp.A[h]) for _, h in sl])
+    D_s = np.array([float(inp.D[h]) for _, h in sl])
+    for s in range(3):
+        st = make_step_inputs(inp, s)
+        z = make_gate_input(st.x, 100 + s)
+        y = torch.full_like(st.x, float("nan"))
+        m3.step(state, (cB, cX), st.x, st.Bm, st.Cm, st.dt, inp.A, st.lam, st.theta, inp.D, y=y, z=z)
+        m3.step(state0, (cB0, cX0), st.x, st.Bm, st.Cm, st.dt, inp.A, st.lam, st.theta, inp.D)
+        torch.cuda.synchronize()
+        p = oracle.slices_of_step(st.x, st.Bm, st.Cm, st.dt, st.lam, st.theta, sl)
+        ry, rs, rb, rx = oracle.step(rs, rb, rx, p["x"], p["B"], p["C"], p["dt"], A_s, p["lam"],
+                                     p["theta"], D_s)
+        ry = oracle.gate(ry, oracle.slices_of_state(z, sl))
+        for k, (b, h) in enumerate(sl):
+            assert oracle.rel_err(y[b, h].double().cpu().numpy(), ry[k]) <= TOL[io]
+        assert torch.equal(state, state0) and torch.equal(cB, cB0) and torch.equal(cX, cX0)

@@ -153,3 +153,32 @@ def test_prefill_bytes_workloads():
     per4 = roofline.prefill_bytes(1, 1, 1, 128, 64, 4, 2) - (128 * 64 * 4 + 4 * (128 + 64) * 2)
     assert per4 == 3336
     assert roofline.decode_bytes_per_slice(128, 64, 4, 2) == 71944
+
+
+def test_gated_host_validation(L):
+    """The gated entry points: z is required (a token array like x, 16-byte
+    aligned); every other check is the ungated call's."""
+    def scan(d, over=None):
+        ptrs = [FAKE] * 16       # x B C dt A lam theta D z init icB icX y fs cB cX
+        for k in (9, 10, 11):
+            ptrs[k] = None
+        for k, v in (over or {}).items():
+            ptrs[k] = v
+        wsb = L.m3_scan_workspace_bytes(ctypes.byref(d))
+        return L.m3_scan_fwd_gated(ctypes.byref(d), *ptrs, FAKE, wsb, None)
+    assert scan(dims(), {8: None}) == m3.M3_ERR_NULL
+    assert scan(dims(), {8: FAKE + 2}) == m3.M3_ERR_ALIGN
+    assert scan(dims(), {0: None}) == m3.M3_ERR_NULL
+    assert scan(dims(chunk=48)) == m3.M3_ERR_UNSUPPORTED
+    assert scan(dims(), {10: FAKE}) == m3.M3_ERR_NULL              # one carry half only
+
+    def step(d, over=None):
+        ptrs = [FAKE] * 13       # state cB cX x B C dt A lam theta D z y
+        for k, v in (over or {}).items():
+            ptrs[k] = v
+        return L.m3_step_gated(ctypes.byref(d), *ptrs, None)
+    assert step(dims(), {11: None}) == m3.M3_ERR_NULL
+    assert step(dims(), {11: FAKE + 4}) == m3.M3_ERR_ALIGN
+    assert step(dims(), {12: None}) == m3.M3_ERR_NULL
+    assert step(dims(io=5)) == m3.M3_ERR_DTYPE
+    assert L.m3_last_hip_error() == 0
