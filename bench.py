@@ -48,7 +48,8 @@ def main():
     import torch
 
     from paper_2603_15569_amd import m3, roofline
-    from paper_2603_15569_amd.inputs import WORKLOADS, make_step_inputs, workload_inputs
+    from paper_2603_15569_amd.inputs import (WORKLOADS, make_gate_input, make_step_inputs,
+                                             workload_inputs)
 
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
@@ -164,6 +165,40 @@ def main():
     step_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
     tot_ms = np.array([e[0].elapsed_time(e[2]) for e in ev])
 
+    # ---------------- output gate y o SiLU(z) (after the timed loop) ----------------
+    zs = [make_gate_input(c.x, i) for i, c in enumerate(copies)]
+    zd = [make_gate_input(st.x, 100 + i) for i, st in enumerate(step_in[:4])]
+
+    def gscan(i):
+        c = copies[i % len(copies)]
+        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.theta, c.D, chunk=Qp, out=out,
+                    workspace=ws, z=zs[i % len(zs)])
+
+    def unfused(i):   # ungated scan, then the gate as a separate elementwise pass
+        scan(i)
+        out[0].mul_(torch.nn.functional.silu(zs[i % len(zs)]))
+
+    def gstep(i):
+        st = step_in[i % n_step_inputs]
+        m3.step(dstate, (dcB, dcX), st.x, st.Bm, st.Cm, st.dt, layer.A, st.lam, st.theta, layer.D,
+                y=yd, z=zd[i % len(zd)])
+
+    def timed(fn, n):
+        for i in range(3):
+            fn(i)
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(n + 1)]
+        torch.cuda.synchronize()
+        e[0].record(stream)
+        for i in range(n):
+            fn(i)
+            e[i + 1].record(stream)
+        torch.cuda.synchronize()
+        return float(np.mean([e[i].elapsed_time(e[i + 1]) for i in range(n)]))
+
+    n_gate = max(10, min(args.steps, 100))
+    g_scan_ms, g_unfused_ms, g_step_ms = timed(gscan, n_gate), timed(unfused, n_gate), timed(gstep, n_gate)
+    b_scan_ms, b_step_ms = timed(scan, n_gate), timed(dstep, n_gate)   # ungated, same back-to-back timing
+
     tokens = Bp * Lp
     prefill_tok_s = tokens / (scan_ms.mean() * 1e-3)
     dec_us = step_ms.mean() * 1e3
@@ -220,6 +255,8 @@ def main():
             "mfma_tflops": round(pre_tfs, 2),
             "mfma_frac": round(pre_tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
         },
+        "gate": gate_figures(g_scan_ms, g_unfused_ms, g_step_ms, b_scan_ms, b_step_ms, tokens, pre_bytes,
+                             Bp * Lp * Hp * Rp * Pp * 2, dec_bytes, Bd * Hd * Rd * Pd * 2, peak_gbs),
         "roofline_prefill_mimo": mimo_roofline(Bm_, Lm_, Hm_, Nm_, Pm_, Rm_, wd["chunk"], mimo_ms,
                                                roofline, peak_gbs),
         "wall_s_timed_loop": round(wall, 3),
@@ -227,6 +264,26 @@ def main():
     if not args.no_cpu:
         result["cpu_baseline"] = cpu_baseline(base, layer, step_in, wp, wd)
     print(json.dumps(result), flush=True)
+
+
+def gate_figures(scan_ms, unfused_ms, step_ms, base_scan_ms, base_step_ms, tokens, pre_bytes,
+                 z_bytes, dec_bytes, zd_bytes, peak_gbs):
+    """The fused output gate y o SiLU(z) on the same two workloads, each call
+    timed back to back: the gated prefill (algorithmic bytes plus z), the
+    ungated prefill alone and followed by the gate as a separate elementwise
+    pass (torch), the gated and the ungated decode step."""
+    pre_gbs = (pre_bytes + z_bytes) / (scan_ms * 1e-3) / 1e9
+    dec_gbs = (dec_bytes + zd_bytes) / (step_ms * 1e-3) / 1e9
+    return {
+        "prefill_ms": round(scan_ms, 5), "prefill_tokens_per_s": round(tokens / (scan_ms * 1e-3), 1),
+        "prefill_bound": "hbm", "prefill_achieved_gbs": round(pre_gbs, 1),
+        "prefill_frac": round(pre_gbs / peak_gbs, 4), "prefill_bytes_per_launch": pre_bytes + z_bytes,
+        "ungated_prefill_ms": round(base_scan_ms, 5), "unfused_prefill_ms": round(unfused_ms, 5),
+        "decode_us_per_step": round(step_ms * 1e3, 3),
+        "ungated_decode_us_per_step": round(base_step_ms * 1e3, 3), "decode_bound": "hbm",
+        "decode_achieved_gbs": round(dec_gbs, 1), "decode_frac": round(dec_gbs / peak_gbs, 4),
+        "decode_bytes_per_launch": dec_bytes + zd_bytes,
+    }
 
 
 def mimo_roofline(B, L, H, N, P, R, Q, ms, roofline, peak_gbs):
