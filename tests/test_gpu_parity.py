@@ -505,3 +505,29 @@ def test_gated_decode_steps(io, N, P, R):
         for k, (b, h) in enumerate(sl):
             assert oracle.rel_err(y[b, h].double().cpu().numpy(), ry[k]) <= TOL[io]
         assert torch.equal(state, state0) and torch.equal(cB, cB0) and torch.equal(cX, cX0)
+
+
+# ---------------------------------------------------------------------------
+# Maximum sizes: the single-pass kernels address a token's rows with a 24-bit
+# stride multiply and a chunk's rows with 32-bit buffer offsets; the widest
+# tokens they accept, and the first ones they hand to the three-kernel path
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("H,Q,L,mode", [
+    (16383, 64, 70, "seg"),          # tokens of 2^24 - 1024 bytes: single pass, several chunks
+    (16384, 64, 70, "seg"),          # 2^24 bytes: three-kernel path
+    (16383, 128, 133, "seg"),        # a chunk's rows span 2^31 - 1.1 MB
+    (16383, 128, 133, "per_chunk"),
+])
+def test_widest_tokens(H, Q, L, mode):
+    """bf16, N=128, P=64, R=4: nheads * rank * dstate elements per token at and
+    just past the single-pass kernels' 2^24-byte row stride (and a 128-token
+    chunk whose rows reach within 1.1 MB of 2 GiB); three sampled heads plus
+    the first and the last checked against the oracle."""
+    say(f"widest tokens H={H} Q={Q} L={L} mode={mode}")
+    inp = make_scan_inputs(1, L, H, 64, 128, 4, io="bf16", seed=91, device=DEV, chunk=Q)
+    y, fs, cB, cX = run_scan(inp, Q, mode=mode)
+    sl = [(0, 0), (0, 1), (0, H // 2), (0, H - 2), (0, H - 1)]
+    check_slices(inp, y, fs, cB, cX, sl, TOL["bf16"], label=f"wide H={H} Q={Q} {mode}")
+    del inp, y, fs, cB, cX
+    torch.cuda.empty_cache()
