@@ -201,9 +201,15 @@ def main():
         return (float(np.mean([x[0].elapsed_time(x[1]) for x in e])),
                 float(np.mean([x[1].elapsed_time(x[2]) for x in e])))
 
+    def pscan(i):   # per-head frequencies omega [H, N/2]: the kernels form dt * omega
+        c = copies[i % len(copies)]
+        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.omega, c.D, chunk=Qp, out=out,
+                    workspace=ws)
+
     n_gate = max(10, min(args.steps, 100))
     g_scan_ms, g_step_ms = timed(gscan, gstep, n_gate)
     g_unfused_ms, _ = timed(unfused, dstep, n_gate)
+    p_scan_ms, _ = timed(pscan, dstep, n_gate)
 
     tokens = Bp * Lp
     prefill_tok_s = tokens / (scan_ms.mean() * 1e-3)
@@ -264,6 +270,9 @@ def main():
         "gate": gate_figures(g_scan_ms, g_unfused_ms, g_step_ms, float(scan_ms.mean()),
                              float(step_ms.mean()), tokens, pre_bytes,
                              Bp * Lp * Hp * Rp * Pp * 2, dec_bytes, Bd * Hd * Rd * Pd * 2, peak_gbs),
+        "theta_per_head": per_head_figures(p_scan_ms, float(scan_ms.mean()), tokens,
+                                           pre_bytes - Bp * Lp * Hp * (Np // 2) * 4 + Hp * (Np // 2) * 4,
+                                           peak_gbs),
         "roofline_prefill_mimo": mimo_roofline(Bm_, Lm_, Hm_, Nm_, Pm_, Rm_, wd["chunk"], mimo_ms,
                                                roofline, peak_gbs),
         "wall_s_timed_loop": round(wall, 3),
@@ -292,6 +301,18 @@ def gate_figures(scan_ms, unfused_ms, step_ms, base_scan_ms, base_step_ms, token
         "decode_achieved_gbs": round(dec_gbs, 1), "decode_frac": round(dec_gbs / peak_gbs, 4),
         "decode_bytes_per_launch": dec_bytes + zd_bytes,
     }
+
+
+def per_head_figures(ms, theta_ms, tokens, nbytes, peak_gbs):
+    """The SISO prefill with per-head rotary frequencies omega (angles dt *
+    omega formed in the kernels, M3_THETA_PER_HEAD) in the timed loop's
+    pattern, against the timed loop's per-token-angle prefill; bytes without
+    the per-token angle array."""
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    return {"prefill_ms": round(ms, 5), "prefill_tokens_per_s": round(tokens / (ms * 1e-3), 1),
+            "per_token_theta_prefill_ms": round(theta_ms, 5), "bound": "hbm",
+            "achieved_gbs": round(gbs, 1), "frac": round(gbs / peak_gbs, 4),
+            "bytes_per_launch": nbytes}
 
 
 def mimo_roofline(B, L, H, N, P, R, Q, ms, roofline, peak_gbs):

@@ -20,7 +20,10 @@
  * rotates every row pair (i, i + N/2) by the angle theta_t[i]:
  *     [h_i; h_{i+N/2}] <- [[cos, -sin], [sin, cos]] [h_i; h_{i+N/2}].
  * theta is the per-step angle (the paper's Delta_t theta_t[i]); the library
- * does not multiply it by dt.  D is a per-head skip (Mamba convention; the
+ * does not multiply it by dt, except with the flag M3_THETA_PER_HEAD, where
+ * theta holds per-head frequencies omega [nheads][dstate/2] and the angle of
+ * token t is dt_t * omega (an fp32 product, formed in the kernels: the
+ * per-token angle array is then never read).  D is a per-head skip (Mamba convention; the
  * paper has no skip term).  With no initial state, h_{-1} = 0 and
  * B_{-1} X_{-1}^T = 0 (the unrolled state starts at gamma_0 B_0 x_0).
  *
@@ -33,6 +36,7 @@
  *     B, C        [batch][seqlen][nheads][rank][dstate]      io dtype
  *     dt, lambda  [batch][seqlen][nheads]                    fp32
  *     theta       [batch][seqlen][nheads][dstate/2]          fp32
+ *                 ([nheads][dstate/2] with M3_THETA_PER_HEAD)
  *     A           A[b*a_stride_b + t*a_stride_t + h*a_stride_h]  fp32 (< 0)
  *     D           [nheads]                                   fp32
  *     state       [batch][nheads][dstate][headdim]           fp32
@@ -90,9 +94,15 @@ typedef enum { M3_F32 = 0, M3_BF16 = 1 } m3_dtype;
  * max(dstate, headdim) elements of at least 16 MiB, or a chunk of such
  * tokens of at least 2 GiB).
  * M3_SCAN_PER_CHUNK: the single-pass kernel with one chunk per workgroup
- * (a look-back across every chunk).  Ignored together with M3_SCAN_SPLIT. */
+ * (a look-back across every chunk).  Ignored together with M3_SCAN_SPLIT.
+ * M3_THETA_PER_HEAD (m3_scan_fwd and m3_step, gated or not): theta / theta_t
+ * are the per-head frequencies omega [nheads][dstate/2] and every angle is
+ * dt * omega (Sec. 3.2: the rotation angle is Delta_t times theta, here with
+ * a data-independent theta per head, as in RoPE); saves reading
+ * 2 * dstate bytes per token and head. */
 #define M3_SCAN_SPLIT 1
 #define M3_SCAN_PER_CHUNK 2
+#define M3_THETA_PER_HEAD 4
 
 typedef struct {
     int64_t batch;     /* >= 1                                              */

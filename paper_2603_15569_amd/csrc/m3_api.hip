@@ -43,7 +43,7 @@ static int io_bytes_of(int32_t io) { return io == M3_F32 ? 4 : io == M3_BF16 ? 2
 static m3_status check_dims_common(const m3_dims *d) {
     if (!d) return M3_ERR_NULL;
     if (d->io != M3_F32 && d->io != M3_BF16) return M3_ERR_DTYPE;
-    if (d->flags & ~(M3_SCAN_SPLIT | M3_SCAN_PER_CHUNK)) return M3_ERR_SHAPE;
+    if (d->flags & ~(M3_SCAN_SPLIT | M3_SCAN_PER_CHUNK | M3_THETA_PER_HEAD)) return M3_ERR_SHAPE;
     if (d->batch < 1 || d->nheads < 1 || d->headdim < 1 || d->dstate < 2 || d->rank < 1)
         return M3_ERR_SHAPE;
     if (d->dstate % 2) return M3_ERR_SHAPE;
@@ -142,6 +142,7 @@ static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const 
     a.dt = dt; a.A = A; a.lam = lambda; a.theta = theta; a.D = D;
     a.init_state = init_state; a.init_cB = init_carryB; a.init_cX = init_carryX;
     a.y = y; a.z = z; a.final_state = final_state; a.cB = carryB; a.cX = carryX;
+    a.theta_ph = (d->flags & M3_THETA_PER_HEAD) ? 1 : 0;
     char *ws = static_cast<char *>(workspace);
     a.M = nullptr; a.Sin = nullptr; a.tot = nullptr;
     a.ctl = nullptr; a.flags = nullptr; a.agg = nullptr; a.inc = nullptr;
@@ -211,6 +212,7 @@ static m3_status step(const m3_dims *d, float *state, void *carryB, void *carryX
     a.x = x_t; a.B = B_t; a.C = C_t;
     a.dt = dt_t; a.A = A; a.lam = lambda_t; a.theta = theta_t; a.D = D;
     a.y = y_t; a.z = z_t;
+    a.theta_ph = (d->flags & M3_THETA_PER_HEAD) ? 1 : 0;
     a.batch = d->batch; a.H = d->nheads;
     a.a_sb = d->a_stride_b; a.a_sh = d->a_stride_h;
     const hipError_t e = fn(a, static_cast<hipStream_t>(stream));

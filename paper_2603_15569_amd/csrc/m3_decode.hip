@@ -78,8 +78,9 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
         vx[k] = *reinterpret_cast<const V8 *>(Xt + pc * VE);
         vxp[k] = *reinterpret_cast<const V8 *>(cX + pc * VE);
     }
-    const float *th = a.theta + bh * NH;
-    const float thv = th[min(tid, NH - 1)];
+    // per-step angles, or dt * omega with the head's frequencies omega
+    const float *th = a.theta_ph ? a.theta + h * NH : a.theta + bh * NH;
+    const float thv = th[min(tid, NH - 1)] * (a.theta_ph ? dtv : 1.f);
     // gate inputs of this thread's outputs (y_t o SiLU(z_t))
     constexpr int TZ = (R * P + NT - 1) / NT;
     float zv[TZ];

@@ -15,6 +15,8 @@ struct ScanArgs {
     const void *init_cB, *init_cX;      // both null or both set
     void *y;
     const void *z;                      // output gate [B,L,H,R,P] (io), or null
+    int theta_ph;                       // theta holds per-head frequencies omega [H][N/2]:
+                                        // the angle of token t is dt_t * omega
     float *final_state;
     void *cB, *cX;
     // workspace regions (see scan_workspace_layout)
@@ -43,6 +45,7 @@ struct StepArgs {
     const float *dt, *A, *lam, *theta, *D;
     void *y;
     const void *z;                      // output gate [B,H,R,P] (io), or null
+    int theta_ph;                       // theta holds omega [H][N/2] (angle dt * omega)
     int64_t batch, H;
     int64_t a_sb, a_sh;
 };

@@ -74,11 +74,14 @@ __device__ void chunk_prologue(const ScanArgs &a, int64_t b, int64_t h, int64_t 
         s_gam[tid] = gam;
         s_sig[tid] = sig;
     }
-    const float *th = a.theta + ((b * a.L + t0) * a.H + h) * S::NH;
-    const int64_t tstride = a.H * S::NH;
+    // per-token angles, or dt * omega with the head's frequencies omega
+    const float *th = a.theta_ph ? a.theta + h * S::NH : a.theta + ((b * a.L + t0) * a.H + h) * S::NH;
+    const int64_t tstride = a.theta_ph ? 0 : a.H * S::NH;
+    const float *dtc = a.dt + (b * a.L + t0) * a.H + h;
     for (int e = tid; e < S::Q * S::NH; e += kBlock) {
         const int t = e / S::NH, i = e % S::NH;
-        s_psi[t * S::LDPSI + i] = (t < nvalid) ? (Acc)th[t * tstride + i] : (Acc)0;
+        const float v = (t < nvalid) ? th[t * tstride + i] * (a.theta_ph ? dtc[t * a.H] : 1.f) : 0.f;
+        s_psi[t * S::LDPSI + i] = (Acc)v;
     }
     __syncthreads();
     // Columns 0..NH-1 are the angle scans, column NH the log-decay scan.

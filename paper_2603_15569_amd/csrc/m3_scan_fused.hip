@@ -212,13 +212,22 @@ void k_scan_fused(ScanArgs a) {
         const int i = tid % NH, seg = tid / NH;
         // (tokens past the end of the sequence read as zeros; the dt and
         // lambda ranges extend to the next chunk's first token if there is one)
-        const Rsrc rth = make_rsrc(a.theta + tok0 * NH, (uint32_t)(((nvalid - 1) * tstr + 1) * NH * 4));
-        const uint32_t thstr_b = (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
+        // (per-head frequencies: every token reads the head's omega row, and
+        // the angle is dt * omega: the segment's dt values are loaded too)
+        const Rsrc rth = a.theta_ph ? make_rsrc(a.theta + h * NH, (uint32_t)(NH * 4))
+                                    : make_rsrc(a.theta + tok0 * NH, (uint32_t)(((nvalid - 1) * tstr + 1) * NH * 4));
+        const uint32_t thstr_b = a.theta_ph ? 0u : (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
         float th[S::TPS];
 #pragma unroll
         for (int k = 0; k < S::TPS; ++k) th[k] = buf_load<float>(rth, tok_off(seg * S::TPS + k, thstr_b) + i * 4);
         const int nvn = nvalid + (t0 + nvalid < a.L ? 1 : 0);
         const Rsrc rdt = make_rsrc(a.dt + tok0, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
+        float dts[S::TPS];
+        if (a.theta_ph) {
+            const Rsrc rdv = make_rsrc(a.dt + tok0, (uint32_t)(((nvalid - 1) * tstr + 1) * 4));   // zero past the end
+#pragma unroll
+            for (int k = 0; k < S::TPS; ++k) dts[k] = buf_load<float>(rdv, tok_off(seg * S::TPS + k, tstr_b));
+        }
         const Rsrc rlam = make_rsrc(a.lam + tok0, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
         const uint32_t o = tok_off(tid, tstr_b);
         const float dtv = buf_load<float>(rdt, o), lamv = buf_load<float>(rlam, o);
@@ -244,7 +253,7 @@ void k_scan_fused(ScanArgs a) {
         const float sig = gam + (1.f - lamn) * dtn;
         Acc ps[S::TPS];
 #pragma unroll
-        for (int k = 0; k < S::TPS; ++k) ps[k] = (Acc)th[k];
+        for (int k = 0; k < S::TPS; ++k) ps[k] = (Acc)(a.theta_ph ? th[k] * dts[k] : th[k]);
         if (tid < Q) {
             s_gam[tid] = gam;
             s_sig[tid] = sig;

@@ -256,10 +256,12 @@ void k_scan_seg(ScanArgs a) {
         const int64_t tk = tok_of(c);
         const int nv = nvalid_of(c);
         const int nvn = nv + (c * Q + nv < a.L ? 1 : 0);
-        const Rsrc rth = make_rsrc(a.theta + tk * NH, (uint32_t)(((nv - 1) * tstr + 1) * NH * 4));
+        // per-head frequencies: every token reads the head's omega row
+        const Rsrc rth = a.theta_ph ? make_rsrc(a.theta + h * NH, (uint32_t)(NH * 4))
+                                    : make_rsrc(a.theta + tk * NH, (uint32_t)(((nv - 1) * tstr + 1) * NH * 4));
         const Rsrc rdt = make_rsrc(a.dt + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
         const Rsrc rlam = make_rsrc(a.lam + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
-        const uint32_t thstr_b = (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
+        const uint32_t thstr_b = a.theta_ph ? 0u : (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
 #pragma unroll
         for (int u = 0; u < TPL; ++u) {
             const int t = lane * TPL + u;
@@ -330,13 +332,17 @@ void k_scan_seg(ScanArgs a) {
             }
         }
         float csv[TPL][PPW], snv[TPL][PPW];
+        // angle of each lane token: theta, or dt * omega (zero past the end)
+        float tsc[TPL];
+#pragma unroll
+        for (int u = 0; u < TPL; ++u) tsc[u] = a.theta_ph ? (lane * TPL + u < nv ? p.dtv[u] : 0.f) : 1.f;
 #pragma unroll
         for (int k = 0; k < PPW; ++k) {
             const int i = wave * PPW + k;
             Acc th[TPL], loc = 0;
 #pragma unroll
             for (int u = 0; u < TPL; ++u) {
-                th[u] = (Acc)p.th[u][k / 4][k % 4];   // zero past the end of the sequence
+                th[u] = (Acc)(p.th[u][k / 4][k % 4] * tsc[u]);   // zero past the end of the sequence
                 loc += th[u];
             }
             Acc psi = lane_scan(loc) - loc;

@@ -392,10 +392,12 @@ void k_scan_ws(ScanArgs a) {
             const int64_t tk = tok_of(c);
             const int nv = nvalid_of(c);
             const int nvn = nv + (c * Q + nv < a.L ? 1 : 0);
-            const Rsrc rth = make_rsrc(a.theta + tk * NH, (uint32_t)(((nv - 1) * tstr + 1) * NH * 4));
+            // per-head frequencies: every token reads the head's omega row
+            const Rsrc rth = a.theta_ph ? make_rsrc(a.theta + h * NH, (uint32_t)(NH * 4))
+                                        : make_rsrc(a.theta + tk * NH, (uint32_t)(((nv - 1) * tstr + 1) * NH * 4));
             const Rsrc rdt = make_rsrc(a.dt + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
             const Rsrc rlam = make_rsrc(a.lam + tk, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
-            const uint32_t thstr_b = (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
+            const uint32_t thstr_b = a.theta_ph ? 0u : (uint32_t)(tstr * NH * 4), tstr_b = (uint32_t)(tstr * 4);
             const int t = lane;
             const uint32_t oth = tok_off(t, thstr_b) + sw * PPW * 4;
 #pragma unroll
@@ -425,11 +427,13 @@ void k_scan_ws(ScanArgs a) {
         auto pro_pairs = [&](int64_t c, const Pro &p, auto K0c, auto Kc) {
             constexpr int K0 = decltype(K0c)::value, K = decltype(Kc)::value;
             const int nv = nvalid_of(c), par = (int)(c & 1);
+            // angle of this lane's token: theta, or dt * omega (zero past the end)
+            const float tsc = a.theta_ph ? (lane < nv ? p.dtv : 0.f) : 1.f;
             float csv[K], snv[K];
 #pragma unroll
             for (int k = 0; k < K; ++k) {
                 const int i = sw * PPW + K0 + k;
-                const float psi = lane_scan(p.th[(K0 + k) / 4][(K0 + k) % 4]);   // zero past the end
+                const float psi = lane_scan(p.th[(K0 + k) / 4][(K0 + k) % 4] * tsc);   // zero past the end
                 float sn, cs;
                 sincos_fast(psi, &sn, &cs);
                 csv[k] = cs;

@@ -19,7 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libm3.so")
 M3_OK, M3_ERR_NULL, M3_ERR_SHAPE, M3_ERR_DTYPE = 0, 1, 2, 3
 M3_ERR_UNSUPPORTED, M3_ERR_ALIGN, M3_ERR_WORKSPACE, M3_ERR_HIP = 4, 5, 6, 7
 M3_F32, M3_BF16 = 0, 1
-M3_SCAN_SPLIT, M3_SCAN_PER_CHUNK = 1, 2
+M3_SCAN_SPLIT, M3_SCAN_PER_CHUNK, M3_THETA_PER_HEAD = 1, 2, 4
 _IO = {torch.float32: M3_F32, torch.bfloat16: M3_BF16}
 
 
@@ -103,12 +103,20 @@ def _a_strides(A: torch.Tensor, batch: int, seqlen: int, nheads: int):
     raise ValueError(f"A must be [H] or [B, L, H], got {tuple(A.shape)}")
 
 
+def _theta_per_head(theta: Optional[torch.Tensor], nheads: int, dstate: int) -> bool:
+    """theta given as per-head frequencies omega [H, N/2] (angle = dt * omega)
+    rather than per-token angles."""
+    return theta is not None and theta.dim() == 2 and tuple(theta.shape) == (nheads, dstate // 2)
+
+
 def scan_dims(x: torch.Tensor, Bm: torch.Tensor, chunk: int, A: Optional[torch.Tensor] = None,
-              split: bool = False, per_chunk: bool = False, seg: int = 0) -> M3Dims:
+              split: bool = False, per_chunk: bool = False, seg: int = 0,
+              theta_per_head: bool = False) -> M3Dims:
     batch, seqlen, nheads, rank, headdim = x.shape
     dstate = Bm.shape[-1]
     sb, st, sh = _a_strides(A, batch, seqlen, nheads) if A is not None else (0, 0, 1)
-    flags = (M3_SCAN_SPLIT if split else 0) | (M3_SCAN_PER_CHUNK if per_chunk else 0)
+    flags = ((M3_SCAN_SPLIT if split else 0) | (M3_SCAN_PER_CHUNK if per_chunk else 0)
+             | (M3_THETA_PER_HEAD if theta_per_head else 0))
     return M3Dims(batch, seqlen, nheads, headdim, dstate, rank, int(chunk),
                   _IO[x.dtype], flags, sb, st, sh, int(seg))
 
@@ -122,13 +130,16 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
              stream=None, split: bool = False, per_chunk: bool = False, seg: int = 0,
              z=None) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
     """m3_scan_fwd (m3_scan_fwd_gated when the gate input `z`, shaped like x,
-    is given: y o SiLU(z)): returns y [B,L,H,R,P], final_state [B,H,N,P] fp32
+    is given: y o SiLU(z)); `theta` is [B,L,H,N/2] per-token angles, or
+    [H,N/2] per-head frequencies omega (M3_THETA_PER_HEAD: angle dt * omega).
+    Returns y [B,L,H,R,P], final_state [B,H,N,P] fp32
     and the carry (B_{L-1} [B,H,R,N], X_{L-1} [B,H,R,P]).  `out` may supply
     (y, final_state, carryB, carryX) to write into.  Kernel choice: `split`
     (M3_SCAN_SPLIT, three kernels), `per_chunk` (M3_SCAN_PER_CHUNK, one chunk
     per workgroup), else the segmented kernel with `seg` chunks per
     workgroup (0: library choice)."""
-    d = scan_dims(x, Bm, chunk, A, split, per_chunk, seg)
+    d = scan_dims(x, Bm, chunk, A, split, per_chunk, seg,
+                  _theta_per_head(theta, x.shape[2], Bm.shape[-1]))
     batch, seqlen, nheads, rank, headdim = x.shape
     dstate = Bm.shape[-1]
     dev = x.device
@@ -158,7 +169,8 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
     return y, fs, (cB, cX)
 
 
-def step_dims(x_t: torch.Tensor, B_t: torch.Tensor, A: torch.Tensor) -> M3Dims:
+def step_dims(x_t: torch.Tensor, B_t: torch.Tensor, A: torch.Tensor,
+              theta_per_head: bool = False) -> M3Dims:
     batch, nheads, rank, headdim = x_t.shape
     dstate = B_t.shape[-1]
     if A.dim() == 1 and A.shape[0] == nheads:
@@ -167,14 +179,16 @@ def step_dims(x_t: torch.Tensor, B_t: torch.Tensor, A: torch.Tensor) -> M3Dims:
         sb, sh = A.stride()
     else:
         raise ValueError(f"A must be [H] or [B, H], got {tuple(A.shape)}")
-    return M3Dims(batch, 1, nheads, headdim, dstate, rank, 1, _IO[x_t.dtype], 0, sb, 0, sh, 0)
+    return M3Dims(batch, 1, nheads, headdim, dstate, rank, 1, _IO[x_t.dtype],
+                  M3_THETA_PER_HEAD if theta_per_head else 0, sb, 0, sh, 0)
 
 
 def step(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, y=None, stream=None, z=None):
     """m3_step (m3_step_gated when the gate input `z`, shaped like x_t, is
-    given: y_t o SiLU(z_t)): advances `state` [B,H,N,P] and `carry`
+    given: y_t o SiLU(z_t); `theta_t` [B,H,N/2] angles or [H,N/2] frequencies
+    omega, as in scan_fwd): advances `state` [B,H,N,P] and `carry`
     (B [B,H,R,N], X [B,H,R,P]) in place by one token; returns y_t [B,H,R,P]."""
-    d = step_dims(x_t, B_t, A)
+    d = step_dims(x_t, B_t, A, _theta_per_head(theta_t, x_t.shape[1], B_t.shape[-1]))
     if y is None:
         y = torch.empty_like(x_t)
     cB, cX = carry

@@ -531,3 +531,69 @@ def test_widest_tokens(H, Q, L, mode):
     check_slices(inp, y, fs, cB, cX, sl, TOL["bf16"], label=f"wide H={H} Q={Q} {mode}")
     del inp, y, fs, cB, cX
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# Per-head rotary frequencies (M3_THETA_PER_HEAD): theta given as omega [H, N/2],
+# every angle dt * omega formed in the kernels
+# ---------------------------------------------------------------------------
+
+PH_CASES = [  # io, N, P, R, Q, mode, seg
+    ("f32", 16, 16, 1, 64, "seg", 0), ("f32", 16, 16, 2, 32, "per_chunk", 0),
+    ("f32", 128, 64, 4, 32, "split", 0), ("f32", 128, 64, 4, 32, "seg", 2),
+    ("bf16", 128, 64, 1, 64, "seg", 0), ("bf16", 128, 64, 1, 64, "seg", 1 << 20),
+    ("bf16", 128, 64, 1, 64, "split", 0), ("bf16", 128, 64, 4, 64, "seg", 1 << 20),
+    ("bf16", 128, 64, 4, 64, "seg", 2), ("bf16", 128, 64, 4, 128, "per_chunk", 0),
+    ("bf16", 128, 64, 2, 64, "per_chunk", 0),
+]
+
+
+@pytest.mark.parametrize("io,N,P,R,Q,mode,seg", PH_CASES)
+def test_theta_per_head(io, N, P, R, Q, mode, seg):
+    """Prefill with per-head frequencies on every kernel (several chunks and a
+    ragged tail): against the oracle on the per-token angles theta = dt * omega
+    that the input generator forms in fp32, and against the same kernel fed
+    those angles."""
+    L = 3 * Q + Q // 2 + 3
+    say(f"theta per head io={io} N={N} R={R} Q={Q} L={L} mode={mode} seg={seg}")
+    inp = make_scan_inputs(2, L, 3, P, N, R, io=io, seed=83 + R + Q, device=DEV, chunk=Q)
+    per_tok = inp.theta
+    inp.theta = inp.omega.contiguous()          # [H, N/2]
+    y, fs, cB, cX = run_scan(inp, Q, mode=mode, seg=seg)
+    inp.theta = per_tok
+    check_slices(inp, y, fs, cB, cX, sample_slices(2, 3, 99, 8), TOL[io],
+                 label=f"omega {io}/{R}/{Q}/{mode}")
+    y0, fs0, cB0, cX0 = run_scan(inp, Q, mode=mode, seg=seg)
+    for a, b0 in ((y, y0), (fs, fs0)):
+        d = (a.double() - b0.double()).abs().max().item()
+        assert d <= (1e-6 if io == "f32" else 1e-2) * b0.double().abs().max().item()
+    assert torch.equal(cB, cB0) and torch.equal(cX, cX0)
+
+
+@pytest.mark.parametrize("io,N,P,R", [("f32", 16, 16, 2), ("bf16", 128, 64, 4)])
+def test_theta_per_head_decode(io, N, P, R):
+    """Decode steps with per-head frequencies against the oracle on the
+    per-step angles dt_t * omega."""
+    say(f"theta per head decode io={io} N={N} R={R}")
+    dt = torch.float32 if io == "f32" else torch.bfloat16
+    inp = make_scan_inputs(3, 4, 5, P, N, R, io=io, seed=41, device=DEV)
+    state = torch.randn(3, 5, N, P, device=DEV)
+    cB = torch.randn(3, 5, R, N, device=DEV).to(dt)
+    cX = torch.randn(3, 5, R, P, device=DEV).to(dt)
+    sl = [(b, h) for b in range(3) for h in range(5)]
+    rs = oracle.slices_of_state(state, sl)
+    rb, rx = oracle.slices_of_state(cB, sl), oracle.slices_of_state(cX, sl)
+    A_s = np.array([float(inp.A[h]) for _, h in sl])
+    D_s = np.array([float(inp.D[h]) for _, h in sl])
+    om = inp.omega.to(DEV).contiguous()
+    for s in range(3):
+        st = make_step_inputs(inp, s)
+        y = torch.full_like(st.x, float("nan"))
+        m3.step(state, (cB, cX), st.x, st.Bm, st.Cm, st.dt, inp.A, st.lam, om, inp.D, y=y)
+        torch.cuda.synchronize()
+        p = oracle.slices_of_step(st.x, st.Bm, st.Cm, st.dt, st.lam, st.theta, sl)
+        ry, rs, rb, rx = oracle.step(rs, rb, rx, p["x"], p["B"], p["C"], p["dt"], A_s, p["lam"],
+                                     p["theta"], D_s)
+        for k, (b, h) in enumerate(sl):
+            assert oracle.rel_err(y[b, h].double().cpu().numpy(), ry[k]) <= TOL[io]
+            assert oracle.rel_err(state[b, h].cpu().numpy(), rs[k]) <= TOL[io]

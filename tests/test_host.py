@@ -74,7 +74,7 @@ def test_scan_host_validation(L):
     assert scan_call(L, dims(batch=0)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(seqlen=-1)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(chunk=0)) == m3.M3_ERR_SHAPE
-    assert scan_call(L, dims(flags=4)) == m3.M3_ERR_SHAPE
+    assert scan_call(L, dims(flags=8)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(seg_chunks=-1)) == m3.M3_ERR_SHAPE
     assert scan_call(L, dims(dstate=64, headdim=64)) == m3.M3_ERR_UNSUPPORTED
     assert scan_call(L, dims(chunk=48)) == m3.M3_ERR_UNSUPPORTED
