@@ -181,6 +181,35 @@ m3_status m3_scan_fwd_gated(const m3_dims *dims,
                             void *workspace, size_t workspace_bytes, void *stream);
 
 /*
+ * Varlen prefill: a batch of sequences of different lengths packed along one
+ * token axis.  dims->batch is the number of sequences S, dims->seqlen the
+ * total number of tokens T; cu_seqlens is a HOST array of S + 1 offsets
+ * (cu_seqlens[0] = 0, nondecreasing, cu_seqlens[S] = T): sequence i is tokens
+ * cu_seqlens[i] .. cu_seqlens[i+1] - 1, scanned from its own initial state
+ * and carry (entry i of init_state / init_carry, or zeros) into entry i of
+ * final_state and of the carry outputs.  Token arrays are those of
+ * m3_scan_fwd without the batch axis: x, y and z [T][nheads][rank][headdim],
+ * B and C [T][nheads][rank][dstate], dt and lambda [T][nheads], theta
+ * [T][nheads][dstate/2] (or [nheads][dstate/2] with M3_THETA_PER_HEAD);
+ * A[t * a_stride_t + h * a_stride_h] over the packed tokens (a_stride_b must
+ * be 0).  z may be NULL (no gate) or a gate input as in m3_scan_fwd_gated.
+ * The sequences run one after another on `stream`, each as one m3_scan_fwd
+ * (so each picks its own kernel), sharing the workspace: size it with
+ * m3_scan_workspace_bytes for one sequence of the largest length.  Every
+ * sequence's arguments are checked before the first launch (errors as
+ * m3_scan_fwd; M3_ERR_NULL for a NULL cu_seqlens, M3_ERR_SHAPE for bad
+ * offsets).
+ */
+m3_status m3_scan_fwd_varlen(const m3_dims *dims, const int64_t *cu_seqlens,
+                             const void *x, const void *B, const void *C,
+                             const float *dt, const float *A, const float *lambda,
+                             const float *theta, const float *D, const void *z,
+                             const float *init_state, const void *init_carryB,
+                             const void *init_carryX,
+                             void *y, float *final_state, void *carryB, void *carryX,
+                             void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * One decode step (one iteration of the recurrence) for every (b, h):
  * state <- h_t, carry <- (B_t, X_t) in place, y_t written.  dims->seqlen
  * and dims->chunk are ignored; A is read at t = 0 (a_stride_t unused).

@@ -109,13 +109,15 @@ extern "C" size_t m3_scan_workspace_bytes(const m3_dims *d) {
         .total;
 }
 
-// Both scan entry points; `gated` requires z (a token array like x).
+// Both scan entry points; `gated` requires z (a token array like x).  With
+// `dry_run` only the checks run (nothing is launched).
 static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const void *C,
                           const float *dt, const float *A, const float *lambda,
                           const float *theta, const float *D, bool gated, const void *z,
                           const float *init_state, const void *init_carryB,
                           const void *init_carryX, void *y, float *final_state, void *carryB,
-                          void *carryX, void *workspace, size_t workspace_bytes, void *stream) {
+                          void *carryX, void *workspace, size_t workspace_bytes, void *stream,
+                          bool dry_run = false) {
     ScanImpl impl;
     int64_t nc = 0;
     m3_status s = check_scan_dims(d, &impl, &nc);
@@ -136,6 +138,7 @@ static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const 
                                                          d->headdim, io_bytes_of(d->io),
                                                          impl.acc_bytes, impl.fused);
     if (nc > 0 && (workspace == nullptr || workspace_bytes < wl.total)) return M3_ERR_WORKSPACE;
+    if (dry_run) return M3_OK;
 
     ScanArgs a;
     a.x = x; a.B = B; a.C = C;
@@ -187,6 +190,55 @@ extern "C" m3_status m3_scan_fwd_gated(const m3_dims *d, const void *x, const vo
                                        void *workspace, size_t workspace_bytes, void *stream) {
     return scan_fwd(d, x, B, C, dt, A, lambda, theta, D, true, z, init_state, init_carryB,
                     init_carryX, y, final_state, carryB, carryX, workspace, workspace_bytes, stream);
+}
+
+// Packed sequences of different lengths: sequence i is tokens cu_seqlens[i]
+// .. cu_seqlens[i+1] - 1 of the token axis; each is scanned on its own (one
+// m3_scan_fwd per sequence, in order on `stream`, sharing the workspace).
+// Every sequence's arguments are checked before the first launch.
+extern "C" m3_status m3_scan_fwd_varlen(const m3_dims *d, const int64_t *cu_seqlens,
+                                        const void *x, const void *B, const void *C,
+                                        const float *dt, const float *A, const float *lambda,
+                                        const float *theta, const float *D, const void *z,
+                                        const float *init_state, const void *init_carryB,
+                                        const void *init_carryX, void *y, float *final_state,
+                                        void *carryB, void *carryX, void *workspace,
+                                        size_t workspace_bytes, void *stream) {
+    m3_status s = check_dims_common(d);
+    if (s != M3_OK) return s;
+    if (!cu_seqlens) return M3_ERR_NULL;
+    if (d->seqlen < 0 || d->a_stride_b != 0 || cu_seqlens[0] != 0 || cu_seqlens[d->batch] != d->seqlen)
+        return M3_ERR_SHAPE;
+    for (int64_t i = 0; i < d->batch; ++i)
+        if (cu_seqlens[i + 1] < cu_seqlens[i]) return M3_ERR_SHAPE;
+    const int64_t H = d->nheads, N = d->dstate, P = d->headdim, R = d->rank;
+    const int64_t io = io_bytes_of(d->io);
+    const bool ph = (d->flags & M3_THETA_PER_HEAD) != 0;
+    auto off = [](const void *p, int64_t bytes) -> const void * {
+        return p ? static_cast<const char *>(p) + bytes : nullptr;
+    };
+    for (int pass = 0; pass < 2; ++pass) {   // 0: every sequence checked, 1: launched
+        for (int64_t i = 0; i < d->batch; ++i) {
+            const int64_t t0 = cu_seqlens[i], len = cu_seqlens[i + 1] - t0;
+            m3_dims di = *d;
+            di.batch = 1;
+            di.seqlen = len;
+            const int64_t tx = t0 * H * R * P * io, tb = t0 * H * R * N * io, ts = t0 * H * 4;
+            s = scan_fwd(&di, off(x, tx), off(B, tb), off(C, tb), static_cast<const float *>(off(dt, ts)),
+                         A ? A + t0 * d->a_stride_t : nullptr, static_cast<const float *>(off(lambda, ts)),
+                         ph ? theta : static_cast<const float *>(off(theta, t0 * H * (N / 2) * 4)), D,
+                         z != nullptr, off(z, tx),
+                         static_cast<const float *>(off(init_state, i * H * N * P * 4)),
+                         off(init_carryB, i * H * R * N * io), off(init_carryX, i * H * R * P * io),
+                         const_cast<void *>(off(y, tx)),
+                         static_cast<float *>(const_cast<void *>(off(final_state, i * H * N * P * 4))),
+                         const_cast<void *>(off(carryB, i * H * R * N * io)),
+                         const_cast<void *>(off(carryX, i * H * R * P * io)), workspace, workspace_bytes,
+                         stream, pass == 0);
+            if (s != M3_OK) return s;
+        }
+    }
+    return M3_OK;
 }
 
 static m3_status step(const m3_dims *d, float *state, void *carryB, void *carryX,

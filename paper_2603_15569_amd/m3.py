@@ -39,8 +39,8 @@ class M3Error(RuntimeError):
         self.status = status
 
 
-EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_step",
-           "m3_step_gated", "m3_status_string", "m3_last_hip_error")
+EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_scan_fwd_varlen",
+           "m3_step", "m3_step_gated", "m3_status_string", "m3_last_hip_error")
 _lib = None
 
 
@@ -59,6 +59,9 @@ def lib() -> ctypes.CDLL:
         L.m3_scan_fwd.restype = ctypes.c_int
         L.m3_scan_fwd_gated.argtypes = [dims_p] + [vp] * 16 + [vp, ctypes.c_size_t, vp]
         L.m3_scan_fwd_gated.restype = ctypes.c_int
+        L.m3_scan_fwd_varlen.argtypes = ([dims_p, ctypes.POINTER(ctypes.c_int64)] + [vp] * 16
+                                         + [vp, ctypes.c_size_t, vp])
+        L.m3_scan_fwd_varlen.restype = ctypes.c_int
         L.m3_step.argtypes = [dims_p] + [vp] * 12 + [vp]
         L.m3_step.restype = ctypes.c_int
         L.m3_step_gated.argtypes = [dims_p] + [vp] * 13 + [vp]
@@ -166,6 +169,46 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
                                        _p(lam), _p(theta), _p(D), _p(z), _p(init_state), _p(icB),
                                        _p(icX), _p(y), _p(fs), _p(cB), _p(cX), _p(workspace), wsb,
                                        _stream(stream)))
+    return y, fs, (cB, cX)
+
+
+def scan_fwd_varlen(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, cu_seqlens,
+                    init_state=None, init_carry=None, z=None, workspace=None, stream=None,
+                    split: bool = False, per_chunk: bool = False, seg: int = 0):
+    """m3_scan_fwd_varlen: sequences packed along the token axis, x [T,H,R,P],
+    Bm/Cm [T,H,R,N], dt/lam [T,H], theta [T,H,N/2] (or [H,N/2] frequencies),
+    A [H] or [T,H]; `cu_seqlens` (S + 1 offsets, host list or tensor).  Returns
+    y [T,H,R,P], final_state [S,H,N,P] and the carry ([S,H,R,N], [S,H,R,P])."""
+    cu = [int(v) for v in (cu_seqlens.tolist() if hasattr(cu_seqlens, "tolist") else cu_seqlens)]
+    T, nheads, rank, headdim = x.shape
+    dstate = Bm.shape[-1]
+    S = len(cu) - 1
+    if A.dim() == 1 and A.shape[0] == nheads:
+        sb, st, sh = 0, 0, 1
+    elif A.dim() == 2 and tuple(A.shape) == (T, nheads):
+        sb, (st, sh) = 0, A.stride()
+    else:
+        raise ValueError(f"A must be [H] or [T, H], got {tuple(A.shape)}")
+    flags = ((M3_SCAN_SPLIT if split else 0) | (M3_SCAN_PER_CHUNK if per_chunk else 0)
+             | (M3_THETA_PER_HEAD if _theta_per_head(theta, nheads, dstate) else 0))
+    d = M3Dims(S, T, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags, sb, st, sh,
+               int(seg))
+    dev = x.device
+    y = torch.empty_like(x)
+    fs = torch.empty((S, nheads, dstate, headdim), dtype=torch.float32, device=dev)
+    cB = torch.empty((S, nheads, rank, dstate), dtype=x.dtype, device=dev)
+    cX = torch.empty((S, nheads, rank, headdim), dtype=x.dtype, device=dev)
+    if workspace is None:
+        longest = max([cu[i + 1] - cu[i] for i in range(S)] + [0])
+        d1 = M3Dims(1, longest, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags,
+                    0, st, sh, int(seg))
+        workspace = torch.empty(max(workspace_bytes(d1), 16), dtype=torch.uint8, device=dev)
+    icB, icX = (None, None) if init_carry is None else init_carry
+    cu_arr = (ctypes.c_int64 * len(cu))(*cu)
+    _check(lib().m3_scan_fwd_varlen(ctypes.byref(d), cu_arr, _p(x), _p(Bm), _p(Cm), _p(dt), _p(A),
+                                    _p(lam), _p(theta), _p(D), _p(z), _p(init_state), _p(icB),
+                                    _p(icX), _p(y), _p(fs), _p(cB), _p(cX), _p(workspace),
+                                    workspace.numel(), _stream(stream)))
     return y, fs, (cB, cX)
 
 

@@ -597,3 +597,68 @@ def test_theta_per_head_decode(io, N, P, R):
         for k, (b, h) in enumerate(sl):
             assert oracle.rel_err(y[b, h].double().cpu().numpy(), ry[k]) <= TOL[io]
             assert oracle.rel_err(state[b, h].cpu().numpy(), rs[k]) <= TOL[io]
+
+
+# ---------------------------------------------------------------------------
+# Varlen: sequences of different lengths packed along one token axis
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("io,N,P,R,Q,gated,per_head", [
+    ("f32", 16, 16, 1, 64, False, False), ("bf16", 128, 64, 1, 64, False, False),
+    ("bf16", 128, 64, 4, 64, True, False), ("bf16", 128, 64, 4, 128, False, True),
+])
+def test_varlen(io, N, P, R, Q, gated, per_head):
+    """Packed sequences (lengths 70, 1, 0, 2Q + 9 and Q; the second with an
+    initial state and carry) against the oracle per sequence, and against
+    separate m3_scan_fwd calls on each sequence (the same launches: equal bit
+    for bit)."""
+    lens = [70, 1, 0, 2 * Q + 9, Q]
+    cu = [0]
+    for n in lens:
+        cu.append(cu[-1] + n)
+    T, H = cu[-1], 3
+    say(f"varlen io={io} R={R} Q={Q} lens={lens} gated={gated} per_head={per_head}")
+    inp = make_scan_inputs(1, T, H, P, N, R, io=io, seed=97 + R + Q, device=DEV, chunk=Q)
+    flat = lambda t: t[0].contiguous()
+    x, Bm, Cm, dt, lam, theta = (flat(inp.x), flat(inp.Bm), flat(inp.Cm), flat(inp.dt),
+                                 flat(inp.lam), flat(inp.theta))
+    th_in = inp.omega.contiguous() if per_head else theta
+    z = make_gate_input(x, 3) if gated else None
+    S = len(lens)
+    iodt = x.dtype
+    init = torch.randn(S, H, N, P, device=DEV)
+    icB = torch.randn(S, H, R, N, device=DEV).to(iodt)
+    icX = torch.randn(S, H, R, P, device=DEV).to(iodt)
+    y, fs, (cB, cX) = m3.scan_fwd_varlen(x, Bm, Cm, dt, inp.A, lam, th_in, inp.D, Q, cu,
+                                         init_state=init, init_carry=(icB, icX), z=z)
+    torch.cuda.synchronize()
+    for i in range(S):
+        t0, t1 = cu[i], cu[i + 1]
+        sl = [(0, h) for h in range(H)]
+        if t1 > t0:
+            ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                        inp.D, sl, t0, t1)
+        else:
+            ref = dict(x=np.zeros((H, 0, R, P)), B=np.zeros((H, 0, R, N)), C=np.zeros((H, 0, R, N)),
+                       dt=np.zeros((H, 0)), A=np.zeros((H, 0)), lam=np.zeros((H, 0)),
+                       theta=np.zeros((H, 0, N // 2)), D=oracle._np(inp.D))
+        ry, rs, rb, rx = oracle.scan(**ref, init_state=oracle._np(init[i]), init_B=oracle._np(icB[i]),
+                                     init_X=oracle._np(icX[i]))
+        for h in range(H):
+            gy = y[t0:t1, h].double().cpu().numpy()
+            ref_y = ry[h] if z is None else oracle.gate(ry[h], oracle._np(z[t0:t1, h]))
+            if t1 > t0:
+                assert oracle.rel_err(gy, ref_y) <= TOL[io], f"seq {i} head {h} y"
+            assert oracle.rel_err(fs[i, h].cpu().numpy(), rs[h]) <= TOL[io], f"seq {i} head {h} state"
+            assert np.array_equal(oracle._np(cB[i, h]), rb[h]) and np.array_equal(oracle._np(cX[i, h]), rx[h])
+        # the same sequence on its own
+        if t1 > t0:
+            one = lambda t: t[None, t0:t1].contiguous()
+            y1, fs1, (cB1, cX1) = m3.scan_fwd(one(x), one(Bm), one(Cm), one(dt), inp.A, one(lam),
+                                              th_in if per_head else one(theta), inp.D, chunk=Q,
+                                              init_state=init[i:i + 1].contiguous(),
+                                              init_carry=(icB[i:i + 1].contiguous(), icX[i:i + 1].contiguous()),
+                                              z=None if z is None else one(z))
+            torch.cuda.synchronize()
+            assert torch.equal(y1[0], y[t0:t1]) and torch.equal(fs1[0], fs[i])
+            assert torch.equal(cB1[0], cB[i]) and torch.equal(cX1[0], cX[i])

@@ -182,3 +182,28 @@ def test_gated_host_validation(L):
     assert step(dims(), {12: None}) == m3.M3_ERR_NULL
     assert step(dims(io=5)) == m3.M3_ERR_DTYPE
     assert L.m3_last_hip_error() == 0
+
+
+def test_varlen_host_validation(L):
+    """m3_scan_fwd_varlen: the offsets are checked on the host, and every
+    sequence's arguments before the first launch."""
+    def call(d, cu, over=None):
+        ptrs = [FAKE] * 16       # x B C dt A lam theta D z init icB icX y fs cB cX
+        for k in (8, 9, 10, 11):
+            ptrs[k] = None
+        for k, v in (over or {}).items():
+            ptrs[k] = v
+        arr = None if cu is None else (ctypes.c_int64 * len(cu))(*cu)
+        return L.m3_scan_fwd_varlen(ctypes.byref(d), arr, *ptrs, FAKE, 1 << 30, None)
+    d = dims(batch=3, seqlen=100)
+    assert call(d, None) == m3.M3_ERR_NULL
+    assert call(d, [1, 10, 50, 100]) == m3.M3_ERR_SHAPE           # must start at 0
+    assert call(d, [0, 60, 50, 100]) == m3.M3_ERR_SHAPE           # decreasing
+    assert call(d, [0, 10, 50, 99]) == m3.M3_ERR_SHAPE            # must end at seqlen
+    assert call(dims(batch=3, seqlen=100, a_stride_b=5), [0, 10, 50, 100]) == m3.M3_ERR_SHAPE
+    # the third sequence's misaligned token offset (fp32, P = 16: 64 B a token)
+    # is fine; a misaligned base is caught before any launch
+    assert call(d, [0, 10, 50, 100], {0: FAKE + 4}) == m3.M3_ERR_ALIGN
+    assert call(d, [0, 10, 50, 100], {12: None}) == m3.M3_ERR_NULL   # y
+    assert call(dims(batch=3, seqlen=100, chunk=48), [0, 10, 50, 100]) == m3.M3_ERR_UNSUPPORTED
+    assert L.m3_last_hip_error() == 0
