@@ -195,7 +195,11 @@ m3_status m3_scan_fwd_gated(const m3_dims *dims,
  * be 0).  z may be NULL (no gate) or a gate input as in m3_scan_fwd_gated.
  * The sequences run one after another on `stream`, each as one m3_scan_fwd
  * (so each picks its own kernel), sharing the workspace: size it with
- * m3_scan_workspace_bytes for one sequence of the largest length.  Every
+ * m3_scan_workspace_bytes for one sequence of the largest length.  A run of
+ * consecutive sequences of equal length goes out as one m3_scan_fwd over a
+ * batch of them (they lie in the packed arrays as that batch would) as far
+ * as the workspace holds what the batch needs (m3_scan_workspace_bytes with
+ * batch = the run's length, a_stride_b = length * a_stride_t).  Every
  * sequence's arguments are checked before the first launch (errors as
  * m3_scan_fwd; M3_ERR_NULL for a NULL cu_seqlens, M3_ERR_SHAPE for bad
  * offsets).

@@ -217,12 +217,29 @@ extern "C" m3_status m3_scan_fwd_varlen(const m3_dims *d, const int64_t *cu_seql
     auto off = [](const void *p, int64_t bytes) -> const void * {
         return p ? static_cast<const char *>(p) + bytes : nullptr;
     };
-    for (int pass = 0; pass < 2; ++pass) {   // 0: every sequence checked, 1: launched
-        for (int64_t i = 0; i < d->batch; ++i) {
+    // Consecutive sequences of equal length lie in the packed arrays exactly
+    // as a batch of them would: such runs go out as one launch, as long as
+    // the workspace holds what that batch needs.
+    auto run_end = [&](int64_t i) -> int64_t {
+        const int64_t len = cu_seqlens[i + 1] - cu_seqlens[i];
+        int64_t j = i + 1;
+        for (; j < d->batch && cu_seqlens[j + 1] - cu_seqlens[j] == len; ++j) {
+            m3_dims dj = *d;
+            dj.batch = j - i + 1;
+            dj.seqlen = len;
+            dj.a_stride_b = len * d->a_stride_t;
+            if (m3_scan_workspace_bytes(&dj) > workspace_bytes) break;
+        }
+        return j;
+    };
+    for (int pass = 0; pass < 2; ++pass) {   // 0: every call checked, 1: launched
+        for (int64_t i = 0, j = 0; i < d->batch; i = j) {
+            j = run_end(i);
             const int64_t t0 = cu_seqlens[i], len = cu_seqlens[i + 1] - t0;
             m3_dims di = *d;
-            di.batch = 1;
+            di.batch = j - i;
             di.seqlen = len;
+            di.a_stride_b = len * d->a_stride_t;
             const int64_t tx = t0 * H * R * P * io, tb = t0 * H * R * N * io, ts = t0 * H * 4;
             s = scan_fwd(&di, off(x, tx), off(B, tb), off(C, tb), static_cast<const float *>(off(dt, ts)),
                          A ? A + t0 * d->a_stride_t : nullptr, static_cast<const float *>(off(lambda, ts)),

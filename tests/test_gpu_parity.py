@@ -662,3 +662,38 @@ def test_varlen(io, N, P, R, Q, gated, per_head):
             torch.cuda.synchronize()
             assert torch.equal(y1[0], y[t0:t1]) and torch.equal(fs1[0], fs[i])
             assert torch.equal(cB1[0], cB[i]) and torch.equal(cX1[0], cX[i])
+
+
+def test_varlen_equal_length_runs():
+    """Runs of consecutive equal-length sequences (3 x 64, 2 x 10, 2 x 0, 33)
+    with a workspace large enough to batch each run: every sequence against
+    the oracle, from its own initial state."""
+    io, N, P, R, Q, H = "bf16", 128, 64, 4, 64, 3
+    lens = [64, 64, 64, 10, 10, 0, 0, 33]
+    cu = [0]
+    for n in lens:
+        cu.append(cu[-1] + n)
+    T, S = cu[-1], len(lens)
+    say(f"varlen runs lens={lens}")
+    inp = make_scan_inputs(1, T, H, P, N, R, io=io, seed=131, device=DEV, chunk=Q)
+    flat = lambda t: t[0].contiguous()
+    init = torch.randn(S, H, N, P, device=DEV)
+    ws = torch.zeros(m3.workspace_bytes(m3.M3Dims(S, 64, H, P, N, R, Q, 1, 0, 0, 0, 1, 0)),
+                     dtype=torch.uint8, device=DEV)
+    y, fs, (cB, cX) = m3.scan_fwd_varlen(flat(inp.x), flat(inp.Bm), flat(inp.Cm), flat(inp.dt),
+                                         inp.A, flat(inp.lam), flat(inp.theta), inp.D, Q, cu,
+                                         init_state=init, workspace=ws)
+    torch.cuda.synchronize()
+    for i in range(S):
+        t0, t1 = cu[i], cu[i + 1]
+        sl = [(0, h) for h in range(H)]
+        if t1 == t0:
+            assert torch.equal(fs[i], init[i]) and not cB[i].abs().any() and not cX[i].abs().any()
+            continue
+        ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                    inp.D, sl, t0, t1)
+        ry, rs, rb, rx = oracle.scan(**ref, init_state=oracle._np(init[i]))
+        for h in range(H):
+            assert oracle.rel_err(y[t0:t1, h].double().cpu().numpy(), ry[h]) <= TOL[io], f"seq {i} y"
+            assert oracle.rel_err(fs[i, h].cpu().numpy(), rs[h]) <= TOL[io], f"seq {i} state"
+            assert np.array_equal(oracle._np(cB[i, h]), rb[h]) and np.array_equal(oracle._np(cX[i, h]), rx[h])
