@@ -188,6 +188,25 @@ __device__ __forceinline__ typename Vec16<T>::type gate_piece(typename Vec16<T>:
     return y;
 }
 
+// One step of the state recurrence on a lane's owned pair (re, im) of state
+// rows: S <- e^{cum} R(psi) S + A (de = e^{cum}, (cs, sn) of psi), every
+// rounding explicit (no contraction), so that a look-back folding a
+// predecessor's published map and the map's owner compute the same bits.
+__device__ __forceinline__ void state_step(float &re, float &im, float de, float cs, float sn,
+                                           float are, float aim) {
+    const float r = __fmul_rn(de, __fsub_rn(__fmul_rn(cs, re), __fmul_rn(sn, im)));
+    const float i = __fmul_rn(de, __fadd_rn(__fmul_rn(sn, re), __fmul_rn(cs, im)));
+    re = __fadd_rn(r, are);
+    im = __fadd_rn(i, aim);
+}
+__device__ __forceinline__ void state_step(float &re, float &im, double de, double cs, double sn,
+                                           float are, float aim) {
+    const double r = __dmul_rn(de, __dsub_rn(__dmul_rn(cs, (double)re), __dmul_rn(sn, (double)im)));
+    const double i = __dmul_rn(de, __dadd_rn(__dmul_rn(sn, (double)re), __dmul_rn(cs, (double)im)));
+    re = __fadd_rn((float)r, are);
+    im = __fadd_rn((float)i, aim);
+}
+
 __device__ __forceinline__ void wait_stores_done() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
 __device__ __forceinline__ void st_coh2(unsigned long long *p, float x, float y) {

@@ -71,7 +71,6 @@ void k_scan_seg(ScanArgs a) {
     constexpr int NSP = S::NW / S::NWO;  // waves sharing a row tile (column split)
     constexpr int PTS = PT / NSP;       // 16-column tiles of y per wave
     static_assert(NSP * S::NWO == S::NW && PTS * NSP == PT, "column split");
-    constexpr int kMaps = 2;            // look-back maps loaded per round trip
 
     // chunk-parity double buffers: the tail of a chunk (state rotation by
     // psi_e, the aggregate's cum_e) may still read them while faster waves
@@ -520,43 +519,22 @@ void k_scan_seg(ScanArgs a) {
             if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagAgg, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
 
+        // Entering state of the segment: the nearest preceding segment whose
+        // inclusive state is published (or the sequence start) is found first,
+        // waiting on any segment in between that has published nothing yet;
+        // the aggregates after it are then folded forward, S <- T_k S + A_k,
+        // with the arithmetic their owners use for their own inclusive states
+        // (state_step): the result does not depend on timing.
+        const int ntl_w = wave % 4;   // all owned pair rows of a lane are 16 ntl_w + 4g + v
         if (sg == 0) {
             load_init(Sst);
         } else {
-            // Decoupled look-back over the preceding segments: compose their
-            // maps S -> T_j S + A_j (nearest first) until an inclusive state.
-            // All owned pair rows of a lane are 16*ntl + 4g + v (ntl = wave % 4),
-            // so the accumulated rotation needs one angle per v.
-            Acc ad = 1;
-            Acc aps[4];
-            float aA[PTW][2][4];
-#pragma unroll
-            for (int v = 0; v < 4; ++v) aps[v] = 0;
-#pragma unroll
-            for (int m2 = 0; m2 < PTW; ++m2)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) aA[m2][0][v] = aA[m2][1][v] = 0.f;
-            auto finish = [&](const float (&X)[PTW][2][4]) {
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    Acc sn, cs;
-                    sincos_fast(aps[v], &sn, &cs);
-                    sn *= ad;
-                    cs *= ad;
-#pragma unroll
-                    for (int m2 = 0; m2 < PTW; ++m2) {
-                        const Acc re = X[m2][0][v], im = X[m2][1][v];
-                        Sst[m2][0][v] = (float)(cs * re - sn * im) + aA[m2][0][v];
-                        Sst[m2][1][v] = (float)(sn * re + cs * im) + aA[m2][1][v];
-                    }
-                }
-            };
-            const int ntl_w = wave % 4;
-            int64_t j = sg - 1;
             const int64_t sbase = sl * a.nseg;
-            while (true) {
-                // probe predecessors j, j-1, ..., j-15 at once (lanes of wave 0)
-                if (wave == 0) {
+            int64_t j = sg - 1;       // next predecessor to probe
+            int64_t jt = -2;          // terminal: -1 sequence start, >= 0 inclusive state
+            bool timed_out = false;
+            while (jt == -2) {
+                if (wave == 0) {   // probe predecessors j, j-1, ..., j-15 at once
                     uint32_t f = 0;
                     if (lane < kProbe) {
                         const int64_t jj = j - lane;
@@ -568,85 +546,19 @@ void k_scan_seg(ScanArgs a) {
                     const uint64_t mzero = __ballot(lane < kProbe && f == 0u);
                     const int ft = mterm ? __ffsll((unsigned long long)mterm) - 1 : kProbe;
                     const int fz = mzero ? __ffsll((unsigned long long)mzero) - 1 : kProbe;
-                    const uint32_t fterm = __shfl(f, ft < kProbe ? ft : 0, kWave);
                     if (lane == 0) {
-                        s_i[1] = (fz < ft) ? fz : ft;                        // aggregates to compose
-                        s_i[2] = (fz < ft || ft == kProbe) ? 0 : (int)fterm;  // terminal kind
-                        s_i[3] = (fz < ft) ? 1 : 0;                          // must wait on a segment
+                        s_i[1] = (fz < ft) ? fz : ft;                  // predecessors passed
+                        s_i[2] = (ft < fz && ft < kProbe) ? 1 : 0;     // terminal found
+                        s_i[3] = (fz < ft) ? 1 : 0;                    // must wait on one
                     }
                 }
                 __syncthreads();
-                const int ncomp = s_i[1], term = s_i[2], needwait = s_i[3];
+                const int adv = s_i[1], found = s_i[2], needwait = s_i[3];
                 __syncthreads();
-                // compose the ready aggregates, loading kMaps maps per round trip
-                for (int k = 0; k < ncomp; k += kMaps) {
-                    const int nk = (ncomp - k) < kMaps ? (ncomp - k) : kMaps;
-                    float d[kMaps][PTW][2][4];
-                    Acc cps[kMaps][4], ccm[kMaps];
-#pragma unroll
-                    for (int u = 0; u < kMaps; ++u) {
-                        if (u < nk) {
-                            const int64_t js = sbase + j - k - u;
-                            const unsigned long long *src =
-                                reinterpret_cast<const unsigned long long *>(a.agg + js * SZ);
-                            const Acc *tp = totp + js * (NH + 1);
-                            ccm[u] = ld_coh(tp);
-#pragma unroll
-                            for (int v = 0; v < 4; ++v) cps[u][v] = ld_coh(tp + 1 + ntl_w * 16 + 4 * g + v);
-#pragma unroll
-                            for (int m2 = 0; m2 < PTW; ++m2)
-#pragma unroll
-                                for (int half = 0; half < 2; ++half)
-#pragma unroll
-                                    for (int vp = 0; vp < 2; ++vp)
-                                        ld_coh2(src + word_index(m2, half, vp), d[u][m2][half][2 * vp],
-                                                d[u][m2][half][2 * vp + 1]);
-                        }
-                    }
-#pragma unroll
-                    for (int u = 0; u < kMaps; ++u) {
-                        if (u < nk) {
-#pragma unroll
-                            for (int v = 0; v < 4; ++v) {
-                                Acc sn, cs;
-                                sincos_fast(aps[v], &sn, &cs);
-                                sn *= ad;
-                                cs *= ad;
-#pragma unroll
-                                for (int m2 = 0; m2 < PTW; ++m2) {
-                                    const Acc re = d[u][m2][0][v], im = d[u][m2][1][v];
-                                    aA[m2][0][v] += (float)(cs * re - sn * im);
-                                    aA[m2][1][v] += (float)(sn * re + cs * im);
-                                }
-                                aps[v] += cps[u][v];
-                                if constexpr (sizeof(Acc) == 4) aps[v] = reduce_angle(aps[v]);
-                            }
-                            ad *= exp_fast(ccm[u]);
-                        }
-                    }
-                }
-                j -= ncomp;
-                if (term == (int)kFlagInc) {
-                    const unsigned long long *src =
-                        reinterpret_cast<const unsigned long long *>(a.inc + (sbase + j) * SZ);
-                    float X[PTW][2][4];
-#pragma unroll
-                    for (int m2 = 0; m2 < PTW; ++m2)
-#pragma unroll
-                        for (int half = 0; half < 2; ++half)
-#pragma unroll
-                            for (int vp = 0; vp < 2; ++vp)
-                                ld_coh2(src + word_index(m2, half, vp), X[m2][half][2 * vp], X[m2][half][2 * vp + 1]);
-                    finish(X);
-                    break;
-                }
-                if (term == (int)kFlagInit) {
-                    float X[PTW][2][4];
-                    load_init(X);
-                    finish(X);
-                    break;
-                }
-                if (needwait) {   // the nearest unfinished predecessor is j: wait for it
+                if (found) {
+                    jt = (j - adv < 0) ? -1 : j - adv;
+                } else if (needwait) {   // segment j - adv has published nothing: wait for it
+                    j -= adv;
                     if (tid == 0) {
                         uint32_t f = 0u;
                         for (uint32_t spin = 0; spin < kSpinMax; ++spin) {
@@ -658,31 +570,99 @@ void k_scan_seg(ScanArgs a) {
                         s_i[1] = (f == 0u) ? 1 : 0;
                     }
                     __syncthreads();
-                    const int timed_out = s_i[1];
+                    timed_out = s_i[1] != 0;
                     __syncthreads();
-                    if (timed_out) {
-                        float X[PTW][2][4] = {};
-                        finish(X);
-                        break;
-                    }
+                    if (timed_out) jt = sg - 1;   // (error path: the entering state is left zero)
+                } else {
+                    j -= kProbe;                 // sixteen aggregates: probe further back
+                }
+            }
+            if (timed_out) {
+#pragma unroll
+                for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) Sst[m2][0][v] = Sst[m2][1][v] = 0.f;
+            } else if (jt < 0) {
+                load_init(Sst);
+            } else {
+                const unsigned long long *src = reinterpret_cast<const unsigned long long *>(a.inc + (sbase + jt) * SZ);
+#pragma unroll
+                for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                    for (int half = 0; half < 2; ++half)
+#pragma unroll
+                        for (int vp = 0; vp < 2; ++vp)
+                            ld_coh2(src + word_index(m2, half, vp), Sst[m2][half][2 * vp], Sst[m2][half][2 * vp + 1]);
+            }
+            // Fold forward from the terminal, one aggregate a round trip; each round
+            // also probes the nearest predecessors, and an inclusive state published
+            // meanwhile replaces the rest of the fold (it is that fold: same bits).
+            for (int64_t k = jt; k < sg - 1;) {
+                if (wave == 0) {
+                    const int64_t jj = sg - 1 - lane;
+                    uint32_t f = 0;
+                    if (lane < kProbe && jj > k + 1)
+                        f = __hip_atomic_load(a.flags + sbase + jj, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    const uint64_t minc = __ballot(f == kFlagInc);
+                    if (lane == 0) s_i[1] = minc ? __ffsll((unsigned long long)minc) - 1 : -1;
+                }
+                const int64_t kn = k + 1;
+                const unsigned long long *src = reinterpret_cast<const unsigned long long *>(a.agg + (sbase + kn) * SZ);
+                const Acc *tp = totp + (sbase + kn) * (NH + 1);
+                float d[PTW][2][4];
+                Acc ps[4];
+                const Acc cm = ld_coh(tp);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) ps[v] = ld_coh(tp + 1 + ntl_w * 16 + 4 * g + v);
+#pragma unroll
+                for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                    for (int half = 0; half < 2; ++half)
+#pragma unroll
+                        for (int vp = 0; vp < 2; ++vp)
+                            ld_coh2(src + word_index(m2, half, vp), d[m2][half][2 * vp], d[m2][half][2 * vp + 1]);
+                __syncthreads();
+                const int near = s_i[1];
+                __syncthreads();
+                if (near >= 0) {   // inclusive state of predecessor sg - 1 - near: continue from it
+                    k = sg - 1 - near;
+                    const unsigned long long *isrc = reinterpret_cast<const unsigned long long *>(a.inc + (sbase + k) * SZ);
+#pragma unroll
+                    for (int m2 = 0; m2 < PTW; ++m2)
+#pragma unroll
+                        for (int half = 0; half < 2; ++half)
+#pragma unroll
+                            for (int vp = 0; vp < 2; ++vp)
+                                ld_coh2(isrc + word_index(m2, half, vp), Sst[m2][half][2 * vp], Sst[m2][half][2 * vp + 1]);
+                    continue;
+                }
+                k = kn;
+                const Acc de = exp_fast(cm);
+#pragma unroll
+                for (int v = 0; v < 4; ++v) {
+                    Acc sn, cs;
+                    sincos_fast(ps[v], &sn, &cs);
+#pragma unroll
+                    for (int m2 = 0; m2 < PTW; ++m2)
+                        state_step(Sst[m2][0][v], Sst[m2][1][v], de, cs, sn, d[m2][0][v], d[m2][1][v]);
                 }
             }
         }
 
-        // outgoing state of the segment: e^{seg_lg} R(segps) S + A
+        // outgoing state of the segment: e^{seg_lg} R(segps) S + A (the same
+        // step a successor's fold takes)
         {
             float Sout[PTW][2][4];
             const Acc de = exp_fast(seg_lg);
 #pragma unroll
-            for (int m2 = 0; m2 < PTW; ++m2) {
-                const int ntl = (wave + NW * m2) % 4;
+            for (int v = 0; v < 4; ++v) {
+                Acc sn, cs;
+                sincos_fast(s_segps[ntl_w * 16 + 4 * g + v], &sn, &cs);
 #pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    Acc sn, cs;
-                    sincos_fast(s_segps[ntl * 16 + 4 * g + v], &sn, &cs);
-                    const Acc re = Sst[m2][0][v], im = Sst[m2][1][v];
-                    Sout[m2][0][v] = (float)(de * (cs * re - sn * im)) + Aseg[m2][0][v];
-                    Sout[m2][1][v] = (float)(de * (sn * re + cs * im)) + Aseg[m2][1][v];
+                for (int m2 = 0; m2 < PTW; ++m2) {
+                    Sout[m2][0][v] = Sst[m2][0][v];
+                    Sout[m2][1][v] = Sst[m2][1][v];
+                    state_step(Sout[m2][0][v], Sout[m2][1][v], de, cs, sn, Aseg[m2][0][v], Aseg[m2][1][v]);
                 }
             }
             if (!last_seg) {

@@ -697,3 +697,23 @@ def test_varlen_equal_length_runs():
             assert oracle.rel_err(y[t0:t1, h].double().cpu().numpy(), ry[h]) <= TOL[io], f"seq {i} y"
             assert oracle.rel_err(fs[i, h].cpu().numpy(), rs[h]) <= TOL[io], f"seq {i} state"
             assert np.array_equal(oracle._np(cB[i, h]), rb[h]) and np.array_equal(oracle._np(cX[i, h]), rx[h])
+
+
+@pytest.mark.parametrize("mode,seg,R,Q", [("per_chunk", 0, 1, 64), ("per_chunk", 0, 4, 128),
+                                          ("seg", 2, 4, 64), ("seg", 4, 1, 64)])
+def test_determinism_many_items(mode, seg, R, Q):
+    """Thousands of look-back items, three runs with other work in between:
+    bitwise-identical outputs.  The entering state of a chunk (segment) is the
+    forward fold from the sequence start whichever predecessors happened to
+    be done when it looked back."""
+    say(f"determinism many items mode={mode} seg={seg} R={R} Q={Q}")
+    L = 2048 if R == 1 else 1024
+    inp = make_scan_inputs(4, L, 16, 64, 128, R, io="bf16", seed=9 + R, device=DEV, chunk=Q)
+    runs = []
+    for k in range(3):
+        runs.append(run_scan(inp, Q, mode=mode, seg=seg, nan_fill=False))
+        if k == 1:   # shift the timing of the next run
+            torch.randn(1 << 24, device=DEV).sum().item()
+    for other in runs[1:]:
+        for u, v in zip(runs[0], other):
+            assert torch.equal(u, v)
