@@ -49,7 +49,10 @@
  * on `stream` (a hipStream_t; NULL is the default stream).  Every argument
  * error is detected on the host before any launch and leaves all outputs
  * untouched; a failed launch returns M3_ERR_HIP.  No call prints, throws or
- * aborts.  Results are deterministic (no floating-point atomics).  Calls on
+ * aborts.  Results are deterministic: no floating-point atomics, and the
+ * single-pass kernels' look-back forms each entering state by the same fold
+ * from the sequence start whatever the timing (bit-equal across runs, given
+ * the same device and kernel choice).  Calls on
  * disjoint buffers may run concurrently; the library has no mutable global
  * state besides a once-initialised cache of device properties.
  */
