@@ -24,11 +24,13 @@
 //   3. aggregate first: per 64-row block, B^ and W x staged row-major in LDS
 //      and M += B^T W x (MFMA, K = rows, operands read with transposing LDS
 //      reads); A_c published (flag AGG);
-//   4. decoupled look-back: predecessors' flags probed 16 at a time, their
-//      maps composed nearest first until an inclusive state (flag INC) or the
-//      sequence start; S_out published (flag INC) before any output work, so
-//      the chain across chunks advances at the speed of the look-back alone;
-//      the last chunk writes the final state and the carry;
+//   4. decoupled look-back: predecessors' flags probed 16 at a time back to
+//      the nearest inclusive state (flag INC) or the sequence start, then the
+//      aggregates after it folded forward with the step the owners use for
+//      their own S_out (the entering state does not depend on timing); S_out
+//      published (flag INC) before any output work, so the chain across
+//      chunks advances at the speed of the look-back alone; the last chunk
+//      writes the final state and the carry;
 //   5. outputs: C^ rows rotated straight into MFMA fragments; y starts as
 //      e^{cum_t} C^ S_in (MFMA, K = N); per block at or below each owned tile
 //      G^T = B^ C^T (MFMA, K = N) masked by w_tj, y += (w o G) x (MFMA,
