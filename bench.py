@@ -1,14 +1,19 @@
 """Benchmark of the Mamba-3 SSM hot path on one MI355X.
 
 One timed step = one pass of the whole hot path:
-  * one m3_scan_fwd over the SISO bf16 prefill batch (B=4, L=2048, H=16,
-    P=64, N=128, R=1, chunk 64), inputs rotated over 4 resident copies so the
-    256 MB Infinity Cache cannot hold them between steps;
+  * one m3_scan_fwd over the long-context MIMO prefill (B=1, L=65536, H=32,
+    P=64, N=128, R=4, chunk 128, bf16 inputs, fp32 state): the largest
+    prefill that fits one GPU, where the chunked algorithm's intensity
+    (~275 FLOP per algorithmic byte) makes bf16 MFMA the roof;
   * one m3_step over the decode batch (B=256, H=32, P=64, N=128, R=4, fp32
     state from a 1024-token prefill), each step with fresh seeded inputs.
-`value` is the prefill tokens/s; `decode_us_per_step` the decode step time.
-Both come from HIP events recorded on the stream the kernels run on.  The
-CPU oracle is timed on a bounded sample of the same workloads on the host.
+`value` is the prefill's tokens/s; `decode_us_per_step` the decode step time.
+Both come from HIP events recorded on the stream the kernels run on; inputs
+are resident in HBM before timing starts.  After the timed loop the other
+prefill workloads are timed on their own (rank-4 B=8 L=4096 chunk 64, the
+SISO B=4 L=2048 chunk 64 with its gated and per-head-frequency variants,
+and the decode state's B=256 L=1024 prefill).  The CPU oracle is timed on
+the host over whole workloads (decode: a sample of slices, scaled).
 
 Usage: python bench.py [--steps K] [--warmup W] [--gpus 1] [--no-cpu]
 """
@@ -26,12 +31,18 @@ sys.path.insert(0, ROOT)
 METRIC = "prefill scan tokens/s + decode step µs @B=256; % of MFMA/HBM roofline"
 
 
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=200)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="only the timed loop (the long-context prefill and the decode step)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 10 plain device copies of 1 GiB (reference for HBM byte counters)")
     ap.add_argument("--scan-workload", type=int, default=None, metavar="K",
@@ -40,8 +51,9 @@ def main():
                          "print their mean time, for hardware-counter runs")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); every (batch, head) "
-              "slice is independent, so more GPUs would only split the batch.", file=sys.stderr)
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}): this build uses a "
+              "single GPU; every (batch, head) slice is independent, so more GPUs would only "
+              "split the batch.", file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
@@ -69,75 +81,59 @@ def main():
         if k not in (1, 2, 3, 4):
             print("--scan-workload takes 1, 2, 3 or 4", file=sys.stderr)
             sys.exit(2)
-        w = WORKLOADS[k]
         inp = workload_inputs(k, device=dev)
+        ms = time_scan(m3, torch, stream, [inp], WORKLOADS[k]["chunk"], 1, args.steps)
         Bk, Lk, Hk, Rk, Pk = inp.x.shape
         Nk = inp.Bm.shape[-1]
-        dims = m3.scan_dims(inp.x, inp.Bm, w["chunk"], inp.A)
-        ws = torch.zeros(m3.workspace_bytes(dims), dtype=torch.uint8, device=dev)
-        args_k = (inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta, inp.D)
-        m3.scan_fwd(*args_k, chunk=w["chunk"], workspace=ws)
-        torch.cuda.synchronize()
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record(stream)
-        for _ in range(args.steps):
-            m3.scan_fwd(*args_k, chunk=w["chunk"], workspace=ws)
-        e1.record(stream)
-        torch.cuda.synchronize()
-        ms = e0.elapsed_time(e1) / max(1, args.steps)
-        fl = Bk * Hk * roofline.chunked_flops(Lk, Nk, Pk, Rk, w["chunk"])
-        print(json.dumps({"scan_workload": k, "shape": [Bk, Lk, Hk, Rk, Pk, Nk], "chunk": w["chunk"],
-                          "calls": args.steps, "ms_per_call": round(ms, 5),
-                          "alg_tflops": round(fl / ms / 1e9, 2)}), flush=True)
+        fl = Bk * Hk * roofline.chunked_flops(Lk, Nk, Pk, Rk, WORKLOADS[k]["chunk"])
+        print(json.dumps({"scan_workload": k, "shape": [Bk, Lk, Hk, Rk, Pk, Nk],
+                          "chunk": WORKLOADS[k]["chunk"], "calls": args.steps,
+                          "ms_per_call": round(ms, 5), "alg_tflops": round(fl / ms / 1e9, 2)}),
+              flush=True)
         return
 
-    # ---------------- prefill workload (SISO bf16) ----------------
-    wp = WORKLOADS[1]
-    base = workload_inputs(1, device=dev)
-    copies = [base] + [type(base)(**{k: (v.clone() if isinstance(v, torch.Tensor) else v)
-                                     for k, v in base.__dict__.items()}) for _ in range(3)]
-    Bp, Lp, Hp, Rp, Pp = base.x.shape
-    Np = base.Bm.shape[-1]
-    Qp = wp["chunk"]
-    dims = m3.scan_dims(base.x, base.Bm, Qp, base.A)
-    ws = torch.empty(max(m3.workspace_bytes(dims), 1), dtype=torch.uint8, device=dev)
-    out = (torch.empty_like(base.x), torch.empty(Bp, Hp, Np, Pp, device=dev),
-           torch.empty(Bp, Hp, Rp, Np, device=dev, dtype=base.x.dtype),
-           torch.empty(Bp, Hp, Rp, Pp, device=dev, dtype=base.x.dtype))
+    peak_gbs = roofline.HBM_BYTES_PER_S / 1e9
+    peak_tfs = roofline.MFMA_BF16_FLOPS / 1e12
 
-    def scan(i):
-        c = copies[i % len(copies)]
-        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.theta, c.D, chunk=Qp, out=out,
-                    workspace=ws)
+    # ---------------- headline prefill: long-context MIMO (workload 3) ----------------
+    log("inputs: long-context prefill")
+    w3 = WORKLOADS[3]
+    Q3 = w3["chunk"]
+    p3 = workload_inputs(3, device=dev)
+    B3, L3, H3, R3, P3 = p3.x.shape
+    N3 = p3.Bm.shape[-1]
+    ws3 = torch.empty(max(m3.workspace_bytes(m3.scan_dims(p3.x, p3.Bm, Q3, p3.A)), 16),
+                      dtype=torch.uint8, device=dev)
+    out3 = (torch.empty_like(p3.x), torch.empty(B3, H3, N3, P3, device=dev),
+            torch.empty(B3, H3, R3, N3, device=dev, dtype=p3.x.dtype),
+            torch.empty(B3, H3, R3, P3, device=dev, dtype=p3.x.dtype))
+
+    def scan3(i):
+        m3.scan_fwd(p3.x, p3.Bm, p3.Cm, p3.dt, p3.A, p3.lam, p3.theta, p3.D, chunk=Q3, out=out3,
+                    workspace=ws3)
 
     # ---------------- decode workload (B=256, MIMO R=4) ----------------
+    log("inputs: decode state prefill")
     wd = WORKLOADS[4]
     layer = workload_inputs(4, device=dev)
     pre_args = (layer.x, layer.Bm, layer.Cm, layer.dt, layer.A, layer.lam, layer.theta, layer.D)
     _, dstate, (dcB, dcX) = m3.scan_fwd(*pre_args, chunk=wd["chunk"])
-    # The same MIMO prefill (rank 4, 8192 slices), timed: a few more calls
-    # writing the same state (the decode steps start from it).
-    mimo_out = (torch.empty_like(layer.x), dstate, dcB, dcX)
-    mimo_ws = torch.empty(max(m3.workspace_bytes(m3.scan_dims(layer.x, layer.Bm, wd["chunk"], layer.A)), 1),
-                          dtype=torch.uint8, device=dev)
-    n_mimo = 3
-    mimo_ev = [torch.cuda.Event(enable_timing=True) for _ in range(n_mimo + 1)]
     torch.cuda.synchronize()
-    mimo_ev[0].record(stream)
-    for i in range(n_mimo):
-        m3.scan_fwd(*pre_args, chunk=wd["chunk"], out=mimo_out, workspace=mimo_ws)
-        mimo_ev[i + 1].record(stream)
-    torch.cuda.synchronize()
-    mimo_ms = float(np.mean([mimo_ev[i].elapsed_time(mimo_ev[i + 1]) for i in range(n_mimo)]))
     Bm_, Lm_, Hm_, Rm_, Pm_ = layer.x.shape
     Nm_ = layer.Bm.shape[-1]
-    del mimo_out, mimo_ws, pre_args
+    mimo_ms = None
+    if not args.no_extras:
+        # the same decode-state prefill (rank 4, 8192 slices), timed over a few
+        # more calls writing the same state (the decode steps start from it)
+        mimo_out = (torch.empty_like(layer.x), dstate, dcB, dcX)
+        mimo_ms = time_scan(m3, torch, stream, [layer], wd["chunk"], 1, 3, out=mimo_out)
+        del mimo_out
+    del pre_args
     del layer.x, layer.Bm, layer.Cm, layer.theta, layer.lam, layer.dt  # free the prefill inputs
     torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     n_step_inputs = max(1, min(args.steps + args.warmup, wd["steps"]))
-    step_in = []
-    for s in range(n_step_inputs):
-        step_in.append(make_step_inputs(_LayerView(layer, wd), s, device=dev))
+    step_in = [make_step_inputs(_LayerView(layer, wd), s, device=dev) for s in range(n_step_inputs)]
     yd = torch.empty_like(step_in[0].x)
 
     def dstep(i):
@@ -146,8 +142,9 @@ def main():
                 y=yd)
 
     # ---------------- timed loop ----------------
+    log(f"timed loop: {args.warmup} warm-up + {args.steps} steps")
     for i in range(args.warmup):
-        scan(i)
+        scan3(i)
         dstep(i)
     torch.cuda.synchronize()
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
@@ -155,7 +152,7 @@ def main():
     t_wall = time.perf_counter()
     for i in range(args.steps):
         ev[i][0].record(stream)
-        scan(i)
+        scan3(i)
         ev[i][1].record(stream)
         dstep(args.warmup + i)
         ev[i][2].record(stream)
@@ -164,28 +161,183 @@ def main():
     scan_ms = np.array([e[0].elapsed_time(e[1]) for e in ev])
     step_ms = np.array([e[1].elapsed_time(e[2]) for e in ev])
     tot_ms = np.array([e[0].elapsed_time(e[2]) for e in ev])
+    assert m3.scan_check(m3.scan_dims(p3.x, p3.Bm, Q3, p3.A), ws3) == 0, "look-back wait timed out"
 
-    # ---------------- output gate y o SiLU(z) (after the timed loop) ----------------
+    tokens3 = B3 * L3
+    pre_ms = float(scan_ms.mean())
+    pre_bytes = roofline.prefill_bytes(B3, L3, H3, N3, P3, R3, 2)
+    pre_flops = B3 * H3 * roofline.chunked_flops(L3, N3, P3, R3, Q3)
+    pre_tfs = pre_flops / (pre_ms * 1e-3) / 1e12
+    pre_gbs = pre_bytes / (pre_ms * 1e-3) / 1e9
+    Bd, Hd, Rd, Pd = step_in[0].x.shape
+    Nd = step_in[0].Bm.shape[-1]
+    dec_us = float(step_ms.mean()) * 1e3
+    dec_bytes = Bd * Hd * roofline.decode_bytes_per_slice(Nd, Pd, Rd, 2)
+    dec_gbs = dec_bytes / (dec_us * 1e-6) / 1e9
+
+    result = {
+        "metric": METRIC,
+        "value": round(tokens3 / (pre_ms * 1e-3), 1),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(float(tot_ms.mean()), 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": (f"long-context MIMO prefill B={B3} L={L3} H={H3} P={P3} N={N3} R={R3} "
+                         f"chunk={Q3} bf16 in, fp32 state + decode step B={Bd} H={Hd} P={Pd} "
+                         f"N={Nd} R={Rd} fp32 state"),
+            "prefill": {"batch": B3, "seqlen": L3, "nheads": H3, "headdim": P3, "dstate": N3,
+                        "rank": R3, "chunk": Q3, "io": "bf16", "state": "fp32"},
+            "decode": {"batch": Bd, "nheads": Hd, "headdim": Pd, "dstate": Nd, "rank": Rd,
+                       "io": "bf16", "state": "fp32"},
+        },
+        "prefill_ms": round(pre_ms, 5),
+        "prefill_ms_p10_p90": [round(float(np.percentile(scan_ms, 10)), 5),
+                               round(float(np.percentile(scan_ms, 90)), 5)],
+        "decode_us_per_step": round(dec_us, 3),
+        "decode_us_p10_p90": [round(float(np.percentile(step_ms, 10)) * 1e3, 3),
+                              round(float(np.percentile(step_ms, 90)) * 1e3, 3)],
+        # the dominant kernel of the step: the long-context scan (one
+        # m3_scan_fwd = the per-chunk kernel, after its reset launch)
+        "roofline": {
+            "kernel": "m3_scan_fwd long-context MIMO prefill (k_scan_fused<bf16,128,4>)",
+            "bound": "mfma", "achieved": round(pre_tfs, 2), "peak": peak_tfs, "unit": "TFLOP/s",
+            "frac": round(pre_tfs / peak_tfs, 4),
+            "traffic": measured_traffic("k_scan_fused_long"),
+            "flops_per_launch": pre_flops,
+            "hbm_achieved_gbs": round(pre_gbs, 1), "hbm_frac": round(pre_gbs / peak_gbs, 4),
+            "bytes_per_launch": pre_bytes,
+        },
+        "roofline_decode": {
+            "kernel": "k_step (m3_step, one launch per step)",
+            "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": peak_gbs, "unit": "GB/s",
+            "frac": round(dec_gbs / peak_gbs, 4), "traffic": measured_traffic("k_step"),
+            "bytes_per_launch": dec_bytes,
+        },
+        "wall_s_timed_loop": round(wall, 3),
+    }
+    if mimo_ms is not None:
+        result["prefill_decode_state"] = prefill_figures(
+            roofline, Bm_, Lm_, Hm_, Nm_, Pm_, Rm_, wd["chunk"], mimo_ms,
+            "warp-specialised kernel, one workgroup per slice", measured_traffic("k_scan_ws_mimo"))
+
+    if not args.no_extras:
+        del ev
+        # ---------------- rank-4 prefill (workload 2) ----------------
+        log("extras: rank-4 prefill")
+        w2 = WORKLOADS[2]
+        p2 = workload_inputs(2, device=dev)
+        ms2 = time_scan(m3, torch, stream, [p2], w2["chunk"], 3, 20)
+        B2, L2, H2, R2, P2 = p2.x.shape
+        result["prefill_mimo"] = prefill_figures(
+            roofline, B2, L2, H2, p2.Bm.shape[-1], P2, R2, w2["chunk"], ms2,
+            "warp-specialised kernel, one workgroup per slice", None)
+        del p2
+        torch.cuda.empty_cache()
+        # ---------------- SISO prefill (workload 1), gated and per-head variants ----------------
+        log("extras: SISO prefill")
+        result.update(siso_figures(m3, roofline, torch, np, stream, dev, WORKLOADS[1],
+                                   workload_inputs, make_gate_input, step_in, dstep, dstate,
+                                   dcB, dcX, layer, yd, peak_gbs))
+
+    if not args.no_cpu:
+        log("CPU baseline")
+        result["cpu_baseline"] = cpu_baseline(p3, layer, step_in, WORKLOADS)
+    print(json.dumps(result), flush=True)
+    torch.cuda.synchronize()
+
+
+def time_scan(m3, torch, stream, copies, chunk, warm, n, out=None, z=None, theta_per_head=False):
+    """Mean ms of n m3_scan_fwd calls (after `warm` untimed ones), rotating
+    over the input copies, one workspace."""
+    c0 = copies[0]
+    ws = torch.empty(max(m3.workspace_bytes(m3.scan_dims(c0.x, c0.Bm, chunk, c0.A)), 16),
+                     dtype=torch.uint8, device=c0.x.device)
+    if out is None:
+        Bb, Lb, Hb, Rb, Pb = c0.x.shape
+        Nb = c0.Bm.shape[-1]
+        out = (torch.empty_like(c0.x), torch.empty(Bb, Hb, Nb, Pb, device=c0.x.device),
+               torch.empty(Bb, Hb, Rb, Nb, device=c0.x.device, dtype=c0.x.dtype),
+               torch.empty(Bb, Hb, Rb, Pb, device=c0.x.device, dtype=c0.x.dtype))
+
+    def call(i):
+        c = copies[i % len(copies)]
+        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.omega if theta_per_head else c.theta,
+                    c.D, chunk=chunk, out=out, workspace=ws,
+                    z=None if z is None else z[i % len(z)])
+
+    for i in range(warm):
+        call(i)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(n):
+        call(warm + i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    return e0.elapsed_time(e1) / max(1, n)
+
+
+def prefill_figures(roofline, B, L, H, N, P, R, Q, ms, kernel, traffic):
+    """Tokens/s and the algorithmic HBM and bf16 MFMA rates of one prefill."""
+    nbytes = roofline.prefill_bytes(B, L, H, N, P, R, 2)
+    flops = B * H * roofline.chunked_flops(L, N, P, R, Q)
+    gbs = nbytes / (ms * 1e-3) / 1e9
+    tfs = flops / (ms * 1e-3) / 1e12
+    return {
+        "workload": f"prefill B={B} L={L} H={H} P={P} N={N} R={R} chunk={Q} bf16",
+        "kernel": kernel, "ms": round(ms, 4), "tokens_per_s": round(B * L / (ms * 1e-3), 1),
+        "hbm_achieved_gbs": round(gbs, 1), "hbm_frac": round(gbs * 1e9 / roofline.HBM_BYTES_PER_S, 4),
+        "bytes_per_launch": nbytes, "traffic": traffic,
+        "mfma_tflops": round(tfs, 2), "mfma_frac": round(tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
+        "flops_per_launch": flops,
+    }
+
+
+def siso_figures(m3, roofline, torch, np, stream, dev, wp, workload_inputs, make_gate_input,
+                 step_in, dstep, dstate, dcB, dcX, layer, yd, peak_gbs):
+    """The SISO bf16 prefill (B=4 L=2048 H=16, chunk 64; inputs rotated over
+    four resident copies, 550 MB, so the 256 MB Infinity Cache cannot hold
+    them), alternating with decode steps as in the timed loop; its fused
+    output gate against the ungated scan and against the ungated scan
+    followed by a separate torch gate pass; and the scan with per-head rotary
+    frequencies (angles dt * omega formed in the kernels)."""
+    base = workload_inputs(1, device=dev)
+    copies = [base] + [type(base)(**{k: (v.clone() if isinstance(v, torch.Tensor) else v)
+                                     for k, v in base.__dict__.items()}) for _ in range(3)]
+    Bp, Lp, Hp, Rp, Pp = base.x.shape
+    Np = base.Bm.shape[-1]
+    Qp = wp["chunk"]
+    ws = torch.empty(max(m3.workspace_bytes(m3.scan_dims(base.x, base.Bm, Qp, base.A)), 16),
+                     dtype=torch.uint8, device=dev)
+    out = (torch.empty_like(base.x), torch.empty(Bp, Hp, Np, Pp, device=dev),
+           torch.empty(Bp, Hp, Rp, Np, device=dev, dtype=base.x.dtype),
+           torch.empty(Bp, Hp, Rp, Pp, device=dev, dtype=base.x.dtype))
     zs = [make_gate_input(c.x, i) for i, c in enumerate(copies)]
     zd = [make_gate_input(st.x, 100 + i) for i, st in enumerate(step_in[:4])]
+    n_in = len(step_in)
 
-    def gscan(i):
+    def scan(i, gated=False, per_head=False):
         c = copies[i % len(copies)]
-        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.theta, c.D, chunk=Qp, out=out,
-                    workspace=ws, z=zs[i % len(zs)])
+        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.omega if per_head else c.theta, c.D,
+                    chunk=Qp, out=out, workspace=ws, z=zs[i % len(zs)] if gated else None)
 
     def unfused(i):   # ungated scan, then the gate as a separate elementwise pass
         scan(i)
         out[0].mul_(torch.nn.functional.silu(zs[i % len(zs)]))
 
     def gstep(i):
-        st = step_in[i % n_step_inputs]
+        st = step_in[i % n_in]
         m3.step(dstate, (dcB, dcX), st.x, st.Bm, st.Cm, st.dt, layer.A, st.lam, st.theta, layer.D,
                 y=yd, z=zd[i % len(zd)])
 
-    def timed(pre, dec, n):
-        # the timed loop's pattern (a prefill, then a decode step), so that
-        # the figures compare with its ungated ones call for call
+    def timed(pre, dec, n=100):
         for i in range(3):
             pre(i)
             dec(i)
@@ -201,135 +353,39 @@ def main():
         return (float(np.mean([x[0].elapsed_time(x[1]) for x in e])),
                 float(np.mean([x[1].elapsed_time(x[2]) for x in e])))
 
-    def pscan(i):   # per-head frequencies omega [H, N/2]: the kernels form dt * omega
-        c = copies[i % len(copies)]
-        m3.scan_fwd(c.x, c.Bm, c.Cm, c.dt, c.A, c.lam, c.omega, c.D, chunk=Qp, out=out,
-                    workspace=ws)
-
-    n_gate = max(10, min(args.steps, 100))
-    g_scan_ms, g_step_ms = timed(gscan, gstep, n_gate)
-    g_unfused_ms, _ = timed(unfused, dstep, n_gate)
-    p_scan_ms, _ = timed(pscan, dstep, n_gate)
-
+    s_ms, d_ms = timed(scan, dstep)
+    g_ms, gd_ms = timed(lambda i: scan(i, gated=True), gstep)
+    u_ms, _ = timed(unfused, dstep)
+    ph_ms, _ = timed(lambda i: scan(i, per_head=True), dstep)
     tokens = Bp * Lp
-    prefill_tok_s = tokens / (scan_ms.mean() * 1e-3)
-    dec_us = step_ms.mean() * 1e3
-
-    # rooflines (algorithmic bytes / FLOPs per launch, see roofline.py)
+    pre_bytes = roofline.prefill_bytes(Bp, Lp, Hp, Np, Pp, Rp, 2)
+    z_bytes = Bp * Lp * Hp * Rp * Pp * 2
     Bd, Hd, Rd, Pd = step_in[0].x.shape
     Nd = step_in[0].Bm.shape[-1]
     dec_bytes = Bd * Hd * roofline.decode_bytes_per_slice(Nd, Pd, Rd, 2)
-    dec_gbs = dec_bytes / (step_ms.mean() * 1e-3) / 1e9
-    pre_bytes = roofline.prefill_bytes(Bp, Lp, Hp, Np, Pp, Rp, 2)
-    pre_flops = Bp * Hp * roofline.chunked_flops(Lp, Np, Pp, Rp, Qp)
-    pre_gbs = pre_bytes / (scan_ms.mean() * 1e-3) / 1e9
-    pre_tfs = pre_flops / (scan_ms.mean() * 1e-3) / 1e12
-    peak_gbs = roofline.HBM_BYTES_PER_S / 1e9
-
-    result = {
-        "metric": METRIC,
-        "value": round(prefill_tok_s, 1),
-        "unit": "tokens/s",
-        "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": round(float(tot_ms.mean()), 5),
-        "higher_is_better": True,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": "bf16",
-        "data": "synthetic",
-        "config": {
-            "workload": (f"prefill B={Bp} L={Lp} H={Hp} P={Pp} N={Np} R={Rp} chunk={Qp} bf16 "
-                         f"+ decode step B={Bd} H={Hd} P={Pd} N={Nd} R={Rd} fp32 state"),
-            "prefill": {"batch": Bp, "seqlen": Lp, "nheads": Hp, "headdim": Pp, "dstate": Np,
-                        "rank": Rp, "chunk": Qp, "io": "bf16"},
-            "decode": {"batch": Bd, "nheads": Hd, "headdim": Pd, "dstate": Nd, "rank": Rd,
-                       "io": "bf16", "state": "fp32"},
-        },
-        "prefill_ms": round(float(scan_ms.mean()), 5),
-        "prefill_ms_p10_p90": [round(float(np.percentile(scan_ms, 10)), 5),
-                               round(float(np.percentile(scan_ms, 90)), 5)],
-        "decode_us_per_step": round(dec_us, 3),
-        "decode_us_p10_p90": [round(float(np.percentile(step_ms, 10)) * 1e3, 3),
-                              round(float(np.percentile(step_ms, 90)) * 1e3, 3)],
-        "roofline": {
-            "kernel": "k_step (m3_step, one launch per step)",
-            "bound": "hbm", "achieved": round(dec_gbs, 1), "peak": peak_gbs, "unit": "GB/s",
-            "frac": round(dec_gbs / peak_gbs, 4), "traffic": measured_traffic("k_step"),
-            "bytes_per_launch": dec_bytes,
-        },
-        "roofline_prefill": {
-            "kernel": "m3_scan_fwd (all launches of one scan)",
-            "bound": "hbm", "achieved": round(pre_gbs, 1), "peak": peak_gbs, "unit": "GB/s",
-            "frac": round(pre_gbs / peak_gbs, 4), "traffic": measured_traffic("k_scan_fused_siso"),
-            "bytes_per_launch": pre_bytes,
-            "mfma_tflops": round(pre_tfs, 2),
-            "mfma_frac": round(pre_tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
-        },
-        "gate": gate_figures(g_scan_ms, g_unfused_ms, g_step_ms, float(scan_ms.mean()),
-                             float(step_ms.mean()), tokens, pre_bytes,
-                             Bp * Lp * Hp * Rp * Pp * 2, dec_bytes, Bd * Hd * Rd * Pd * 2, peak_gbs),
-        "theta_per_head": per_head_figures(p_scan_ms, float(scan_ms.mean()), tokens,
-                                           pre_bytes - Bp * Lp * Hp * (Np // 2) * 4 + Hp * (Np // 2) * 4,
-                                           peak_gbs),
-        "roofline_prefill_mimo": mimo_roofline(Bm_, Lm_, Hm_, Nm_, Pm_, Rm_, wd["chunk"], mimo_ms,
-                                               roofline, peak_gbs),
-        "wall_s_timed_loop": round(wall, 3),
-    }
-    if not args.no_cpu:
-        result["cpu_baseline"] = cpu_baseline(base, layer, step_in, wp, wd)
-    print(json.dumps(result), flush=True)
-
-
-def gate_figures(scan_ms, unfused_ms, step_ms, base_scan_ms, base_step_ms, tokens, pre_bytes,
-                 z_bytes, dec_bytes, zd_bytes, peak_gbs):
-    """The fused output gate y o SiLU(z) on the same two workloads, timed in
-    the timed loop's pattern: the gated prefill (algorithmic bytes plus z)
-    against the ungated one and against the ungated one followed by the gate
-    as a separate elementwise pass (torch), the gated decode step against the
-    ungated one (the ungated figures are the timed loop's)."""
-    pre_gbs = (pre_bytes + z_bytes) / (scan_ms * 1e-3) / 1e9
-    dec_gbs = (dec_bytes + zd_bytes) / (step_ms * 1e-3) / 1e9
+    zd_bytes = Bd * Hd * Rd * Pd * 2
+    ph_bytes = pre_bytes - Bp * Lp * Hp * (Np // 2) * 4 + Hp * (Np // 2) * 4
+    siso = prefill_figures(roofline, Bp, Lp, Hp, Np, Pp, Rp, Qp, s_ms,
+                           "one chunk per workgroup, look-back", measured_traffic("k_scan_fused_siso"))
     return {
-        "prefill_ms": round(scan_ms, 5), "prefill_tokens_per_s": round(tokens / (scan_ms * 1e-3), 1),
-        "prefill_bound": "hbm", "prefill_achieved_gbs": round(pre_gbs, 1),
-        "prefill_frac": round(pre_gbs / peak_gbs, 4), "prefill_bytes_per_launch": pre_bytes + z_bytes,
-        "ungated_prefill_ms": round(base_scan_ms, 5), "unfused_prefill_ms": round(unfused_ms, 5),
-        "decode_us_per_step": round(step_ms * 1e3, 3),
-        "ungated_decode_us_per_step": round(base_step_ms * 1e3, 3), "decode_bound": "hbm",
-        "decode_achieved_gbs": round(dec_gbs, 1), "decode_frac": round(dec_gbs / peak_gbs, 4),
-        "decode_bytes_per_launch": dec_bytes + zd_bytes,
-    }
-
-
-def per_head_figures(ms, theta_ms, tokens, nbytes, peak_gbs):
-    """The SISO prefill with per-head rotary frequencies omega (angles dt *
-    omega formed in the kernels, M3_THETA_PER_HEAD) in the timed loop's
-    pattern, against the timed loop's per-token-angle prefill; bytes without
-    the per-token angle array."""
-    gbs = nbytes / (ms * 1e-3) / 1e9
-    return {"prefill_ms": round(ms, 5), "prefill_tokens_per_s": round(tokens / (ms * 1e-3), 1),
-            "per_token_theta_prefill_ms": round(theta_ms, 5), "bound": "hbm",
-            "achieved_gbs": round(gbs, 1), "frac": round(gbs / peak_gbs, 4),
-            "bytes_per_launch": nbytes}
-
-
-def mimo_roofline(B, L, H, N, P, R, Q, ms, roofline, peak_gbs):
-    """HBM and MFMA rates of the rank-4 prefill that builds the decode state
-    (mean over a few calls; not part of the timed step)."""
-    nbytes = roofline.prefill_bytes(B, L, H, N, P, R, 2)
-    flops = B * H * roofline.chunked_flops(L, N, P, R, Q)
-    gbs = nbytes / (ms * 1e-3) / 1e9
-    tfs = flops / (ms * 1e-3) / 1e12
-    return {
-        "kernel": "m3_scan_fwd (warp-specialised kernel, one workgroup per slice)",
-        "workload": f"prefill B={B} L={L} H={H} P={P} N={N} R={R} chunk={Q} bf16",
-        "ms": round(ms, 4), "tokens_per_s": round(B * L / (ms * 1e-3), 1),
-        "bound": "hbm", "achieved": round(gbs, 1), "peak": peak_gbs, "unit": "GB/s",
-        "frac": round(gbs / peak_gbs, 4), "traffic": measured_traffic("k_scan_ws_mimo"),
-        "bytes_per_launch": nbytes,
-        "mfma_tflops": round(tfs, 2), "mfma_frac": round(tfs * 1e12 / roofline.MFMA_BF16_FLOPS, 4),
+        "prefill_siso": siso,
+        "gate": {
+            "prefill_ms": round(g_ms, 5), "prefill_tokens_per_s": round(tokens / (g_ms * 1e-3), 1),
+            "prefill_achieved_gbs": round((pre_bytes + z_bytes) / (g_ms * 1e-3) / 1e9, 1),
+            "prefill_bytes_per_launch": pre_bytes + z_bytes,
+            "ungated_prefill_ms": round(s_ms, 5), "unfused_prefill_ms": round(u_ms, 5),
+            "decode_us_per_step": round(gd_ms * 1e3, 3),
+            "ungated_decode_us_per_step": round(d_ms * 1e3, 3),
+            "decode_achieved_gbs": round((dec_bytes + zd_bytes) / (gd_ms * 1e-3) / 1e9, 1),
+            "decode_frac": round((dec_bytes + zd_bytes) / (gd_ms * 1e-3) / 1e9 / peak_gbs, 4),
+            "decode_bytes_per_launch": dec_bytes + zd_bytes,
+        },
+        "theta_per_head": {
+            "prefill_ms": round(ph_ms, 5), "prefill_tokens_per_s": round(tokens / (ph_ms * 1e-3), 1),
+            "per_token_theta_prefill_ms": round(s_ms, 5),
+            "achieved_gbs": round(ph_bytes / (ph_ms * 1e-3) / 1e9, 1),
+            "frac": round(ph_bytes / (ph_ms * 1e-3) / 1e9 / peak_gbs, 4), "bytes_per_launch": ph_bytes,
+        },
     }
 
 
@@ -361,20 +417,54 @@ class _LayerView:
         self.omega = layer.omega
 
 
-def cpu_baseline(base, layer, step_in, wp, wd):
-    """The fp64 oracle on the host: all 64 slices of the whole prefill batch
-    (tokens/s), and one decode step on 64 of the 8192 slices (scaled to the
-    whole batch)."""
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(p3, layer, step_in, W):
+    """The fp64 oracle (-O3 -march=native, built here for this host) on the
+    host cores: every slice of the long-context prefill (the headline; in
+    two halves of 16 slices to bound host memory), every slice of the rank-4
+    and of the SISO prefill batches, and one decode step on 64 of the 8192
+    slices scaled to the batch."""
     import numpy as np
+    import torch
     import oracle
-    sl = [(b, h) for b in range(wp["batch"]) for h in range(wp["nheads"])]
-    Ls = wp["seqlen"]
-    ref = oracle.slices_of_scan(base.x, base.Bm, base.Cm, base.dt, base.A, base.lam, base.theta,
-                                base.D, sl, 0, Ls)
-    t0 = time.perf_counter()
-    _, used = oracle.scan(**ref, return_threads=True)
-    dt = time.perf_counter() - t0
-    tok_s = wp["batch"] * Ls / dt
+    from paper_2603_15569_amd.inputs import workload_inputs
+    flags = oracle.use_native()
+
+    def run(inp, slices, L):
+        ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                    inp.D, slices, 0, L)
+        t0 = time.perf_counter()
+        _, used = oracle.scan(**ref, return_threads=True)
+        return time.perf_counter() - t0, used
+
+    w3 = W[3]
+    t3, used = 0.0, 1
+    all3 = [(b, h) for b in range(w3["batch"]) for h in range(w3["nheads"])]
+    for half in (all3[:len(all3) // 2], all3[len(all3) // 2:]):
+        dt_, used = run(p3, half, w3["seqlen"])
+        t3 += dt_
+    out = {"value": round(w3["batch"] * w3["seqlen"] / t3, 1), "unit": "tokens/s",
+           "cores": int(used), "kind": "oracle"}
+    detail = {"long_context_s": round(t3, 2)}
+    for k, key in ((2, "mimo"), (1, "siso")):
+        w = W[k]
+        inp = workload_inputs(k, device=p3.x.device)
+        dt_, _ = run(inp, [(b, h) for b in range(w["batch"]) for h in range(w["nheads"])], w["seqlen"])
+        detail[f"{key}_s"] = round(dt_, 2)
+        detail[f"{key}_tokens_per_s"] = round(w["batch"] * w["seqlen"] / dt_, 1)
+        del inp
+    wd = W[4]
     dsl = [(b, h) for b in range(0, wd["batch"], 4) for h in range(0, wd["nheads"], 8)][:64]
     st = step_in[0]
     p = oracle.slices_of_step(st.x, st.Bm, st.Cm, st.dt, st.lam, st.theta, dsl)
@@ -390,12 +480,17 @@ def cpu_baseline(base, layer, step_in, wp, wd):
     for _ in range(reps):
         oracle.step(state, cb, cx, p["x"], p["B"], p["C"], p["dt"], A_s, p["lam"], p["theta"], D_s)
     ddt = (time.perf_counter() - t0) / reps
-    dec_us = ddt * (wd["batch"] * wd["nheads"] / S) * 1e6
-    return {"value": round(tok_s, 1), "unit": "tokens/s", "cores": int(used), "kind": "oracle",
-            "sample": (f"prefill: all {len(sl)} (batch, head) slices of the SISO bf16 batch, "
-                       f"first {Ls} of {wp['seqlen']} tokens, fp64, {dt:.2f} s; decode: one step "
-                       f"on {S} of {wd['batch'] * wd['nheads']} slices x {reps} reps, scaled"),
-            "decode_us_per_step": round(dec_us, 1)}
+    detail["decode_us_per_step"] = round(ddt * (wd["batch"] * wd["nheads"] / S) * 1e6, 1)
+    out["sample"] = (f"prefill: all {len(all3)} (batch, head) slices x {w3['seqlen']} tokens of the "
+                     f"long-context batch in two halves, fp64, {t3:.1f} s (also every slice of the "
+                     f"rank-4 and SISO batches, below); decode: one step on {S} of "
+                     f"{wd['batch'] * wd['nheads']} slices x {reps} reps, scaled (extrapolated)")
+    out.update(detail)
+    out["cpu_model"] = cpu_model()
+    out["nproc"] = os.cpu_count()
+    out["build"] = flags
+    del torch
+    return out
 
 
 if __name__ == "__main__":

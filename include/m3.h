@@ -53,8 +53,18 @@
  * single-pass kernels' look-back forms each entering state by the same fold
  * from the sequence start whatever the timing (bit-equal across runs, given
  * the same device and kernel choice).  Calls on
- * disjoint buffers may run concurrently; the library has no mutable global
- * state besides a once-initialised cache of device properties.
+ * disjoint buffers may run concurrently; the library's only mutable global
+ * state is a once-initialised cache of device properties and the look-back
+ * wait limit (m3_set_wait_limit).
+ *
+ * Look-back waits: the single-pass prefill kernels link the chunks (or
+ * segments) of a slice by waiting on their predecessors' published states.
+ * Every such wait is bounded; one that gives up counts a timeout in the
+ * workspace and makes the entering state NaN, so y from that chunk on and the
+ * final state of the slice come out NaN.  m3_scan_check reads the count; a
+ * non-zero count means y and the final state of that call are invalid.  The
+ * work-item order makes a timeout unreachable in normal operation (every
+ * predecessor of a waiting workgroup is running or done).
  */
 #ifndef M3_H
 #define M3_H
@@ -202,10 +212,14 @@ m3_status m3_scan_fwd_gated(const m3_dims *dims,
  * consecutive sequences of equal length goes out as one m3_scan_fwd over a
  * batch of them (they lie in the packed arrays as that batch would) as far
  * as the workspace holds what the batch needs (m3_scan_workspace_bytes with
- * batch = the run's length, a_stride_b = length * a_stride_t).  Every
- * sequence's arguments are checked before the first launch (errors as
- * m3_scan_fwd; M3_ERR_NULL for a NULL cu_seqlens, M3_ERR_SHAPE for bad
- * offsets).
+ * batch = the run's length, a_stride_b = length * a_stride_t).  The kernel
+ * (and its segment count) is chosen per launch, so the last bits of a
+ * sequence's results can depend on how many equal-length neighbours it is
+ * batched with and hence on workspace_bytes; every grouping is within the
+ * scan's tolerance of the recurrence.  Every call's arguments are checked
+ * before the first launch (errors as m3_scan_fwd; M3_ERR_NULL for a NULL
+ * cu_seqlens, M3_ERR_SHAPE for bad offsets).  m3_scan_check after a varlen
+ * call reads the timeouts of its last launch only.
  */
 m3_status m3_scan_fwd_varlen(const m3_dims *dims, const int64_t *cu_seqlens,
                              const void *x, const void *B, const void *C,
@@ -245,6 +259,30 @@ m3_status m3_step_gated(const m3_dims *dims,
                         const float *dt_t, const float *A, const float *lambda_t,
                         const float *theta_t, const float *D, const void *z_t,
                         void *y_t, void *stream);
+
+/*
+ * Count of look-back waits that gave up in the last m3_scan_fwd (gated or
+ * not) run with `dims` on `workspace` (Sec. 3.3: the inter-chunk state
+ * passing whose waits these are).  Copies one word from the workspace to
+ * *timeouts after all work queued on `stream` (synchronises the stream).
+ * *timeouts = 0 without touching the device for dims that select the
+ * three-kernel path or an empty sequence (no waits there).  A non-zero count
+ * means that call's y and final state are invalid (they hold NaN from the
+ * chunk that gave up on).  Errors: those of m3_scan_fwd for `dims`,
+ * M3_ERR_NULL for a NULL `timeouts`, M3_ERR_WORKSPACE when the workspace is
+ * smaller than m3_scan_workspace_bytes(dims), M3_ERR_ALIGN, M3_ERR_HIP.
+ */
+m3_status m3_scan_check(const m3_dims *dims, const void *workspace, size_t workspace_bytes,
+                        uint32_t *timeouts, void *stream);
+
+/*
+ * Polls a look-back wait makes before it gives up (process-wide, all
+ * devices, read at each scan call; 0 restores the default, 2^22 polls of a
+ * few hundred nanoseconds each).  For tests of the timeout path: with a
+ * limit of 1 a waiting workgroup gives up at once, so the scan finishes with
+ * NaN results and a non-zero m3_scan_check count instead of waiting.
+ */
+void m3_set_wait_limit(uint32_t polls);
 
 /* Static description of a status code. */
 const char *m3_status_string(m3_status status);

@@ -18,26 +18,41 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "m3_oracle.c")
 _LIB = os.path.join(_HERE, "libm3_oracle.so")
+_LIB_NATIVE = os.path.join(_HERE, "libm3_oracle_native.so")
 _lib = None
+_lib_path = _LIB
+BUILD_FLAGS = ["-O3", "-fopenmp", "-shared", "-fPIC", "-std=c11"]
 
 
-def build(force: bool = True) -> str:
-    """Compile the oracle with gcc (OpenMP over slices).  The target ISA is
-    the portable x86-64-v3 so the library runs on any AVX2 host."""
-    if force or not os.path.exists(_LIB):
-        tmp = _LIB + ".tmp"
-        subprocess.run(["gcc", "-O2", "-march=x86-64-v3", "-fopenmp", "-shared",
-                        "-fPIC", "-std=c11", _SRC, "-o", tmp, "-lm"], check=True)
-        os.replace(tmp, _LIB)
-    return _LIB
+def build(force: bool = True, native: bool = False) -> str:
+    """Compile the oracle with gcc -O3 (OpenMP over slices).  The default
+    target ISA is the portable x86-64-v3, so the library built here runs on
+    any AVX2 host; `native` builds a -march=native copy for the host it runs
+    on (the CPU baseline's timing build, made where it is timed)."""
+    out = _LIB_NATIVE if native else _LIB
+    if force or not os.path.exists(out):
+        tmp = out + f".tmp{os.getpid()}"
+        march = "-march=native" if native else "-march=x86-64-v3"
+        subprocess.run(["gcc", *BUILD_FLAGS, march, _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, out)
+    return out
+
+
+def use_native() -> str:
+    """Build the -march=native copy on this host and route every later call
+    through it; returns the gcc flags used."""
+    global _lib, _lib_path
+    build(force=True, native=True)
+    _lib, _lib_path = None, _LIB_NATIVE
+    return " ".join(["gcc", *BUILD_FLAGS, "-march=native"])
 
 
 def _load():
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB):
-            build()
-        lib = ctypes.CDLL(_LIB)
+        if not os.path.exists(_lib_path):
+            build(native=_lib_path == _LIB_NATIVE)
+        lib = ctypes.CDLL(_lib_path)
         i64, dp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
         lib.m3o_scan.argtypes = [i64] * 5 + [dp] * 8 + [dp] * 3 + [dp] * 4 + [ci]
         lib.m3o_scan.restype = ci

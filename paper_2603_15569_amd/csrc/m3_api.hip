@@ -2,12 +2,16 @@
 // call), workspace layout, dispatch to the shape-specialised kernels.
 #include <limits.h>
 
+#include <atomic>
+
 #include "m3.h"
 #include "m3_internal.h"
 
 namespace m3 {
 
 static thread_local int g_last_hip_error = 0;
+// bound of the single-pass kernels' look-back waits (m3_set_wait_limit)
+static std::atomic<uint32_t> g_spin_max{kSpinMaxDefault};
 
 static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 
@@ -163,6 +167,7 @@ static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const 
     a.batch = d->batch; a.L = d->seqlen; a.H = d->nheads; a.nchunks = nc;
     a.a_sb = d->a_stride_b; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
     a.G = d->seg_chunks; a.nseg = 0; a.per_chunk = impl.per_chunk;
+    a.spin_max = g_spin_max.load(std::memory_order_relaxed);
     const hipError_t e = impl.launch(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) {
         g_last_hip_error = (int)e;
@@ -193,9 +198,11 @@ extern "C" m3_status m3_scan_fwd_gated(const m3_dims *d, const void *x, const vo
 }
 
 // Packed sequences of different lengths: sequence i is tokens cu_seqlens[i]
-// .. cu_seqlens[i+1] - 1 of the token axis; each is scanned on its own (one
-// m3_scan_fwd per sequence, in order on `stream`, sharing the workspace).
-// Every sequence's arguments are checked before the first launch.
+// .. cu_seqlens[i+1] - 1 of the token axis.  Runs of consecutive sequences of
+// equal length go out as one m3_scan_fwd over a batch of them (as far as the
+// workspace holds what that batch needs), every other sequence as an
+// m3_scan_fwd of its own; the calls run in order on `stream` and share the
+// workspace.  Every call's arguments are checked before the first launch.
 extern "C" m3_status m3_scan_fwd_varlen(const m3_dims *d, const int64_t *cu_seqlens,
                                         const void *x, const void *B, const void *C,
                                         const float *dt, const float *A, const float *lambda,
@@ -228,7 +235,10 @@ extern "C" m3_status m3_scan_fwd_varlen(const m3_dims *d, const int64_t *cu_seql
             dj.batch = j - i + 1;
             dj.seqlen = len;
             dj.a_stride_b = len * d->a_stride_t;
-            if (m3_scan_workspace_bytes(&dj) > workspace_bytes) break;
+            // (0: the batched dims are invalid, e.g. too many chunk items,
+            // while the sequences alone may be fine: stop the run)
+            const size_t need = m3_scan_workspace_bytes(&dj);
+            if ((need == 0 && len > 0) || need > workspace_bytes) break;
         }
         return j;
     };
@@ -307,4 +317,37 @@ extern "C" m3_status m3_step_gated(const m3_dims *d, float *state, void *carryB,
                                    void *y_t, void *stream) {
     return step(d, state, carryB, carryX, x_t, B_t, C_t, dt_t, A, lambda_t, theta_t, D, true, z_t,
                 y_t, stream);
+}
+
+extern "C" void m3_set_wait_limit(uint32_t polls) {
+    g_spin_max.store(polls ? polls : kSpinMaxDefault, std::memory_order_relaxed);
+}
+
+extern "C" m3_status m3_scan_check(const m3_dims *d, const void *workspace, size_t workspace_bytes,
+                                   uint32_t *timeouts, void *stream) {
+    ScanImpl impl;
+    int64_t nc = 0;
+    m3_status s = check_scan_dims(d, &impl, &nc);
+    if (s != M3_OK) return s;
+    if (!timeouts) return M3_ERR_NULL;
+    if (nc == 0 || !impl.fused) {   // the three-kernel path and the empty scan never wait
+        *timeouts = 0;
+        return M3_OK;
+    }
+    const ScanWorkspaceLayout wl = scan_workspace_layout(d->batch * d->nheads, nc, d->dstate,
+                                                         d->headdim, io_bytes_of(d->io),
+                                                         impl.acc_bytes, impl.fused);
+    if (!workspace || workspace_bytes < wl.total) return M3_ERR_WORKSPACE;
+    if (!aligned16(workspace)) return M3_ERR_ALIGN;
+    const char *ctl = static_cast<const char *>(workspace) + wl.off_ctl;
+    uint32_t v = 0;
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(&v, ctl + sizeof(uint32_t), sizeof(uint32_t), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return M3_ERR_HIP;
+    }
+    *timeouts = v;
+    return M3_OK;
 }

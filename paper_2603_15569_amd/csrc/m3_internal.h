@@ -36,6 +36,9 @@ struct ScanArgs {
     // segments per slice (null: none)
     int64_t G, nseg;
     hipError_t (*per_chunk)(const ScanArgs &, hipStream_t);
+    // polls of a look-back wait before it gives up (counts a timeout in
+    // ctl[1] and makes the entering state NaN)
+    uint32_t spin_max;
 };
 
 struct StepArgs {
@@ -49,6 +52,9 @@ struct StepArgs {
     int64_t batch, H;
     int64_t a_sb, a_sh;
 };
+
+// default bound of a look-back wait (polls; ~seconds), then an error count
+constexpr uint32_t kSpinMaxDefault = 1u << 22;
 
 typedef hipError_t (*scan_launch_fn)(const ScanArgs &, hipStream_t);
 typedef hipError_t (*step_launch_fn)(const StepArgs &, hipStream_t);

@@ -9,7 +9,6 @@ namespace m3 {
 namespace scan {
 
 constexpr uint32_t kFlagAgg = 1, kFlagInc = 2;
-constexpr uint32_t kSpinMax = 1u << 22;   // bounded wait: ~seconds, then error exit
 
 struct alignas(4) h2 { _Float16 c, s; };
 template <typename T> struct CsOf { typedef h2 type; };          // bf16 path: fp16 cos/sin

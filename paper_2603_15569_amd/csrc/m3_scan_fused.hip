@@ -594,7 +594,7 @@ void k_scan_fused(ScanArgs a) {
                 j -= adv;
                 if (tid == 0) {
                     uint32_t f = 0u;
-                    for (uint32_t spin = 0; spin < kSpinMax; ++spin) {
+                    for (uint32_t spin = 0; spin < a.spin_max; ++spin) {
                         f = __hip_atomic_load(a.flags + sbase + j, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
                         if (f != 0u) break;
                         __builtin_amdgcn_s_sleep(2);
@@ -605,16 +605,16 @@ void k_scan_fused(ScanArgs a) {
                 __syncthreads();
                 timed_out = s_i[1] != 0;
                 __syncthreads();
-                if (timed_out) jt = c - 1;   // (error path: the entering state is left zero)
+                if (timed_out) jt = c - 1;   // (error path: the entering state is NaN)
             } else {
                 j -= kProbe;                 // sixteen aggregates: probe further back
             }
         }
-        if (timed_out) {
+        if (timed_out) {   // y of this chunk and of every later one, and the final state, become NaN
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2)
 #pragma unroll
-                for (int v = 0; v < 4; ++v) Sin[m2][0][v] = Sin[m2][1][v] = 0.f;
+                for (int v = 0; v < 4; ++v) Sin[m2][0][v] = Sin[m2][1][v] = __builtin_nanf("");
         } else if (jt < 0) {
             load_init(Sin);
         } else {

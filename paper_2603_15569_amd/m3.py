@@ -40,7 +40,8 @@ class M3Error(RuntimeError):
 
 
 EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_scan_fwd_varlen",
-           "m3_step", "m3_step_gated", "m3_status_string", "m3_last_hip_error")
+           "m3_step", "m3_step_gated", "m3_scan_check", "m3_set_wait_limit", "m3_status_string",
+           "m3_last_hip_error")
 _lib = None
 
 
@@ -66,6 +67,10 @@ def lib() -> ctypes.CDLL:
         L.m3_step.restype = ctypes.c_int
         L.m3_step_gated.argtypes = [dims_p] + [vp] * 13 + [vp]
         L.m3_step_gated.restype = ctypes.c_int
+        L.m3_scan_check.argtypes = [dims_p, vp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_uint32), vp]
+        L.m3_scan_check.restype = ctypes.c_int
+        L.m3_set_wait_limit.argtypes = [ctypes.c_uint32]
+        L.m3_set_wait_limit.restype = None
         L.m3_status_string.argtypes = [ctypes.c_int]
         L.m3_status_string.restype = ctypes.c_char_p
         L.m3_last_hip_error.argtypes = []
@@ -128,10 +133,30 @@ def workspace_bytes(dims: M3Dims) -> int:
     return int(lib().m3_scan_workspace_bytes(ctypes.byref(dims)))
 
 
+class LookBackTimeout(RuntimeError):
+    """A single-pass scan's look-back wait gave up: its y and final state are invalid."""
+
+
+def scan_check(dims: M3Dims, workspace, stream=None) -> int:
+    """m3_scan_check: the number of look-back waits that gave up in the last
+    scan run with `dims` on `workspace` (synchronises the stream)."""
+    n = ctypes.c_uint32(0)
+    wsb = workspace.numel() if workspace is not None else 0
+    _check(lib().m3_scan_check(ctypes.byref(dims), _p(workspace), wsb, ctypes.byref(n),
+                               _stream(stream)))
+    return int(n.value)
+
+
+def set_wait_limit(polls: int) -> None:
+    """m3_set_wait_limit: polls before a look-back wait gives up (0: default)."""
+    lib().m3_set_wait_limit(int(polls))
+
+
 def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
              init_state=None, init_carry=None, out=None, workspace=None,
              stream=None, split: bool = False, per_chunk: bool = False, seg: int = 0,
-             z=None) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
+             z=None, check: bool = False
+             ) -> Tuple[torch.Tensor, torch.Tensor, Tuple[torch.Tensor, torch.Tensor]]:
     """m3_scan_fwd (m3_scan_fwd_gated when the gate input `z`, shaped like x,
     is given: y o SiLU(z)); `theta` is [B,L,H,N/2] per-token angles, or
     [H,N/2] per-head frequencies omega (M3_THETA_PER_HEAD: angle dt * omega).
@@ -140,7 +165,8 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
     (y, final_state, carryB, carryX) to write into.  Kernel choice: `split`
     (M3_SCAN_SPLIT, three kernels), `per_chunk` (M3_SCAN_PER_CHUNK, one chunk
     per workgroup), else the segmented kernel with `seg` chunks per
-    workgroup (0: library choice)."""
+    workgroup (0: library choice).  With `check`, the call synchronises and
+    raises LookBackTimeout when a look-back wait gave up (m3_scan_check)."""
     d = scan_dims(x, Bm, chunk, A, split, per_chunk, seg,
                   _theta_per_head(theta, x.shape[2], Bm.shape[-1]))
     batch, seqlen, nheads, rank, headdim = x.shape
@@ -169,6 +195,10 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
                                        _p(lam), _p(theta), _p(D), _p(z), _p(init_state), _p(icB),
                                        _p(icX), _p(y), _p(fs), _p(cB), _p(cX), _p(workspace), wsb,
                                        _stream(stream)))
+    if check:
+        n = scan_check(d, workspace, stream)
+        if n:
+            raise LookBackTimeout(f"{n} look-back wait(s) gave up: y and the final state are invalid")
     return y, fs, (cB, cX)
 
 

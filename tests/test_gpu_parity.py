@@ -50,9 +50,12 @@ def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, mode="
                                   chunk=chunk, init_state=init_state, init_carry=init_carry,
                                   out=out, workspace=ws, z=z, **kw)
     torch.cuda.synchronize()
+    # no look-back wait gave up (m3_scan_check; zero without a device read
+    # for the three-kernel path)
+    assert m3.scan_check(m3.scan_dims(x, inp.Bm, chunk, inp.A, **kw), ws) == 0, "look-back wait timed out"
     if single_pass and L > 0:
-        # single-pass kernels: word 1 of the workspace counts look-back waits that timed out
-        assert int(ws[4:8].view(torch.int32).item()) == 0, "look-back wait timed out"
+        # the same word read directly: word 1 of the single-pass workspace
+        assert int(ws[4:8].view(torch.int32).item()) == 0
     return y, fs, cB, cX
 
 
@@ -125,24 +128,47 @@ def test_workload2_mimo_bf16():
                  TOL["bf16"], label="w2")
 
 
+def check_tail_chunks(inp, y, slices, chunk, nlast, tol, label):
+    """The last `nlast` chunks of each slice checked on their own (error
+    normalised by that chunk's largest output), so that drift late in a long
+    sequence cannot hide under the slice-wide maximum."""
+    L = y.shape[1]
+    t0 = max(0, L - nlast * chunk)
+    ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                inp.D, slices)
+    ry = oracle.scan(**ref)[0]
+    worst = 0.0
+    for k, (b, h) in enumerate(slices):
+        gy = y[b, :, h].double().cpu().numpy()
+        for c0 in range(t0, L, chunk):
+            c1 = min(L, c0 + chunk)
+            e = oracle.rel_err(gy[c0:c1], ry[k][c0:c1])
+            worst = max(worst, e)
+            assert e <= tol, f"{label} slice {(b, h)} tokens {c0}..{c1 - 1}: rel err {e:.3g}"
+    say(f"{label}: worst per-chunk rel err {worst:.3g} over the last {nlast} chunks")
+
+
 def test_workload3_long_mimo_bf16():
-    say("workload 3: long-context MIMO prefill L=65536, 4 sampled slices")
     w = WORKLOADS[3]
+    slices = sample_slices(w["batch"], w["nheads"], 18, 3)   # 16 seeded + first and last
+    assert (0, 0) in slices and (w["batch"] - 1, w["nheads"] - 1) in slices and len(slices) == 18
+    say(f"workload 3: long-context MIMO prefill L=65536, {len(slices)} sampled slices")
     inp = workload_inputs(3, device=DEV)
     y, fs, cB, cX = run_scan(inp, w["chunk"])
-    check_slices(inp, y, fs, cB, cX, sample_slices(w["batch"], w["nheads"], 4, 3),
-                 TOL["bf16"], label="w3")
+    check_slices(inp, y, fs, cB, cX, slices, TOL["bf16"], label="w3")
+    check_tail_chunks(inp, y, slices[:4] + slices[-2:], w["chunk"], 8, TOL["bf16"], label="w3 tail")
 
 
 def test_workload4_decode_loop():
     """State from a 1024-token prefill (B=256, H=32, R=4), then 1024 decode
-    steps with fresh inputs; every step's y and the final state checked on 16
-    sampled slices."""
+    steps with fresh inputs; every step's y and the final state checked on 18
+    slices (16 seeded, the first and the last)."""
     w = WORKLOADS[4]
-    say("workload 4: prefill B=256 L=1024 then 1024 steps, 16 sampled slices")
+    slices = sample_slices(w["batch"], w["nheads"], 18, 4)   # 16 seeded + first and last
+    assert (0, 0) in slices and (w["batch"] - 1, w["nheads"] - 1) in slices and len(slices) == 18
+    say(f"workload 4: prefill B=256 L=1024 then 1024 steps, {len(slices)} sampled slices")
     inp = workload_inputs(4, device=DEV)
     y, fs, cB, cX = run_scan(inp, w["chunk"], nan_fill=False)
-    slices = sample_slices(w["batch"], w["nheads"], 16, 4)
     ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
                                 inp.D, slices)
     ry, rs, rb, rx = oracle.scan(**ref)
@@ -664,25 +690,35 @@ def test_varlen(io, N, P, R, Q, gated, per_head):
             assert torch.equal(cB1[0], cB[i]) and torch.equal(cX1[0], cX[i])
 
 
-def test_varlen_equal_length_runs():
+@pytest.mark.parametrize("variant", ["plain", "per_token_A", "gated_per_head"])
+def test_varlen_equal_length_runs(variant):
     """Runs of consecutive equal-length sequences (3 x 64, 2 x 10, 2 x 0, 33)
     with a workspace large enough to batch each run: every sequence against
-    the oracle, from its own initial state."""
+    the oracle, from its own initial state; with per-token A [T, H] (the
+    batched launch then strides A by the sequence length), and gated with
+    per-head frequencies omega."""
     io, N, P, R, Q, H = "bf16", 128, 64, 4, 64, 3
     lens = [64, 64, 64, 10, 10, 0, 0, 33]
     cu = [0]
     for n in lens:
         cu.append(cu[-1] + n)
     T, S = cu[-1], len(lens)
-    say(f"varlen runs lens={lens}")
+    say(f"varlen runs lens={lens} variant={variant}")
     inp = make_scan_inputs(1, T, H, P, N, R, io=io, seed=131, device=DEV, chunk=Q)
     flat = lambda t: t[0].contiguous()
     init = torch.randn(S, H, N, P, device=DEV)
-    ws = torch.zeros(m3.workspace_bytes(m3.M3Dims(S, 64, H, P, N, R, Q, 1, 0, 0, 0, 1, 0)),
+    A_in, A_ref = inp.A, None
+    if variant == "per_token_A":
+        A_in = (-torch.rand(T, H, device=DEV) * 4 - 0.1).contiguous()
+        A_ref = A_in
+    th_in = inp.omega.contiguous() if variant == "gated_per_head" else flat(inp.theta)
+    z = make_gate_input(flat(inp.x), 5) if variant == "gated_per_head" else None
+    st_t = 0 if A_ref is None else H
+    ws = torch.zeros(m3.workspace_bytes(m3.M3Dims(S, 64, H, P, N, R, Q, 1, 0, 64 * st_t, st_t, 1, 0)),
                      dtype=torch.uint8, device=DEV)
     y, fs, (cB, cX) = m3.scan_fwd_varlen(flat(inp.x), flat(inp.Bm), flat(inp.Cm), flat(inp.dt),
-                                         inp.A, flat(inp.lam), flat(inp.theta), inp.D, Q, cu,
-                                         init_state=init, workspace=ws)
+                                         A_in, flat(inp.lam), th_in, inp.D, Q, cu,
+                                         init_state=init, workspace=ws, z=z)
     torch.cuda.synchronize()
     for i in range(S):
         t0, t1 = cu[i], cu[i + 1]
@@ -692,9 +728,12 @@ def test_varlen_equal_length_runs():
             continue
         ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
                                     inp.D, sl, t0, t1)
+        if A_ref is not None:
+            ref["A"] = np.stack([A_ref[t0:t1, h].double().cpu().numpy() for h in range(H)])
         ry, rs, rb, rx = oracle.scan(**ref, init_state=oracle._np(init[i]))
         for h in range(H):
-            assert oracle.rel_err(y[t0:t1, h].double().cpu().numpy(), ry[h]) <= TOL[io], f"seq {i} y"
+            ref_y = ry[h] if z is None else oracle.gate(ry[h], oracle._np(z[t0:t1, h]))
+            assert oracle.rel_err(y[t0:t1, h].double().cpu().numpy(), ref_y) <= TOL[io], f"seq {i} y"
             assert oracle.rel_err(fs[i, h].cpu().numpy(), rs[h]) <= TOL[io], f"seq {i} state"
             assert np.array_equal(oracle._np(cB[i, h]), rb[h]) and np.array_equal(oracle._np(cX[i, h]), rx[h])
 
@@ -717,3 +756,41 @@ def test_determinism_many_items(mode, seg, R, Q):
     for other in runs[1:]:
         for u, v in zip(runs[0], other):
             assert torch.equal(u, v)
+
+
+# ---------------------------------------------------------------------------
+# Look-back timeouts: reported through m3_scan_check, results NaN
+# ---------------------------------------------------------------------------
+
+@pytest.mark.parametrize("mode,seg", [("per_chunk", 0), ("seg", 2)])
+def test_lookback_timeout_reported(mode, seg):
+    """With a wait limit of one poll, workgroups that find their predecessor
+    unpublished give up at once (every kernel still exits normally): the
+    scan's check count is non-zero and the invalid results are NaN, not
+    plausible numbers; with the default limit restored the same scan is
+    clean and matches the oracle."""
+    R, Q = 1, 64
+    say(f"look-back timeout mode={mode} seg={seg}")
+    inp = make_scan_inputs(4, 2048, 16, 64, 128, R, io="bf16", seed=17, device=DEV, chunk=Q)
+    kw = dict(per_chunk=mode == "per_chunk", seg=seg)
+    d = m3.scan_dims(inp.x, inp.Bm, Q, inp.A, **kw)
+    ws = torch.zeros(m3.workspace_bytes(d), dtype=torch.uint8, device=DEV)
+    args = (inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta, inp.D)
+    try:
+        m3.set_wait_limit(1)
+        y, fs, _ = m3.scan_fwd(*args, chunk=Q, workspace=ws, **kw)
+        n = m3.scan_check(d, ws)
+        with pytest.raises(m3.LookBackTimeout):
+            m3.scan_fwd(*args, chunk=Q, workspace=ws, check=True, **kw)
+    finally:
+        m3.set_wait_limit(0)
+    say(f"timeouts with a one-poll limit: {n}")
+    assert n > 0
+    assert torch.isnan(fs).any() and torch.isnan(y.float()).any()
+    # a slice with a NaN final state has NaN outputs from some chunk on
+    bad = torch.isnan(fs).flatten(2).any(-1).nonzero()
+    b, h = (int(v) for v in bad[0])
+    assert torch.isnan(y[b, -1, h].float()).all()
+    y2, fs2, (cB2, cX2) = m3.scan_fwd(*args, chunk=Q, workspace=ws, check=True, **kw)
+    assert m3.scan_check(d, ws) == 0
+    check_slices(inp, y2, fs2, cB2, cX2, sample_slices(4, 16, 6, 12), TOL["bf16"], label="after timeout")

@@ -207,3 +207,27 @@ def test_varlen_host_validation(L):
     assert call(d, [0, 10, 50, 100], {12: None}) == m3.M3_ERR_NULL   # y
     assert call(dims(batch=3, seqlen=100, chunk=48), [0, 10, 50, 100]) == m3.M3_ERR_UNSUPPORTED
     assert L.m3_last_hip_error() == 0
+
+
+def test_scan_check_host_validation(L):
+    """m3_scan_check: argument errors on the host; the three-kernel path and
+    the empty sequence report zero waits without touching the device."""
+    n = ctypes.c_uint32(123)
+    d = dims(io=m3.M3_BF16, headdim=64, dstate=128, rank=4, chunk=64, seqlen=300)
+    need = L.m3_scan_workspace_bytes(ctypes.byref(d))
+    assert need > 0
+    assert L.m3_scan_check(None, FAKE, need, ctypes.byref(n), None) == m3.M3_ERR_NULL
+    assert L.m3_scan_check(ctypes.byref(d), FAKE, need, None, None) == m3.M3_ERR_NULL
+    assert L.m3_scan_check(ctypes.byref(dims(dstate=15)), FAKE, need, ctypes.byref(n), None) == m3.M3_ERR_SHAPE
+    assert L.m3_scan_check(ctypes.byref(d), None, need, ctypes.byref(n), None) == m3.M3_ERR_WORKSPACE
+    assert L.m3_scan_check(ctypes.byref(d), FAKE, need - 1, ctypes.byref(n), None) == m3.M3_ERR_WORKSPACE
+    assert L.m3_scan_check(ctypes.byref(d), FAKE + 4, need, ctypes.byref(n), None) == m3.M3_ERR_ALIGN
+    assert n.value == 123   # errors leave the output untouched
+    ds = dims(io=m3.M3_BF16, headdim=64, dstate=128, rank=4, chunk=64, seqlen=300, flags=m3.M3_SCAN_SPLIT)
+    assert L.m3_scan_check(ctypes.byref(ds), None, 0, ctypes.byref(n), None) == m3.M3_OK
+    assert n.value == 0
+    n.value = 5
+    d0 = dims(io=m3.M3_BF16, headdim=64, dstate=128, rank=4, chunk=64, seqlen=0)
+    assert L.m3_scan_check(ctypes.byref(d0), None, 0, ctypes.byref(n), None) == m3.M3_OK
+    assert n.value == 0
+    L.m3_set_wait_limit(0)   # restores the default; no device access

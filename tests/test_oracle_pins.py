@@ -284,3 +284,20 @@ def test_gate_is_elementwise_product():
     z = rng.normal(size=y.shape)
     lhs = oracle.gate(y, z) + oracle.gate(y, -z)
     np.testing.assert_allclose(lhs, y * z * np.tanh(z / 2.0), rtol=1e-13, atol=1e-15)
+
+
+def test_rel_err_definition():
+    """The parity metric max|got - ref| / max|ref| (infinity norms over the
+    whole array), on values worked out by hand: a slip that normalises by the
+    other operand, drops an absolute value, takes a mean or a norm of another
+    order changes at least one of these."""
+    assert oracle.rel_err([1.0, 2.0], [1.0, 4.0]) == 0.5            # 2 / 4
+    assert oracle.rel_err([1.0, 4.0], [1.0, 2.0]) == 1.0            # 2 / 2 (not 2 / 4)
+    assert oracle.rel_err([-3.0, 0.0], [-1.0, 0.5]) == 2.0          # |-2| / |-1|
+    assert oracle.rel_err([0.0, 0.0], [-2.0, 1.0]) == 1.0           # max|ref| is 2, not max(ref) = 1
+    assert oracle.rel_err([1.0, 1.0, 1.0], [0.0, 0.0, 4.0]) == 0.75  # max error 3 over 4, not a mean
+    assert oracle.rel_err([[0.5, -1.5], [2.0, 3.0]], [[1.0, -1.0], [2.0, 4.0]]) == 0.25
+    assert oracle.rel_err([0.0, 0.0], [0.0, 0.0]) == 0.0            # both zero
+    assert oracle.rel_err([0.0, 3.0], [0.0, 0.0]) == 3.0            # zero reference: absolute error
+    assert oracle.rel_err([], []) == 0.0
+    assert oracle.rel_err(np.full(5, 7.0), np.full(5, 7.0)) == 0.0
