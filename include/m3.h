@@ -261,6 +261,34 @@ m3_status m3_step_gated(const m3_dims *dims,
                         void *y_t, void *stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, serving loops, harnesses that forbid hipMalloc): m3_scan_fwd
+ * without a workspace argument.  The workspace is a library-owned device
+ * array of M3_SCRATCH_BYTES (256 MiB), one per device the library runs on,
+ * held until the process ends; its device address is looked up once per
+ * device on the first call made with that device current (that call is not
+ * capturable; later ones are).  Nothing is allocated: no hipMalloc, hipFree
+ * or allocating library call.  Kernels, results and errors are those of
+ * m3_scan_fwd with a workspace (the same bits), except that a scan whose
+ * m3_scan_workspace_bytes(dims) exceeds M3_SCRATCH_BYTES returns
+ * M3_ERR_WORKSPACE before any device call.  Every call on a device shares
+ * that device's array: calls that overlap in time on one device (other
+ * streams, other threads) race and give wrong results; calls ordered on
+ * one stream are safe (each clears what its kernels need zeroed).  The
+ * look-back timeout count of these calls is not readable (m3_scan_check
+ * takes a workspace); a timeout still shows as NaN results.
+ */
+#define M3_SCRATCH_BYTES ((size_t)256 << 20)
+m3_status m3_scan_fwd_noalloc(const m3_dims *dims,
+                              const void *x, const void *B, const void *C,
+                              const float *dt, const float *A, const float *lambda,
+                              const float *theta, const float *D,
+                              const float *init_state, const void *init_carryB,
+                              const void *init_carryX,
+                              void *y, float *final_state, void *carryB, void *carryX,
+                              void *stream);
+
+/*
  * Count of look-back waits that gave up in the last m3_scan_fwd (gated or
  * not) run with `dims` on `workspace` (Sec. 3.3: the inter-chunk state
  * passing whose waits these are).  Copies one word from the workspace to

@@ -351,3 +351,65 @@ extern "C" m3_status m3_scan_check(const m3_dims *d, const void *workspace, size
     *timeouts = v;
     return M3_OK;
 }
+
+// ---------------------------------------------------------------------------
+// Allocation-free prefill: the workspace is a library-owned device array.
+// ---------------------------------------------------------------------------
+
+namespace m3 {
+namespace {
+
+// Each device the library runs on holds one copy of this array (in the code
+// object's zero-initialised data) until the process ends.  Host code never
+// uses the array's name as an address: it takes each device's copy from
+// hipGetSymbolAddress once per device (scratch_ptr) and passes that pointer.
+static __device__ __align__(256) unsigned char scratch[M3_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void *> g_scratch[kMaxDevices];
+
+// Device address of this device's scratch array (looked up once per device,
+// with the device current), or null on error (g_last_hip_error set).
+void *scratch_ptr() {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+        g_last_hip_error = (int)(e != hipSuccess ? e : hipErrorInvalidDevice);
+        return nullptr;
+    }
+    void *p = g_scratch[dev].load(std::memory_order_acquire);
+    if (p) return p;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || p == nullptr) {
+        g_last_hip_error = (int)(e != hipSuccess ? e : hipErrorInvalidSymbol);
+        return nullptr;
+    }
+    g_scratch[dev].store(p, std::memory_order_release);   // (a racing first call stores the same address)
+    return p;
+}
+
+}  // namespace
+}  // namespace m3
+
+extern "C" m3_status m3_scan_fwd_noalloc(const m3_dims *d, const void *x, const void *B,
+                                         const void *C, const float *dt, const float *A,
+                                         const float *lambda, const float *theta, const float *D,
+                                         const float *init_state, const void *init_carryB,
+                                         const void *init_carryX, void *y, float *final_state,
+                                         void *carryB, void *carryX, void *stream) {
+    // every argument check of m3_scan_fwd first (no device call), then the size
+    m3_status s = scan_fwd(d, x, B, C, dt, A, lambda, theta, D, false, nullptr, init_state,
+                           init_carryB, init_carryX, y, final_state, carryB, carryX,
+                           reinterpret_cast<void *>(uintptr_t(256)), M3_SCRATCH_BYTES, stream,
+                           /*dry_run=*/true);
+    if (s != M3_OK) return s;
+    const size_t need = m3_scan_workspace_bytes(d);
+    if (need > M3_SCRATCH_BYTES) return M3_ERR_WORKSPACE;
+    void *ws = nullptr;
+    if (need > 0) {
+        ws = scratch_ptr();
+        if (!ws) return M3_ERR_HIP;
+    }
+    return scan_fwd(d, x, B, C, dt, A, lambda, theta, D, false, nullptr, init_state, init_carryB,
+                    init_carryX, y, final_state, carryB, carryX, ws, M3_SCRATCH_BYTES, stream);
+}

@@ -40,8 +40,9 @@ class M3Error(RuntimeError):
 
 
 EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_scan_fwd_varlen",
-           "m3_step", "m3_step_gated", "m3_scan_check", "m3_set_wait_limit", "m3_status_string",
-           "m3_last_hip_error")
+           "m3_step", "m3_step_gated", "m3_scan_check", "m3_set_wait_limit", "m3_scan_fwd_noalloc",
+           "m3_status_string", "m3_last_hip_error")
+SCRATCH_BYTES = 256 << 20   # M3_SCRATCH_BYTES: the allocation-free scan's fixed workspace
 _lib = None
 
 
@@ -67,6 +68,8 @@ def lib() -> ctypes.CDLL:
         L.m3_step.restype = ctypes.c_int
         L.m3_step_gated.argtypes = [dims_p] + [vp] * 13 + [vp]
         L.m3_step_gated.restype = ctypes.c_int
+        L.m3_scan_fwd_noalloc.argtypes = [dims_p] + [vp] * 15 + [vp]
+        L.m3_scan_fwd_noalloc.restype = ctypes.c_int
         L.m3_scan_check.argtypes = [dims_p, vp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_uint32), vp]
         L.m3_scan_check.restype = ctypes.c_int
         L.m3_set_wait_limit.argtypes = [ctypes.c_uint32]
@@ -199,6 +202,23 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
         n = scan_check(d, workspace, stream)
         if n:
             raise LookBackTimeout(f"{n} look-back wait(s) gave up: y and the final state are invalid")
+    return y, fs, (cB, cX)
+
+
+def scan_fwd_noalloc(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, out,
+                     init_state=None, init_carry=None, stream=None, split: bool = False,
+                     per_chunk: bool = False, seg: int = 0):
+    """m3_scan_fwd_noalloc: the scan with the library's fixed device scratch
+    as its workspace (no allocation in the library).  `out` = (y,
+    final_state, carryB, carryX) must be given (this call allocates nothing
+    either); arguments otherwise as scan_fwd."""
+    d = scan_dims(x, Bm, chunk, A, split, per_chunk, seg,
+                  _theta_per_head(theta, x.shape[2], Bm.shape[-1]))
+    y, fs, cB, cX = out
+    icB, icX = (None, None) if init_carry is None else init_carry
+    _check(lib().m3_scan_fwd_noalloc(ctypes.byref(d), _p(x), _p(Bm), _p(Cm), _p(dt), _p(A),
+                                     _p(lam), _p(theta), _p(D), _p(init_state), _p(icB), _p(icX),
+                                     _p(y), _p(fs), _p(cB), _p(cX), _stream(stream)))
     return y, fs, (cB, cX)
 
 

@@ -231,3 +231,20 @@ def test_scan_check_host_validation(L):
     assert L.m3_scan_check(ctypes.byref(d0), None, 0, ctypes.byref(n), None) == m3.M3_OK
     assert n.value == 0
     L.m3_set_wait_limit(0)   # restores the default; no device access
+
+
+def test_noalloc_host_validation(L):
+    """m3_scan_fwd_noalloc: the argument checks of m3_scan_fwd, and a scan
+    whose workspace would exceed the fixed scratch is refused before any
+    device call."""
+    ptrs = [FAKE] * 15
+    for k in (8, 9, 10):
+        ptrs[k] = None
+    assert L.m3_scan_fwd_noalloc(None, *ptrs, None) == m3.M3_ERR_NULL
+    assert L.m3_scan_fwd_noalloc(ctypes.byref(dims(dstate=15)), *ptrs, None) == m3.M3_ERR_SHAPE
+    bad = list(ptrs)
+    bad[0] = FAKE + 2
+    assert L.m3_scan_fwd_noalloc(ctypes.byref(dims()), *bad, None) == m3.M3_ERR_ALIGN
+    big = dims(io=m3.M3_BF16, headdim=64, dstate=128, rank=1, chunk=64, batch=8, seqlen=4096, nheads=32)
+    assert L.m3_scan_workspace_bytes(ctypes.byref(big)) > m3.SCRATCH_BYTES
+    assert L.m3_scan_fwd_noalloc(ctypes.byref(big), *ptrs, None) == m3.M3_ERR_WORKSPACE
