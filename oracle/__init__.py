@@ -139,6 +139,47 @@ def gate(y, z):
 
 
 # ---------------------------------------------------------------------------
+# Block prologue: the cheap per-token operations of the Mamba-3 block that
+# produce the SSM's B, C, X (and the gate's Z) from the projections' outputs.
+#   * BCNorm (Sec. 3.4, paragraph "BC / QK Normalization"): an RMS
+#     normalisation of B and C after their projection, here over the state
+#     axis N of every (token, head, rank-column), with an optional per-channel
+#     gain;
+#   * B, C biases (Sec. 3.4, paragraph "B, C Biases"; App. "B, C Bias
+#     Parameterization"): head-specific, channel-wise, added after the norm;
+#   * structured MIMO input (App. "MIMO for Mamba-3", paragraph "Mamba with
+#     MIMO"): X_t = contract(PR, P -> PR)(W_X, X'_t), i.e. X_t[p, r] =
+#     W_X[p, r] X'_t[p]; the gate input Z is formed the same way from Z'.
+# All in fp64.
+# ---------------------------------------------------------------------------
+
+def rms_norm(v, gain=None, bias=None, eps=1e-6):
+    """v [..., N] -> gain * v / sqrt(mean_N(v^2) + eps) + bias, the mean over
+    the last (state) axis of each vector.  gain and bias broadcast against v
+    (per head, rank and channel); None means ones / zeros."""
+    v = _f64(v)
+    out = v / np.sqrt(np.mean(v * v, axis=-1, keepdims=True) + eps)
+    if gain is not None:
+        out = out * _f64(gain)
+    if bias is not None:
+        out = out + _f64(bias)
+    return out
+
+
+def add_bias(v, bias):
+    """The bias alone (no norm): v + bias, broadcast."""
+    return _f64(v) if bias is None else _f64(v) + _f64(bias)
+
+
+def structured_input(xp, w):
+    """X_t[r, p] = W[r, p] X'_t[p] for every token: xp [S, L, P] (one P-vector
+    per token and head), w [S, R, P] (the head's weights, one row per rank)
+    -> [S, L, R, P]."""
+    xp, w = _f64(xp), _f64(w)
+    return w[:, None, :, :] * xp[:, :, None, :]
+
+
+# ---------------------------------------------------------------------------
 # Slice extraction from tensors in the library layout.
 # ---------------------------------------------------------------------------
 

@@ -301,3 +301,100 @@ def test_rel_err_definition():
     assert oracle.rel_err([0.0, 3.0], [0.0, 0.0]) == 3.0            # zero reference: absolute error
     assert oracle.rel_err([], []) == 0.0
     assert oracle.rel_err(np.full(5, 7.0), np.full(5, 7.0)) == 0.0
+
+
+# ---------------------------------------------------------------------------
+# Block prologue: BCNorm, B/C biases, structured MIMO input (Sec. 3.4; App.
+# "MIMO for Mamba-3", paragraph "Mamba with MIMO").
+# ---------------------------------------------------------------------------
+
+def test_bcnorm_unit_rms_over_state_axis():
+    """With eps = 0 and no gain or bias every (token, rank) column comes out
+    with mean square exactly 1 over N, pointing the same way as its input.
+    The columns are given scales 1e-3 .. 1e3, so a norm over another axis
+    (ranks, tokens) or over all of them fails."""
+    rng = np.random.default_rng(20)
+    v = rng.standard_normal((3, 5, 4, 16)) * np.logspace(-3, 3, 4)[None, None, :, None]
+    out = oracle.rms_norm(v, eps=0.0)
+    np.testing.assert_allclose(np.mean(out * out, axis=-1), 1.0, rtol=1e-13)
+    cos = np.sum(out * v, axis=-1) / np.sqrt(np.sum(out * out, axis=-1) * np.sum(v * v, axis=-1))
+    np.testing.assert_allclose(cos, 1.0, rtol=1e-13)
+
+
+def test_bcnorm_constant_vector_closed_form():
+    """A constant vector c: c / sqrt(c^2 + eps) in every channel.  c = 0.5,
+    eps = 0.25 gives 0.5 / sqrt(0.5) = 1 / sqrt(2); eps added outside the
+    root (c / (|c| + eps) = 2/3) or to the root mean (c / (sqrt(c^2) + eps))
+    would not."""
+    out = oracle.rms_norm(np.full((1, 8), 0.5), eps=0.25)
+    np.testing.assert_allclose(out, 1.0 / math.sqrt(2.0), rtol=1e-15)
+    out = oracle.rms_norm(np.full((1, 8), -3.0), eps=0.0)
+    np.testing.assert_array_equal(out, -1.0)
+
+
+def test_bcnorm_scale_invariance_and_oddness():
+    """Without eps the norm does not see the scale: f(k v) = f(v), k > 0, and
+    f(-v) = -f(v)."""
+    rng = np.random.default_rng(21)
+    v = rng.standard_normal((6, 32))
+    f = oracle.rms_norm(v, eps=0.0)
+    np.testing.assert_allclose(oracle.rms_norm(7.25 * v, eps=0.0), f, rtol=1e-14)
+    np.testing.assert_allclose(oracle.rms_norm(-v, eps=0.0), -f, rtol=1e-14)
+
+
+def test_bcnorm_gain_then_bias_after_norm():
+    """Gain multiplies the normalised channels and the bias is added after
+    the norm: (out - bias) / gain has unit mean square whatever the bias (a
+    bias added before the norm changes it), and a worked example: v = (3, 4)
+    has RMS sqrt(12.5); gain (2, 1), bias (1, -1) give (2*3/sqrt(12.5) + 1,
+    4/sqrt(12.5) - 1)."""
+    rng = np.random.default_rng(22)
+    v = rng.standard_normal((4, 2, 16))
+    gain = rng.uniform(0.5, 2.0, (2, 16))
+    bias = rng.standard_normal((2, 16)) + 1.0
+    out = oracle.rms_norm(v, gain=gain, bias=bias, eps=0.0)
+    np.testing.assert_allclose(np.mean(((out - bias) / gain) ** 2, axis=-1), 1.0, rtol=1e-13)
+    got = oracle.rms_norm(np.array([3.0, 4.0]), gain=np.array([2.0, 1.0]),
+                          bias=np.array([1.0, -1.0]), eps=0.0)
+    r = math.sqrt(12.5)
+    np.testing.assert_allclose(got, [6.0 / r + 1.0, 4.0 / r - 1.0], rtol=1e-15)
+    np.testing.assert_array_equal(oracle.add_bias(v, bias), v + bias)
+
+
+def test_structured_input_worked_example():
+    """X_t[r, p] = W[r, p] X'_t[p]: W[2, 3] = 7 and X'_t[3] = 2 give 14 at
+    (t, r=2, p=3) and W[0, 3] X'_t[3] at r = 0; R != P so a transposed W
+    fails on shape or value."""
+    S, L, R, P = 1, 2, 3, 5
+    xp = np.zeros((S, L, P))
+    xp[0, 1, 3] = 2.0
+    xp[0, 0, 1] = -1.5
+    w = np.arange(R * P, dtype=float).reshape(1, R, P)
+    w[0, 2, 3] = 7.0
+    X = oracle.structured_input(xp, w)
+    assert X.shape == (S, L, R, P)
+    assert X[0, 1, 2, 3] == 14.0
+    assert X[0, 1, 0, 3] == 2.0 * 3.0          # W[0, 3] = 3
+    assert X[0, 0, 1, 1] == -1.5 * 6.0         # W[1, 1] = 6
+    assert np.count_nonzero(X[0, 1]) == R and np.count_nonzero(X[0, 0]) == R
+
+
+def test_structured_input_feeds_rank_columns(oracle_lib):
+    """With W rows c_r (constants per rank) the MIMO layer's input columns
+    are c_r X': by linearity in X (Sec. 3.3), the output of the scan on the
+    structured input equals sum_r c_r times the scan with X' in column r
+    alone (D = 0)."""
+    rng = np.random.default_rng(23)
+    R, P = 3, 4
+    s = tiny_slice(rng, 21, 8, P, R)
+    s["D"] = 0.0
+    xp = rng.standard_normal((1, 21, P))
+    c = np.array([0.5, -2.0, 1.25])
+    w = np.repeat(c[:, None], P, axis=1)[None]
+    y, *_ = run1(dict(s, x=oracle.structured_input(xp, w)[0]))
+    ref = np.zeros_like(y)
+    for r in range(R):
+        xr = np.zeros((21, R, P))
+        xr[:, r, :] = xp[0]
+        ref += c[r] * run1(dict(s, x=xr))[0]
+    assert np.max(np.abs(y - ref)) <= 1e-12 * np.max(np.abs(ref))
