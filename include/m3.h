@@ -261,6 +261,75 @@ m3_status m3_step_gated(const m3_dims *dims,
                         void *y_t, void *stream);
 
 /*
+ * The block prologue: the cheap per-token operations of the Mamba-3 block
+ * that turn the projections' outputs into the SSM's B, C, X (and the gate's
+ * Z), fused into the kernels' input loads so that no separate pass over
+ * them touches HBM.
+ *   - BCNorm (Sec. 3.4, paragraph "BC / QK Normalization"): with bc_norm,
+ *     every rank column of B and C (dstate values of one token, head and
+ *     rank) is divided by sqrt(mean of its squares + eps) and multiplied
+ *     elementwise by the gain norm_B / norm_C [nheads][rank][dstate] (NULL:
+ *     ones).  eps must be > 0 with bc_norm; the gains need bc_norm.
+ *   - B, C biases (Sec. 3.4, paragraph "B, C Biases"; App. "B, C Bias
+ *     Parameterization"): head-specific, channel-wise bias_B / bias_C
+ *     [nheads][rank][dstate] added after the norm (NULL: none; allowed
+ *     without bc_norm).
+ *   - Structured MIMO input (App. "MIMO for Mamba-3", paragraph "Mamba with
+ *     MIMO"): with w_x [nheads][rank][headdim], x holds X'
+ *     [..][nheads][headdim] (one headdim-vector per token and head) and the
+ *     recurrence uses X[r][p] = w_x[h][r][p] X'[p] (rounded to the io dtype);
+ *     w_z does the same for the gate input z (Z = w_z o Z'), and needs z.
+ * All tables are fp32 device arrays, 16-byte aligned.  The norm, gain and
+ * bias are evaluated in fp32.  The carry written (and read back as
+ * init_carry) holds the B and X that the recurrence used, after the
+ * prologue.
+ */
+typedef struct {
+    int32_t bc_norm;                  /* nonzero: RMS-normalise B and C columns  */
+    float eps;                        /* > 0 when bc_norm                         */
+    const float *norm_B, *norm_C;     /* gains [nheads][rank][dstate] or NULL     */
+    const float *bias_B, *bias_C;     /* biases [nheads][rank][dstate] or NULL    */
+    const float *w_x;                 /* [nheads][rank][headdim] or NULL          */
+    const float *w_z;                 /* [nheads][rank][headdim] or NULL          */
+} m3_prologue;
+
+/*
+ * m3_scan_fwd (m3_scan_fwd_gated when z is not NULL) with the block
+ * prologue `pro` (not NULL) applied to B, C, x and z as they are read.  x
+ * (and z with w_z) is [batch][seqlen][nheads][headdim] when w_x (w_z) is
+ * given, else as in m3_scan_fwd.  Runs the one-chunk-per-workgroup
+ * single-pass kernel (M3_SCAN_PER_CHUNK; the workspace is sized by
+ * m3_scan_workspace_bytes(dims) as usual).  Supported shapes: io bf16,
+ * dstate 128, headdim 64, rank 1/2/4 and chunk 32/64/128 with chunk*rank a
+ * multiple of 64 and at most 512 (else M3_ERR_UNSUPPORTED, also with
+ * M3_SCAN_SPLIT).  Errors as m3_scan_fwd; M3_ERR_NULL for a NULL pro, or
+ * w_z without z; M3_ERR_SHAPE for bc_norm with eps <= 0 (or NaN) and for
+ * gains without bc_norm; M3_ERR_ALIGN for a misaligned table.
+ */
+m3_status m3_scan_fwd_pro(const m3_dims *dims, const m3_prologue *pro,
+                          const void *x, const void *B, const void *C,
+                          const float *dt, const float *A, const float *lambda,
+                          const float *theta, const float *D, const void *z,
+                          const float *init_state, const void *init_carryB,
+                          const void *init_carryX,
+                          void *y, float *final_state, void *carryB, void *carryX,
+                          void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * m3_step (m3_step_gated when z_t is not NULL) with the block prologue:
+ * B_t and C_t normalised, biased; x_t (z_t) is [batch][nheads][headdim]
+ * when w_x (w_z) is given.  The new carry holds the prologue's B_t and X_t.
+ * Supported shapes: io bf16, dstate 128, headdim 64, rank 1/2/4.  Errors as
+ * m3_step and m3_scan_fwd_pro.
+ */
+m3_status m3_step_pro(const m3_dims *dims, const m3_prologue *pro,
+                      float *state, void *carryB, void *carryX,
+                      const void *x_t, const void *B_t, const void *C_t,
+                      const float *dt_t, const float *A, const float *lambda_t,
+                      const float *theta_t, const float *D, const void *z_t,
+                      void *y_t, void *stream);
+
+/*
  * For callers that cannot allocate device memory (code under HIP graph
  * capture, serving loops, harnesses that forbid hipMalloc): m3_scan_fwd
  * without a workspace argument.  The workspace is a library-owned device

@@ -40,6 +40,25 @@ ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N
 static bool aligned16(const void *p) { return p == nullptr || ((uintptr_t)p & 15u) == 0; }
 static bool aligned4(const void *p) { return p == nullptr || ((uintptr_t)p & 3u) == 0; }
 
+// Checks a block prologue and converts it (pro may be null: none).
+static m3_status check_prologue(const m3_prologue *pro, bool have_z, Prologue *out) {
+    *out = Prologue{};
+    if (!pro) return M3_OK;
+    if (pro->bc_norm && !(pro->eps > 0.f)) return M3_ERR_SHAPE;   // (also NaN)
+    if (!pro->bc_norm && (pro->norm_B || pro->norm_C)) return M3_ERR_SHAPE;
+    if (pro->w_z && !have_z) return M3_ERR_NULL;
+    const void *tabs[] = {pro->norm_B, pro->norm_C, pro->bias_B, pro->bias_C, pro->w_x, pro->w_z};
+    for (const void *p : tabs)
+        if (!aligned16(p)) return M3_ERR_ALIGN;
+    out->on = 1;
+    out->bcnorm = pro->bc_norm ? 1 : 0;
+    out->eps = pro->eps;
+    out->gB = pro->norm_B; out->gC = pro->norm_C;
+    out->bB = pro->bias_B; out->bC = pro->bias_C;
+    out->wx = pro->w_x; out->wz = pro->w_z;
+    return M3_OK;
+}
+
 static int io_bytes_of(int32_t io) { return io == M3_F32 ? 4 : io == M3_BF16 ? 2 : 0; }
 
 // Sizes shared by both entry points.  Limits keep every element offset and
@@ -121,11 +140,24 @@ static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const 
                           const float *init_state, const void *init_carryB,
                           const void *init_carryX, void *y, float *final_state, void *carryB,
                           void *carryX, void *workspace, size_t workspace_bytes, void *stream,
-                          bool dry_run = false) {
+                          bool dry_run = false, const m3_prologue *pro = nullptr) {
     ScanImpl impl;
     int64_t nc = 0;
     m3_status s = check_scan_dims(d, &impl, &nc);
     if (s != M3_OK) return s;
+    Prologue pr;
+    s = check_prologue(pro, gated, &pr);
+    if (s != M3_OK) return s;
+    if (pr.on) {   // the block prologue runs in the per-chunk kernel (same workspace layout)
+        scan_launch_fn f = (d->flags & M3_SCAN_SPLIT) ? nullptr
+                                                      : find_fused_pro_impl(d->io, d->dstate, d->headdim,
+                                                                            d->rank, d->chunk);
+        if (!f) return M3_ERR_UNSUPPORTED;
+        if (nc > 0) {
+            if (!impl.fused) return M3_ERR_UNSUPPORTED;
+            impl.launch = f;
+        }
+    }
     // token arrays may be NULL only for an empty sequence (empty tensors)
     const bool tok_ok = d->seqlen == 0 || (x && B && C && dt && lambda && theta && y && (z || !gated));
     if (!tok_ok || !A || !D || !final_state || !carryB || !carryX) return M3_ERR_NULL;
@@ -168,6 +200,7 @@ static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const 
     a.a_sb = d->a_stride_b; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
     a.G = d->seg_chunks; a.nseg = 0; a.per_chunk = impl.per_chunk;
     a.spin_max = g_spin_max.load(std::memory_order_relaxed);
+    a.pro = pr;
     const hipError_t e = impl.launch(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) {
         g_last_hip_error = (int)e;
@@ -184,6 +217,19 @@ extern "C" m3_status m3_scan_fwd(const m3_dims *d, const void *x, const void *B,
                                  size_t workspace_bytes, void *stream) {
     return scan_fwd(d, x, B, C, dt, A, lambda, theta, D, false, nullptr, init_state, init_carryB,
                     init_carryX, y, final_state, carryB, carryX, workspace, workspace_bytes, stream);
+}
+
+extern "C" m3_status m3_scan_fwd_pro(const m3_dims *d, const m3_prologue *pro, const void *x,
+                                     const void *B, const void *C, const float *dt, const float *A,
+                                     const float *lambda, const float *theta, const float *D,
+                                     const void *z, const float *init_state,
+                                     const void *init_carryB, const void *init_carryX, void *y,
+                                     float *final_state, void *carryB, void *carryX,
+                                     void *workspace, size_t workspace_bytes, void *stream) {
+    if (!pro) return M3_ERR_NULL;
+    return scan_fwd(d, x, B, C, dt, A, lambda, theta, D, z != nullptr, z, init_state, init_carryB,
+                    init_carryX, y, final_state, carryB, carryX, workspace, workspace_bytes, stream,
+                    false, pro);
 }
 
 extern "C" m3_status m3_scan_fwd_gated(const m3_dims *d, const void *x, const void *B,
@@ -271,10 +317,15 @@ extern "C" m3_status m3_scan_fwd_varlen(const m3_dims *d, const int64_t *cu_seql
 static m3_status step(const m3_dims *d, float *state, void *carryB, void *carryX,
                       const void *x_t, const void *B_t, const void *C_t, const float *dt_t,
                       const float *A, const float *lambda_t, const float *theta_t, const float *D,
-                      bool gated, const void *z_t, void *y_t, void *stream) {
+                      bool gated, const void *z_t, void *y_t, void *stream,
+                      const m3_prologue *pro = nullptr) {
     m3_status s = check_dims_common(d);
     if (s != M3_OK) return s;
-    step_launch_fn fn = find_step_impl(d->io, d->dstate, d->headdim, d->rank);
+    Prologue pr;
+    s = check_prologue(pro, gated, &pr);
+    if (s != M3_OK) return s;
+    step_launch_fn fn = pr.on ? find_step_pro_impl(d->io, d->dstate, d->headdim, d->rank)
+                              : find_step_impl(d->io, d->dstate, d->headdim, d->rank);
     if (!fn) return M3_ERR_UNSUPPORTED;
     if (!state || !carryB || !carryX || !x_t || !B_t || !C_t || !dt_t || !A || !lambda_t ||
         !theta_t || !D || !y_t || (gated && !z_t))
@@ -294,6 +345,7 @@ static m3_status step(const m3_dims *d, float *state, void *carryB, void *carryX
     a.theta_ph = (d->flags & M3_THETA_PER_HEAD) ? 1 : 0;
     a.batch = d->batch; a.H = d->nheads;
     a.a_sb = d->a_stride_b; a.a_sh = d->a_stride_h;
+    a.pro = pr;
     const hipError_t e = fn(a, static_cast<hipStream_t>(stream));
     if (e != hipSuccess) {
         g_last_hip_error = (int)e;
@@ -308,6 +360,16 @@ extern "C" m3_status m3_step(const m3_dims *d, float *state, void *carryB, void 
                              const float *theta_t, const float *D, void *y_t, void *stream) {
     return step(d, state, carryB, carryX, x_t, B_t, C_t, dt_t, A, lambda_t, theta_t, D, false,
                 nullptr, y_t, stream);
+}
+
+extern "C" m3_status m3_step_pro(const m3_dims *d, const m3_prologue *pro, float *state,
+                                 void *carryB, void *carryX, const void *x_t, const void *B_t,
+                                 const void *C_t, const float *dt_t, const float *A,
+                                 const float *lambda_t, const float *theta_t, const float *D,
+                                 const void *z_t, void *y_t, void *stream) {
+    if (!pro) return M3_ERR_NULL;
+    return step(d, state, carryB, carryX, x_t, B_t, C_t, dt_t, A, lambda_t, theta_t, D,
+                z_t != nullptr, z_t, y_t, stream, pro);
 }
 
 extern "C" m3_status m3_step_gated(const m3_dims *d, float *state, void *carryB, void *carryX,

@@ -23,7 +23,10 @@ template <typename T> struct Vec8;
 template <> struct Vec8<bf16> { typedef bf16x8 type; static constexpr int n = 8; };
 template <> struct Vec8<float> { typedef f32x4 type; static constexpr int n = 4; };
 
-template <typename T, int N, int P, int R, int NT, bool kGate>
+// kPro: the block prologue on the step's inputs (B_t and C_t: RMS norm over
+// N, gain, bias; x_t and z_t: X = W_X o X', Z = W_Z o Z'); the new carry
+// holds the B_t and X_t that the recurrence used.
+template <typename T, int N, int P, int R, int NT, bool kGate, bool kPro>
 __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     constexpr int NH = N / 2;
     constexpr int TX = P / 4;                   // threads across columns (float4 each)
@@ -51,7 +54,8 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     // per-slice vectors into LDS
     const T *Bt = static_cast<const T *>(a.B) + bh * (R * N);
     const T *Ct = static_cast<const T *>(a.C) + bh * (R * N);
-    const T *Xt = static_cast<const T *>(a.x) + bh * (R * P);
+    const bool sx = kPro && a.pro.wx != nullptr, sz = kPro && a.pro.wz != nullptr;
+    const T *Xt = static_cast<const T *>(a.x) + bh * (sx ? P : R * P);
     T *cB = static_cast<T *>(a.cB) + bh * (R * N);
     T *cX = static_cast<T *>(a.cX) + bh * (R * P);
     const float dtv = a.dt[bh], lamv = a.lam[bh], Av = a.A[b * a.a_sb + h * a.a_sh];
@@ -75,7 +79,8 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
 #pragma unroll
     for (int k = 0; k < TPX; ++k) {
         const int pc = min(tid + k * NT, PX - 1);
-        vx[k] = *reinterpret_cast<const V8 *>(Xt + pc * VE);
+        // (structured input: piece pc of rank row r reads X' at its column)
+        vx[k] = *reinterpret_cast<const V8 *>(Xt + (sx ? (pc * VE) % P : pc * VE));
         vxp[k] = *reinterpret_cast<const V8 *>(cX + pc * VE);
     }
     // per-step angles, or dt * omega with the head's frequencies omega
@@ -85,9 +90,18 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     constexpr int TZ = (R * P + NT - 1) / NT;
     float zv[TZ];
     if constexpr (kGate) {
-        const T *Zt = static_cast<const T *>(a.z) + bh * (R * P);
+        if (sz) {   // structured gate input: Z = W_Z o Z' (Z' [batch][nheads][headdim])
+            const T *Zp = static_cast<const T *>(a.z) + bh * P;
 #pragma unroll
-        for (int k = 0; k < TZ; ++k) zv[k] = to_f32(Zt[min(tid + k * NT, R * P - 1)]);
+            for (int k = 0; k < TZ; ++k) {
+                const int e = min(tid + k * NT, R * P - 1);
+                zv[k] = to_f32(Zp[e % P]) * a.pro.wz[h * (R * P) + e];
+            }
+        } else {
+            const T *Zt = static_cast<const T *>(a.z) + bh * (R * P);
+#pragma unroll
+            for (int k = 0; k < TZ; ++k) zv[k] = to_f32(Zt[min(tid + k * NT, R * P - 1)]);
+        }
     }
     // 1. the state: the bytes that matter
     float *st = a.state + bh * (int64_t)(N * P);
@@ -102,6 +116,42 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     }
     const float alpha = (float)exp_fast((typename AccOf<T>::type)dtv * Av);
     const float bprev = (1.f - lamv) * dtv, gam = lamv * dtv;
+    if constexpr (kPro) {
+        // B_t, C_t: a rank row's N / VE pieces are consecutive threads of one
+        // wave, so its sum of squares is a lane sum; then gain and bias
+        static_assert(kWave % (N / VE) == 0 && PB <= NT, "a row's pieces in one wave");
+        const int pc = min(tid, PB - 1), r = (pc * VE) / N, n0 = (pc * VE) % N;
+        float sb = 0.f, sc = 0.f;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+            sb += to_f32(vb[0][e]) * to_f32(vb[0][e]);
+            sc += to_f32(vc[0][e]) * to_f32(vc[0][e]);
+        }
+#pragma unroll
+        for (int o = 1; o < N / VE; o <<= 1) {
+            sb += __shfl_xor(sb, o, kWave);
+            sc += __shfl_xor(sc, o, kWave);
+        }
+        const float kb = a.pro.bcnorm ? rsqrtf(sb * (1.f / N) + a.pro.eps) : 1.f;
+        const float kc = a.pro.bcnorm ? rsqrtf(sc * (1.f / N) + a.pro.eps) : 1.f;
+        const int64_t hb = h * (R * N) + r * N + n0;
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+            const float gb = a.pro.gB ? a.pro.gB[hb + e] : 1.f, bb = a.pro.bB ? a.pro.bB[hb + e] : 0.f;
+            const float gc = a.pro.gC ? a.pro.gC[hb + e] : 1.f, bc = a.pro.bC ? a.pro.bC[hb + e] : 0.f;
+            vb[0][e] = from_f32<T>(kb * gb * to_f32(vb[0][e]) + bb);
+            vc[0][e] = from_f32<T>(kc * gc * to_f32(vc[0][e]) + bc);
+        }
+        if (sx) {   // X = W_X o X' (rounded to the io dtype, as a stored x would be)
+#pragma unroll
+            for (int k = 0; k < TPX; ++k) {
+                const int px = min(tid + k * NT, PX - 1);
+#pragma unroll
+                for (int e = 0; e < VE; ++e)
+                    vx[k][e] = from_f32<T>(to_f32(vx[k][e]) * a.pro.wx[h * (R * P) + px * VE + e]);
+            }
+        }
+    }
 #pragma unroll
     for (int k = 0; k < TPB; ++k) {
         const int pc = tid + k * NT;
@@ -240,14 +290,14 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
 // threads per slice measured slower: longer per-thread update chains).
 template <int N, int P> struct StepThreads { static constexpr int value = N * P >= 8192 ? 256 : 64; };
 
-template <typename T, int N, int P, int R>
+template <typename T, int N, int P, int R, bool kPro = false>
 hipError_t launch_step(const StepArgs &a, hipStream_t stream) {
     constexpr int NT = StepThreads<N, P>::value;
     if (a.z)
-        hipLaunchKernelGGL((k_step<T, N, P, R, NT, true>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
+        hipLaunchKernelGGL((k_step<T, N, P, R, NT, true, kPro>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
                            stream, a);
     else
-        hipLaunchKernelGGL((k_step<T, N, P, R, NT, false>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
+        hipLaunchKernelGGL((k_step<T, N, P, R, NT, false, kPro>), dim3((unsigned)(a.batch * a.H)), dim3(NT), 0,
                            stream, a);
     return hipGetLastError();
 }
@@ -270,6 +320,15 @@ step_launch_fn find_step_impl(int io, int64_t N, int64_t P, int64_t R) {
     if (io == IO && N == N_ && P == P_ && R == R_) return &launch_step<T, N_, P_, R_>;
     M3_STEP_SHAPES(M3_CASE)
 #undef M3_CASE
+    return nullptr;
+}
+
+// The block prologue is built into the bf16 step kernels.
+step_launch_fn find_step_pro_impl(int io, int64_t N, int64_t P, int64_t R) {
+    if (io != 1 || N != 128 || P != 64) return nullptr;
+    if (R == 1) return &launch_step<bf16, 128, 64, 1, true>;
+    if (R == 2) return &launch_step<bf16, 128, 64, 2, true>;
+    if (R == 4) return &launch_step<bf16, 128, 64, 4, true>;
     return nullptr;
 }
 

@@ -7,6 +7,17 @@
 
 namespace m3 {
 
+// The block prologue fused into the input loads (active when `on`): B and
+// C columns RMS-normalised over N when `bcnorm` (gain gB / gC [H][R][N] or
+// null for ones), then the biases bB / bC [H][R][N] (null: zeros); x (and z)
+// hold X' (Z') [.., H, P] and X = wx o X' (Z = wz o Z'), wx / wz [H][R][P],
+// when those pointers are set.
+struct Prologue {
+    int on, bcnorm;
+    float eps;
+    const float *gB, *gC, *bB, *bC, *wx, *wz;
+};
+
 // Arguments of one prefill scan, already validated by the front end.
 struct ScanArgs {
     const void *x, *B, *C;
@@ -39,6 +50,7 @@ struct ScanArgs {
     // polls of a look-back wait before it gives up (counts a timeout in
     // ctl[1] and makes the entering state NaN)
     uint32_t spin_max;
+    Prologue pro;
 };
 
 struct StepArgs {
@@ -51,6 +63,7 @@ struct StepArgs {
     int theta_ph;                       // theta holds omega [H][N/2] (angle dt * omega)
     int64_t batch, H;
     int64_t a_sb, a_sh;
+    Prologue pro;
 };
 
 // default bound of a look-back wait (polls; ~seconds), then an error count
@@ -73,6 +86,9 @@ scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t 
 scan_launch_fn find_seg_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 // warp-specialised kernel for one segment per slice (null: none for the shape)
 scan_launch_fn find_ws_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+// kernels built with the block prologue (null: none for the shape)
+scan_launch_fn find_fused_pro_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+step_launch_fn find_step_pro_impl(int io, int64_t N, int64_t P, int64_t R);
 
 // Control words of the single-pass scans (start of their workspace): ctl[0]
 // the ticket counter, ctl[1] the count of look-back waits that timed out, and

@@ -84,6 +84,23 @@ __device__ __forceinline__ void fset(float &v, int, float x) { v = x; }
 __device__ __forceinline__ float fget(const f32x4 &v, int e) { return v[e]; }
 __device__ __forceinline__ void fset(f32x4 &v, int e, float x) { v[e] = x; }
 
+// Sum of squares of a 16-byte vector, accumulated in fp32 straight from the
+// packed elements (v_dot2_f32_bf16 for bf16: no unpacked copy of the
+// vector is formed, so nothing extra stays live until the values are used).
+__device__ __forceinline__ float sumsq(const bf16x8 &v) {
+    typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+    float s = 0.f;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const bf16x2 p = {v[2 * q], v[2 * q + 1]};
+        s = __builtin_amdgcn_fdot2_f32_bf16(p, p, s, false);
+    }
+    return s;
+}
+__device__ __forceinline__ float sumsq(const f32x4 &v) {
+    return v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
+}
+
 // Look-back traffic uses device-scope atomic accesses only (the sc1 scope
 // bit): they are coherent across the XCDs' L2 caches by themselves, so no
 // cache-wide write-back or invalidate is needed.  A publisher waits until its

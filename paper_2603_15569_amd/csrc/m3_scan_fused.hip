@@ -49,10 +49,13 @@ namespace {
 
 using namespace scan;
 
-template <typename T, int Q, int R, bool kGate>
+template <typename T, int Q, int R, bool kGate, bool kPro>
 // Two waves per SIMD: two 4-wave workgroups or one 8-wave workgroup per CU
 // (more waves spill the tile registers of the output phase).  kGate: the
-// stored y is multiplied by SiLU(z) (the block's output gate).
+// stored y is multiplied by SiLU(z) (the block's output gate).  kPro: the
+// block prologue is applied as the rows arrive (B and C: RMS norm over N,
+// gain, bias; x and z: X = W_X o X', Z = W_Z o Z'), from per-head tables in
+// LDS.
 __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2)
 void k_scan_fused(ScanArgs a) {
     typedef FShape<T, Q, R> S;
@@ -90,6 +93,11 @@ void k_scan_fused(ScanArgs a) {
     __shared__ __attribute__((aligned(16))) T s_XW[2 * NBUF * kSXr];  // x blocks, then W x blocks [row][p]
     __shared__ __attribute__((aligned(16))) T s_S[P * S::LDN];        // S_in^T [p][n] (io dtype)
     __shared__ int s_i[4];
+    // block prologue tables of the head (fp32): B gain, B bias, C gain, C bias
+    // [R][N], then W_X, W_Z [R][P] (ones / zeros where not given)
+    constexpr int kPB = 0, kPBb = R * N, kPC = 2 * R * N, kPCb = 3 * R * N, kPWX = 4 * R * N,
+                  kPWZ = 4 * R * N + R * P;
+    __shared__ __attribute__((aligned(16))) float s_pro[kPro ? 4 * R * N + 2 * R * P : 4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
     static_assert(P <= S::JB && NW * 16 <= 2 * NBUF * S::JB, "y staging fits in the x / W x buffers");
@@ -119,8 +127,14 @@ void k_scan_fused(ScanArgs a) {
 
     const T *Cg = static_cast<const T *>(a.C) + tok0 * (R * N);
     const T *Bg = static_cast<const T *>(a.B) + tok0 * (R * N);
-    const T *Xg = static_cast<const T *>(a.x) + tok0 * (R * P);
-    const int64_t bstr = tstr * R * N, xstr = tstr * R * P;   // token strides of B/C and x
+    const int64_t bstr = tstr * R * N, xstr = tstr * R * P;   // token strides of B/C and x (y, z)
+    // x as read: P x R per token-head, or (structured input) the P-vector X'
+    // that every rank row reads (row offset 0)
+    const bool sx = kPro && a.pro.wx != nullptr, sz = kPro && a.pro.wz != nullptr;
+    const int64_t xin_tok = sx ? (int64_t)P : (int64_t)(R * P);
+    const int xr_el = sx ? 0 : P;
+    const T *Xg = static_cast<const T *>(a.x) + tok0 * xin_tok;
+    const int64_t xin_str = tstr * xin_tok;
 
     // Rows jb*64 .. of the chunk are staged in two steps so that the global
     // loads of the next block overlap the MFMA work on this one: fetch()
@@ -138,13 +152,20 @@ void k_scan_fused(ScanArgs a) {
     // compiler's waits stop at exactly the loads a step needs, leaving later
     // prefetches in flight.
     const uint32_t bstr_b = (uint32_t)(bstr * sizeof(T)), xstr_b = (uint32_t)(xstr * sizeof(T));
+    const uint32_t xin_b = (uint32_t)(xin_str * sizeof(T));
     const Rsrc rb = make_rsrc(Bg, (uint32_t)(((nvalid - 1) * bstr + R * N) * (int64_t)sizeof(T)));
     const Rsrc rc = make_rsrc(Cg, (uint32_t)(((nvalid - 1) * bstr + R * N) * (int64_t)sizeof(T)));
-    const Rsrc rx = make_rsrc(Xg, (uint32_t)(((nvalid - 1) * xstr + R * P) * (int64_t)sizeof(T)));
+    const Rsrc rx = make_rsrc(Xg, (uint32_t)(((nvalid - 1) * xin_str + (R - 1) * xr_el + P) * (int64_t)sizeof(T)));
+    // B row pieces: consecutive lanes take consecutive rows (conflict-free
+    // cos/sin reads); with the prologue the NH / CE pieces of a row sit in
+    // consecutive lanes of one wave instead, so that its norm is a lane sum.
+    constexpr int BPR = NH / S::CE;   // 16-byte pieces per half row
+    auto brow = [](int task) { return kPro ? task / BPR : task % S::JB; };
+    auto bpiece = [](int task) { return kPro ? task % BPR : task / S::JB; };
     auto fetch = [&](int jb, Blk &f) {
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
-            const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
+            const int task = tid + k * S::NTHR, jr = brow(task), cp = bpiece(task);
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
             const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + cp * S::CE) * sizeof(T));
             f.lo[k] = buf_load<V16>(rb, off);
@@ -154,7 +175,7 @@ void k_scan_fused(ScanArgs a) {
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
             const int row = jb * S::JB + jr, t = row / R, r = row % R;
-            f.xv[k] = buf_load<V16>(rx, tok_off(t, xstr_b) + (uint32_t)((r * P + pc * S::CE) * sizeof(T)));
+            f.xv[k] = buf_load<V16>(rx, tok_off(t, xin_b) + (uint32_t)((r * xr_el + pc * S::CE) * sizeof(T)));
         }
     };
     // kAgg: stage W x too (operand of M); kOut: stage x too (operand of y)
@@ -162,14 +183,32 @@ void k_scan_fused(ScanArgs a) {
         T *sB = s_B + (jb % NBUF) * kSB, *sX = s_XW + (jb % NBUF) * kSXr, *sWX = s_XW + (NBUF + jb % NBUF) * kSXr;
 #pragma unroll
         for (int k = 0; k < TB; ++k) {
-            const int task = tid + k * S::NTHR, jr = task % S::JB, cp = task / S::JB;
+            const int task = tid + k * S::NTHR, jr = brow(task), cp = bpiece(task);
             const int t = (jb * S::JB + jr) / R;
             V16 lo = f.lo[k], hi = f.hi[k];
             float csv[S::CE], snv[S::CE];
             cs_getn<S::CE>(&s_cs[t * LDT + cp * S::CE], csv, snv);
+            float sc = 1.f, bsc = 1.f;
+            int pb = 0;
+            if constexpr (kPro) {   // B = g o B' / rms(B') + b (rows past the end stay zero)
+                float ss = sumsq(lo) + sumsq(hi);
+#pragma unroll
+                for (int o = 1; o < BPR; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+                const bool ok = t < nvalid;
+                sc = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
+                bsc = ok ? 1.f : 0.f;
+                pb = ((jb * S::JB + jr) % R) * N + cp * S::CE;
+                // (opaque per block: table reads that do not depend on the
+                // block are not hoisted out of the block loop and held)
+                asm volatile("" : "+v"(pb));
+            }
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
-                const float u = fget(lo, e), w = fget(hi, e);
+                float u = fget(lo, e), w = fget(hi, e);
+                if constexpr (kPro) {
+                    u = sc * s_pro[kPB + pb + e] * u + bsc * s_pro[kPBb + pb + e];
+                    w = sc * s_pro[kPB + pb + NH + e] * w + bsc * s_pro[kPBb + pb + NH + e];
+                }
                 fset(lo, e, csv[e] * u + snv[e] * w);
                 fset(hi, e, csv[e] * w - snv[e] * u);
             }
@@ -179,12 +218,19 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
         for (int k = 0; k < TX; ++k) {
             const int task = tid + k * S::NTHR, jr = task % S::JB, pc = task / S::JB;
-            if constexpr (decltype(kOut)::value) *reinterpret_cast<V16 *>(&sX[jr * LDP + pc * S::CE]) = f.xv[k];
+            V16 xv = f.xv[k];
+            if constexpr (kPro) {   // X = W_X o X' (ones without structured input)
+                int pw = kPWX + ((jb * S::JB + jr) % R) * P + pc * S::CE;
+                asm volatile("" : "+v"(pw));
+#pragma unroll
+                for (int e = 0; e < S::CE; ++e) fset(xv, e, fget(xv, e) * s_pro[pw + e]);
+            }
+            if constexpr (decltype(kOut)::value) *reinterpret_cast<V16 *>(&sX[jr * LDP + pc * S::CE]) = xv;
             if constexpr (decltype(kAgg)::value) {
                 const float wt = s_w[(jb * S::JB + jr) / R];
                 V16 wx;
 #pragma unroll
-                for (int e = 0; e < S::CE; ++e) fset(wx, e, wt * fget(f.xv[k], e));
+                for (int e = 0; e < S::CE; ++e) fset(wx, e, wt * fget(xv, e));
                 *reinterpret_cast<V16 *>(&sWX[jr * LDP + pc * S::CE]) = wx;
             }
         }
@@ -209,6 +255,19 @@ void k_scan_fused(ScanArgs a) {
         }
     };
     // ---- 2. prologue ----
+    if constexpr (kPro) {   // the head's prologue tables (read after the prologue's barriers)
+        const int64_t hn = h * (R * N), hp = h * (R * P);
+        for (int e = tid; e < R * N; e += S::NTHR) {
+            s_pro[kPB + e] = a.pro.gB ? a.pro.gB[hn + e] : 1.f;
+            s_pro[kPBb + e] = a.pro.bB ? a.pro.bB[hn + e] : 0.f;
+            s_pro[kPC + e] = a.pro.gC ? a.pro.gC[hn + e] : 1.f;
+            s_pro[kPCb + e] = a.pro.bC ? a.pro.bC[hn + e] : 0.f;
+        }
+        for (int e = tid; e < R * P; e += S::NTHR) {
+            s_pro[kPWX + e] = a.pro.wx ? a.pro.wx[hp + e] : 1.f;
+            s_pro[kPWZ + e] = a.pro.wz ? a.pro.wz[hp + e] : 1.f;
+        }
+    }
     {
         // angles first (the largest prologue load): thread (pair i, segment seg)
         const int i = tid % NH, seg = tid / NH;
@@ -306,7 +365,28 @@ void k_scan_fused(ScanArgs a) {
     auto rotate_cf = [&]() {
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
-            const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
+            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R;
+            if constexpr (kPro) {   // C = g o C' / rms(C') + b: a row sits in lanes l16 + 16 g
+                float ss = 0.f;
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk) ss += sumsq(cf[m][kk]);
+                ss += __shfl_xor(ss, 16, kWave);
+                ss += __shfl_xor(ss, 32, kWave);
+                const bool ok = t < nvalid;
+                const float sc = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
+                const float bsc = ok ? 1.f : 0.f;
+                // (applied in place, one fragment at a time, and rounded to
+                // the operand type before the rotation: an fp32 copy of the
+                // row alongside the fragments does not fit in the registers)
+                const int pcr = kPC + (row % R) * N + MM::KPL * g;
+#pragma unroll
+                for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+                    for (int e = 0; e < MM::KPL; ++e) {
+                        const int pc = pcr + kk * MM::K + e;
+                        fset(cf[m][kk], e, sc * s_pro[pc] * fget(cf[m][kk], e) + bsc * s_pro[pc - kPC + kPCb]);
+                    }
+            }
 #pragma unroll
             for (int kk = 0; kk < NK / 2; ++kk) {
                 float csv[MM::KPL], snv[MM::KPL];
@@ -723,9 +803,25 @@ void k_scan_fused(ScanArgs a) {
             T *cX = static_cast<T *>(a.cX) + sl * (R * P);
             const int64_t kl = (b * a.L + a.L - 1) * a.H + h;
             const T *Bl = static_cast<const T *>(a.B) + kl * (R * N);
-            const T *Xl = static_cast<const T *>(a.x) + kl * (R * P);
-            for (int e = tid; e < R * N; e += S::NTHR) cB[e] = Bl[e];
-            for (int e = tid; e < R * P; e += S::NTHR) cX[e] = Xl[e];
+            const T *Xl = static_cast<const T *>(a.x) + kl * xin_tok;
+            if constexpr (kPro) {   // the carry holds the B and X the recurrence used
+                static_assert(N == 2 * kWave, "two elements of a B row per lane");
+                for (int r = wave; r < R; r += NW) {
+                    const float v0 = to_f32(Bl[r * N + lane]), v1 = to_f32(Bl[r * N + kWave + lane]);
+                    float ss = v0 * v0 + v1 * v1;
+#pragma unroll
+                    for (int o = 1; o < kWave; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+                    const float sc = a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f;
+                    const int e0 = r * N + lane, e1 = e0 + kWave;
+                    cB[e0] = from_f32<T>(sc * s_pro[kPB + e0] * v0 + s_pro[kPBb + e0]);
+                    cB[e1] = from_f32<T>(sc * s_pro[kPB + e1] * v1 + s_pro[kPBb + e1]);
+                }
+                for (int e = tid; e < R * P; e += S::NTHR)
+                    cX[e] = from_f32<T>(to_f32(Xl[sx ? e % P : e]) * s_pro[kPWX + e]);
+            } else {
+                for (int e = tid; e < R * N; e += S::NTHR) cB[e] = Bl[e];
+                for (int e = tid; e < R * P; e += S::NTHR) cX[e] = Xl[e];
+            }
         }
     }
 
@@ -755,15 +851,20 @@ void k_scan_fused(ScanArgs a) {
     static_assert(NPC * kWave == 16 * RP, "store pieces");
     V16 zp[kGate ? TPW : 1][NPC];
     if constexpr (kGate) {
-        const Rsrc rz = make_rsrc(static_cast<const T *>(a.z) + tok0 * (R * P),
-                                  (uint32_t)(((nvalid - 1) * xstr + R * P) * (int64_t)sizeof(T)));
+        // z as read: like x, or (structured) the P-vector Z' of each token
+        const int64_t zin_tok = sz ? (int64_t)P : (int64_t)(R * P);
+        const int zr_el = sz ? 0 : P;
+        const uint32_t zin_b = (uint32_t)(tstr * zin_tok * sizeof(T));
+        const Rsrc rz = make_rsrc(static_cast<const T *>(a.z) + tok0 * zin_tok,
+                                  (uint32_t)(((nvalid - 1) * tstr * zin_tok + (R - 1) * zr_el + P) *
+                                             (int64_t)sizeof(T)));
 #pragma unroll
         for (int m = 0; m < TPW; ++m)
 #pragma unroll
             for (int i = 0; i < NPC; ++i) {
                 const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * S::CE;
                 const int row = owned_tile<S>(wave, m) * 16 + rl, t = row / R, r = row % R;
-                zp[m][i] = buf_load<V16>(rz, tok_off(t, xstr_b) + (uint32_t)((r * P + col) * sizeof(T)));
+                zp[m][i] = buf_load<V16>(rz, tok_off(t, zin_b) + (uint32_t)((r * zr_el + col) * sizeof(T)));
             }
     }
     if constexpr (!kMerged) {
@@ -821,7 +922,13 @@ void k_scan_fused(ScanArgs a) {
             const int row = TT * 16 + rl, t = row / R, r = row % R;
             if (t < nvalid) {
                 V16 yv = *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
-                if constexpr (kGate) yv = gate_piece<T>(yv, zp[m][i]);
+                if constexpr (kGate && kPro) {   // Z = W_Z o Z' in fp32, then the gate
+#pragma unroll
+                    for (int e = 0; e < S::CE; ++e)
+                        fset(yv, e, fget(yv, e) * silu(fget(zp[m][i], e) * s_pro[kPWZ + r * P + col + e]));
+                } else if constexpr (kGate) {
+                    yv = gate_piece<T>(yv, zp[m][i]);
+                }
                 *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) = yv;
             }
         }
@@ -829,7 +936,7 @@ void k_scan_fused(ScanArgs a) {
     }
 }
 
-template <typename T, int Q, int R>
+template <typename T, int Q, int R, bool kPro = false>
 hipError_t launch_fused(const ScanArgs &a, hipStream_t stream) {
     typedef FShape<T, Q, R> S;
     const int64_t nsl = a.batch * a.H;
@@ -837,11 +944,11 @@ hipError_t launch_fused(const ScanArgs &a, hipStream_t stream) {
     const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);
     hipLaunchKernelGGL(k_reset, dim3(rblocks), dim3(256), 0, stream, a.ctl, a.flags, nflags);
     if (a.z)
-        hipLaunchKernelGGL((k_scan_fused<T, Q, R, true>), dim3((unsigned)(nsl * a.nchunks)), dim3(S::NTHR), 0,
-                           stream, a);
+        hipLaunchKernelGGL((k_scan_fused<T, Q, R, true, kPro>), dim3((unsigned)(nsl * a.nchunks)),
+                           dim3(S::NTHR), 0, stream, a);
     else
-        hipLaunchKernelGGL((k_scan_fused<T, Q, R, false>), dim3((unsigned)(nsl * a.nchunks)), dim3(S::NTHR), 0,
-                           stream, a);
+        hipLaunchKernelGGL((k_scan_fused<T, Q, R, false, kPro>), dim3((unsigned)(nsl * a.nchunks)),
+                           dim3(S::NTHR), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -865,6 +972,17 @@ scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t 
 #define M3_CASE(IO, T, R_, Q_) \
     if (io == IO && R == R_ && Q == Q_) return &launch_fused<T, Q_, R_>;
     M3_FUSED_SHAPES(M3_CASE)
+#undef M3_CASE
+    return nullptr;
+}
+
+// The block prologue is built into the bf16 per-chunk kernels.
+scan_launch_fn find_fused_pro_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q) {
+    if (N != 128 || P != 64 || io != 1) return nullptr;
+#define M3_CASE(R_, Q_) \
+    if (R == R_ && Q == Q_) return &launch_fused<bf16, Q_, R_, true>;
+    M3_CASE(1, 64) M3_CASE(1, 128) M3_CASE(2, 32) M3_CASE(2, 64) M3_CASE(2, 128)
+    M3_CASE(4, 32) M3_CASE(4, 64) M3_CASE(4, 128)
 #undef M3_CASE
     return nullptr;
 }

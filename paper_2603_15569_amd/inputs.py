@@ -161,3 +161,68 @@ def make_gate_input(like: torch.Tensor, seed: int) -> torch.Tensor:
     g.manual_seed(5000 + int(seed))
     z = torch.randn(tuple(like.shape), device=like.device, dtype=torch.float32, generator=g)
     return z.to(like.dtype).contiguous()
+
+
+@dataclass
+class PrologueInputs:
+    """Raw projection outputs and block parameters for the fused prologue
+    (BCNorm, B/C biases, structured MIMO input and gate)."""
+    Bp: torch.Tensor       # [B, L, H, R, N] io dtype: B before the norm
+    Cp: torch.Tensor       # [B, L, H, R, N] io dtype
+    xp: torch.Tensor       # [B, L, H, P]    io dtype: X' (one vector per token and head)
+    zp: torch.Tensor       # [B, L, H, P]    io dtype: Z'
+    gB: torch.Tensor       # [H, R, N] fp32 norm gains
+    gC: torch.Tensor
+    bB: torch.Tensor       # [H, R, N] fp32 biases
+    bC: torch.Tensor
+    wx: torch.Tensor       # [H, R, P] fp32 structured-input weights
+    wz: torch.Tensor
+
+
+def make_prologue_inputs(batch, seqlen, nheads, headdim, dstate, rank, io="bf16", seed=0,
+                         device="cpu") -> PrologueInputs:
+    """Draw the prologue's inputs (own seed 6000 + seed).  Draw order: B', C'
+    (N(0, 1) times a scale U[0.25, 4] per token, head and rank column, like
+    projection outputs of varying size), X', Z' (N(0, 1)), gains U[0.5, 1.5],
+    biases 1 + 0.25 N(0, 1) (the all-ones initialisation of App. "B, C Bias
+    Parameterization", perturbed), W_X, W_Z (N(0, 1))."""
+    g = torch.Generator(device=device)
+    g.manual_seed(6000 + int(seed))
+    f32 = dict(device=device, dtype=torch.float32, generator=g)
+    iod = TORCH_IO[io]
+    col = (batch, seqlen, nheads, rank, 1)
+    Bp = torch.randn((batch, seqlen, nheads, rank, dstate), **f32) * (torch.rand(col, **f32) * 3.75 + 0.25)
+    Cp = torch.randn((batch, seqlen, nheads, rank, dstate), **f32) * (torch.rand(col, **f32) * 3.75 + 0.25)
+    xp = torch.randn((batch, seqlen, nheads, headdim), **f32)
+    zp = torch.randn((batch, seqlen, nheads, headdim), **f32)
+    gB = torch.rand((nheads, rank, dstate), **f32) + 0.5
+    gC = torch.rand((nheads, rank, dstate), **f32) + 0.5
+    bB = 1.0 + 0.25 * torch.randn((nheads, rank, dstate), **f32)
+    bC = 1.0 + 0.25 * torch.randn((nheads, rank, dstate), **f32)
+    wx = torch.randn((nheads, rank, headdim), **f32)
+    wz = torch.randn((nheads, rank, headdim), **f32)
+    return PrologueInputs(Bp=Bp.to(iod).contiguous(), Cp=Cp.to(iod).contiguous(),
+                          xp=xp.to(iod).contiguous(), zp=zp.to(iod).contiguous(),
+                          gB=gB.contiguous(), gC=gC.contiguous(), bB=bB.contiguous(),
+                          bC=bC.contiguous(), wx=wx.contiguous(), wz=wz.contiguous())
+
+
+def make_prologue_step_inputs(pro: PrologueInputs, batch: int, step: int) -> PrologueInputs:
+    """Fresh raw token inputs (B', C' [B,H,R,N], X', Z' [B,H,P]) for decode
+    step `step` with the layer's prologue parameters; seed 7000 + step, draw
+    order B', C', X', Z'."""
+    device = pro.Bp.device
+    _, _, nheads, rank, dstate = pro.Bp.shape
+    headdim = pro.xp.shape[-1]
+    g = torch.Generator(device=device)
+    g.manual_seed(7000 + int(step))
+    f32 = dict(device=device, dtype=torch.float32, generator=g)
+    iod = pro.Bp.dtype
+    col = (batch, nheads, rank, 1)
+    Bp = torch.randn((batch, nheads, rank, dstate), **f32) * (torch.rand(col, **f32) * 3.75 + 0.25)
+    Cp = torch.randn((batch, nheads, rank, dstate), **f32) * (torch.rand(col, **f32) * 3.75 + 0.25)
+    xp = torch.randn((batch, nheads, headdim), **f32)
+    zp = torch.randn((batch, nheads, headdim), **f32)
+    return PrologueInputs(Bp=Bp.to(iod).contiguous(), Cp=Cp.to(iod).contiguous(),
+                          xp=xp.to(iod).contiguous(), zp=zp.to(iod).contiguous(),
+                          gB=pro.gB, gC=pro.gC, bB=pro.bB, bC=pro.bC, wx=pro.wx, wz=pro.wz)

@@ -33,6 +33,14 @@ class M3Dims(ctypes.Structure):
                 ("seg_chunks", ctypes.c_int64)]
 
 
+class M3Prologue(ctypes.Structure):
+    """m3_prologue: the block prologue fused into the kernels' input loads."""
+    _fields_ = [("bc_norm", ctypes.c_int32), ("eps", ctypes.c_float),
+                ("norm_B", ctypes.c_void_p), ("norm_C", ctypes.c_void_p),
+                ("bias_B", ctypes.c_void_p), ("bias_C", ctypes.c_void_p),
+                ("w_x", ctypes.c_void_p), ("w_z", ctypes.c_void_p)]
+
+
 class M3Error(RuntimeError):
     def __init__(self, status: int, msg: str):
         super().__init__(f"libm3 status {status}: {msg}")
@@ -41,7 +49,7 @@ class M3Error(RuntimeError):
 
 EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_scan_fwd_varlen",
            "m3_step", "m3_step_gated", "m3_scan_check", "m3_set_wait_limit", "m3_scan_fwd_noalloc",
-           "m3_status_string", "m3_last_hip_error")
+           "m3_scan_fwd_pro", "m3_step_pro", "m3_status_string", "m3_last_hip_error")
 SCRATCH_BYTES = 256 << 20   # M3_SCRATCH_BYTES: the allocation-free scan's fixed workspace
 _lib = None
 
@@ -68,6 +76,11 @@ def lib() -> ctypes.CDLL:
         L.m3_step.restype = ctypes.c_int
         L.m3_step_gated.argtypes = [dims_p] + [vp] * 13 + [vp]
         L.m3_step_gated.restype = ctypes.c_int
+        pro_p = ctypes.POINTER(M3Prologue)
+        L.m3_scan_fwd_pro.argtypes = [dims_p, pro_p] + [vp] * 16 + [vp, ctypes.c_size_t, vp]
+        L.m3_scan_fwd_pro.restype = ctypes.c_int
+        L.m3_step_pro.argtypes = [dims_p, pro_p] + [vp] * 13 + [vp]
+        L.m3_step_pro.restype = ctypes.c_int
         L.m3_scan_fwd_noalloc.argtypes = [dims_p] + [vp] * 15 + [vp]
         L.m3_scan_fwd_noalloc.restype = ctypes.c_int
         L.m3_scan_check.argtypes = [dims_p, vp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_uint32), vp]
@@ -295,4 +308,77 @@ def step(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, y=None, stream
         _check(lib().m3_step_gated(ctypes.byref(d), _p(state), _p(cB), _p(cX), _p(x_t), _p(B_t),
                                    _p(C_t), _p(dt_t), _p(A), _p(lam_t), _p(theta_t), _p(D), _p(z),
                                    _p(y), _stream(stream)))
+    return y
+
+
+def prologue(bc_norm: bool = False, eps: float = 1e-6, norm_B=None, norm_C=None, bias_B=None,
+             bias_C=None, w_x=None, w_z=None) -> M3Prologue:
+    """An m3_prologue over fp32 device tables: gains and biases [H,R,N],
+    w_x / w_z [H,R,P] (None: not applied)."""
+    for t in (norm_B, norm_C, bias_B, bias_C, w_x, w_z):
+        if t is not None and t.dtype != torch.float32:
+            raise ValueError("prologue tables are fp32")
+    return M3Prologue(1 if bc_norm else 0, float(eps), _p(norm_B), _p(norm_C), _p(bias_B),
+                      _p(bias_C), _p(w_x), _p(w_z))
+
+
+def scan_fwd_pro(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, pro: M3Prologue, rank: int,
+                 z=None, init_state=None, init_carry=None, out=None, workspace=None,
+                 stream=None, check: bool = False):
+    """m3_scan_fwd_pro: the scan with the block prologue `pro` applied to the
+    raw B', C' [B,L,H,R,N] and to x (X' [B,L,H,P] when pro.w_x is set, else
+    [B,L,H,R,P]) and z as they are read.  Returns y [B,L,H,R,P], the final
+    state and the carry (the prologue's B_{L-1}, X_{L-1})."""
+    batch, seqlen, nheads = x.shape[:3]
+    headdim, dstate = x.shape[-1], Bm.shape[-1]
+    if tuple(Bm.shape) != (batch, seqlen, nheads, rank, dstate):
+        raise ValueError("B must be [B, L, H, R, N]")
+    sb, st, sh = _a_strides(A, batch, seqlen, nheads)
+    flags = M3_THETA_PER_HEAD if _theta_per_head(theta, nheads, dstate) else 0
+    d = M3Dims(batch, seqlen, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags,
+               sb, st, sh, 0)
+    dev = x.device
+    if out is None:
+        y = torch.empty((batch, seqlen, nheads, rank, headdim), dtype=x.dtype, device=dev)
+        fs = torch.empty((batch, nheads, dstate, headdim), dtype=torch.float32, device=dev)
+        cB = torch.empty((batch, nheads, rank, dstate), dtype=x.dtype, device=dev)
+        cX = torch.empty((batch, nheads, rank, headdim), dtype=x.dtype, device=dev)
+    else:
+        y, fs, cB, cX = out
+    nbytes = workspace_bytes(d)
+    if workspace is None and nbytes > 0:
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+    icB, icX = (None, None) if init_carry is None else init_carry
+    wsb = workspace.numel() if workspace is not None else 0
+    _check(lib().m3_scan_fwd_pro(ctypes.byref(d), ctypes.byref(pro), _p(x), _p(Bm), _p(Cm),
+                                 _p(dt), _p(A), _p(lam), _p(theta), _p(D), _p(z),
+                                 _p(init_state), _p(icB), _p(icX), _p(y), _p(fs), _p(cB), _p(cX),
+                                 _p(workspace), wsb, _stream(stream)))
+    if check:
+        n = scan_check(d, workspace, stream)
+        if n:
+            raise LookBackTimeout(f"{n} look-back wait(s) gave up: y and the final state are invalid")
+    return y, fs, (cB, cX)
+
+
+def step_pro(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, pro: M3Prologue,
+             z=None, y=None, stream=None):
+    """m3_step_pro: one decode step with the block prologue; x_t (z) is
+    [B,H,P] when pro.w_x (pro.w_z) is set.  Returns y_t [B,H,R,P]."""
+    batch, nheads, rank, dstate = B_t.shape
+    headdim = x_t.shape[-1]
+    if A.dim() == 1 and A.shape[0] == nheads:
+        sb, sh = 0, 1
+    elif A.dim() == 2 and tuple(A.shape) == (batch, nheads):
+        sb, sh = A.stride()
+    else:
+        raise ValueError(f"A must be [H] or [B, H], got {tuple(A.shape)}")
+    flags = M3_THETA_PER_HEAD if _theta_per_head(theta_t, nheads, dstate) else 0
+    d = M3Dims(batch, 1, nheads, headdim, dstate, rank, 1, _IO[x_t.dtype], flags, sb, 0, sh, 0)
+    if y is None:
+        y = torch.empty((batch, nheads, rank, headdim), dtype=x_t.dtype, device=x_t.device)
+    cB, cX = carry
+    _check(lib().m3_step_pro(ctypes.byref(d), ctypes.byref(pro), _p(state), _p(cB), _p(cX),
+                             _p(x_t), _p(B_t), _p(C_t), _p(dt_t), _p(A), _p(lam_t), _p(theta_t),
+                             _p(D), _p(z), _p(y), _stream(stream)))
     return y

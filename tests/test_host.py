@@ -248,3 +248,51 @@ def test_noalloc_host_validation(L):
     big = dims(io=m3.M3_BF16, headdim=64, dstate=128, rank=1, chunk=64, batch=8, seqlen=4096, nheads=32)
     assert L.m3_scan_workspace_bytes(ctypes.byref(big)) > m3.SCRATCH_BYTES
     assert L.m3_scan_fwd_noalloc(ctypes.byref(big), *ptrs, None) == m3.M3_ERR_WORKSPACE
+
+
+def test_prologue_host_validation(L):
+    """m3_scan_fwd_pro / m3_step_pro: the prologue is checked on the host
+    before any launch (eps > 0 with the norm, gains only with the norm, w_z
+    only with z, aligned tables) and only the built shapes are accepted."""
+    bf = dict(io=m3.M3_BF16, headdim=64, dstate=128, rank=4, chunk=64, seqlen=300)
+
+    def pro(**kw):
+        p = dict(bc_norm=1, eps=1e-6, norm_B=None, norm_C=None, bias_B=None, bias_C=None,
+                 w_x=None, w_z=None)
+        p.update(kw)
+        return m3.M3Prologue(**p)
+
+    def scan(d, p, over=None):
+        ptrs = [FAKE] * 16       # x B C dt A lam theta D z init icB icX y fs cB cX
+        for k in (8, 9, 10, 11):
+            ptrs[k] = None
+        for k, v in (over or {}).items():
+            ptrs[k] = v
+        wsb = L.m3_scan_workspace_bytes(ctypes.byref(d))
+        return L.m3_scan_fwd_pro(ctypes.byref(d), None if p is None else ctypes.byref(p), *ptrs,
+                                 FAKE, wsb, None)
+    assert scan(dims(**bf), None) == m3.M3_ERR_NULL
+    assert scan(dims(**bf), pro(eps=0.0)) == m3.M3_ERR_SHAPE
+    assert scan(dims(**bf), pro(eps=float("nan"))) == m3.M3_ERR_SHAPE
+    assert scan(dims(**bf), pro(bc_norm=0, norm_B=FAKE)) == m3.M3_ERR_SHAPE
+    assert scan(dims(**bf), pro(w_z=FAKE)) == m3.M3_ERR_NULL          # no z
+    assert scan(dims(**bf), pro(bias_C=FAKE + 4)) == m3.M3_ERR_ALIGN
+    assert scan(dims(**bf), pro(w_x=FAKE + 8)) == m3.M3_ERR_ALIGN
+    assert scan(dims(), pro()) == m3.M3_ERR_UNSUPPORTED                # fp32: not built
+    assert scan(dims(**dict(bf, flags=m3.M3_SCAN_SPLIT)), pro()) == m3.M3_ERR_UNSUPPORTED
+    assert scan(dims(**dict(bf, chunk=48)), pro()) == m3.M3_ERR_UNSUPPORTED
+    assert scan(dims(**bf), pro(), {0: None}) == m3.M3_ERR_NULL
+
+    def step(d, p, over=None):
+        ptrs = [FAKE] * 13       # state cB cX x B C dt A lam theta D z y
+        ptrs[11] = None
+        for k, v in (over or {}).items():
+            ptrs[k] = v
+        return L.m3_step_pro(ctypes.byref(d), None if p is None else ctypes.byref(p), *ptrs, None)
+    assert step(dims(**bf), None) == m3.M3_ERR_NULL
+    assert step(dims(**bf), pro(eps=-1.0)) == m3.M3_ERR_SHAPE
+    assert step(dims(**bf), pro(w_z=FAKE)) == m3.M3_ERR_NULL
+    assert step(dims(**bf), pro(norm_C=FAKE + 12)) == m3.M3_ERR_ALIGN
+    assert step(dims(), pro()) == m3.M3_ERR_UNSUPPORTED
+    assert step(dims(**bf), pro(), {0: None}) == m3.M3_ERR_NULL
+    assert L.m3_last_hip_error() == 0
