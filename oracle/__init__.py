@@ -58,6 +58,8 @@ def _load():
         lib.m3o_scan.restype = ci
         lib.m3o_step.argtypes = [i64] * 4 + [dp] * 3 + [dp] * 8 + [dp, ci]
         lib.m3o_step.restype = ci
+        lib.m3o_scan_bwd.argtypes = [i64] * 5 + [dp] * 9 + [dp] * 2 + [dp] * 9 + [ci]
+        lib.m3o_scan_bwd.restype = ci
         _lib = lib
     return _lib
 
@@ -101,6 +103,31 @@ def scan(x, B, C, dt, A, lam, theta, D, init_state=None, init_B=None,
                             int(nthreads))
     out = (y, state, cB, cX)
     return (out, used) if return_threads else out
+
+
+def scan_bwd(x, B, C, dt, A, lam, theta, D, dy, dfinal=None, init_state=None, nthreads=0):
+    """Gradients of J = <dy, y> + <dfinal, final_state> for the scan on S
+    slices (no initial carry), by reverse mode through the sequential
+    recurrence (m3o_scan_bwd).  Shapes as scan(); dy like y, dfinal like the
+    state.  Returns a dict: dx, dB, dC, ddt, dA (per token), dlam, dtheta,
+    dD [S], dinit [S,N,P]."""
+    x, B, C = _f64(x), _f64(B), _f64(C)
+    dt, A, lam, theta, D, dy = _f64(dt), _f64(A), _f64(lam), _f64(theta), _f64(D), _f64(dy)
+    S, L, R, P = x.shape
+    N = B.shape[-1]
+    assert dy.shape == x.shape and theta.shape == (S, L, N // 2)
+    dfinal = None if dfinal is None else _f64(dfinal)
+    init_state = None if init_state is None else _f64(init_state)
+    out = dict(dx=np.empty_like(x), dB=np.empty_like(B), dC=np.empty_like(C),
+               ddt=np.empty_like(dt), dA=np.empty_like(A), dlam=np.empty_like(lam),
+               dtheta=np.empty_like(theta), dD=np.empty(S), dinit=np.empty((S, N, P)))
+    _load().m3o_scan_bwd(S, L, N, P, R, _ptr(x), _ptr(B), _ptr(C), _ptr(dt), _ptr(A),
+                         _ptr(lam), _ptr(theta), _ptr(D), _ptr(init_state), _ptr(dy),
+                         _ptr(dfinal), _ptr(out["dx"]), _ptr(out["dB"]), _ptr(out["dC"]),
+                         _ptr(out["ddt"]), _ptr(out["dA"]), _ptr(out["dlam"]),
+                         _ptr(out["dtheta"]), _ptr(out["dD"]), _ptr(out["dinit"]),
+                         int(nthreads))
+    return out
 
 
 def step(state, carryB, carryX, x, B, C, dt, A, lam, theta, D, nthreads=0):
