@@ -330,6 +330,41 @@ m3_status m3_step_pro(const m3_dims *dims, const m3_prologue *pro,
                       void *y_t, void *stream);
 
 /*
+ * Backward pass of the scan (training): the gradients of a scalar loss J
+ * with respect to every input of m3_scan_fwd, given dy = dJ/dy and
+ * dfinal_state = dJ/d(final state) (NULL: zero), for the recurrence above
+ * started from init_state (NULL: zero) with no initial carry.  It runs the
+ * chunked algorithm (Sec. 3.3 "Chunked Algorithm for MIMO SSMs") in reverse:
+ * the chunk states are recomputed, the state gradient is passed from the last
+ * chunk to the first, and each chunk's gradients are formed from its own
+ * rows with bf16 MFMA and fp32 accumulation.
+ * Outputs: dx, dB, dC shaped and typed like x, B, C (io dtype); ddt,
+ * dlambda [batch][seqlen][nheads], dtheta [batch][seqlen][nheads][dstate/2]
+ * (fp32; the gradient of the per-step angle); dD [nheads]; dA [nheads] (the
+ * sum over batch and tokens) when A is per head (a_stride_b = a_stride_t =
+ * 0), else dA [batch][seqlen][nheads] (A per token, a_stride_t != 0);
+ * dinit_state [batch][nheads][dstate][headdim] when not NULL.  Everything is
+ * overwritten.  Supported (else M3_ERR_UNSUPPORTED): io bf16, dstate 128,
+ * headdim 64, chunk * rank = 64 (rank 1 chunk 64, rank 2 chunk 32, rank 4
+ * chunk 16), no M3_THETA_PER_HEAD; A strided per head or per token.
+ * Workspace: m3_scan_bwd_workspace_bytes(dims) bytes (16-byte aligned; four
+ * fp32 N x P maps per chunk).  Token arrays may be NULL when seqlen == 0.
+ * Alignment: x, B, C, dy, dx, dB, dC, the states and the workspace 16 bytes,
+ * the rest 4 bytes (else M3_ERR_ALIGN).  Outputs must not overlap inputs.
+ * Deterministic (no atomics).  Errors as m3_scan_fwd.
+ */
+size_t m3_scan_bwd_workspace_bytes(const m3_dims *dims);
+m3_status m3_scan_bwd(const m3_dims *dims,
+                      const void *x, const void *B, const void *C,
+                      const float *dt, const float *A, const float *lambda,
+                      const float *theta, const float *D, const float *init_state,
+                      const void *dy, const float *dfinal_state,
+                      void *dx, void *dB, void *dC,
+                      float *ddt, float *dA, float *dlambda, float *dtheta, float *dD,
+                      float *dinit_state,
+                      void *workspace, size_t workspace_bytes, void *stream);
+
+/*
  * For callers that cannot allocate device memory (code under HIP graph
  * capture, serving loops, harnesses that forbid hipMalloc): m3_scan_fwd
  * without a workspace argument.  The workspace is a library-owned device

@@ -15,7 +15,8 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 OUT_DIR = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libm3.so")
-SOURCES = ["m3_api.hip", "m3_prefill.hip", "m3_scan_fused.hip", "m3_scan_seg.hip", "m3_scan_ws.hip", "m3_decode.hip"]
+SOURCES = ["m3_api.hip", "m3_prefill.hip", "m3_scan_fused.hip", "m3_scan_seg.hip", "m3_scan_ws.hip",
+           "m3_decode.hip", "m3_backward.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 

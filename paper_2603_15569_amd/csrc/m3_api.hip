@@ -381,6 +381,83 @@ extern "C" m3_status m3_step_gated(const m3_dims *d, float *state, void *carryB,
                 y_t, stream);
 }
 
+// ---------------------------------------------------------------------------
+// Backward scan
+// ---------------------------------------------------------------------------
+
+static m3_status check_bwd_dims(const m3_dims *d, bwd_launch_fn *fn, int64_t *nchunks) {
+    m3_status s = check_dims_common(d);
+    if (s != M3_OK) return s;
+    if (d->seqlen < 0 || d->chunk < 1 || d->seg_chunks < 0) return M3_ERR_SHAPE;
+    const int64_t per_tok = d->nheads * d->rank * (d->dstate > d->headdim ? d->dstate : d->headdim);
+    if (d->seqlen > (INT64_MAX / 4) / (d->batch * per_tok)) return M3_ERR_SHAPE;
+    const int64_t nc = (d->seqlen + d->chunk - 1) / d->chunk;
+    if (d->batch * d->nheads * nc > (int64_t)INT_MAX) return M3_ERR_SHAPE;
+    if (d->flags & M3_THETA_PER_HEAD) return M3_ERR_UNSUPPORTED;
+    // A per head (summed gradient) or per token (gradient per token)
+    if (!(d->a_stride_t != 0 || d->a_stride_b == 0)) return M3_ERR_UNSUPPORTED;
+    *fn = find_bwd_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
+    if (!*fn) return M3_ERR_UNSUPPORTED;
+    *nchunks = nc;
+    return M3_OK;
+}
+
+extern "C" size_t m3_scan_bwd_workspace_bytes(const m3_dims *d) {
+    bwd_launch_fn fn;
+    int64_t nc = 0;
+    if (check_bwd_dims(d, &fn, &nc) != M3_OK) return 0;
+    return bwd_workspace_layout(d->batch * d->nheads, nc, d->dstate, d->headdim).total;
+}
+
+extern "C" m3_status m3_scan_bwd(const m3_dims *d, const void *x, const void *B, const void *C,
+                                 const float *dt, const float *A, const float *lambda,
+                                 const float *theta, const float *D, const float *init_state,
+                                 const void *dy, const float *dfinal_state, void *dx, void *dB,
+                                 void *dC, float *ddt, float *dA, float *dlambda, float *dtheta,
+                                 float *dD, float *dinit_state, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
+    bwd_launch_fn fn;
+    int64_t nc = 0;
+    m3_status s = check_bwd_dims(d, &fn, &nc);
+    if (s != M3_OK) return s;
+    const bool tok_ok = d->seqlen == 0 || (x && B && C && dt && lambda && theta && dy && dx && dB &&
+                                           dC && ddt && dlambda && dtheta);
+    if (!tok_ok || !A || !D || !dA || !dD) return M3_ERR_NULL;
+    const void *vec[] = {x, B, C, dy, dx, dB, dC, init_state, dfinal_state, dinit_state, workspace};
+    for (const void *p : vec)
+        if (!aligned16(p)) return M3_ERR_ALIGN;
+    const void *scal[] = {dt, A, lambda, theta, D, ddt, dA, dlambda, dtheta, dD};
+    for (const void *p : scal)
+        if (!aligned4(p)) return M3_ERR_ALIGN;
+    const BwdWorkspaceLayout wl = bwd_workspace_layout(d->batch * d->nheads, nc, d->dstate, d->headdim);
+    if (workspace == nullptr || workspace_bytes < wl.total) return M3_ERR_WORKSPACE;
+    BwdArgs a;
+    a.x = x; a.B = B; a.C = C; a.dy = dy;
+    a.dt = dt; a.A = A; a.lam = lambda; a.theta = theta; a.D = D;
+    a.init_state = init_state; a.dfinal = dfinal_state;
+    a.dx = dx; a.dB = dB; a.dC = dC;
+    a.ddt = ddt; a.dA = dA; a.dlam = dlambda; a.dtheta = dtheta; a.dD = dD; a.dinit = dinit_state;
+    a.dA_per_token = d->a_stride_t != 0 ? 1 : 0;
+    char *ws = static_cast<char *>(workspace);
+    a.Af = reinterpret_cast<float *>(ws + wl.off_Af);
+    a.Mb = reinterpret_cast<float *>(ws + wl.off_Mb);
+    a.Sst = reinterpret_cast<float *>(ws + wl.off_Sst);
+    a.Ust = reinterpret_cast<float *>(ws + wl.off_Ust);
+    a.tot = reinterpret_cast<float *>(ws + wl.off_tot);
+    a.pst = reinterpret_cast<float *>(ws + wl.off_pst);
+    a.dsig = reinterpret_cast<float *>(ws + wl.off_dsig);
+    a.dApart = reinterpret_cast<float *>(ws + wl.off_dA);
+    a.dDpart = reinterpret_cast<float *>(ws + wl.off_dD);
+    a.batch = d->batch; a.L = d->seqlen; a.H = d->nheads; a.nchunks = nc;
+    a.a_sb = d->a_stride_b; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
+    const hipError_t e = fn(a, static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return M3_ERR_HIP;
+    }
+    return M3_OK;
+}
+
 extern "C" void m3_set_wait_limit(uint32_t polls) {
     g_spin_max.store(polls ? polls : kSpinMaxDefault, std::memory_order_relaxed);
 }

@@ -66,6 +66,35 @@ struct StepArgs {
     Prologue pro;
 };
 
+// Arguments of one backward scan (gradients of a loss through y and the
+// final state), already validated by the front end.
+struct BwdArgs {
+    const void *x, *B, *C, *dy;
+    const float *dt, *A, *lam, *theta, *D, *init_state, *dfinal;
+    void *dx, *dB, *dC;
+    float *ddt, *dA, *dlam, *dtheta, *dD, *dinit;
+    int dA_per_token;                   // dA [B][L][H] (else [H], summed)
+    // workspace regions (bwd_workspace_layout), per (slice, chunk)
+    float *Af;      // [N][P] chunk aggregate R(psi_e) sum_j v_j B^_j x_j^T
+    float *Mb;      // [N][P] sum_t e^{cum_t} C^_t dy_t^T
+    float *tot;     // [1 + N/2] cum_e, psi_e
+    float *Sst;     // [N][P] state entering the chunk
+    float *Ust;     // [N][P] R(-psi_e) dJ/dS_out
+    float *pst;     // [2][N/2] state terms of dpsi_e and dcum_e (per pair)
+    float *dsig;    // [1] dJ/dsigma of the chunk's last token
+    float *dApart;  // [1] sum over the chunk of dt dJ/d(dt A)
+    float *dDpart;  // [1] sum over the chunk of <x, dy>
+    int64_t batch, L, H, nchunks;
+    int64_t a_sb, a_st, a_sh;
+};
+typedef hipError_t (*bwd_launch_fn)(const BwdArgs &, hipStream_t);
+// backward kernels for the shape (null: none built)
+bwd_launch_fn find_bwd_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+struct BwdWorkspaceLayout {
+    size_t off_Af, off_Mb, off_tot, off_Sst, off_Ust, off_pst, off_dsig, off_dA, off_dD, total;
+};
+BwdWorkspaceLayout bwd_workspace_layout(int64_t BH, int64_t nchunks, int64_t N, int64_t P);
+
 // default bound of a look-back wait (polls; ~seconds), then an error count
 constexpr uint32_t kSpinMaxDefault = 1u << 22;
 

@@ -49,7 +49,8 @@ class M3Error(RuntimeError):
 
 EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_scan_fwd_varlen",
            "m3_step", "m3_step_gated", "m3_scan_check", "m3_set_wait_limit", "m3_scan_fwd_noalloc",
-           "m3_scan_fwd_pro", "m3_step_pro", "m3_status_string", "m3_last_hip_error")
+           "m3_scan_fwd_pro", "m3_step_pro", "m3_scan_bwd", "m3_scan_bwd_workspace_bytes",
+           "m3_status_string", "m3_last_hip_error")
 SCRATCH_BYTES = 256 << 20   # M3_SCRATCH_BYTES: the allocation-free scan's fixed workspace
 _lib = None
 
@@ -81,6 +82,10 @@ def lib() -> ctypes.CDLL:
         L.m3_scan_fwd_pro.restype = ctypes.c_int
         L.m3_step_pro.argtypes = [dims_p, pro_p] + [vp] * 13 + [vp]
         L.m3_step_pro.restype = ctypes.c_int
+        L.m3_scan_bwd_workspace_bytes.argtypes = [dims_p]
+        L.m3_scan_bwd_workspace_bytes.restype = ctypes.c_size_t
+        L.m3_scan_bwd.argtypes = [dims_p] + [vp] * 20 + [vp, ctypes.c_size_t, vp]
+        L.m3_scan_bwd.restype = ctypes.c_int
         L.m3_scan_fwd_noalloc.argtypes = [dims_p] + [vp] * 15 + [vp]
         L.m3_scan_fwd_noalloc.restype = ctypes.c_int
         L.m3_scan_check.argtypes = [dims_p, vp, ctypes.c_size_t, ctypes.POINTER(ctypes.c_uint32), vp]
@@ -382,3 +387,34 @@ def step_pro(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, pro: M3Pro
                              _p(x_t), _p(B_t), _p(C_t), _p(dt_t), _p(A), _p(lam_t), _p(theta_t),
                              _p(D), _p(z), _p(y), _stream(stream)))
     return y
+
+
+def scan_bwd(x, Bm, Cm, dt, A, lam, theta, D, dy, chunk: int, dfinal=None, init_state=None,
+             want_dinit: bool = False, workspace=None, stream=None):
+    """m3_scan_bwd: gradients of J = <dy, y> + <dfinal, final_state> for the
+    scan of these inputs.  Returns a dict: dx, dB, dC (io dtype), ddt, dlam,
+    dtheta, dD, dA ([H] for a per-head A, [B,L,H] for a per-token A) and
+    dinit (when `want_dinit`)."""
+    d = scan_dims(x, Bm, chunk, A)
+    batch, seqlen, nheads, rank, headdim = x.shape
+    dstate = Bm.shape[-1]
+    dev = x.device
+    f32 = dict(dtype=torch.float32, device=dev)
+    out = dict(dx=torch.empty_like(x), dB=torch.empty_like(Bm), dC=torch.empty_like(Cm),
+               ddt=torch.empty((batch, seqlen, nheads), **f32),
+               dlam=torch.empty((batch, seqlen, nheads), **f32),
+               dtheta=torch.empty((batch, seqlen, nheads, dstate // 2), **f32),
+               dD=torch.empty((nheads,), **f32),
+               dA=torch.empty((nheads,) if A.dim() == 1 else (batch, seqlen, nheads), **f32))
+    dinit = torch.empty((batch, nheads, dstate, headdim), **f32) if want_dinit else None
+    if dinit is not None:
+        out["dinit"] = dinit
+    nbytes = int(lib().m3_scan_bwd_workspace_bytes(ctypes.byref(d)))
+    if workspace is None:
+        workspace = torch.empty(max(nbytes, 16), dtype=torch.uint8, device=dev)
+    _check(lib().m3_scan_bwd(ctypes.byref(d), _p(x), _p(Bm), _p(Cm), _p(dt), _p(A), _p(lam),
+                             _p(theta), _p(D), _p(init_state), _p(dy), _p(dfinal),
+                             _p(out["dx"]), _p(out["dB"]), _p(out["dC"]), _p(out["ddt"]),
+                             _p(out["dA"]), _p(out["dlam"]), _p(out["dtheta"]), _p(out["dD"]),
+                             _p(dinit), _p(workspace), workspace.numel(), _stream(stream)))
+    return out

@@ -1,0 +1,156 @@
+"""GPU parity of the backward scan (m3_scan_bwd, through the C ABI) against
+the oracle's fp64 reverse mode (oracle.scan_bwd, pinned by finite
+differences and autograd of the masked form).
+
+Every gradient is compared per (batch, head) slice with the parity metric
+max|gpu - oracle| / max|oracle| at the bf16 bar 2e-2: dx, dB, dC, ddt,
+dlambda, dtheta, dinit per slice (and dA per token for a per-token A).  dD
+and a per-head dA are sums over batch and tokens of terms of both signs; each
+term carries the per-token error, so their bar is 2e-2 times the sum of the
+terms' magnitudes (the oracle's per-token values), not times the (possibly
+cancelled) sum itself.  The oracle reads the exact bf16 inputs and the same
+dy, dfinal and initial state.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+from paper_2603_15569_amd import m3
+from paper_2603_15569_amd.inputs import make_scan_inputs, workload_inputs, WORKLOADS
+
+pytestmark = pytest.mark.gpu
+
+DEV = "cuda:0"
+TOL = 2e-2
+
+
+def say(msg):
+    print(f"[gpu-case] {msg}", flush=True)
+
+
+def grads_case(inp, chunk, seed, with_final=True, with_init=True, per_token_A=False):
+    B_, L, H, R, P = inp.x.shape
+    N = inp.Bm.shape[-1]
+    g = torch.Generator(DEV).manual_seed(seed)
+    dy = torch.randn(inp.x.shape, device=DEV, generator=g).to(inp.x.dtype)
+    dfin = torch.randn((B_, H, N, P), device=DEV, generator=g) * 0.1 if with_final else None
+    h0 = torch.randn((B_, H, N, P), device=DEV, generator=g) * 0.5 if with_init else None
+    A = inp.A
+    if per_token_A:
+        A = (inp.A[None, None, :] * (0.5 + torch.rand((B_, L, H), device=DEV, generator=g))).contiguous()
+    out = m3.scan_bwd(inp.x, inp.Bm, inp.Cm, inp.dt, A, inp.lam, inp.theta, inp.D, dy, chunk,
+                      dfinal=dfin, init_state=h0, want_dinit=True)
+    torch.cuda.synchronize()
+    return out, dy, dfin, h0, A
+
+
+def oracle_grads(inp, A, dy, dfin, h0, slices):
+    ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                inp.D, slices)
+    if A.dim() == 3:
+        ref["A"] = np.stack([oracle._np(A[b, :, h]) for b, h in slices])
+    kw = {}
+    if dfin is not None:
+        kw["dfinal"] = oracle.slices_of_state(dfin, slices)
+    if h0 is not None:
+        kw["init_state"] = oracle.slices_of_state(h0, slices)
+    dys = np.stack([oracle._np(dy[b, :, h]) for b, h in slices])
+    return oracle.scan_bwd(**ref, dy=dys, **kw)
+
+
+def compare(out, ref, slices, label, A, H):
+    worst = {}
+    per_slice = {"dx": "dx", "dB": "dB", "dC": "dC", "ddt": "ddt", "dlam": "dlam",
+                 "dtheta": "dtheta", "dinit": "dinit"}
+    for k, (b, h) in enumerate(slices):
+        for gk, rk in per_slice.items():
+            got = out[gk][b, :, h] if gk != "dinit" else out[gk][b, h]
+            got = got.double().cpu().numpy()
+            assert np.all(np.isfinite(got)), f"{label} {gk} non-finite at {(b, h)}"
+            e = oracle.rel_err(got, ref[rk][k])
+            worst[gk] = max(worst.get(gk, 0.0), e)
+            assert e <= TOL, f"{label} {gk} slice {(b, h)}: rel err {e:.3g}"
+        if A.dim() == 3:
+            e = oracle.rel_err(out["dA"][b, :, h].double().cpu().numpy(), ref["dA"][k])
+            worst["dA"] = max(worst.get("dA", 0.0), e)
+            assert e <= TOL, f"{label} dA slice {(b, h)}: rel err {e:.3g}"
+    say(f"{label}: " + ", ".join(f"{k} {v:.2g}" for k, v in sorted(worst.items())))
+
+
+def per_head(ref, slices, H, key, sum_tokens):
+    """Per-head sums of the oracle's per-slice terms, and the sums of their
+    magnitudes (the scale of the sums' error bar)."""
+    out, mag = np.zeros(H), np.zeros(H)
+    for k, (b, h) in enumerate(slices):
+        out[h] += np.sum(ref[key][k]) if sum_tokens else ref[key][k]
+        mag[h] += np.sum(np.abs(ref[key][k])) if sum_tokens else abs(ref[key][k])
+    return out, mag
+
+
+def check_head_sums(out, ref, slices, H, label):
+    """dD and the per-head dA against the oracle's sums, each within 2e-2 of
+    the sum of its terms' magnitudes."""
+    errs = []
+    for key, sum_tokens in (("dD", False), ("dA", True)):
+        r, mag = per_head(ref, slices, H, key, sum_tokens)
+        got = out[key].double().cpu().numpy()
+        e = float(np.max(np.abs(got - r) / np.maximum(mag, 1e-30)))
+        errs.append(e)
+        assert e <= TOL, f"{label} {key}: {e:.3g} of the terms' magnitude"
+    say(f"{label}: dD {errs[0]:.2g}, dA {errs[1]:.2g} (of the terms' magnitudes)")
+
+
+@pytest.mark.parametrize("R,Q,L", [(1, 64, 200), (2, 32, 130), (4, 16, 77), (1, 64, 64),
+                                   (4, 16, 1), (1, 64, 5)])
+def test_backward_shapes(R, Q, L):
+    say(f"backward R={R} Q={Q} L={L}")
+    B_, H = 2, 3
+    inp = make_scan_inputs(B_, L, H, 64, 128, R, io="bf16", seed=500 + R * 10 + L, device=DEV,
+                           chunk=Q)
+    out, dy, dfin, h0, A = grads_case(inp, Q, seed=R + L)
+    slices = [(b, h) for b in range(B_) for h in range(H)]
+    ref = oracle_grads(inp, A, dy, dfin, h0, slices)
+    compare(out, ref, slices, f"bwd R={R} Q={Q} L={L}", A, H)
+    check_head_sums(out, ref, slices, H, f"bwd R={R} Q={Q} L={L}")
+
+
+@pytest.mark.parametrize("R,Q", [(1, 64), (4, 16)])
+def test_backward_per_token_A_no_final_no_init(R, Q):
+    say(f"backward per-token A R={R}")
+    B_, H, L = 2, 2, 150
+    inp = make_scan_inputs(B_, L, H, 64, 128, R, io="bf16", seed=900 + R, device=DEV, chunk=Q)
+    out, dy, dfin, h0, A = grads_case(inp, Q, seed=7, with_final=False, with_init=False,
+                                      per_token_A=True)
+    slices = [(b, h) for b in range(B_) for h in range(H)]
+    ref = oracle_grads(inp, A, dy, dfin, h0, slices)
+    compare(out, ref, slices, f"bwd per-token A R={R}", A, H)
+    # no initial state: the first token's angle and decay act on nothing (the
+    # oracle's are exactly zero; the chunked form reaches zero through sums
+    # that cancel, so they are zero to within the bar)
+    for b in range(B_):
+        for h in range(H):
+            for key in ("dtheta", "dA"):
+                full = out[key][b, :, h].abs().max().item()
+                assert out[key][b, 0, h].abs().max().item() <= TOL * full, (key, b, h)
+
+
+def test_backward_workload1_shape():
+    """The SISO prefill workload's shape (B=4, L=2048, H=16, chunk 64): every
+    slice."""
+    w = WORKLOADS[1]
+    say("backward workload 1 shape, all 64 slices")
+    inp = workload_inputs(1, device=DEV)
+    out, dy, dfin, h0, A = grads_case(inp, w["chunk"], seed=11)
+    slices = [(b, h) for b in range(w["batch"]) for h in range(w["nheads"])]
+    ref = oracle_grads(inp, A, dy, dfin, h0, slices)
+    compare(out, ref, slices, "bwd workload 1", A, w["nheads"])
+    check_head_sums(out, ref, slices, w["nheads"], "bwd workload 1")
+
+
+def test_backward_deterministic():
+    inp = make_scan_inputs(2, 300, 4, 64, 128, 1, io="bf16", seed=3, device=DEV, chunk=64)
+    o1, *_ = grads_case(inp, 64, seed=5)
+    o2, *_ = grads_case(inp, 64, seed=5)
+    for k in o1:
+        assert torch.equal(o1[k], o2[k]), k

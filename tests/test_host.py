@@ -296,3 +296,36 @@ def test_prologue_host_validation(L):
     assert step(dims(), pro()) == m3.M3_ERR_UNSUPPORTED
     assert step(dims(**bf), pro(), {0: None}) == m3.M3_ERR_NULL
     assert L.m3_last_hip_error() == 0
+
+
+def test_backward_host_validation(L):
+    """m3_scan_bwd: shapes, pointers, alignment and workspace are checked on
+    the host before any launch; the workspace query agrees."""
+    bf = dict(io=m3.M3_BF16, headdim=64, dstate=128, rank=1, chunk=64, seqlen=300)
+
+    def call(d, over=None, ws_bytes=None):
+        # x B C dt A lam theta D init dy dfinal dx dB dC ddt dA dlam dtheta dD dinit
+        ptrs = [FAKE] * 20
+        for k in (8, 10, 19):
+            ptrs[k] = None
+        for k, v in (over or {}).items():
+            ptrs[k] = v
+        need = L.m3_scan_bwd_workspace_bytes(ctypes.byref(d)) if ws_bytes is None else ws_bytes
+        return L.m3_scan_bwd(ctypes.byref(d), *ptrs, FAKE, need, None)
+    d = dims(**bf)
+    need = L.m3_scan_bwd_workspace_bytes(ctypes.byref(d))
+    nc = (300 + 63) // 64
+    assert need >= 2 * nc * 4 * 128 * 64 * 4          # four fp32 N x P maps per chunk and slice
+    assert call(dims(**dict(bf, rank=4, chunk=64))) == m3.M3_ERR_UNSUPPORTED   # chunk*rank 256
+    assert L.m3_scan_bwd_workspace_bytes(ctypes.byref(dims(**dict(bf, rank=4, chunk=16)))) > 0
+    assert call(dims()) == m3.M3_ERR_UNSUPPORTED                                  # fp32 not built
+    assert call(dims(**dict(bf, flags=m3.M3_THETA_PER_HEAD))) == m3.M3_ERR_UNSUPPORTED
+    assert call(dims(**dict(bf, a_stride_b=5, a_stride_t=0))) == m3.M3_ERR_UNSUPPORTED
+    assert call(dims(**bf), {0: None}) == m3.M3_ERR_NULL
+    assert call(dims(**bf), {9: None}) == m3.M3_ERR_NULL          # dy
+    assert call(dims(**bf), {15: None}) == m3.M3_ERR_NULL         # dA
+    assert call(dims(**bf), {9: FAKE + 2}) == m3.M3_ERR_ALIGN
+    assert call(dims(**bf), {14: FAKE + 2}) == m3.M3_ERR_ALIGN    # ddt
+    assert call(dims(**bf), ws_bytes=need - 1) == m3.M3_ERR_WORKSPACE
+    assert L.m3_scan_bwd_workspace_bytes(ctypes.byref(dims())) == 0
+    assert L.m3_last_hip_error() == 0
