@@ -45,6 +45,9 @@ def main():
                     help="only the timed loop (the long-context prefill and the decode step)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run 10 plain device copies of 1 GiB (reference for HBM byte counters)")
+    ap.add_argument("--bwd-calls", type=int, default=None, metavar="K",
+                    help="only run K m3_scan_bwd calls (after one warm-up call) on the SISO "
+                         "prefill workload's shape and print their mean time")
     ap.add_argument("--scan-workload", type=int, default=None, metavar="K",
                     help="only run --steps m3_scan_fwd calls (after one warm-up call) on prefill "
                          "workload K (1-4; the scan of workload 4 is its decode-state prefill) and "
@@ -74,6 +77,14 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         print(json.dumps({"calibrate_copy_bytes_each_way": 1 << 30, "launches": 10}), flush=True)
+        return
+
+    if args.bwd_calls is not None:
+        bw = BackwardCase(m3, torch, dev, WORKLOADS[1], workload_inputs)
+        bw.call()
+        ms = bw.time(stream, args.bwd_calls)
+        print(json.dumps({"bwd_workload": 1, "calls": args.bwd_calls, "ms_per_call": round(ms, 5)}),
+              flush=True)
         return
 
     if args.scan_workload is not None:
@@ -246,6 +257,16 @@ def main():
                                    workload_inputs, make_gate_input, step_in, dstep, dstate,
                                    dcB, dcX, layer, yd, peak_gbs))
 
+    if not args.no_extras:
+        log("extras: backward")
+        bw = BackwardCase(m3, torch, dev, WORKLOADS[1], workload_inputs)
+        for _ in range(3):
+            bw.call()
+        ms = bw.time(stream, 20)
+        result["backward_siso"] = bw.figures(roofline, ms, peak_gbs, peak_tfs)
+        del bw
+        torch.cuda.empty_cache()
+
     if not args.no_cpu:
         log("CPU baseline")
         result["cpu_baseline"] = cpu_baseline(p3, layer, step_in, WORKLOADS)
@@ -387,6 +408,63 @@ def siso_figures(m3, roofline, torch, np, stream, dev, wp, workload_inputs, make
             "frac": round(ph_bytes / (ph_ms * 1e-3) / 1e9 / peak_gbs, 4), "bytes_per_launch": ph_bytes,
         },
     }
+
+
+class BackwardCase:
+    """m3_scan_bwd on the SISO prefill workload's shape (B=4, L=2048, H=16,
+    P=64, N=128, chunk 64): inputs, dy, dJ/d(final state) and the outputs
+    and workspace allocated once."""
+
+    def __init__(self, m3, torch, dev, w, workload_inputs):
+        import ctypes
+        self.m3, self.torch, self.ctypes = m3, torch, ctypes
+        self.inp = inp = workload_inputs(1, device=dev)
+        self.chunk = w["chunk"]
+        g = torch.Generator(dev).manual_seed(77)
+        B, L, H, R, P = inp.x.shape
+        N = inp.Bm.shape[-1]
+        self.shape = (B, L, H, R, P, N)
+        self.dy = torch.randn(inp.x.shape, device=dev, generator=g).to(inp.x.dtype)
+        self.dfin = torch.randn((B, H, N, P), device=dev, generator=g) * 0.1
+        self.d = m3.scan_dims(inp.x, inp.Bm, self.chunk, inp.A)
+        f32 = dict(dtype=torch.float32, device=dev)
+        self.out = [torch.empty_like(inp.x), torch.empty_like(inp.Bm), torch.empty_like(inp.Cm),
+                    torch.empty((B, L, H), **f32), torch.empty((H,), **f32),
+                    torch.empty((B, L, H), **f32), torch.empty((B, L, H, N // 2), **f32),
+                    torch.empty((H,), **f32)]
+        nb = int(m3.lib().m3_scan_bwd_workspace_bytes(ctypes.byref(self.d)))
+        self.ws = torch.empty(nb, dtype=torch.uint8, device=dev)
+
+    def call(self):
+        m3, i, o = self.m3, self.inp, self.out
+        p = m3._p
+        m3._check(m3.lib().m3_scan_bwd(
+            self.ctypes.byref(self.d), p(i.x), p(i.Bm), p(i.Cm), p(i.dt), p(i.A), p(i.lam),
+            p(i.theta), p(i.D), None, p(self.dy), p(self.dfin), p(o[0]), p(o[1]), p(o[2]),
+            p(o[3]), p(o[4]), p(o[5]), p(o[6]), p(o[7]), None, p(self.ws), self.ws.numel(),
+            m3._stream(None)))
+
+    def time(self, stream, n):
+        torch = self.torch
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(n):
+            self.call()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    def figures(self, roofline, ms, peak_gbs, peak_tfs):
+        B, L, H, R, P, N = self.shape
+        nbytes = roofline.backward_bytes(B, L, H, N, P, R, 2)
+        flops = B * H * roofline.backward_flops(L, N, P, R, self.chunk)
+        gbs = nbytes / (ms * 1e-3) / 1e9
+        return {"workload": f"backward B={B} L={L} H={H} P={P} N={N} R={R} chunk={self.chunk} bf16",
+                "ms": round(ms, 5), "tokens_per_s": round(B * L / (ms * 1e-3), 1),
+                "bound": "hbm", "achieved_gbs": round(gbs, 1), "frac": round(gbs / peak_gbs, 4),
+                "bytes_per_launch": nbytes, "flops_per_launch": flops,
+                "mfma_tflops": round(flops / (ms * 1e-3) / 1e12, 2)}
 
 
 def measured_traffic(key):

@@ -54,50 +54,72 @@ constexpr int LDN = kN + 8;   // bf16 row strides (16-byte padding)
 constexpr int LDP = kP + 8;
 typedef Mma<bf16> MM;
 
-// Per-chunk scalars shared by the chunk kernels.
-template <int Q>
+// Per-chunk scalars shared by the chunk kernels (NT threads a workgroup).
+template <int Q, int NT>
 struct alignas(16) Pro {
+    static constexpr int kSeg = NT / kNH;     // token segments of the angle scans
     float cum[Q], gam[Q], sig[Q], v[Q], ec[Q];
     h2 cs[Q * kNH];      // cos / sin of psi_t[i]
     float psie[kNH];
+    float seg[kSeg][kNH];
 };
 
-// Chunk-local prefix sums (one wavefront scan for the log-decay, a serial
-// scan per angle pair), trapezoid weights, v_j and e^{cum_t}.  Tokens past
-// the end of the sequence get zero weights.
-template <int Q>
+// Chunk-local prefix sums, trapezoid weights, v_j and e^{cum_t}: the
+// log-decay by one wavefront scan over the tokens; the angles by thread
+// (pair i, token segment), all of a thread's angle loads issued together,
+// segment totals combined through LDS.  Tokens past the end of the sequence
+// get zero weights and zero angles.
+template <int Q, int NT>
 __device__ void bwd_prologue(const BwdArgs &a, int64_t b, int64_t h, int64_t t0, int nvalid,
-                             Pro<Q> &sp) {
+                             Pro<Q, NT> &sp) {
+    constexpr int TPS = (Q + Pro<Q, NT>::kSeg - 1) / Pro<Q, NT>::kSeg;
     const int tid = threadIdx.x, lane = tid & (kWave - 1);
+    const int i = tid % kNH, seg = tid / kNH;
+    const float *th = a.theta + ((b * a.L + t0) * a.H + h) * kNH + i;
+    float ps[TPS];
+#pragma unroll
+    for (int k = 0; k < TPS; ++k) {
+        const int t = seg * TPS + k;
+        ps[k] = t < nvalid ? th[(int64_t)t * a.H * kNH] : 0.f;
+    }
+    float lg = 0.f, gam = 0.f, sig = 0.f;
+    if (tid < kWave && tid < nvalid) {
+        const int64_t t = t0 + tid, k = (b * a.L + t) * a.H + h;
+        const float dtv = a.dt[k], lamv = a.lam[k];
+        lg = dtv * a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
+        gam = lamv * dtv;
+        sig = gam;
+        if (t + 1 < a.L) sig += (1.f - a.lam[k + a.H]) * a.dt[k + a.H];
+    }
+    float run = 0.f;
+#pragma unroll
+    for (int k = 0; k < TPS; ++k) {
+        run += ps[k];
+        ps[k] = run;
+    }
+    sp.seg[seg][i] = run;
     if (tid < kWave) {
-        float lg = 0.f, gam = 0.f, sig = 0.f;
-        if (tid < nvalid) {
-            const int64_t t = t0 + tid, k = (b * a.L + t) * a.H + h;
-            const float dtv = a.dt[k], lamv = a.lam[k];
-            lg = dtv * a.A[b * a.a_sb + t * a.a_st + h * a.a_sh];
-            gam = lamv * dtv;
-            sig = gam;
-            if (t + 1 < a.L) sig += (1.f - a.lam[k + a.H]) * a.dt[k + a.H];
-        }
         const float cum = wave_incl_scan(lg, lane);
         if (tid < Q) {
             sp.cum[tid] = cum;
             sp.gam[tid] = gam;
             sp.sig[tid] = sig;
         }
-    } else if (tid < 2 * kWave) {
-        const int i = tid - kWave;
-        const float *th = a.theta + ((b * a.L + t0) * a.H + h) * kNH + i;
-        float psi = 0.f;
-        for (int t = 0; t < Q; ++t) {
-            if (t < nvalid) psi += th[(int64_t)t * a.H * kNH];
-            float s, c;
-            sincosf(psi, &s, &c);
-            cs_put(&sp.cs[t * kNH + i], c, s);
+    }
+    __syncthreads();
+    float off = 0.f;
+    for (int s2 = 0; s2 < seg; ++s2) off += sp.seg[s2][i];
+#pragma unroll
+    for (int k = 0; k < TPS; ++k) {
+        const int t = seg * TPS + k;
+        if (t < Q) {
+            const float psi = ps[k] + off;
+            float sn, cs;
+            sincos_fast(psi, &sn, &cs);
+            cs_put(&sp.cs[t * kNH + i], cs, sn);
             if (t == nvalid - 1) sp.psie[i] = psi;
         }
     }
-    __syncthreads();
     if (tid < Q) {
         const float cume = sp.cum[nvalid - 1];
         sp.v[tid] = tid < nvalid ? __expf(cume - sp.cum[tid]) * sp.sig[tid] : 0.f;
@@ -108,9 +130,9 @@ __device__ void bwd_prologue(const BwdArgs &a, int64_t b, int64_t h, int64_t t0,
 
 // B or C rows of the chunk rotated by -psi_t into LDS [row][LDN] (bf16);
 // rows past the end are zero.  Row = (token, rank).
-template <int R>
+template <int R, int NT>
 __device__ void stage_rot(bf16 *dst, const bf16 *src, int64_t tokstr, int nvalid, const h2 *cs) {
-    for (int task = threadIdx.x; task < kRows * 8; task += kThr) {
+    for (int task = threadIdx.x; task < kRows * 8; task += NT) {
         const int row = task / 8, cp = task % 8, t = row / R, r = row % R;
         bf16x8 lo, hi;
         if (t < nvalid) {
@@ -135,9 +157,9 @@ __device__ void stage_rot(bf16 *dst, const bf16 *src, int64_t tokstr, int nvalid
 }
 
 // x-like rows (P wide) into LDS [row][LDP], optionally scaled per token.
-template <int R>
+template <int R, int NT>
 __device__ void stage_rows(bf16 *dst, const bf16 *src, int64_t tokstr, int nvalid, const float *scale) {
-    for (int task = threadIdx.x; task < kRows * 8; task += kThr) {
+    for (int task = threadIdx.x; task < kRows * 8; task += NT) {
         const int row = task / 8, cp = task % 8, t = row / R, r = row % R;
         bf16x8 v;
         if (t < nvalid) {
@@ -163,7 +185,7 @@ __device__ void stage_rows(bf16 *dst, const bf16 *src, int64_t tokstr, int nvali
 template <int R>
 __global__ __launch_bounds__(kThr) void k_bwd_aggr(BwdArgs a) {
     constexpr int Q = kRows / R;
-    __shared__ Pro<Q> sp;
+    __shared__ Pro<Q, kThr> sp;
     __shared__ __attribute__((aligned(16))) bf16 s_B[kRows * LDN];
     __shared__ __attribute__((aligned(16))) bf16 s_C[kRows * LDN];
     __shared__ __attribute__((aligned(16))) bf16 s_vX[kRows * LDP];
@@ -174,13 +196,13 @@ __global__ __launch_bounds__(kThr) void k_bwd_aggr(BwdArgs a) {
     const int nvalid = (int)min((int64_t)Q, a.L - t0);
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int g = lane >> 4, l16 = lane & 15;
-    bwd_prologue<Q>(a, b, h, t0, nvalid, sp);
+    bwd_prologue<Q, kThr>(a, b, h, t0, nvalid, sp);
 
     const int64_t tok0 = (b * a.L + t0) * a.H + h;
-    stage_rot<R>(s_B, static_cast<const bf16 *>(a.B) + tok0 * (R * kN), a.H * R * kN, nvalid, sp.cs);
-    stage_rot<R>(s_C, static_cast<const bf16 *>(a.C) + tok0 * (R * kN), a.H * R * kN, nvalid, sp.cs);
-    stage_rows<R>(s_vX, static_cast<const bf16 *>(a.x) + tok0 * (R * kP), a.H * R * kP, nvalid, sp.v);
-    stage_rows<R>(s_eY, static_cast<const bf16 *>(a.dy) + tok0 * (R * kP), a.H * R * kP, nvalid, sp.ec);
+    stage_rot<R, kThr>(s_B, static_cast<const bf16 *>(a.B) + tok0 * (R * kN), a.H * R * kN, nvalid, sp.cs);
+    stage_rot<R, kThr>(s_C, static_cast<const bf16 *>(a.C) + tok0 * (R * kN), a.H * R * kN, nvalid, sp.cs);
+    stage_rows<R, kThr>(s_vX, static_cast<const bf16 *>(a.x) + tok0 * (R * kP), a.H * R * kP, nvalid, sp.v);
+    stage_rows<R, kThr>(s_eY, static_cast<const bf16 *>(a.dy) + tok0 * (R * kP), a.H * R * kP, nvalid, sp.ec);
     __syncthreads();
 
     f32x4 am[2][4], bm[2][4];
@@ -213,7 +235,7 @@ __global__ __launch_bounds__(kThr) void k_bwd_aggr(BwdArgs a) {
     for (int v = 0; v < 4; ++v) {
         const int i = wave * 16 + 4 * g + v;          // pair (i, i + N/2)
         float sn, cs;
-        sincosf(sp.psie[i], &sn, &cs);
+        sincos_fast(sp.psie[i], &sn, &cs);
 #pragma unroll
         for (int pt = 0; pt < 4; ++pt) {
             const int p = pt * 16 + l16;
@@ -241,24 +263,36 @@ __global__ __launch_bounds__(kThr) void k_bwd_pass(BwdArgs a, int per) {
     const int i = idx / kP, p = idx % kP;   // (a wavefront: one i, all p)
     const int64_t NP = kN * kP, base = bh * a.nchunks;
     const int o_re = i * kP + p, o_im = (i + kNH) * kP + p;
+    constexpr int DEPTH = 8;   // chunks whose loads are issued together
     float sre = 0.f, sim = 0.f;
     if (a.init_state) {
         sre = a.init_state[bh * NP + o_re];
         sim = a.init_state[bh * NP + o_im];
     }
-    for (int64_t c = 0; c < a.nchunks; ++c) {
-        const int64_t s = base + c;
-        const float ce = a.tot[s * (1 + kNH)], ps = a.tot[s * (1 + kNH) + 1 + i];
-        const float are = a.Af[s * NP + o_re], aim = a.Af[s * NP + o_im];
-        a.Sst[s * NP + o_re] = sre;
-        a.Sst[s * NP + o_im] = sim;
-        const float e = __expf(ce);
-        float sn, cs;
-        sincosf(ps, &sn, &cs);
-        const float nre = e * (cs * sre - sn * sim) + are;
-        const float nim = e * (sn * sre + cs * sim) + aim;
-        sre = nre;
-        sim = nim;
+    for (int64_t c0 = 0; c0 < a.nchunks; c0 += DEPTH) {
+        float ce[DEPTH], ps[DEPTH], are[DEPTH], aim[DEPTH];
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t s = base + min(c0 + d, a.nchunks - 1);
+            ce[d] = a.tot[s * (1 + kNH)];
+            ps[d] = a.tot[s * (1 + kNH) + 1 + i];
+            are[d] = a.Af[s * NP + o_re];
+            aim[d] = a.Af[s * NP + o_im];
+        }
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            if (c0 + d >= a.nchunks) break;
+            const int64_t s = base + c0 + d;
+            a.Sst[s * NP + o_re] = sre;
+            a.Sst[s * NP + o_im] = sim;
+            const float e = __expf(ce[d]);
+            float sn, cs;
+            sincos_fast(ps[d], &sn, &cs);
+            const float nre = e * (cs * sre - sn * sim) + are[d];
+            const float nim = e * (sn * sre + cs * sim) + aim[d];
+            sre = nre;
+            sim = nim;
+        }
     }
     float gre = 0.f, gim = 0.f;
     if (a.dfinal) {
@@ -266,32 +300,45 @@ __global__ __launch_bounds__(kThr) void k_bwd_pass(BwdArgs a, int per) {
         gim = a.dfinal[bh * NP + o_im];
     }
     float xre = sre, xim = sim;   // S_c, from the last chunk down
-    for (int64_t c = a.nchunks - 1; c >= 0; --c) {
-        const int64_t s = base + c;
-        const float ce = a.tot[s * (1 + kNH)], ps = a.tot[s * (1 + kNH) + 1 + i];
-        const float pre = a.Sst[s * NP + o_re], pim = a.Sst[s * NP + o_im];
-        const float mre = a.Mb[s * NP + o_re], mim = a.Mb[s * NP + o_im];
-        float sn, cs;
-        sincosf(ps, &sn, &cs);
-        const float e = __expf(ce);
-        float dps = gim * xre - gre * xim;                  // rotation of S_c by psi_e
-        const float ure = cs * gre + sn * gim, uim = -sn * gre + cs * gim;
-        float dcm = e * (ure * pre + uim * pim);            // decay e^{cum_e} of S_{c-1}
+    for (int64_t c1 = a.nchunks - 1; c1 >= 0; c1 -= DEPTH) {
+        float ce[DEPTH], ps[DEPTH], pre[DEPTH], pim[DEPTH], mre[DEPTH], mim[DEPTH];
 #pragma unroll
-        for (int o = 1; o < kWave; o <<= 1) {
-            dps += __shfl_xor(dps, o, kWave);
-            dcm += __shfl_xor(dcm, o, kWave);
+        for (int d = 0; d < DEPTH; ++d) {
+            const int64_t s = base + max(c1 - d, (int64_t)0);
+            ce[d] = a.tot[s * (1 + kNH)];
+            ps[d] = a.tot[s * (1 + kNH) + 1 + i];
+            pre[d] = a.Sst[s * NP + o_re];
+            pim[d] = a.Sst[s * NP + o_im];
+            mre[d] = a.Mb[s * NP + o_re];
+            mim[d] = a.Mb[s * NP + o_im];
         }
-        if (p == 0) {
-            a.pst[s * (2 * kNH) + i] = dps;
-            a.pst[s * (2 * kNH) + kNH + i] = dcm;
+#pragma unroll
+        for (int d = 0; d < DEPTH; ++d) {
+            if (c1 - d < 0) break;
+            const int64_t s = base + c1 - d;
+            float sn, cs;
+            sincos_fast(ps[d], &sn, &cs);
+            const float e = __expf(ce[d]);
+            float dps = gim * xre - gre * xim;                  // rotation of S_c by psi_e
+            const float ure = cs * gre + sn * gim, uim = -sn * gre + cs * gim;
+            float dcm = e * (ure * pre[d] + uim * pim[d]);      // decay e^{cum_e} of S_{c-1}
+#pragma unroll
+            for (int o = 1; o < kWave; o <<= 1) {
+                dps += __shfl_xor(dps, o, kWave);
+                dcm += __shfl_xor(dcm, o, kWave);
+            }
+            if (p == 0) {
+                a.pst[s * (2 * kNH) + i] = dps;
+                a.pst[s * (2 * kNH) + kNH + i] = dcm;
+            }
+            bf16 *Ub = reinterpret_cast<bf16 *>(a.Ust);   // (bf16: read only as an MFMA operand)
+            Ub[s * NP + o_re] = (bf16)ure;
+            Ub[s * NP + o_im] = (bf16)uim;
+            gre = e * ure + mre[d];
+            gim = e * uim + mim[d];
+            xre = pre[d];
+            xim = pim[d];
         }
-        a.Ust[s * NP + o_re] = ure;
-        a.Ust[s * NP + o_im] = uim;
-        gre = e * ure + mre;
-        gim = e * uim + mim;
-        xre = pre;
-        xim = pim;
     }
     if (a.dinit) {
         a.dinit[bh * NP + o_re] = gre;
@@ -307,22 +354,24 @@ __device__ __forceinline__ float sum16(float v) {
 }
 
 // ---------------------------------------------------------------------------
-// k_bwd_chunk: every gradient of one chunk.  Wave w owns row tile w as a
-// column block (j rows: dx, dB^, the masked-score columns) and as a row
-// block (t rows: dC^, the y state term); the causal tiles split evenly (w
-// has 4 - w tiles of the first kind and w + 1 of the second).
+// k_bwd_chunk: every gradient of one chunk, eight waves.  Waves 0-3 own row
+// tile w as a column block (j rows: dx, dB^, the masked-score columns),
+// waves 4-7 row tile w - 4 as a row block (t rows: dC^, the y state term);
+// the two halves only read the staged operands, so they run side by side
+// (two waves a SIMD).
 // ---------------------------------------------------------------------------
+constexpr int kThrC = 512;
 template <int R>
-__global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
+__global__ __launch_bounds__(kThrC) void k_bwd_chunk(BwdArgs a) {
     constexpr int Q = kRows / R;
-    __shared__ Pro<Q> sp;
+    __shared__ Pro<Q, kThrC> sp;
     __shared__ __attribute__((aligned(16))) bf16 s_B[kRows * LDN];
     __shared__ __attribute__((aligned(16))) bf16 s_C[kRows * LDN];
     __shared__ __attribute__((aligned(16))) bf16 s_X[kRows * LDP];
     __shared__ __attribute__((aligned(16))) bf16 s_dY[kRows * LDP];
     __shared__ __attribute__((aligned(16))) bf16 s_S[kN * LDP];   // S_{c-1} [n][p]
     __shared__ __attribute__((aligned(16))) bf16 s_U[kN * LDP];   // U_c [n][p]
-    __shared__ float s_dpsi[kRows * kNH];                         // per row, per pair
+    __shared__ float s_dpsi[2][kRows * kNH];                      // per row, per pair: B^ and C^ parts
     __shared__ float s_rc[4][kRows], s_rg[4][kRows];              // per-wave row sums of the mask terms
     __shared__ float s_cc[kRows], s_cs[kRows];                    // column sums (cum, sigma)
     __shared__ float s_dv[kRows], s_dcy[kRows];                   // dJ/dv_j, y state term of cum_t
@@ -334,31 +383,32 @@ __global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
     const int nvalid = (int)min((int64_t)Q, a.L - t0);
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
     const int g = lane >> 4, l16 = lane & 15;
-    bwd_prologue<Q>(a, b, h, t0, nvalid, sp);
+    bwd_prologue<Q, kThrC>(a, b, h, t0, nvalid, sp);
 
     const int64_t tok0 = (b * a.L + t0) * a.H + h;
     const int64_t bstr = a.H * R * kN, xstr = a.H * R * kP;
-    stage_rot<R>(s_B, static_cast<const bf16 *>(a.B) + tok0 * (R * kN), bstr, nvalid, sp.cs);
-    stage_rot<R>(s_C, static_cast<const bf16 *>(a.C) + tok0 * (R * kN), bstr, nvalid, sp.cs);
-    stage_rows<R>(s_X, static_cast<const bf16 *>(a.x) + tok0 * (R * kP), xstr, nvalid, nullptr);
-    stage_rows<R>(s_dY, static_cast<const bf16 *>(a.dy) + tok0 * (R * kP), xstr, nvalid, nullptr);
+    stage_rot<R, kThrC>(s_B, static_cast<const bf16 *>(a.B) + tok0 * (R * kN), bstr, nvalid, sp.cs);
+    stage_rot<R, kThrC>(s_C, static_cast<const bf16 *>(a.C) + tok0 * (R * kN), bstr, nvalid, sp.cs);
+    stage_rows<R, kThrC>(s_X, static_cast<const bf16 *>(a.x) + tok0 * (R * kP), xstr, nvalid, nullptr);
+    stage_rows<R, kThrC>(s_dY, static_cast<const bf16 *>(a.dy) + tok0 * (R * kP), xstr, nvalid, nullptr);
     {
         const int64_t NP = kN * kP;
         const float4 *Sg = reinterpret_cast<const float4 *>(a.Sst + slot * NP);
-        const float4 *Ug = reinterpret_cast<const float4 *>(a.Ust + slot * NP);
-        for (int q = tid; q < kN * kP / 4; q += kThr) {
+        const bf16x4 *Ug = reinterpret_cast<const bf16x4 *>(reinterpret_cast<const bf16 *>(a.Ust) + slot * NP);
+        for (int q = tid; q < kN * kP / 4; q += kThrC) {
             const int n = (4 * q) / kP, p = (4 * q) % kP;
-            const float4 sv = Sg[q], uv = Ug[q];
-            bf16x4 s4, u4;
+            const float4 sv = Sg[q];
+            bf16x4 s4;
             s4[0] = (bf16)sv.x; s4[1] = (bf16)sv.y; s4[2] = (bf16)sv.z; s4[3] = (bf16)sv.w;
-            u4[0] = (bf16)uv.x; u4[1] = (bf16)uv.y; u4[2] = (bf16)uv.z; u4[3] = (bf16)uv.w;
             *reinterpret_cast<bf16x4 *>(&s_S[n * LDP + p]) = s4;
-            *reinterpret_cast<bf16x4 *>(&s_U[n * LDP + p]) = u4;
+            *reinterpret_cast<bf16x4 *>(&s_U[n * LDP + p]) = Ug[q];
         }
     }
     __syncthreads();
     const float Dh = a.D[h];
 
+    float xdy = 0.f;
+    if (wave < 4) {
     // ============ column block J = wave: dx and dB^ of rows j ============
     const int J = wave;
     f32x4 gt[4], dg[4];   // G and dG tiles (T, J): lane element (t = 16T + 4g + v, j = 16J + l16)
@@ -449,7 +499,6 @@ __global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
         for (int pt = 0; pt < 4; ++pt)
             bu[pt] = MM::mma(ab, load_kt(s_U, LDP, kk * 32, pt * 16, g, l16), bu[pt]);
     }
-    float xdy = 0.f;
     {
         bf16 *dxg = static_cast<bf16 *>(a.dx) + tok0 * (R * kP);
 #pragma unroll
@@ -511,7 +560,7 @@ __global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
                 const int i = nt * 16 + l16;
                 const float re = db[nt][v] + vj * xu[nt][v], im = db[nt + 4][v] + vj * xu[nt + 4][v];
                 const float bre = (float)s_B[j * LDN + i], bim = (float)s_B[j * LDN + i + kNH];
-                s_dpsi[j * kNH + i] = re * bim - im * bre;
+                s_dpsi[0][j * kNH + i] = re * bim - im * bre;
                 float cs, sn;
                 cs_get(sp.cs[t * kNH + i], cs, sn);
                 if (t < nvalid) {
@@ -522,8 +571,9 @@ __global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
         }
     }
 
-    // ============ row block T = wave: dC^ of rows t ============
-    const int T = wave;
+    } else {
+    // ============ row block T = wave - 4: dC^ of rows t ============
+    const int T = wave - 4;
     f32x4 gT[4];   // dG^T tiles (J, T): lane element (j = 16J + 4g + v, t = 16T + l16)
 #pragma unroll
     for (int Jt = 0; Jt < 4; ++Jt) {
@@ -589,7 +639,7 @@ __global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
                 const int i = nt * 16 + l16;
                 const float re = dc[nt][v] + ec * t2[nt][v], im = dc[nt + 4][v] + ec * t2[nt + 4][v];
                 const float cre = (float)s_C[trow * LDN + i], cim = (float)s_C[trow * LDN + i + kNH];
-                s_dpsi[trow * kNH + i] += re * cim - im * cre;
+                s_dpsi[1][trow * kNH + i] = re * cim - im * cre;
                 float cs, sn;
                 cs_get(sp.cs[t * kNH + i], cs, sn);
                 if (t < nvalid) {
@@ -599,10 +649,12 @@ __global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
             }
         }
     }
-    // <x, dy> over the chunk (the skip term's gradient), one value per wave
+    }
+    // <x, dy> over the chunk (the skip term's gradient), one value per
+    // column-block wave
 #pragma unroll
     for (int o = 1; o < kWave; o <<= 1) xdy += __shfl_xor(xdy, o, kWave);
-    if (lane == 0) s_red[0][wave] = xdy;
+    if (lane == 0 && wave < 4) s_red[0][wave] = xdy;
     __syncthreads();
 
     // ============ per-token scalars ============
@@ -679,7 +731,8 @@ __global__ __launch_bounds__(kThr) void k_bwd_chunk(BwdArgs a) {
         for (int t = nvalid - 1; t >= 0; --t) {
             float d = 0.f;
 #pragma unroll
-            for (int r = 0; r < R; ++r) d += s_dpsi[(t * R + r) * kNH + i];
+            for (int r = 0; r < R; ++r)
+                d += s_dpsi[0][(t * R + r) * kNH + i] + s_dpsi[1][(t * R + r) * kNH + i];
             if (t == nvalid - 1) d += pst[i];
             acc += d;
             dth[(int64_t)t * a.H * kNH] = acc;
@@ -739,7 +792,7 @@ hipError_t launch_bwd(const BwdArgs &a, hipStream_t stream) {
     constexpr int per = kNH * kP / kThr;
     hipLaunchKernelGGL(k_bwd_pass, dim3((unsigned)(BH * per)), dim3(kThr), 0, stream, a, per);
     if (a.nchunks > 0) {
-        hipLaunchKernelGGL((k_bwd_chunk<R>), dim3((unsigned)nslot), dim3(kThr), 0, stream, a);
+        hipLaunchKernelGGL((k_bwd_chunk<R>), dim3((unsigned)nslot), dim3(kThrC), 0, stream, a);
         hipLaunchKernelGGL(k_bwd_finish, dim3((unsigned)((nslot + kThr - 1) / kThr)), dim3(kThr), 0,
                            stream, a, Q);
     }

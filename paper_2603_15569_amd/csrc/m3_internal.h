@@ -79,7 +79,7 @@ struct BwdArgs {
     float *Mb;      // [N][P] sum_t e^{cum_t} C^_t dy_t^T
     float *tot;     // [1 + N/2] cum_e, psi_e
     float *Sst;     // [N][P] state entering the chunk
-    float *Ust;     // [N][P] R(-psi_e) dJ/dS_out
+    float *Ust;     // [N][P] R(-psi_e) dJ/dS_out, stored as bf16 (an MFMA operand only)
     float *pst;     // [2][N/2] state terms of dpsi_e and dcum_e (per pair)
     float *dsig;    // [1] dJ/dsigma of the chunk's last token
     float *dApart;  // [1] sum over the chunk of dt dJ/d(dt A)

@@ -63,3 +63,27 @@ def decode_flops_per_slice(N: int, P: int, R: int) -> int:
     state (6 N P / 2 ... 3 N P), the rank-R output contraction (2 N P R), the
     skip term (2 P R)."""
     return 2 * N * P * R * 3 + 3 * N * P + 2 * P * R
+
+
+def backward_bytes(batch: int, L: int, H: int, N: int, P: int, R: int, io_bytes: int) -> int:
+    """Algorithmic HBM bytes of one backward scan: the forward's inputs x, B, C
+    (io dtype), dt, lambda and N/2 angles (fp32) and dy (io dtype) read once;
+    dx, dB, dC (io dtype), ddt, dlambda and the N/2 angle gradients (fp32)
+    written once; dJ/d(final state) read once (fp32).  Per-head A, D and their
+    gradients are negligible and not counted."""
+    per_token_head_in = R * (2 * N + 2 * P) * io_bytes + 4 + 4 + 4 * (N // 2)
+    per_token_head_out = R * (2 * N + P) * io_bytes + 4 + 4 + 4 * (N // 2)
+    return batch * L * H * (per_token_head_in + per_token_head_out) + batch * H * N * P * 4
+
+
+def backward_flops(T: int, N: int, P: int, R: int, C: int) -> float:
+    """Matrix-product FLOPs of the chunked backward over T tokens of one head,
+    counted like the forward's (Sec. 3.3): per chunk of CR rows, the two
+    state-sized contractions of the recomputed forward aggregate and of the
+    reverse state input (2 x 2 N P CR), the scores C^ B^T and the two
+    orientations of dy x^T (2 (CR)^2 (N + 2P)), the three products with the
+    masked scores (dx, dB^, dC^: 2 (CR)^2 (P + 2N)), and the four products with
+    the state maps (B^ U, x U^T, dy S^T: 2 CR N P each, and the forward
+    aggregate's second operand) — 2 (CR)^2 (3N + 3P) + 12 N P CR in all."""
+    nch = T / C
+    return nch * (2 * (C * R) ** 2 * (3 * N + 3 * P) + 12 * N * P * (C * R))
