@@ -258,6 +258,10 @@ def main():
                                    dcB, dcX, layer, yd, peak_gbs))
 
     if not args.no_extras:
+        log("extras: block prologue")
+        result["prologue"] = prologue_figures(m3, roofline, torch, stream, dev, WORKLOADS,
+                                              workload_inputs, peak_gbs, peak_tfs)
+        torch.cuda.empty_cache()
         log("extras: backward")
         bw = BackwardCase(m3, torch, dev, WORKLOADS[1], workload_inputs)
         for _ in range(3):
@@ -408,6 +412,69 @@ def siso_figures(m3, roofline, torch, np, stream, dev, wp, workload_inputs, make
             "frac": round(ph_bytes / (ph_ms * 1e-3) / 1e9 / peak_gbs, 4), "bytes_per_launch": ph_bytes,
         },
     }
+
+
+def prologue_figures(m3, roofline, torch, stream, dev, W, workload_inputs, peak_gbs, peak_tfs):
+    """The prefill with the block prologue fused (BCNorm with gains, B/C
+    biases, structured MIMO input X = W_X o X') on the three prefill
+    workloads' shapes, against the plain scan of the same shape (the
+    library's default kernel, and the one-chunk-per-workgroup kernel that the
+    prologue runs in)."""
+    from paper_2603_15569_amd.inputs import make_prologue_inputs
+    out = {}
+    for k in (1, 2, 3):
+        w = W[k]
+        inp = workload_inputs(k, device=dev)
+        pin = make_prologue_inputs(w["batch"], w["seqlen"], w["nheads"], w["headdim"], w["dstate"],
+                                   w["rank"], io="bf16", seed=k, device=dev)
+        pro = m3.prologue(bc_norm=True, eps=1e-6, norm_B=pin.gB, norm_C=pin.gC, bias_B=pin.bB,
+                          bias_C=pin.bC, w_x=pin.wx)
+        B, L, H, R, P = inp.x.shape
+        N = inp.Bm.shape[-1]
+        Q = w["chunk"]
+        d = m3.scan_dims(inp.x, inp.Bm, Q, inp.A)
+        ws = torch.empty(max(m3.workspace_bytes(d), 16), dtype=torch.uint8, device=dev)
+        o = (torch.empty_like(inp.x), torch.empty((B, H, N, P), device=dev),
+             torch.empty((B, H, R, N), device=dev, dtype=inp.x.dtype),
+             torch.empty((B, H, R, P), device=dev, dtype=inp.x.dtype))
+
+        def plain(per_chunk):
+            return lambda: m3.scan_fwd(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                       inp.D, chunk=Q, out=o, workspace=ws, per_chunk=per_chunk)
+
+        def fused():
+            m3.scan_fwd_pro(pin.xp, pin.Bp, pin.Cp, inp.dt, inp.A, inp.lam, inp.theta, inp.D, Q,
+                            pro, R, out=o, workspace=ws)
+
+        def timed(fn, n):
+            for _ in range(2):
+                fn()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            for _ in range(n):
+                fn()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            return e0.elapsed_time(e1) / n
+        n = 20 if k == 1 else 5
+        t_pro, t_def, t_pc = timed(fused, n), timed(plain(False), n), timed(plain(True), n)
+        nbytes = roofline.prologue_prefill_bytes(B, L, H, N, P, R, 2)
+        flops = B * H * roofline.chunked_flops(L, N, P, R, Q)
+        gbs = nbytes / (t_pro * 1e-3) / 1e9
+        out[f"workload{k}"] = {
+            "workload": f"prefill B={B} L={L} H={H} P={P} N={N} R={R} chunk={Q} bf16, BCNorm + gains + "
+                        "biases + structured input",
+            "ms": round(t_pro, 4), "tokens_per_s": round(B * L / (t_pro * 1e-3), 1),
+            "bytes_per_launch": nbytes, "achieved_gbs": round(gbs, 1),
+            "hbm_frac": round(gbs / peak_gbs, 4),
+            "mfma_frac": round(flops / (t_pro * 1e-3) / 1e12 / peak_tfs, 4),
+            "plain_default_ms": round(t_def, 4), "plain_per_chunk_ms": round(t_pc, 4),
+            "plain_bytes_per_launch": roofline.prefill_bytes(B, L, H, N, P, R, 2),
+        }
+        del inp, pin, ws, o
+        torch.cuda.empty_cache()
+    return out
 
 
 class BackwardCase:

@@ -254,6 +254,32 @@ void k_scan_fused(ScanArgs a) {
             for (int kk = 0; kk < NK; ++kk) cf[m][kk] = buf_load<Frag>(rc, off + kk * MM::K * sizeof(T));
         }
     };
+    // Block prologue on the C fragments: C = g o C' / rms(C') + b, applied in
+    // place and rounded to the operand type before the rotation (a row sits
+    // in lanes l16 + 16 g).  Chunks of several row blocks do it at the end of
+    // the prologue, while the registers of the later phases are still free.
+    auto norm_cf = [&]() {
+#pragma unroll
+        for (int m = 0; m < TPW; ++m) {
+            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R;
+            float ss = 0.f;
+#pragma unroll
+            for (int kk = 0; kk < NK; ++kk) ss += sumsq(cf[m][kk]);
+            ss += __shfl_xor(ss, 16, kWave);
+            ss += __shfl_xor(ss, 32, kWave);
+            const bool ok = t < nvalid;
+            const float sc = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
+            const float bsc = ok ? 1.f : 0.f;
+            const int pcr = kPC + (row % R) * N + MM::KPL * g;
+#pragma unroll
+            for (int kk = 0; kk < NK; ++kk)
+#pragma unroll
+                for (int e = 0; e < MM::KPL; ++e) {
+                    const int pc = pcr + kk * MM::K + e;
+                    fset(cf[m][kk], e, sc * s_pro[pc] * fget(cf[m][kk], e) + bsc * s_pro[pc - kPC + kPCb]);
+                }
+        }
+    };
     // ---- 2. prologue ----
     if constexpr (kPro) {   // the head's prologue tables (read after the prologue's barriers)
         const int64_t hn = h * (R * N), hp = h * (R * P);
@@ -353,6 +379,7 @@ void k_scan_fused(ScanArgs a) {
             const Acc cum_e = s_cum[nvalid - 1];
             s_w[tid] = (tid < nvalid) ? (float)(exp_fast(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
         }
+        if constexpr (kPro && kEarlyC) norm_cf();
         __syncthreads();
     }
 
@@ -363,30 +390,10 @@ void k_scan_fused(ScanArgs a) {
     // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
     // end of the sequence were loaded as zeros)
     auto rotate_cf = [&]() {
+        if constexpr (kPro && !kEarlyC) norm_cf();
 #pragma unroll
         for (int m = 0; m < TPW; ++m) {
             const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R;
-            if constexpr (kPro) {   // C = g o C' / rms(C') + b: a row sits in lanes l16 + 16 g
-                float ss = 0.f;
-#pragma unroll
-                for (int kk = 0; kk < NK; ++kk) ss += sumsq(cf[m][kk]);
-                ss += __shfl_xor(ss, 16, kWave);
-                ss += __shfl_xor(ss, 32, kWave);
-                const bool ok = t < nvalid;
-                const float sc = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
-                const float bsc = ok ? 1.f : 0.f;
-                // (applied in place, one fragment at a time, and rounded to
-                // the operand type before the rotation: an fp32 copy of the
-                // row alongside the fragments does not fit in the registers)
-                const int pcr = kPC + (row % R) * N + MM::KPL * g;
-#pragma unroll
-                for (int kk = 0; kk < NK; ++kk)
-#pragma unroll
-                    for (int e = 0; e < MM::KPL; ++e) {
-                        const int pc = pcr + kk * MM::K + e;
-                        fset(cf[m][kk], e, sc * s_pro[pc] * fget(cf[m][kk], e) + bsc * s_pro[pc - kPC + kPCb]);
-                    }
-            }
 #pragma unroll
             for (int kk = 0; kk < NK / 2; ++kk) {
                 float csv[MM::KPL], snv[MM::KPL];

@@ -87,3 +87,11 @@ def backward_flops(T: int, N: int, P: int, R: int, C: int) -> float:
     aggregate's second operand) — 2 (CR)^2 (3N + 3P) + 12 N P CR in all."""
     nch = T / C
     return nch * (2 * (C * R) ** 2 * (3 * N + 3 * P) + 12 * N * P * (C * R))
+
+
+def prologue_prefill_bytes(batch: int, L: int, H: int, N: int, P: int, R: int, io_bytes: int) -> int:
+    """Algorithmic HBM bytes of a prefill scan with the block prologue and the
+    structured MIMO input: as prefill_bytes, but x is read as X' (P values per
+    token and head instead of P x R); the raw B', C' have the size of B, C;
+    the per-head tables are negligible."""
+    return prefill_bytes(batch, L, H, N, P, R, io_bytes) - batch * L * H * (R - 1) * P * io_bytes
