@@ -100,6 +100,7 @@ __device__ __forceinline__ float sumsq(const bf16x8 &v) {
 __device__ __forceinline__ float sumsq(const f32x4 &v) {
     return v[0] * v[0] + v[1] * v[1] + v[2] * v[2] + v[3] * v[3];
 }
+__device__ __forceinline__ float sumsq(float v) { return v * v; }   // (fp32 MFMA fragments)
 
 // Look-back traffic uses device-scope atomic accesses only (the sc1 scope
 // bit): they are coherent across the XCDs' L2 caches by themselves, so no
