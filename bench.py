@@ -248,7 +248,7 @@ def main():
         B2, L2, H2, R2, P2 = p2.x.shape
         result["prefill_mimo"] = prefill_figures(
             roofline, B2, L2, H2, p2.Bm.shape[-1], P2, R2, w2["chunk"], ms2,
-            "warp-specialised kernel, one workgroup per slice", None)
+            "warp-specialised kernel, one workgroup per slice", measured_traffic("k_scan_ws_w2"))
         del p2
         torch.cuda.empty_cache()
         # ---------------- SISO prefill (workload 1), gated and per-head variants ----------------
@@ -268,6 +268,7 @@ def main():
             bw.call()
         ms = bw.time(stream, 20)
         result["backward_siso"] = bw.figures(roofline, ms, peak_gbs, peak_tfs)
+        result["backward_siso"]["traffic"] = measured_traffic("backward_siso")
         del bw
         torch.cuda.empty_cache()
 
