@@ -113,7 +113,7 @@ def main():
     p3 = workload_inputs(3, device=dev)
     B3, L3, H3, R3, P3 = p3.x.shape
     N3 = p3.Bm.shape[-1]
-    ws3 = torch.empty(max(m3.workspace_bytes(m3.scan_dims(p3.x, p3.Bm, Q3, p3.A)), 16),
+    ws3 = torch.zeros(max(m3.workspace_bytes(m3.scan_dims(p3.x, p3.Bm, Q3, p3.A)), 16),
                       dtype=torch.uint8, device=dev)
     out3 = (torch.empty_like(p3.x), torch.empty(B3, H3, N3, P3, device=dev),
             torch.empty(B3, H3, R3, N3, device=dev, dtype=p3.x.dtype),
@@ -283,7 +283,7 @@ def time_scan(m3, torch, stream, copies, chunk, warm, n, out=None, z=None, theta
     """Mean ms of n m3_scan_fwd calls (after `warm` untimed ones), rotating
     over the input copies, one workspace."""
     c0 = copies[0]
-    ws = torch.empty(max(m3.workspace_bytes(m3.scan_dims(c0.x, c0.Bm, chunk, c0.A)), 16),
+    ws = torch.zeros(max(m3.workspace_bytes(m3.scan_dims(c0.x, c0.Bm, chunk, c0.A)), 16),
                      dtype=torch.uint8, device=c0.x.device)
     if out is None:
         Bb, Lb, Hb, Rb, Pb = c0.x.shape
@@ -340,7 +340,7 @@ def siso_figures(m3, roofline, torch, np, stream, dev, wp, workload_inputs, make
     Bp, Lp, Hp, Rp, Pp = base.x.shape
     Np = base.Bm.shape[-1]
     Qp = wp["chunk"]
-    ws = torch.empty(max(m3.workspace_bytes(m3.scan_dims(base.x, base.Bm, Qp, base.A)), 16),
+    ws = torch.zeros(max(m3.workspace_bytes(m3.scan_dims(base.x, base.Bm, Qp, base.A)), 16),
                      dtype=torch.uint8, device=dev)
     out = (torch.empty_like(base.x), torch.empty(Bp, Hp, Np, Pp, device=dev),
            torch.empty(Bp, Hp, Rp, Np, device=dev, dtype=base.x.dtype),
@@ -434,7 +434,7 @@ def prologue_figures(m3, roofline, torch, stream, dev, W, workload_inputs, peak_
         N = inp.Bm.shape[-1]
         Q = w["chunk"]
         d = m3.scan_dims(inp.x, inp.Bm, Q, inp.A)
-        ws = torch.empty(max(m3.workspace_bytes(d), 16), dtype=torch.uint8, device=dev)
+        ws = torch.zeros(max(m3.workspace_bytes(d), 16), dtype=torch.uint8, device=dev)
         o = (torch.empty_like(inp.x), torch.empty((B, H, N, P), device=dev),
              torch.empty((B, H, R, N), device=dev, dtype=inp.x.dtype),
              torch.empty((B, H, R, P), device=dev, dtype=inp.x.dtype))

@@ -137,8 +137,18 @@ typedef struct {
 /*
  * Bytes of device workspace m3_scan_fwd needs for `dims` (0 on invalid
  * dims).  The workspace holds the per-chunk state contributions and the
- * states entering each chunk.
+ * states entering each chunk, after a control block of M3_CTL_BYTES at its
+ * start (work-item counters, the look-back timeout count, a call counter).
+ * The control block must be zero before the workspace's first use with any
+ * m3_scan_* call (a zero-filled allocation, or a memset of its first
+ * M3_CTL_BYTES); every call then leaves it ready for the next one (the call's last
+ * workgroup resets it), so a single-pass scan is one kernel launch.  No m3
+ * call writes anything else there (m3_scan_bwd's workspace layout skips it
+ * too), so one workspace can serve every scan entry point and dims in turn;
+ * a caller that reuses its memory for anything else zeroes the block again
+ * before the next scan.  The rest of the workspace needs no initialisation.
  */
+#define M3_CTL_BYTES ((size_t)1280)
 size_t m3_scan_workspace_bytes(const m3_dims *dims);
 
 /*
@@ -348,7 +358,8 @@ m3_status m3_step_pro(const m3_dims *dims, const m3_prologue *pro,
  * headdim 64, chunk * rank = 64 (rank 1 chunk 64, rank 2 chunk 32, rank 4
  * chunk 16), no M3_THETA_PER_HEAD; A strided per head or per token.
  * Workspace: m3_scan_bwd_workspace_bytes(dims) bytes (16-byte aligned; four
- * fp32 N x P maps per chunk).  Token arrays may be NULL when seqlen == 0.
+ * fp32 N x P maps per chunk, after the scans' control block of M3_CTL_BYTES, which
+ * this call neither reads nor writes; no initialisation).  Token arrays may be NULL when seqlen == 0.
  * Alignment: x, B, C, dy, dx, dB, dC, the states and the workspace 16 bytes,
  * the rest 4 bytes (else M3_ERR_ALIGN).  Outputs must not overlap inputs.
  * Deterministic (no atomics).  Errors as m3_scan_fwd.
@@ -378,7 +389,8 @@ m3_status m3_scan_bwd(const m3_dims *dims,
  * M3_ERR_WORKSPACE before any device call.  Every call on a device shares
  * that device's array: calls that overlap in time on one device (other
  * streams, other threads) race and give wrong results; calls ordered on
- * one stream are safe (each clears what its kernels need zeroed).  The
+ * one stream are safe (the array starts zero-filled, and each call leaves
+ * its control block ready for the next).  The
  * look-back timeout count of these calls is not readable (m3_scan_check
  * takes a workspace); a timeout still shows as NaN results.
  */
@@ -412,7 +424,11 @@ m3_status m3_scan_check(const m3_dims *dims, const void *workspace, size_t works
  * devices, read at each scan call; 0 restores the default, 2^22 polls of a
  * few hundred nanoseconds each).  For tests of the timeout path: with a
  * limit of 1 a waiting workgroup gives up at once, so the scan finishes with
- * NaN results and a non-zero m3_scan_check count instead of waiting.
+ * NaN results and a non-zero m3_scan_check count instead of waiting.  The
+ * wait at the end of a scan for every work item to be past its look-back
+ * (before the workspace's control block is reset for the next call) is
+ * bounded by the larger of this limit and the default, so that a short limit
+ * leaves the control block clean.
  */
 void m3_set_wait_limit(uint32_t polls);
 

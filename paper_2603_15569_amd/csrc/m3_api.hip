@@ -14,6 +14,7 @@ static thread_local int g_last_hip_error = 0;
 static std::atomic<uint32_t> g_spin_max{kSpinMaxDefault};
 
 static size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+static_assert(kCtlBytes == M3_CTL_BYTES, "control block size as documented");
 
 ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N, int64_t P,
                                           int io_bytes, int acc_bytes, bool fused) {
@@ -21,14 +22,16 @@ ScanWorkspaceLayout scan_workspace_layout(int64_t BH, int64_t nchunks, int64_t N
     const size_t per = (size_t)BH * (size_t)nchunks;
     const size_t tot_bytes = per * (size_t)(N / 2 + 1) * (size_t)acc_bytes;
     const size_t state_bytes = per * (size_t)(N * P) * sizeof(float);
+    // the control block of the single-pass paths comes first on every path,
+    // so that a workspace shared by calls of either kind keeps it
     if (!fused) {
-        w.off_M = 0;
-        w.off_Sin = align_up(state_bytes, 256);
+        w.off_M = kCtlBytes;
+        w.off_Sin = align_up(w.off_M + state_bytes, 256);
         w.off_tot = align_up(w.off_Sin + per * (size_t)(N * P) * (size_t)io_bytes, 256);
         w.total = align_up(w.off_tot + tot_bytes, 256);
     } else {
         w.off_ctl = 0;
-        w.off_flags = align_up(kCtlWords * sizeof(uint32_t), 256);
+        w.off_flags = kCtlBytes;
         w.off_tot = align_up(w.off_flags + per * sizeof(uint32_t), 256);
         w.off_agg = align_up(w.off_tot + tot_bytes, 256);
         w.off_inc = align_up(w.off_agg + state_bytes, 256);
@@ -478,16 +481,20 @@ extern "C" m3_status m3_scan_check(const m3_dims *d, const void *workspace, size
                                                          impl.acc_bytes, impl.fused);
     if (!workspace || workspace_bytes < wl.total) return M3_ERR_WORKSPACE;
     if (!aligned16(workspace)) return M3_ERR_ALIGN;
+    // the control words up to group 0's ticket counter: the last finished
+    // call ran with epoch (group 0's epoch - 1) and counted its timeouts in
+    // that epoch's word (a call without look-back zeroes both words)
     const char *ctl = static_cast<const char *>(workspace) + wl.off_ctl;
-    uint32_t v = 0;
+    uint32_t w[kGroupStride + 2] = {};
     const hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e = hipMemcpyAsync(&v, ctl + sizeof(uint32_t), sizeof(uint32_t), hipMemcpyDeviceToHost, st);
+    hipError_t e = hipMemcpyAsync(w, ctl, sizeof(w), hipMemcpyDeviceToHost, st);
     if (e == hipSuccess) e = hipStreamSynchronize(st);
     if (e != hipSuccess) {
         g_last_hip_error = (int)e;
         return M3_ERR_HIP;
     }
-    *timeouts = v;
+    const uint32_t last_epoch = w[kGroupStride + 1] - 1u;
+    *timeouts = w[(last_epoch & 1u) ? kCtlTimeouts1 : kCtlTimeouts0];
     return M3_OK;
 }
 

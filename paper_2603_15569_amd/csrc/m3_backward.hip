@@ -807,7 +807,7 @@ BwdWorkspaceLayout bwd_workspace_layout(int64_t BH, int64_t nchunks, int64_t N, 
     const size_t per = (size_t)BH * (size_t)nchunks;
     const size_t st = per * (size_t)(N * P) * sizeof(float);
     BwdWorkspaceLayout w = {};
-    w.off_Af = 0;
+    w.off_Af = kCtlBytes;   // (the scans' control block, left untouched in a shared workspace)
     w.off_Mb = up(w.off_Af + st);
     w.off_Sst = up(w.off_Mb + st);
     w.off_Ust = up(w.off_Sst + st);

@@ -119,13 +119,23 @@ scan_launch_fn find_ws_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 scan_launch_fn find_fused_pro_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 step_launch_fn find_step_pro_impl(int io, int64_t N, int64_t P, int64_t R);
 
-// Control words of the single-pass scans (start of their workspace): ctl[0]
-// the ticket counter, ctl[1] the count of look-back waits that timed out, and
-// one ticket counter per slice group at ctl[kGroupStride * (y + 1)] (128
-// bytes apart, so that the groups' atomics do not share a cache line).
+// Control block of the single-pass scans (the first kCtlBytes of every scan
+// workspace; no other path writes there).  Zero before a workspace's first
+// use, the scans keep it valid from one call to the next:
+//   ctl[kCtlTimeouts0], ctl[kCtlTimeouts1]  look-back waits that gave up in
+//                      the call of an even / odd epoch (the call's janitor
+//                      zeroes the next epoch's word)
+//   ctl[kCtlReady]     epoch + 1 once the running call's flags are cleared
+// and per slice group y, 128 bytes apart (so that the groups' atomics do not
+// share a cache line), at ctl[kGroupStride * (y + 1)] the group's 64-bit
+// ticket counter: ticket, a flags-cleared bit, and the call epoch (the count
+// of calls finished on the workspace).  The last call's timeout count is
+// the word of epoch (group 0's epoch - 1).
+constexpr int kCtlTimeouts0 = 1, kCtlTimeouts1 = 3, kCtlReady = 5;
 constexpr int kGroups = 8;           // slice groups (one per XCD)
 constexpr int kGroupStride = 32;     // words
 constexpr int kCtlWords = kGroupStride * (kGroups + 1);
+constexpr size_t kCtlBytes = (kCtlWords * sizeof(uint32_t) + 255) / 256 * 256;
 
 // Byte offsets of the workspace regions for a scan.
 struct ScanWorkspaceLayout {

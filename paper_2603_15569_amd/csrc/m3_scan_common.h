@@ -1,6 +1,6 @@
 // Pieces shared by the single-pass prefill kernels (one chunk per workgroup,
 // and G chunks per workgroup): shape traits of the N = 128, P = 64 tiling,
-// element helpers, coherent accesses of the look-back, the reset kernel.
+// element helpers, coherent accesses of the look-back, the control block.
 #pragma once
 #include "m3_device.h"
 #include "m3_internal.h"
@@ -283,14 +283,13 @@ __device__ __forceinline__ int owned_tile(int w, int m) {
     return (m % 2 == 0) ? base + w : base + 2 * S::NWO - 1 - w;
 }
 
-// Clears the ticket counters, the timeout counter and the flags (one kernel
-// per translation unit: internal linkage).
-static __global__ void k_reset(uint32_t *ctl, uint32_t *flags, int64_t nflags) {
-    const int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i0 < 2) ctl[i0] = 0u;
-    if (i0 < kGroups) ctl[kGroupStride * (i0 + 1)] = 0u;
-    for (int64_t i = i0; i < nflags; i += (int64_t)gridDim.x * blockDim.x) flags[i] = 0u;
+// Control block words of slice group y: the 64-bit ticket counter (ticket in
+// bits 0-30, bit 31 set once the call's flags are cleared, the call epoch in
+// bits 32-63).
+__device__ __forceinline__ unsigned long long *group_counter(uint32_t *ctl, int y) {
+    return reinterpret_cast<unsigned long long *>(ctl + kGroupStride * (y + 1));
 }
+constexpr uint32_t kTicketReady = 0x80000000u;
 
 // Work item of a one-item-per-workgroup launch (grid = nsl * nchunks) whose
 // chunks chain within a slice: slices are split into kGroups groups (slice %
@@ -299,24 +298,109 @@ static __global__ void k_reset(uint32_t *ctl, uint32_t *flags, int64_t nflags) {
 // the same counter and is resident or done (forward progress).  A workgroup
 // asks the group of the XCD it runs on first (workgroups are spread over the
 // XCDs, so the eight counters share the traffic), then the others; since the
-// grid has exactly one workgroup per item, every workgroup finds one.
-// Called by one thread.
+// grid has exactly one workgroup per item, every workgroup finds one.  The
+// ticket's word also brings the call epoch and whether the flags were
+// already cleared.  Called by one thread.
 __device__ __forceinline__ void take_item(uint32_t *ctl, int64_t nsl, int64_t nchunks, int64_t *c,
-                                          int64_t *sl) {
+                                          int64_t *sl, uint32_t *epoch, bool *ready) {
     const int x = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & (kGroups - 1));   // XCC id
     for (int tries = 0; tries < kGroups; ++tries) {
         const int y = (x + tries) & (kGroups - 1);
         const int64_t ny = (nsl - y + kGroups - 1) / kGroups;   // slices of group y
         if (ny <= 0) continue;
-        const int64_t k = atomicAdd(ctl + kGroupStride * (y + 1), 1u);
+        const unsigned long long w =
+            __hip_atomic_fetch_add(group_counter(ctl, y), 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int64_t k = (int64_t)((uint32_t)w & ~kTicketReady);
         if (k < ny * nchunks) {
             *c = k / ny;
             *sl = y + kGroups * (k % ny);
+            *epoch = (uint32_t)(w >> 32);
+            *ready = ((uint32_t)w & kTicketReady) != 0;
             return;
         }
     }
     *c = -1;   // unreachable with one workgroup per item
     *sl = -1;
+    *epoch = 0;
+    *ready = false;
+}
+
+// The call's first item clears the look-back flags [0, n) (all threads of the
+// workgroup), then marks them cleared: the ready bit of every group's counter
+// (seen by the items that take their tickets after), and, once those have
+// landed, the ready word (polled by items that took theirs before, and by the
+// janitor before it resets the counters).
+__device__ __forceinline__ void clear_flags(uint32_t *ctl, uint32_t *flags, int64_t n, uint32_t epoch,
+                                            int tid, int nthr) {
+    unsigned long long *f2 = reinterpret_cast<unsigned long long *>(flags);   // 256-byte aligned
+    for (int64_t i = tid; i < n / 2; i += nthr)
+        __hip_atomic_store(f2 + i, 0ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if ((n & 1) && tid == 0) __hip_atomic_store(flags + n - 1, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    wait_stores_done();
+    __syncthreads();
+    if (tid == 0) {
+        for (int y = 0; y < kGroups; ++y)   // (the low word of each counter)
+            __hip_atomic_fetch_or(reinterpret_cast<uint32_t *>(group_counter(ctl, y)), kTicketReady,
+                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        wait_stores_done();
+        __hip_atomic_store(ctl + kCtlReady, epoch + 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+
+// A look-back wait of the call of this epoch gave up (counted in the epoch's
+// own timeout word: the janitor never resets it while the call runs).
+__device__ __forceinline__ void count_timeout(uint32_t *ctl, uint32_t epoch) {
+    atomicAdd(ctl + ((epoch & 1u) ? kCtlTimeouts1 : kCtlTimeouts0), 1u);
+}
+
+// Bounded wait (one thread) until the flags of this epoch are cleared; false
+// (and a timeout counted) if the wait gave up.
+__device__ __forceinline__ bool wait_flags_ready(uint32_t *ctl, uint32_t epoch, uint32_t spin_max) {
+    for (uint32_t spin = 0; spin < spin_max; ++spin) {
+        if (__hip_atomic_load(ctl + kCtlReady, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == epoch + 1u)
+            return true;
+        __builtin_amdgcn_s_sleep(2);
+    }
+    count_timeout(ctl, epoch);
+    return false;
+}
+
+// The call's janitor (the item of group 0's last ticket, one of the last to
+// start), at its very end, one thread: waits (bounded) until every group has
+// handed out all its tickets (so every workgroup holds its own and will touch
+// no counter again) and the flags-cleared marks have landed, then resets the
+// counters for the next epoch (ticket 0, flags not cleared) and zeroes the
+// next epoch's timeout word, so the next call on the workspace starts from a
+// clean block without a reset launch.  The wait is bounded by at least the
+// default limit; one that gives up counts a timeout and resets all the same.
+__device__ __forceinline__ void janitor_reset(uint32_t *ctl, int64_t nsl, int64_t nunits, uint32_t epoch,
+                                              uint32_t spin_max) {
+    const uint32_t lim = spin_max > kSpinMaxDefault ? spin_max : kSpinMaxDefault;
+    bool all = false;
+    for (uint32_t spin = 0; spin < lim && !all; ++spin) {
+        all = __hip_atomic_load(ctl + kCtlReady, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == epoch + 1u;
+#pragma unroll
+        for (int y = 0; y < kGroups; ++y) {
+            const int64_t items = (nsl - y + kGroups - 1) / kGroups * nunits;   // (0 past the last slice)
+            const uint32_t w = __hip_atomic_load(reinterpret_cast<uint32_t *>(group_counter(ctl, y)),
+                                                 __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            all = all && (int64_t)(w & ~kTicketReady) >= (items > 0 ? items : 0);
+        }
+        if (!all) __builtin_amdgcn_s_sleep(2);
+    }
+    if (!all) count_timeout(ctl, epoch);
+    __hip_atomic_store(ctl + ((epoch & 1u) ? kCtlTimeouts0 : kCtlTimeouts1), 0u, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+    const unsigned long long next = (unsigned long long)(epoch + 1u) << 32;
+    for (int y = 0; y < kGroups; ++y)
+        __hip_atomic_store(group_counter(ctl, y), next, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Whether item (unit u, slice sl) holds group 0's last ticket: the last unit
+// of group 0's last slice.
+__device__ __forceinline__ bool is_janitor(int64_t u, int64_t sl, int64_t nsl, int64_t nunits) {
+    const int64_t ny0 = (nsl + kGroups - 1) / kGroups;
+    return u == nunits - 1 && sl == (int64_t)kGroups * (ny0 - 1);
 }
 
 constexpr uint32_t kFlagInit = 3;   // probe result for "before the first chunk"

@@ -37,7 +37,11 @@
 //      K = rows); D x added; y staged per wave from the (transposed)
 //      accumulator tiles and stored.  A chunk of a single 64-row block
 //      stages B^ once for both uses; longer chunks restage it from cache.
-// A tiny reset kernel clears the ticket counters and the flags first.
+// The workspace's control block carries the tickets from call to call: the
+// call's first item clears the flags (every other item waits for that before
+// its first flag access), every item counts itself done after its last flag
+// access, and the item of group 0's last ticket resets the counters once all
+// are done, so a scan is one launch.
 #include <type_traits>
 
 #include "m3_device.h"
@@ -93,6 +97,7 @@ void k_scan_fused(ScanArgs a) {
     __shared__ __attribute__((aligned(16))) T s_XW[2 * NBUF * kSXr];  // x blocks, then W x blocks [row][p]
     __shared__ __attribute__((aligned(16))) T s_S[P * S::LDN];        // S_in^T [p][n] (io dtype)
     __shared__ int s_i[4];
+    __shared__ uint32_t s_ctl[2];   // call epoch, whether this item is the janitor
     // block prologue tables of the head (fp32): B gain, B bias, C gain, C bias
     // [R][N], then W_X, W_Z [R][P] (ones / zeros where not given)
     constexpr int kPB = 0, kPBb = R * N, kPC = 2 * R * N, kPCb = 3 * R * N, kPWX = 4 * R * N,
@@ -110,13 +115,26 @@ void k_scan_fused(ScanArgs a) {
     const int64_t nsl = a.batch * a.H;
     if (tid == 0) {
         int64_t ci, si;
-        take_item(a.ctl, nsl, a.nchunks, &ci, &si);
+        uint32_t ep;
+        bool rd;
+        take_item(a.ctl, nsl, a.nchunks, &ci, &si, &ep, &rd);
         s_i[0] = (int)ci;
         s_i[1] = (int)si;
+        s_i[2] = (int)ep;
+        s_i[3] = rd ? 1 : 0;
+        s_ctl[0] = ep;
+        s_ctl[1] = is_janitor(ci, si, nsl, a.nchunks) ? 1u : 0u;
     }
     __syncthreads();
     const int64_t c = s_i[0], sl = s_i[1];
+    const uint32_t epoch = (uint32_t)s_i[2];
+    bool flags_ready = s_i[3] != 0;
+    __syncthreads();
     if (c < 0) return;   // (cannot happen: one workgroup per item)
+    if (c == 0 && sl == 0) {   // the call's first item clears the look-back flags
+        clear_flags(a.ctl, a.flags, nsl * a.nchunks, epoch, tid, S::NTHR);
+        flags_ready = true;
+    }
     const int64_t b = sl / a.H, h = sl % a.H;
     const int64_t t0 = c * Q;
     const int nvalid = (int)min((int64_t)Q, a.L - t0);
@@ -582,7 +600,14 @@ void k_scan_fused(ScanArgs a) {
     // several row blocks) the predecessor's inclusive state is already there:
     // this chunk's own then follows at once, and successors that find no flag
     // wait for it.  (Single-block chunks measured faster always publishing.)
-    bool publish_agg = c > 0 && !last;
+    bool flags_lost = false;   // the wait for cleared flags gave up (error path)
+    if (!flags_ready && (c > 0 || !last)) {
+        if (tid == 0) s_i[0] = wait_flags_ready(a.ctl, s_ctl[0], a.spin_max) ? 0 : 1;
+        __syncthreads();
+        flags_lost = s_i[0] != 0;
+        __syncthreads();
+    }
+    bool publish_agg = c > 0 && !last && !flags_lost;
     if (S::NJB > 1 && publish_agg) {
         if (tid == 0)
             s_i[0] = __hip_atomic_load(a.flags + slot - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != kFlagInc;
@@ -650,8 +675,8 @@ void k_scan_fused(ScanArgs a) {
     } else {
         const int64_t sbase = sl * a.nchunks;
         int64_t j = c - 1;        // next predecessor to probe
-        int64_t jt = -2;          // terminal: -1 sequence start, >= 0 inclusive state
-        bool timed_out = false;
+        int64_t jt = flags_lost ? c - 1 : -2;   // terminal: -1 sequence start, >= 0 inclusive state
+        bool timed_out = flags_lost;
         while (jt == -2) {
             // probe predecessors j, j-1, ..., j-15 at once (lanes of wave 0)
             if (wave == 0) {
@@ -686,7 +711,7 @@ void k_scan_fused(ScanArgs a) {
                         if (f != 0u) break;
                         __builtin_amdgcn_s_sleep(2);
                     }
-                    if (f == 0u) atomicAdd(a.ctl + 1, 1u);   // timed out: report and stop waiting
+                    if (f == 0u) count_timeout(a.ctl, s_ctl[0]);   // timed out: report and stop waiting
                     s_i[1] = (f == 0u) ? 1 : 0;
                 }
                 __syncthreads();
@@ -783,7 +808,7 @@ void k_scan_fused(ScanArgs a) {
                 state_step(Sout[m2][0][v], Sout[m2][1][v], de, cs, sn, Ast[m2][0][v], Ast[m2][1][v]);
             }
         }
-        if (!last) {
+        if (!last && !flags_lost) {
             unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.inc + slot * SZ);
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2)
@@ -795,7 +820,7 @@ void k_scan_fused(ScanArgs a) {
             wait_stores_done();
             __syncthreads();
             if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagInc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        } else {
+        } else if (last) {
             float *fs = a.final_state + sl * SZ;
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2) {
@@ -941,15 +966,13 @@ void k_scan_fused(ScanArgs a) {
         }
         asm volatile("" ::: "memory");
     }
+    if (tid == 0 && s_ctl[1]) janitor_reset(a.ctl, nsl, a.nchunks, s_ctl[0], a.spin_max);
 }
 
 template <typename T, int Q, int R, bool kPro = false>
 hipError_t launch_fused(const ScanArgs &a, hipStream_t stream) {
     typedef FShape<T, Q, R> S;
     const int64_t nsl = a.batch * a.H;
-    const int64_t nflags = nsl * a.nchunks;
-    const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);
-    hipLaunchKernelGGL(k_reset, dim3(rblocks), dim3(256), 0, stream, a.ctl, a.flags, nflags);
     if (a.z)
         hipLaunchKernelGGL((k_scan_fused<T, Q, R, true, kPro>), dim3((unsigned)(nsl * a.nchunks)),
                            dim3(S::NTHR), 0, stream, a);

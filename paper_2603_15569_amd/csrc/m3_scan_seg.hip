@@ -97,6 +97,7 @@ void k_scan_seg(ScanArgs a) {
     __shared__ __attribute__((aligned(16))) T s_B[NBUF * kSB];        // B^ blocks [row][n]; S^T [p][n]
     __shared__ __attribute__((aligned(16))) T s_XW[2 * NBUF * kSXr];  // x blocks, then W x blocks [row][p]
     __shared__ int s_i[4];
+    __shared__ uint32_t s_ctl[2];   // call epoch, whether this item is the janitor
     static_assert(P == S::JB, "S^T [p][n] fits in the B^ block");
     static_assert(NW * 16 <= 2 * NBUF * S::JB, "y staging fits in the x / W x buffers");
 
@@ -122,19 +123,34 @@ void k_scan_seg(ScanArgs a) {
     // counters (segment-major within a group: every predecessor segment holds
     // an earlier ticket); independent slices take their block index
     int64_t sg = 0, sl = blockIdx.x;
+    uint32_t epoch = 0;
+    bool flags_ready = true;
     if (a.nseg > 1) {
         if (tid == 0) {
             int64_t si, sli;
-            take_item(a.ctl, nsl, a.nseg, &si, &sli);
+            uint32_t ep;
+            bool rd;
+            take_item(a.ctl, nsl, a.nseg, &si, &sli, &ep, &rd);
             s_i[0] = (int)si;
             s_i[1] = (int)sli;
+            s_i[2] = (int)ep;
+            s_i[3] = rd ? 1 : 0;
+            s_ctl[0] = ep;
+            s_ctl[1] = is_janitor(si, sli, nsl, a.nseg) ? 1u : 0u;
         }
         __syncthreads();
         sg = s_i[0];
         sl = s_i[1];
+        epoch = (uint32_t)s_i[2];
+        flags_ready = s_i[3] != 0;
+        __syncthreads();
         if (sg < 0) return;   // (cannot happen: one workgroup per item)
+        if (sg == 0 && sl == 0) {   // the call's first item clears the look-back flags
+            clear_flags(a.ctl, a.flags, nsl * a.nseg, epoch, tid, S::NTHR);
+            flags_ready = true;
+        }
     } else if (sl == 0 && tid == 0) {
-        a.ctl[1] = 0u;        // no look-back: the timeout count reads zero
+        a.ctl[kCtlTimeouts0] = a.ctl[kCtlTimeouts1] = 0u;   // no look-back: no timeouts
     }
     const int64_t b = sl / a.H, h = sl % a.H;
     const int64_t cbeg = sg * a.G, cend = min(cbeg + a.G, a.nchunks);
@@ -505,7 +521,14 @@ void k_scan_seg(ScanArgs a) {
             return (int64_t)((m2 * 2 + half) * 2 + vp) * S::NTHR + tid;
         };
         Acc *totp = static_cast<Acc *>(a.tot);
-        if (sg > 0 && !last_seg) {   // publish the aggregate (only successors read it)
+        bool flags_lost = false;   // the wait for cleared flags gave up (error path)
+        if (!flags_ready) {
+            if (tid == 0) s_i[0] = wait_flags_ready(a.ctl, s_ctl[0], a.spin_max) ? 0 : 1;
+            __syncthreads();
+            flags_lost = s_i[0] != 0;
+            __syncthreads();
+        }
+        if (sg > 0 && !last_seg && !flags_lost) {   // publish the aggregate (only successors read it)
             unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.agg + slot * SZ);
 #pragma unroll
             for (int m2 = 0; m2 < PTW; ++m2)
@@ -533,8 +556,8 @@ void k_scan_seg(ScanArgs a) {
         } else {
             const int64_t sbase = sl * a.nseg;
             int64_t j = sg - 1;       // next predecessor to probe
-            int64_t jt = -2;          // terminal: -1 sequence start, >= 0 inclusive state
-            bool timed_out = false;
+            int64_t jt = flags_lost ? sg - 1 : -2;   // terminal: -1 sequence start, >= 0 inclusive state
+            bool timed_out = flags_lost;
             while (jt == -2) {
                 if (wave == 0) {   // probe predecessors j, j-1, ..., j-15 at once
                     uint32_t f = 0;
@@ -568,7 +591,7 @@ void k_scan_seg(ScanArgs a) {
                             if (f != 0u) break;
                             __builtin_amdgcn_s_sleep(2);
                         }
-                        if (f == 0u) atomicAdd(a.ctl + 1, 1u);   // timed out: report and stop waiting
+                        if (f == 0u) count_timeout(a.ctl, s_ctl[0]);   // timed out: report and stop waiting
                         s_i[1] = (f == 0u) ? 1 : 0;
                     }
                     __syncthreads();
@@ -667,7 +690,7 @@ void k_scan_seg(ScanArgs a) {
                     state_step(Sout[m2][0][v], Sout[m2][1][v], de, cs, sn, Aseg[m2][0][v], Aseg[m2][1][v]);
                 }
             }
-            if (!last_seg) {
+            if (!last_seg && !flags_lost) {
                 unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.inc + slot * SZ);
 #pragma unroll
                 for (int m2 = 0; m2 < PTW; ++m2)
@@ -679,7 +702,7 @@ void k_scan_seg(ScanArgs a) {
                 wait_stores_done();
                 __syncthreads();
                 if (tid == 0) __hip_atomic_store(a.flags + slot, kFlagInc, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            } else {
+            } else if (last_seg) {
                 write_final(Sout);
             }
         }
@@ -957,6 +980,7 @@ void k_scan_seg(ScanArgs a) {
             asm volatile("" ::: "memory");
         }
     }
+    if (run_agg && tid == 0 && s_ctl[1]) janitor_reset(a.ctl, nsl, a.nseg, s_ctl[0], a.spin_max);
 }
 
 template <typename T, int Q, int R>
@@ -988,11 +1012,6 @@ hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
     // one segment per slice: the warp-specialised kernel, where built
     if (a.nseg == 1 && std::is_same<T, bf16>::value) {
         if (scan_launch_fn f = find_ws_impl(1, S::N, S::P, R, Q)) return f(a, stream);
-    }
-    if (a.nseg > 1) {
-        const int64_t nflags = nsl * a.nseg;
-        const int rblocks = (int)min((nflags + 255) / 256 + 1, (int64_t)1024);
-        hipLaunchKernelGGL(k_reset, dim3(rblocks), dim3(256), 0, stream, a.ctl, a.flags, nflags);
     }
     if (gate)
         hipLaunchKernelGGL((k_scan_seg<T, Q, R, true>), dim3((unsigned)(nsl * a.nseg)), dim3(S::NTHR), 0, stream, a);

@@ -97,7 +97,7 @@ void k_scan_ws(ScanArgs a) {
 
     const int64_t sl = blockIdx.x;
     // no look-back here: the timeout count of the workspace reads zero
-    if (sl == 0 && tid == 0) a.ctl[1] = 0u;
+    if (sl == 0 && tid == 0) a.ctl[kCtlTimeouts0] = a.ctl[kCtlTimeouts1] = 0u;
     const int64_t b = sl / a.H, h = sl % a.H;
     const int64_t nch = a.nchunks;
     const int64_t tstr = a.H;

@@ -52,6 +52,7 @@ EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_sc
            "m3_scan_fwd_pro", "m3_step_pro", "m3_scan_bwd", "m3_scan_bwd_workspace_bytes",
            "m3_status_string", "m3_last_hip_error")
 SCRATCH_BYTES = 256 << 20   # M3_SCRATCH_BYTES: the allocation-free scan's fixed workspace
+CTL_BYTES = 1280            # M3_CTL_BYTES: a scan workspace's control block (zero before first use)
 _lib = None
 
 
@@ -202,7 +203,7 @@ def scan_fwd(x, Bm, Cm, dt, A, lam, theta, D, chunk: int,
         y, fs, cB, cX = out
     nbytes = workspace_bytes(d)
     if workspace is None and nbytes > 0:
-        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        workspace = torch.zeros(nbytes, dtype=torch.uint8, device=dev)   # control block zero
     icB, icX = (None, None) if init_carry is None else init_carry
     wsb = workspace.numel() if workspace is not None else 0
     if z is None:
@@ -270,7 +271,7 @@ def scan_fwd_varlen(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, cu_seqlens,
         longest = max([cu[i + 1] - cu[i] for i in range(S)] + [0])
         d1 = M3Dims(1, longest, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags,
                     0, st, sh, int(seg))
-        workspace = torch.empty(max(workspace_bytes(d1), 16), dtype=torch.uint8, device=dev)
+        workspace = torch.zeros(max(workspace_bytes(d1), 16), dtype=torch.uint8, device=dev)
     icB, icX = (None, None) if init_carry is None else init_carry
     cu_arr = (ctypes.c_int64 * len(cu))(*cu)
     _check(lib().m3_scan_fwd_varlen(ctypes.byref(d), cu_arr, _p(x), _p(Bm), _p(Cm), _p(dt), _p(A),
@@ -352,7 +353,7 @@ def scan_fwd_pro(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, pro: M3Prologue, r
         y, fs, cB, cX = out
     nbytes = workspace_bytes(d)
     if workspace is None and nbytes > 0:
-        workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        workspace = torch.zeros(nbytes, dtype=torch.uint8, device=dev)   # control block zero
     icB, icX = (None, None) if init_carry is None else init_carry
     wsb = workspace.numel() if workspace is not None else 0
     _check(lib().m3_scan_fwd_pro(ctypes.byref(d), ctypes.byref(pro), _p(x), _p(Bm), _p(Cm),

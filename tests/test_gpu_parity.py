@@ -54,8 +54,10 @@ def run_scan(inp, chunk, init_state=None, init_carry=None, nan_fill=True, mode="
     # for the three-kernel path)
     assert m3.scan_check(m3.scan_dims(x, inp.Bm, chunk, inp.A, **kw), ws) == 0, "look-back wait timed out"
     if single_pass and L > 0:
-        # the same word read directly: word 1 of the single-pass workspace
-        assert int(ws[4:8].view(torch.int32).item()) == 0
+        # the same read directly: after a clean call both timeout words of the
+        # control block (words 1 and 3, for even and odd call epochs) are zero
+        w = ws[:16].view(torch.int32).cpu().numpy()
+        assert w[1] == 0 and w[3] == 0
     return y, fs, cB, cX
 
 
@@ -794,3 +796,67 @@ def test_lookback_timeout_reported(mode, seg):
     y2, fs2, (cB2, cX2) = m3.scan_fwd(*args, chunk=Q, workspace=ws, check=True, **kw)
     assert m3.scan_check(d, ws) == 0
     check_slices(inp, y2, fs2, cB2, cX2, sample_slices(4, 16, 6, 12), TOL["bf16"], label="after timeout")
+
+
+def ctl_words(ws):
+    """The workspace's control block as int32 words (copied to the host)."""
+    return ws[:m3.CTL_BYTES].view(torch.int32).cpu().numpy()
+
+
+def test_workspace_shared_across_calls():
+    """One zero-filled workspace serves scans of different kernels and shapes
+    and a backward call in turn.  Each single-pass call's last workgroup
+    resets the control block for the next call (no reset launch): after
+    every call the work-item and timeout counters read zero and the call
+    counter has advanced once per single-pass call; every result matches the
+    oracle, and repeating the first scan later gives the same bits."""
+    cases = [(1, 64, "per_chunk", 0, 700), (1, 64, "seg", 2, 700), (1, 64, "split", 0, 300),
+             (4, 32, "per_chunk", 0, 333), (2, 64, "seg", 3, 900)]
+    B_, H = 2, 4
+    inps = [make_scan_inputs(B_, L, H, 64, 128, R, io="bf16", seed=2100 + k, device=DEV, chunk=Q)
+            for k, (R, Q, mode, seg, L) in enumerate(cases)]
+    kws = [dict(split=mode == "split", per_chunk=mode == "per_chunk", seg=seg)
+           for (R, Q, mode, seg, L) in cases]
+    need = [m3.workspace_bytes(m3.scan_dims(i.x, i.Bm, c[1], i.A, **kw))
+            for i, c, kw in zip(inps, cases, kws)]
+    binp = make_scan_inputs(1, 200, 3, 64, 128, 1, io="bf16", seed=2199, device=DEV, chunk=64)
+    bd = m3.scan_dims(binp.x, binp.Bm, 64, binp.A)
+    need.append(int(m3.lib().m3_scan_bwd_workspace_bytes(__import__("ctypes").byref(bd))))
+    ws = torch.zeros(max(need), dtype=torch.uint8, device=DEV)
+    groups = [32 * (y + 1) for y in range(8)]
+    epoch = 0
+    first = None
+    for rep in range(2):
+        for k, ((R, Q, mode, seg, L), inp, kw) in enumerate(zip(cases, inps, kws)):
+            if rep == 1 and k > 0:
+                break
+            say(f"shared workspace: call R={R} Q={Q} mode={mode} seg={seg} L={L}")
+            y, fs, (cB, cX) = m3.scan_fwd(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                          inp.D, chunk=Q, workspace=ws, check=True, **kw)
+            torch.cuda.synchronize()
+            w = ctl_words(ws)
+            epoch += 0 if mode == "split" else 1
+            # both timeout words zero; every group's ticket counter at ticket 0
+            # with the flags-cleared bit off and the epoch (the count of
+            # single-pass calls) in its high word; the ready word at the last
+            # call's epoch + 1
+            assert w[1] == 0 and w[3] == 0, w[:8]
+            assert all(w[g] == 0 and w[g + 1] == epoch for g in groups), \
+                [(w[g], w[g + 1]) for g in groups]
+            assert w[5] == epoch, (w[5], epoch)
+            if rep == 0:
+                check_slices(inp, y, fs, cB, cX, [(b, h) for b in range(B_) for h in range(H)],
+                             TOL["bf16"], label=f"shared workspace {mode} R={R}")
+                if k == 0:
+                    first = (y.clone(), fs.clone())
+            else:
+                assert torch.equal(y, first[0]) and torch.equal(fs, first[1])
+        if rep == 0:   # a backward call on the same workspace leaves the block alone
+            say("shared workspace: backward call")
+            g = torch.Generator(DEV).manual_seed(3)
+            dy = torch.randn(binp.x.shape, device=DEV, generator=g).to(binp.x.dtype)
+            before = ctl_words(ws)
+            m3.scan_bwd(binp.x, binp.Bm, binp.Cm, binp.dt, binp.A, binp.lam, binp.theta, binp.D,
+                        dy, 64, workspace=ws)
+            torch.cuda.synchronize()
+            assert np.array_equal(ctl_words(ws), before)

@@ -103,9 +103,16 @@ def test_workspace_bytes(L):
     assert nb % 256 == 0
     d.flags = m3.M3_SCAN_SPLIT
     nb = L.m3_scan_workspace_bytes(ctypes.byref(d))
-    # three-kernel: per-chunk fp32 contributions, bf16 entering states, totals
-    assert nb >= per * 128 * 64 * (4 + 2) + per * 65 * 4
+    # three-kernel: the control block it leaves alone, per-chunk fp32
+    # contributions, bf16 entering states, totals
+    assert nb >= m3.CTL_BYTES + per * 128 * 64 * (4 + 2) + per * 65 * 4
     assert nb % 256 == 0
+
+
+def test_control_block_size_matches_header():
+    hdr = open(os.path.join(ROOT, "include", "m3.h")).read()
+    m = re.search(r"#define M3_CTL_BYTES \(\(size_t\)(\d+)\)", hdr)
+    assert m and int(m.group(1)) == m3.CTL_BYTES and m3.CTL_BYTES % 256 == 0
 
 
 def test_step_host_validation(L):
