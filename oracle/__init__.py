@@ -207,6 +207,44 @@ def structured_input(xp, w):
 
 
 # ---------------------------------------------------------------------------
+# Optional output norm of the block (Sec. 4, hybrid models; App. table of the
+# norm type and placement ablation): a grouped RMS normalisation of the SSM
+# output, either before the output gate (pre-gate: g o norm(Y) o SiLU(Z)) or
+# after it (post-gate: g o norm(Y o SiLU(Z))).  Grouped: the mean of squares
+# runs over `group` consecutive channels of one (token, head, rank) row of Y
+# (the paper gives no group size: it is a parameter here, group = headdim
+# being one RMS per row).  fp64.
+# ---------------------------------------------------------------------------
+
+def group_rms(v, group, eps):
+    """v [..., P] -> v / sqrt(mean of squares over each run of `group`
+    consecutive channels + eps), P a multiple of group."""
+    v = _f64(v)
+    P = v.shape[-1]
+    if group <= 0 or P % group:
+        raise ValueError("group must divide the channel count")
+    g = v.reshape(v.shape[:-1] + (P // group, group))
+    out = g / np.sqrt(np.mean(g * g, axis=-1, keepdims=True) + eps)
+    return out.reshape(v.shape)
+
+
+def out_norm(y, group, eps=1e-6, gain=None, z=None, pre_gate=True):
+    """Output norm of the block: y [..., P] (the SSM output, D skip
+    included), z like y or None (no output gate), gain broadcast against y
+    (per head, rank and channel; None: ones).  pre_gate: gain o
+    group_rms(y) o SiLU(z); else gain o group_rms(y o SiLU(z))."""
+    y = _f64(y)
+    if pre_gate:
+        out = group_rms(y, group, eps)
+        if gain is not None:
+            out = out * _f64(gain)
+        return out if z is None else out * silu(z)
+    u = y if z is None else y * silu(z)
+    out = group_rms(u, group, eps)
+    return out if gain is None else out * _f64(gain)
+
+
+# ---------------------------------------------------------------------------
 # Slice extraction from tensors in the library layout.
 # ---------------------------------------------------------------------------
 

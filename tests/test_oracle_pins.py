@@ -398,3 +398,70 @@ def test_structured_input_feeds_rank_columns(oracle_lib):
         xr[:, r, :] = xp[0]
         ref += c[r] * run1(dict(s, x=xr))[0]
     assert np.max(np.abs(y - ref)) <= 1e-12 * np.max(np.abs(ref))
+
+
+# ---------------------------------------------------------------------------
+# Output norm (Sec. 4 hybrid models; App. norm type / placement ablation):
+# grouped RMS of the SSM output before or after the output gate.
+# ---------------------------------------------------------------------------
+
+def test_out_norm_worked_example():
+    """y row [3, 4, 0, 2] in groups of two: the first group's RMS is
+    sqrt(12.5), the second's sqrt(2); no gain, no gate, eps 0."""
+    y = np.array([[3.0, 4.0, 0.0, 2.0]])
+    got = oracle.out_norm(y, 2, eps=0.0)
+    want = np.array([[3 / math.sqrt(12.5), 4 / math.sqrt(12.5), 0.0, 2 / math.sqrt(2.0)]])
+    np.testing.assert_allclose(got, want, rtol=1e-15)
+
+
+def test_out_norm_groups_are_independent_and_unit_rms():
+    rng = np.random.default_rng(70)
+    y = rng.standard_normal((3, 5, 64))
+    a = oracle.out_norm(y, 16, eps=1e-12)
+    # every group of 16 channels has unit RMS
+    g = a.reshape(3, 5, 4, 16)
+    np.testing.assert_allclose(np.sqrt(np.mean(g * g, axis=-1)), 1.0, rtol=1e-9)
+    # scaling one group changes only that group (and not even it: scale invariance)
+    y2 = y.copy()
+    y2[..., 16:32] *= -7.5
+    b = oracle.out_norm(y2, 16, eps=1e-12)
+    np.testing.assert_allclose(b[..., :16], a[..., :16], rtol=1e-12)
+    np.testing.assert_allclose(b[..., 32:], a[..., 32:], rtol=1e-12)
+    np.testing.assert_allclose(b[..., 16:32], -a[..., 16:32], rtol=1e-9)
+
+
+def test_out_norm_constant_group_closed_form():
+    y = np.full((2, 32), 0.25)
+    gain = np.linspace(0.5, 2.0, 32)
+    got = oracle.out_norm(y, 8, eps=1e-3, gain=gain)
+    np.testing.assert_allclose(got, np.broadcast_to(gain * 0.25 / math.sqrt(0.0625 + 1e-3), got.shape),
+                               rtol=1e-14)
+
+
+def test_out_norm_whole_row_group_is_bcnorm_form():
+    """group = the row length: one RMS over the row, the same form as the
+    (separately pinned) state-axis norm."""
+    rng = np.random.default_rng(71)
+    y = rng.standard_normal((4, 64))
+    gain = rng.uniform(0.5, 1.5, 64)
+    np.testing.assert_allclose(oracle.out_norm(y, 64, eps=1e-5, gain=gain),
+                               oracle.rms_norm(y, gain=gain, eps=1e-5), rtol=1e-13)
+
+
+def test_out_norm_pre_and_post_gate():
+    """The gate enters after the norm (pre-gate) or inside it (post-gate): with
+    SiLU(z) constant s over a group, post-gate = (pre-gate) / |s|
+    (eps -> 0); with varying z the two differ; without z they agree."""
+    rng = np.random.default_rng(72)
+    y = rng.standard_normal((2, 3, 32))
+    zc = np.repeat(rng.uniform(-3, 3, (2, 3, 4, 1)), 8, axis=-1).reshape(2, 3, 32)
+    s = oracle.silu(zc)
+    pre = oracle.out_norm(y, 8, eps=1e-14, z=zc, pre_gate=True)
+    post = oracle.out_norm(y, 8, eps=1e-14, z=zc, pre_gate=False)
+    np.testing.assert_allclose(post, pre / np.abs(s), rtol=1e-7)
+    np.testing.assert_allclose(pre, oracle.group_rms(y, 8, 1e-14) * s, rtol=1e-14)
+    z = rng.standard_normal((2, 3, 32))
+    assert np.max(np.abs(oracle.out_norm(y, 8, z=z) - oracle.out_norm(y, 8, z=z, pre_gate=False))) > 0.1
+    np.testing.assert_array_equal(oracle.out_norm(y, 8), oracle.out_norm(y, 8, pre_gate=False))
+    with pytest.raises(ValueError):
+        oracle.group_rms(y, 12, 1e-6)
