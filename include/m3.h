@@ -289,11 +289,25 @@ m3_status m3_step_gated(const m3_dims *dims,
  *     [..][nheads][headdim] (one headdim-vector per token and head) and the
  *     recurrence uses X[r][p] = w_x[h][r][p] X'[p] (rounded to the io dtype);
  *     w_z does the same for the gate input z (Z = w_z o Z'), and needs z.
+ *   - Output norm (Sec. 4, hybrid models; App. table of the norm type and
+ *     placement ablation), the block's epilogue, fused into the y store:
+ *     with out_norm = M3_OUT_NORM_PRE_GATE, y becomes
+ *     out_gain o rms(y) o SiLU(z) (z NULL: no SiLU factor); with
+ *     M3_OUT_NORM_POST_GATE, out_gain o rms(y o SiLU(z)).  rms divides each
+ *     run of out_group consecutive channels of a (token, head, rank) row of
+ *     y by sqrt(mean of their squares + out_eps); out_group is a power of two
+ *     with 8 <= out_group <= headdim (headdim: one RMS per row).  y here is
+ *     the SSM output with the D skip, rounded to the io dtype, as the plain
+ *     scan would store it; out_gain [nheads][rank][headdim] (NULL: ones);
+ *     out_eps > 0.  The paper gives no group size: it is the caller's.
  * All tables are fp32 device arrays, 16-byte aligned.  The norm, gain and
  * bias are evaluated in fp32.  The carry written (and read back as
  * init_carry) holds the B and X that the recurrence used, after the
  * prologue.
  */
+#define M3_OUT_NORM_NONE 0
+#define M3_OUT_NORM_PRE_GATE 1
+#define M3_OUT_NORM_POST_GATE 2
 typedef struct {
     int32_t bc_norm;                  /* nonzero: RMS-normalise B and C columns  */
     float eps;                        /* > 0 when bc_norm                         */
@@ -301,6 +315,10 @@ typedef struct {
     const float *bias_B, *bias_C;     /* biases [nheads][rank][dstate] or NULL    */
     const float *w_x;                 /* [nheads][rank][headdim] or NULL          */
     const float *w_z;                 /* [nheads][rank][headdim] or NULL          */
+    int32_t out_norm;                 /* M3_OUT_NORM_*                            */
+    int32_t out_group;                /* channels per RMS group (with out_norm)   */
+    float out_eps;                    /* > 0 with out_norm                        */
+    const float *out_gain;            /* [nheads][rank][headdim] or NULL          */
 } m3_prologue;
 
 /*
@@ -313,8 +331,10 @@ typedef struct {
  * dstate 128, headdim 64, rank 1/2/4 and chunk 32/64/128 with chunk*rank a
  * multiple of 64 and at most 512 (else M3_ERR_UNSUPPORTED, also with
  * M3_SCAN_SPLIT).  Errors as m3_scan_fwd; M3_ERR_NULL for a NULL pro, or
- * w_z without z; M3_ERR_SHAPE for bc_norm with eps <= 0 (or NaN) and for
- * gains without bc_norm; M3_ERR_ALIGN for a misaligned table.
+ * w_z without z; M3_ERR_SHAPE for bc_norm with eps <= 0 (or NaN), for
+ * gains without bc_norm, for an unknown out_norm, and with out_norm for
+ * out_eps <= 0 (or NaN), an out_gain without it, or an out_group that is
+ * not a power of two in [8, headdim]; M3_ERR_ALIGN for a misaligned table.
  */
 m3_status m3_scan_fwd_pro(const m3_dims *dims, const m3_prologue *pro,
                           const void *x, const void *B, const void *C,

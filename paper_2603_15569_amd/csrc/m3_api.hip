@@ -44,13 +44,21 @@ static bool aligned16(const void *p) { return p == nullptr || ((uintptr_t)p & 15
 static bool aligned4(const void *p) { return p == nullptr || ((uintptr_t)p & 3u) == 0; }
 
 // Checks a block prologue and converts it (pro may be null: none).
-static m3_status check_prologue(const m3_prologue *pro, bool have_z, Prologue *out) {
+static m3_status check_prologue(const m3_prologue *pro, bool have_z, int64_t headdim, Prologue *out) {
     *out = Prologue{};
     if (!pro) return M3_OK;
     if (pro->bc_norm && !(pro->eps > 0.f)) return M3_ERR_SHAPE;   // (also NaN)
     if (!pro->bc_norm && (pro->norm_B || pro->norm_C)) return M3_ERR_SHAPE;
+    if (pro->out_norm < M3_OUT_NORM_NONE || pro->out_norm > M3_OUT_NORM_POST_GATE) return M3_ERR_SHAPE;
+    if (pro->out_norm) {
+        const int32_t gs = pro->out_group;
+        if (!(pro->out_eps > 0.f) || gs < 8 || gs > headdim || (gs & (gs - 1))) return M3_ERR_SHAPE;
+    } else if (pro->out_gain) {
+        return M3_ERR_SHAPE;
+    }
     if (pro->w_z && !have_z) return M3_ERR_NULL;
-    const void *tabs[] = {pro->norm_B, pro->norm_C, pro->bias_B, pro->bias_C, pro->w_x, pro->w_z};
+    const void *tabs[] = {pro->norm_B, pro->norm_C, pro->bias_B, pro->bias_C, pro->w_x, pro->w_z,
+                          pro->out_gain};
     for (const void *p : tabs)
         if (!aligned16(p)) return M3_ERR_ALIGN;
     out->on = 1;
@@ -59,6 +67,10 @@ static m3_status check_prologue(const m3_prologue *pro, bool have_z, Prologue *o
     out->gB = pro->norm_B; out->gC = pro->norm_C;
     out->bB = pro->bias_B; out->bC = pro->bias_C;
     out->wx = pro->w_x; out->wz = pro->w_z;
+    out->onorm = pro->out_norm;
+    out->ogroup = pro->out_norm ? pro->out_group : 0;
+    out->oeps = pro->out_eps;
+    out->og = pro->out_gain;
     return M3_OK;
 }
 
@@ -149,7 +161,7 @@ static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const 
     m3_status s = check_scan_dims(d, &impl, &nc);
     if (s != M3_OK) return s;
     Prologue pr;
-    s = check_prologue(pro, gated, &pr);
+    s = check_prologue(pro, gated, d->headdim, &pr);
     if (s != M3_OK) return s;
     if (pr.on) {   // the block prologue runs in the per-chunk kernel (same workspace layout)
         scan_launch_fn f = (d->flags & M3_SCAN_SPLIT) ? nullptr
@@ -325,7 +337,7 @@ static m3_status step(const m3_dims *d, float *state, void *carryB, void *carryX
     m3_status s = check_dims_common(d);
     if (s != M3_OK) return s;
     Prologue pr;
-    s = check_prologue(pro, gated, &pr);
+    s = check_prologue(pro, gated, d->headdim, &pr);
     if (s != M3_OK) return s;
     step_launch_fn fn = pr.on ? find_step_pro_impl(d->io, d->dstate, d->headdim, d->rank)
                               : find_step_impl(d->io, d->dstate, d->headdim, d->rank);

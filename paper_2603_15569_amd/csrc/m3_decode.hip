@@ -274,15 +274,32 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     const float Dh = a.D[h];
 #pragma unroll
     for (int k = 0; k < TZ; ++k) {
-        const int e = tid + k * NT;
-        if (e < R * P) {
-            float v = 0.f;
+        const int e = tid + k * NT, ec = min(e, R * P - 1);
+        float v = 0.f;
 #pragma unroll
-            for (int w = 0; w < NW; ++w) v += s_red[w * R * P + e];
-            v += Dh * s_X[e];
-            if constexpr (kGate) v *= silu(zv[k]);
-            yt[e] = from_f32<T>(v);
+        for (int w = 0; w < NW; ++w) v += s_red[w * R * P + ec];
+        v += Dh * s_X[ec];
+        if constexpr (kPro) {
+            // output norm (optional) on y as stored (io dtype): a group's
+            // channels are consecutive lanes of one wave (R P is a multiple
+            // of the wave, so lanes past the outputs fill whole waves)
+            static_assert((R * P) % kWave == 0, "whole waves of outputs");
+            const float gz = kGate ? silu(zv[k]) : 1.f;
+            if (a.pro.onorm) {
+                const bool post = a.pro.onorm == 2;
+                v = to_f32(from_f32<T>(v));
+                if (post) v *= gz;
+                float ss = v * v;
+                for (int o = 1; o < a.pro.ogroup; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+                v *= rsqrtf(ss / (float)a.pro.ogroup + a.pro.oeps) * (a.pro.og ? a.pro.og[h * (R * P) + ec] : 1.f);
+                if (!post) v *= gz;
+            } else {
+                v *= gz;
+            }
+        } else if constexpr (kGate) {
+            v *= silu(zv[k]);
         }
+        if (e < R * P) yt[e] = from_f32<T>(v);
     }
 }
 

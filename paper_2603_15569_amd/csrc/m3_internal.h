@@ -16,6 +16,9 @@ struct Prologue {
     int on, bcnorm;
     float eps;
     const float *gB, *gC, *bB, *bC, *wx, *wz;
+    int onorm, ogroup;     // output norm: 0 none, 1 before the gate, 2 after it; channels a group
+    float oeps;
+    const float *og;       // output norm gain [nheads][rank][headdim] (null: ones)
 };
 
 // Arguments of one prefill scan, already validated by the front end.

@@ -99,10 +99,11 @@ void k_scan_fused(ScanArgs a) {
     __shared__ int s_i[4];
     __shared__ uint32_t s_ctl[2];   // call epoch, whether this item is the janitor
     // block prologue tables of the head (fp32): B gain, B bias, C gain, C bias
-    // [R][N], then W_X, W_Z [R][P] (ones / zeros where not given)
+    // [R][N], then W_X, W_Z and the output norm's gain [R][P] (ones / zeros
+    // where not given)
     constexpr int kPB = 0, kPBb = R * N, kPC = 2 * R * N, kPCb = 3 * R * N, kPWX = 4 * R * N,
-                  kPWZ = 4 * R * N + R * P;
-    __shared__ __attribute__((aligned(16))) float s_pro[kPro ? 4 * R * N + 2 * R * P : 4];
+                  kPWZ = 4 * R * N + R * P, kPGY = 4 * R * N + 2 * R * P;
+    __shared__ __attribute__((aligned(16))) float s_pro[kPro ? 4 * R * N + 3 * R * P : 4];
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
     static_assert(P <= S::JB && NW * 16 <= 2 * NBUF * S::JB, "y staging fits in the x / W x buffers");
@@ -310,6 +311,7 @@ void k_scan_fused(ScanArgs a) {
         for (int e = tid; e < R * P; e += S::NTHR) {
             s_pro[kPWX + e] = a.pro.wx ? a.pro.wx[hp + e] : 1.f;
             s_pro[kPWZ + e] = a.pro.wz ? a.pro.wz[hp + e] : 1.f;
+            s_pro[kPGY + e] = a.pro.og ? a.pro.og[hp + e] : 1.f;
         }
     }
     {
@@ -952,17 +954,44 @@ void k_scan_fused(ScanArgs a) {
         for (int i = 0; i < NPC; ++i) {
             const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * S::CE;
             const int row = TT * 16 + rl, t = row / R, r = row % R;
-            if (t < nvalid) {
-                V16 yv = *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
-                if constexpr (kGate && kPro) {   // Z = W_Z o Z' in fp32, then the gate
+            V16 yv = *reinterpret_cast<const V16 *>(&s_y[rl * LDP + col]);
+            if constexpr (kPro) {
+                // gate factor SiLU(W_Z o Z') in fp32, then (optionally) the
+                // output norm: the group's pieces sit in consecutive lanes
+                // (a row's RP pieces are RP consecutive lanes), so its sum of
+                // squares is a lane sum (rows past the end of the sequence
+                // hold finite values and are not stored)
+                float yf[S::CE], gz[S::CE];
 #pragma unroll
-                    for (int e = 0; e < S::CE; ++e)
-                        fset(yv, e, fget(yv, e) * silu(fget(zp[m][i], e) * s_pro[kPWZ + r * P + col + e]));
-                } else if constexpr (kGate) {
-                    yv = gate_piece<T>(yv, zp[m][i]);
+                for (int e = 0; e < S::CE; ++e) {
+                    yf[e] = fget(yv, e);
+                    gz[e] = kGate ? silu(fget(zp[m][i], e) * s_pro[kPWZ + r * P + col + e]) : 1.f;
                 }
-                *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) = yv;
+                if (a.pro.onorm) {   // (uniform)
+                    const bool post = a.pro.onorm == 2;
+                    float ss = 0.f;
+#pragma unroll
+                    for (int e = 0; e < S::CE; ++e) {
+                        if (post) yf[e] *= gz[e];
+                        ss += yf[e] * yf[e];
+                    }
+                    for (int o = 1; o < a.pro.ogroup / S::CE; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+                    const float sc = rsqrtf(ss / (float)a.pro.ogroup + a.pro.oeps);
+#pragma unroll
+                    for (int e = 0; e < S::CE; ++e) {
+                        yf[e] *= sc * s_pro[kPGY + r * P + col + e];
+                        if (!post) yf[e] *= gz[e];
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < S::CE; ++e) yf[e] *= gz[e];
+                }
+#pragma unroll
+                for (int e = 0; e < S::CE; ++e) fset(yv, e, yf[e]);
+            } else if constexpr (kGate) {
+                yv = gate_piece<T>(yv, zp[m][i]);
             }
+            if (t < nvalid) *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) = yv;
         }
         asm volatile("" ::: "memory");
     }

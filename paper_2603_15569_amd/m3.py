@@ -34,11 +34,17 @@ class M3Dims(ctypes.Structure):
 
 
 class M3Prologue(ctypes.Structure):
-    """m3_prologue: the block prologue fused into the kernels' input loads."""
+    """m3_prologue: the block prologue fused into the kernels' input loads,
+    and the optional output norm fused into the y store."""
     _fields_ = [("bc_norm", ctypes.c_int32), ("eps", ctypes.c_float),
                 ("norm_B", ctypes.c_void_p), ("norm_C", ctypes.c_void_p),
                 ("bias_B", ctypes.c_void_p), ("bias_C", ctypes.c_void_p),
-                ("w_x", ctypes.c_void_p), ("w_z", ctypes.c_void_p)]
+                ("w_x", ctypes.c_void_p), ("w_z", ctypes.c_void_p),
+                ("out_norm", ctypes.c_int32), ("out_group", ctypes.c_int32),
+                ("out_eps", ctypes.c_float), ("out_gain", ctypes.c_void_p)]
+
+
+M3_OUT_NORM_NONE, M3_OUT_NORM_PRE_GATE, M3_OUT_NORM_POST_GATE = 0, 1, 2
 
 
 class M3Error(RuntimeError):
@@ -318,14 +324,18 @@ def step(state, carry, x_t, B_t, C_t, dt_t, A, lam_t, theta_t, D, y=None, stream
 
 
 def prologue(bc_norm: bool = False, eps: float = 1e-6, norm_B=None, norm_C=None, bias_B=None,
-             bias_C=None, w_x=None, w_z=None) -> M3Prologue:
+             bias_C=None, w_x=None, w_z=None, out_norm: int = M3_OUT_NORM_NONE,
+             out_group: int = 0, out_eps: float = 1e-6, out_gain=None) -> M3Prologue:
     """An m3_prologue over fp32 device tables: gains and biases [H,R,N],
-    w_x / w_z [H,R,P] (None: not applied)."""
-    for t in (norm_B, norm_C, bias_B, bias_C, w_x, w_z):
+    w_x / w_z [H,R,P] (None: not applied); the output norm (M3_OUT_NORM_*)
+    over groups of out_group channels with gain out_gain [H,R,P] (None:
+    ones)."""
+    for t in (norm_B, norm_C, bias_B, bias_C, w_x, w_z, out_gain):
         if t is not None and t.dtype != torch.float32:
             raise ValueError("prologue tables are fp32")
     return M3Prologue(1 if bc_norm else 0, float(eps), _p(norm_B), _p(norm_C), _p(bias_B),
-                      _p(bias_C), _p(w_x), _p(w_z))
+                      _p(bias_C), _p(w_x), _p(w_z), int(out_norm), int(out_group),
+                      float(out_eps), _p(out_gain))
 
 
 def scan_fwd_pro(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, pro: M3Prologue, rank: int,

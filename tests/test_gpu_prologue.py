@@ -230,3 +230,165 @@ def test_prologue_workloads(k):
     slices = sample_slices(w["batch"], w["nheads"], 10**6 if k == 1 else 18, 60 + k)
     ref, _ = oracle_prologue(inp, pin, "full", slices)
     compare(y, fs, cB, cX, ref, None, slices, f"pro workload {k}")
+
+
+# ---------------------------------------------------------------------------
+# Output norm fused into the y store (Sec. 4 hybrid models; App. norm type /
+# placement ablation): grouped RMS of y before or after the output gate.
+# The kernel normalises y as the plain scan would store it (bf16); the oracle
+# normalises its fp64 y.  The bar is y's own (|dy| <= d = 2e-2 of the
+# slice's max |y|) carried through the norm: for n = u / r over a group, r =
+# sqrt(mean(u^2) + eps) (1-Lipschitz in u: r' >= r - d_u), an error of at
+# most d_u per element gives |n'_e - n_e| <= |du_e| / r' + |n_e| |r - r'| / r'
+# <= (1 + |n_e|) d_u / (r - d_u) when r > d_u, and at most sqrt(group) +
+# |n_e| in any case (unit-RMS vectors); u = y (pre-gate; the factor
+# gain |SiLU(z)| follows, d_u = d) or u = y o SiLU(z) (post-gate, d_u =
+# max_group |SiLU(z)| d); plus the bf16 rounding of the output (2^-8 of each
+# element).  A flat relative bar on the output would not hold for small
+# groups: their RMS can be far below the slice's max |y|, and the norm
+# divides y's absolute error by it.
+# ---------------------------------------------------------------------------
+
+ONORM = {
+    # name: (pre-gate, group, gate: None / "z" / "wz", gain)
+    "pre16_z": (True, 16, "z", True),
+    "post64_z": (False, 64, "z", True),
+    "pre8_nogate": (True, 8, None, False),
+    "post32_wz": (False, 32, "wz", True),
+    "pre64_wz": (True, 64, "wz", False),
+}
+OEPS = 1e-5
+
+
+def onorm_pro(pin, name, gain_t):
+    pre, group, gate, gain = ONORM[name]
+    variant = {"z": "gated_z", "wz": "gated_wz", None: "full"}[gate]
+    base = pro_of(pin, variant)
+    base.out_norm = m3.M3_OUT_NORM_PRE_GATE if pre else m3.M3_OUT_NORM_POST_GATE
+    base.out_group = group
+    base.out_eps = OEPS
+    base.out_gain = m3._p(gain_t) if gain else None
+    return base, variant
+
+
+def gain_for(gain_t, hs, ry):
+    """The heads' gains [S, R, P], with a token axis when y has one."""
+    g = oracle._np(gain_t)[hs]
+    return g[:, None] if ry.ndim == 4 else g
+
+
+def onorm_reference(ry, zref, name, gain_t, hs):
+    pre, group, gate, gain = ONORM[name]
+    g = gain_for(gain_t, hs, ry) if gain else None
+    return oracle.out_norm(ry, group, eps=OEPS, gain=g, z=zref, pre_gate=pre)
+
+
+def onorm_bound(ry, zref, name, gain_t, hs):
+    """Per-element bar of the normalised output (above), from the oracle's
+    y [S, L, R, P] and gate input."""
+    pre, group, gate, gain = ONORM[name]
+    sg = np.ones_like(ry) if zref is None else np.abs(oracle.silu(zref))
+    g = np.abs(gain_for(gain_t, hs, ry)) if gain else 1.0
+    u = ry if pre else ry * (np.ones_like(ry) if zref is None else oracle.silu(zref))
+    shp = u.shape[:-1] + (u.shape[-1] // group, group)
+    rms = np.sqrt(np.mean(u.reshape(shp) ** 2, axis=-1, keepdims=True) + OEPS)
+    n = np.abs(u.reshape(shp) / rms).reshape(u.shape)
+    rms = np.broadcast_to(rms, shp).reshape(u.shape)
+    smax = np.broadcast_to(np.max(sg.reshape(shp), axis=-1, keepdims=True), shp).reshape(u.shape)
+    dy = TOL * np.max(np.abs(ry).reshape(ry.shape[0], -1), axis=1).reshape((-1,) + (1,) * (ry.ndim - 1))
+    du = dy * (1.0 if pre else smax)
+    fac = g * (sg if pre else 1.0)
+    near = (1.0 + n) * du / np.maximum(rms - du, 1e-300)
+    return fac * np.where(rms > du, np.minimum(near, np.sqrt(group) + n), np.sqrt(group) + n)
+
+
+def check_onorm(got, want, bound, label):
+    """|got - want| within the propagated bar plus the output rounding; the
+    plain relative error is reported beside it."""
+    err = np.abs(got - want)
+    lim = bound + 2.0 ** -8 * np.abs(want) + 1e-30
+    worst = float(np.max(err / lim))
+    assert worst <= 1.0, f"{label}: error {worst:.3g} of the propagated bar"
+    return worst, oracle.rel_err(got, want)
+
+
+@pytest.mark.parametrize("name", list(ONORM))
+@pytest.mark.parametrize("R,Q,L", [(1, 64, 300), (4, 64, 200), (2, 32, 77), (4, 128, 130)])
+def test_out_norm_scan(R, Q, L, name):
+    say(f"output norm scan R={R} Q={Q} L={L} {name}")
+    B, H = 2, 3
+    inp, pin = make_case(B, L, H, R, Q, seed=R * 50 + Q + L + 7)
+    zfull = torch.randn(inp.x.shape, device=DEV, generator=torch.Generator(DEV).manual_seed(19)
+                        ).to(torch.bfloat16)
+    gain_t = 0.5 + torch.rand((H, R, 64), device=DEV, generator=torch.Generator(DEV).manual_seed(5))
+    p, variant = onorm_pro(pin, name, gain_t)
+    x, z = gpu_args(inp, pin, variant, zfull)
+    y, fs, (cB, cX) = m3.scan_fwd_pro(x, pin.Bp, pin.Cp, inp.dt, inp.A, inp.lam, inp.theta, inp.D,
+                                      Q, p, R, z=z, check=True)
+    torch.cuda.synchronize()
+    slices = [(b, h) for b in range(B) for h in range(H)]
+    ref, zref = oracle_prologue(inp, pin, variant, slices, zfull=zfull)
+    ry, rs, _, _ = oracle.scan(**ref)
+    hs = [h for _, h in slices]
+    want = onorm_reference(ry, zref, name, gain_t, hs)
+    bound = onorm_bound(ry, zref, name, gain_t, hs)
+    worst, worst_rel = 0.0, 0.0
+    for k, (b, h) in enumerate(slices):
+        gy = y[b, :, h].double().cpu().numpy()
+        assert np.all(np.isfinite(gy)), (b, h)
+        w, r = check_onorm(gy, want[k], bound[k], f"{name} slice {(b, h)}")
+        worst, worst_rel = max(worst, w), max(worst_rel, r)
+        e = oracle.rel_err(fs[b, h].double().cpu().numpy(), rs[k])
+        assert e <= TOL, f"{name} slice {(b, h)}: final state rel err {e:.3g}"
+    say(f"output norm scan R={R} Q={Q} L={L} {name}: {worst:.3g} of the bar "
+        f"(plain rel err {worst_rel:.3g})")
+
+
+@pytest.mark.parametrize("name", ["pre16_z", "post64_z", "pre8_nogate"])
+@pytest.mark.parametrize("R", [1, 4])
+def test_out_norm_decode(R, name):
+    """Decode steps with the output norm after a prefill with it: each step's
+    y against the oracle's step output normalised the same way."""
+    say(f"output norm decode R={R} {name}")
+    B, H, L, steps = 4, 3, 100, 3
+    inp, pin = make_case(B, L, H, R, 64, seed=41 + R)
+    gain_t = 0.5 + torch.rand((H, R, 64), device=DEV, generator=torch.Generator(DEV).manual_seed(6))
+    p, variant = onorm_pro(pin, name, gain_t)
+    gate = ONORM[name][2]
+    zfull = torch.randn(inp.x.shape, device=DEV, generator=torch.Generator(DEV).manual_seed(20)
+                        ).to(torch.bfloat16)
+    x, z = gpu_args(inp, pin, variant, zfull)
+    _, fs, (cB, cX) = m3.scan_fwd_pro(x, pin.Bp, pin.Cp, inp.dt, inp.A, inp.lam, inp.theta,
+                                      inp.D, 64, p, R, z=z)
+    slices = [(b, h) for b in range(B) for h in range(H)]
+    hs = [h for _, h in slices]
+    ref, _ = oracle_prologue(inp, pin, variant, slices, zfull=zfull)
+    _, rs, rb, rx = oracle.scan(**ref)
+    sx = VARIANTS[variant][3]
+    for s in range(steps):
+        st = make_step_inputs(inp, s)
+        sp = make_prologue_step_inputs(pin, B, s)
+        zs_full = torch.randn((B, H, R, 64), device=DEV,
+                              generator=torch.Generator(DEV).manual_seed(100 + s)).to(torch.bfloat16)
+        zt = None if gate is None else (sp.zp if gate == "wz" else zs_full)
+        xt = sp.xp if sx else st.x
+        y = m3.step_pro(fs, (cB, cX), xt, sp.Bp, sp.Cp, st.dt, inp.A, st.lam, st.theta,
+                        inp.D, p, z=zt)
+        torch.cuda.synchronize()
+        stp = oracle.slices_of_step(xt, sp.Bp, sp.Cp, st.dt, st.lam, st.theta, slices)
+        Bn = oracle.rms_norm(stp["B"], oracle._np(pin.gB)[hs], oracle._np(pin.bB)[hs], EPS)
+        Cn = oracle.rms_norm(stp["C"], oracle._np(pin.gC)[hs], oracle._np(pin.bC)[hs], EPS)
+        Xn = oracle._np(pin.wx)[hs] * stp["x"][:, None, :] if sx else stp["x"]
+        ry, rs, rb, rx = oracle.step(rs, rb, rx, Xn, Bn, Cn, stp["dt"], ref["A"][:, 0],
+                                     stp["lam"], stp["theta"], ref["D"])
+        zref = None
+        if gate == "wz":
+            zref = oracle._np(pin.wz)[hs] * np.stack([oracle._np(sp.zp[b, h]) for b, h in slices])[:, None, :]
+        elif gate == "z":
+            zref = np.stack([oracle._np(zs_full[b, h]) for b, h in slices])
+        want = onorm_reference(ry, zref, name, gain_t, hs)
+        bound = onorm_bound(ry, zref, name, gain_t, hs)
+        for k, (b, h) in enumerate(slices):
+            check_onorm(y[b, h].double().cpu().numpy(), want[k], bound[k],
+                        f"{name} step {s} slice {(b, h)}")
+    say(f"output norm decode R={R} {name}: ok")

@@ -289,6 +289,17 @@ def test_prologue_host_validation(L):
     assert scan(dims(**dict(bf, flags=m3.M3_SCAN_SPLIT)), pro()) == m3.M3_ERR_UNSUPPORTED
     assert scan(dims(**dict(bf, chunk=48)), pro()) == m3.M3_ERR_UNSUPPORTED
     assert scan(dims(**bf), pro(), {0: None}) == m3.M3_ERR_NULL
+    # output norm: a known kind, eps > 0, a power-of-two group in [8, headdim],
+    # a gain only with the norm, an aligned gain
+    on = dict(out_norm=m3.M3_OUT_NORM_PRE_GATE, out_group=16, out_eps=1e-6)
+    assert scan(dims(**bf), pro(out_norm=3, out_group=16, out_eps=1e-6)) == m3.M3_ERR_SHAPE
+    assert scan(dims(**bf), pro(out_norm=-1)) == m3.M3_ERR_SHAPE
+    assert scan(dims(**bf), pro(**dict(on, out_eps=0.0))) == m3.M3_ERR_SHAPE
+    assert scan(dims(**bf), pro(**dict(on, out_eps=float("nan")))) == m3.M3_ERR_SHAPE
+    for bad_group in (0, 4, 12, 128, -16):
+        assert scan(dims(**bf), pro(**dict(on, out_group=bad_group))) == m3.M3_ERR_SHAPE
+    assert scan(dims(**bf), pro(out_gain=FAKE)) == m3.M3_ERR_SHAPE     # gain without the norm
+    assert scan(dims(**bf), pro(**dict(on, out_gain=FAKE + 4))) == m3.M3_ERR_ALIGN
 
     def step(d, p, over=None):
         ptrs = [FAKE] * 13       # state cB cX x B C dt A lam theta D z y
@@ -298,6 +309,8 @@ def test_prologue_host_validation(L):
         return L.m3_step_pro(ctypes.byref(d), None if p is None else ctypes.byref(p), *ptrs, None)
     assert step(dims(**bf), None) == m3.M3_ERR_NULL
     assert step(dims(**bf), pro(eps=-1.0)) == m3.M3_ERR_SHAPE
+    assert step(dims(**bf), pro(out_norm=m3.M3_OUT_NORM_POST_GATE, out_group=128,
+                                out_eps=1e-6)) == m3.M3_ERR_SHAPE
     assert step(dims(**bf), pro(w_z=FAKE)) == m3.M3_ERR_NULL
     assert step(dims(**bf), pro(norm_C=FAKE + 12)) == m3.M3_ERR_ALIGN
     assert step(dims(), pro()) == m3.M3_ERR_UNSUPPORTED
