@@ -164,8 +164,12 @@ size_t m3_scan_workspace_bytes(const m3_dims *dims);
  *
  * Supported shapes (else M3_ERR_UNSUPPORTED): io bf16 with dstate 128,
  * headdim 64, rank 1/2/4 and chunk*rank a multiple of 64 with chunk in
- * {32, 64, 128}; io fp32 with (dstate, headdim) = (16, 16) or (128, 64),
- * rank 1/2/4, chunk in {16, 32, 64} and chunk*rank a multiple of 64.
+ * {32, 64, 128}; io bf16 with headdim 64 and the smaller states of the
+ * paper's state-size sweep on the three-kernel path: dstate 64 with (rank,
+ * chunk) in {(1, 64), (1, 128), (2, 32), (2, 64), (4, 16), (4, 32)}, dstate 32
+ * with (1, 64), (2, 32), (4, 16); io fp32 with (dstate, headdim) = (16, 16) or
+ * (128, 64), rank 1/2/4, chunk in {16, 32, 64} and chunk*rank a multiple of
+ * 64.
  * x, B, C, theta, y, the states, the carries and the workspace must be
  * 16-byte aligned; dt, A, lambda and D 4-byte aligned (else M3_ERR_ALIGN).
  * Output buffers must not overlap the inputs.  A must be <= 0 (a positive
@@ -247,8 +251,8 @@ m3_status m3_scan_fwd_varlen(const m3_dims *dims, const int64_t *cu_seqlens,
  * Tensors: x_t [batch][nheads][rank][headdim], B_t and C_t
  * [batch][nheads][rank][dstate] (io dtype), dt_t and lambda_t
  * [batch][nheads], theta_t [batch][nheads][dstate/2] (fp32),
- * y_t [batch][nheads][rank][headdim] (io dtype).  Supported shapes: those
- * of m3_scan_fwd (chunk ignored).
+ * y_t [batch][nheads][rank][headdim] (io dtype).  Supported shapes: the
+ * (io, dstate, headdim, rank) of m3_scan_fwd (chunk ignored).
  */
 m3_status m3_step(const m3_dims *dims,
                   float *state, void *carryB, void *carryX,

@@ -303,9 +303,13 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     }
 }
 
-// Threads per (batch, head): four waves for the 128 x 64 state (fewer
-// threads per slice measured slower: longer per-thread update chains).
-template <int N, int P> struct StepThreads { static constexpr int value = N * P >= 8192 ? 256 : 64; };
+// Threads per (batch, head): four row pairs per thread (four waves for the
+// 128 x 64 state; fewer threads per slice measured slower there: longer
+// per-thread update chains), at least one wave.
+template <int N, int P> struct StepThreads {
+    static constexpr int v = (N / 8) * (P / 4);
+    static constexpr int value = v < 64 ? 64 : v;
+};
 
 template <typename T, int N, int P, int R, bool kPro = false>
 hipError_t launch_step(const StepArgs &a, hipStream_t stream) {
@@ -328,6 +332,12 @@ hipError_t launch_step(const StepArgs &a, hipStream_t stream) {
     X(0, float, 128, 64, 1)    \
     X(0, float, 128, 64, 2)    \
     X(0, float, 128, 64, 4)    \
+    X(1, bf16, 32, 64, 1)      \
+    X(1, bf16, 32, 64, 2)      \
+    X(1, bf16, 32, 64, 4)      \
+    X(1, bf16, 64, 64, 1)      \
+    X(1, bf16, 64, 64, 2)      \
+    X(1, bf16, 64, 64, 4)      \
     X(1, bf16, 128, 64, 1)     \
     X(1, bf16, 128, 64, 2)     \
     X(1, bf16, 128, 64, 4)

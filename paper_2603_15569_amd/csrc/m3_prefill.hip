@@ -516,6 +516,15 @@ hipError_t launch_scan(const ScanArgs &a, hipStream_t stream) {
     X(0, float, 128, 64, 2, 32)    \
     X(0, float, 128, 64, 4, 16)    \
     X(0, float, 128, 64, 4, 32)    \
+    X(1, bf16, 32, 64, 1, 64)      \
+    X(1, bf16, 32, 64, 2, 32)      \
+    X(1, bf16, 32, 64, 4, 16)      \
+    X(1, bf16, 64, 64, 1, 64)      \
+    X(1, bf16, 64, 64, 1, 128)     \
+    X(1, bf16, 64, 64, 2, 32)      \
+    X(1, bf16, 64, 64, 2, 64)      \
+    X(1, bf16, 64, 64, 4, 16)      \
+    X(1, bf16, 64, 64, 4, 32)      \
     X(1, bf16, 128, 64, 1, 64)     \
     X(1, bf16, 128, 64, 1, 128)    \
     X(1, bf16, 128, 64, 2, 32)     \

@@ -210,6 +210,9 @@ SHAPES = [  # io, N, P, R, Q
     ("f32", 128, 64, 4, 32),
     ("bf16", 128, 64, 1, 64), ("bf16", 128, 64, 1, 128), ("bf16", 128, 64, 2, 64),
     ("bf16", 128, 64, 4, 32), ("bf16", 128, 64, 4, 64), ("bf16", 128, 64, 4, 128),
+    # smaller states (the paper's state-size sweep): the three-kernel path
+    ("bf16", 64, 64, 1, 64), ("bf16", 64, 64, 2, 64), ("bf16", 64, 64, 4, 32),
+    ("bf16", 32, 64, 1, 64), ("bf16", 32, 64, 4, 16),
 ]
 
 
@@ -426,7 +429,9 @@ def test_determinism(mode, seg):
 
 
 @pytest.mark.parametrize("io,N,P,R", [("f32", 16, 16, 1), ("f32", 128, 64, 4),
-                                      ("bf16", 128, 64, 1), ("bf16", 128, 64, 4)])
+                                      ("bf16", 128, 64, 1), ("bf16", 128, 64, 4),
+                                      ("bf16", 64, 64, 1), ("bf16", 64, 64, 4),
+                                      ("bf16", 32, 64, 2)])
 def test_decode_steps_small(io, N, P, R):
     """A few decode steps from a random state and carry, every output checked."""
     say(f"decode small io={io} N={N} R={R}")
@@ -503,7 +508,8 @@ def test_gated_workload1_siso():
 
 
 @pytest.mark.parametrize("io,N,P,R", [("f32", 16, 16, 1), ("f32", 128, 64, 4),
-                                      ("bf16", 128, 64, 1), ("bf16", 128, 64, 4)])
+                                      ("bf16", 128, 64, 1), ("bf16", 128, 64, 4),
+                                      ("bf16", 64, 64, 4)])
 def test_gated_decode_steps(io, N, P, R):
     """Gated decode steps: y_t o SiLU(z_t) against the oracle, state and
     carry advanced as by the ungated step."""
