@@ -220,21 +220,33 @@ m3_status m3_scan_fwd_gated(const m3_dims *dims,
  * [T][nheads][dstate/2] (or [nheads][dstate/2] with M3_THETA_PER_HEAD);
  * A[t * a_stride_t + h * a_stride_h] over the packed tokens (a_stride_b must
  * be 0).  z may be NULL (no gate) or a gate input as in m3_scan_fwd_gated.
- * The sequences run one after another on `stream`, each as one m3_scan_fwd
- * (so each picks its own kernel), sharing the workspace: size it with
- * m3_scan_workspace_bytes for one sequence of the largest length.  A run of
- * consecutive sequences of equal length goes out as one m3_scan_fwd over a
- * batch of them (they lie in the packed arrays as that batch would) as far
- * as the workspace holds what the batch needs (m3_scan_workspace_bytes with
- * batch = the run's length, a_stride_b = length * a_stride_t).  The kernel
- * (and its segment count) is chosen per launch, so the last bits of a
- * sequence's results can depend on how many equal-length neighbours it is
- * batched with and hence on workspace_bytes; every grouping is within the
- * scan's tolerance of the recurrence.  Every call's arguments are checked
- * before the first launch (errors as m3_scan_fwd; M3_ERR_NULL for a NULL
- * cu_seqlens, M3_ERR_SHAPE for bad offsets).  m3_scan_check after a varlen
- * call reads the timeouts of its last launch only.
+ * One launch: when m3_scan_varlen_workspace_bytes(dims, cu_seqlens) is
+ * non-zero and workspace_bytes is at least that, every (sequence, head,
+ * chunk) item of the batch runs in one launch of the one-chunk-per-workgroup
+ * kernel (small tables built on the host from cu_seqlens are copied into the
+ * workspace first, on `stream`); its results are bit-identical to the same
+ * sequences scanned alone with M3_SCAN_PER_CHUNK.  Otherwise (a shape
+ * without that kernel, an empty sequence, M3_SCAN_SPLIT, a seg_chunks
+ * request, or a smaller workspace) the sequences run one after another on
+ * `stream`, each as one m3_scan_fwd (so each picks its own kernel), sharing
+ * the workspace: size it at least with m3_scan_workspace_bytes for one
+ * sequence of the largest length.  A run of consecutive sequences of equal
+ * length then goes out as one m3_scan_fwd over a batch of them (they lie in
+ * the packed arrays as that batch would) as far as the workspace holds what
+ * the batch needs (m3_scan_workspace_bytes with batch = the run's length,
+ * a_stride_b = length * a_stride_t).  The kernel (and its segment count) is
+ * chosen per launch, so the last bits of a sequence's results can depend on
+ * how many equal-length neighbours it is batched with and hence on
+ * workspace_bytes; every grouping is within the scan's tolerance of the
+ * recurrence.  Every call's arguments are checked before the first launch
+ * (errors as m3_scan_fwd; M3_ERR_NULL for a NULL cu_seqlens, M3_ERR_SHAPE
+ * for bad offsets).  m3_scan_varlen_check reads the look-back timeouts of
+ * the call (of its last launch when it made several).
  */
+size_t m3_scan_varlen_workspace_bytes(const m3_dims *dims, const int64_t *cu_seqlens);
+m3_status m3_scan_varlen_check(const m3_dims *dims, const int64_t *cu_seqlens,
+                               const void *workspace, size_t workspace_bytes,
+                               uint32_t *timeouts, void *stream);
 m3_status m3_scan_fwd_varlen(const m3_dims *dims, const int64_t *cu_seqlens,
                              const void *x, const void *B, const void *C,
                              const float *dt, const float *A, const float *lambda,

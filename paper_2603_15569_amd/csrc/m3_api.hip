@@ -2,7 +2,9 @@
 // call), workspace layout, dispatch to the shape-specialised kernels.
 #include <limits.h>
 
+#include <algorithm>
 #include <atomic>
+#include <vector>
 
 #include "m3.h"
 #include "m3_internal.h"
@@ -264,6 +266,166 @@ extern "C" m3_status m3_scan_fwd_gated(const m3_dims *d, const void *x, const vo
 // workspace holds what that batch needs), every other sequence as an
 // m3_scan_fwd of its own; the calls run in order on `stream` and share the
 // workspace.  Every call's arguments are checked before the first launch.
+// ---------------------------------------------------------------------------
+// Varlen single launch: every (sequence, head, chunk) item of the packed
+// batch in one launch of the per-chunk kernel, from tables the host builds
+// out of the offsets and copies into the workspace.
+// ---------------------------------------------------------------------------
+
+namespace m3 {
+namespace {
+
+struct VarlenPlan {
+    scan_launch_fn launch = nullptr;   // null: the single launch does not apply
+    int64_t slots = 0, maxn = 0;
+    size_t off_flags = 0, off_tot = 0, off_agg = 0, off_inc = 0, off_tab = 0, tab_bytes = 0, total = 0;
+};
+
+// Whether one launch serves the packed batch (the per-chunk kernel built for
+// the shape, no M3_SCAN_SPLIT and no segment length asked for, every
+// sequence non-empty, token rows within
+// the kernel's 32-bit offsets, items within its ticket range), and its
+// workspace layout.  d and cu_seqlens already validated.
+VarlenPlan varlen_plan(const m3_dims *d, const int64_t *cu) {
+    VarlenPlan p;
+    if ((d->flags & M3_SCAN_SPLIT) || d->seg_chunks > 0 || d->batch < 1) return p;
+    scan_launch_fn f = find_fused_var_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
+    const ScanImpl impl = find_scan_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk);
+    if (!f || !impl.launch) return p;
+    const int64_t per_tok = d->nheads * d->rank * (d->dstate > d->headdim ? d->dstate : d->headdim);
+    const int64_t tok_bytes = per_tok * (int64_t)io_bytes_of(d->io);
+    if (!(tok_bytes < (INT64_C(1) << 24) && d->chunk * tok_bytes < (INT64_C(1) << 31))) return p;
+    int64_t chunks = 0, maxn = 0;
+    for (int64_t s = 0; s < d->batch; ++s) {
+        const int64_t len = cu[s + 1] - cu[s];
+        if (len <= 0) return p;
+        const int64_t n = (len + d->chunk - 1) / d->chunk;
+        chunks += n;
+        maxn = n > maxn ? n : maxn;
+    }
+    const int64_t slots = chunks * d->nheads, nsl = d->batch * d->nheads;
+    if (slots >= (int64_t)INT_MAX || maxn >= (int64_t)INT_MAX / kGroups) return p;
+    const size_t N = d->dstate, P = d->headdim;
+    p.launch = f;
+    p.slots = slots;
+    p.maxn = maxn;
+    p.off_flags = kCtlBytes;
+    p.off_tot = align_up(p.off_flags + (size_t)slots * 4, 256);
+    p.off_agg = align_up(p.off_tot + (size_t)slots * (N / 2 + 1) * (size_t)impl.acc_bytes, 256);
+    p.off_inc = align_up(p.off_agg + (size_t)slots * N * P * 4, 256);
+    p.off_tab = align_up(p.off_inc + (size_t)slots * N * P * 4, 256);
+    p.tab_bytes = (size_t)d->batch * 20 + 4 * ((size_t)(kGroups + 1) + (size_t)kGroups * (maxn + 1) + (size_t)nsl);
+    p.total = align_up(p.off_tab + p.tab_bytes, 256);
+    return p;
+}
+
+// The tables (layout of varlen_plan's table block): first packed token,
+// first flag slot (int64) and length (int32) of each sequence; per slice
+// group the start of its slice list, the item counts below each chunk level,
+// and the slice lists (each group's slices by decreasing chunk count).
+void varlen_tables(const m3_dims *d, const int64_t *cu, const VarlenPlan &p, std::vector<char> &buf) {
+    const int64_t S = d->batch, H = d->nheads, Q = d->chunk, nsl = S * H, maxn = p.maxn;
+    buf.assign(p.tab_bytes, 0);
+    int64_t *tok = reinterpret_cast<int64_t *>(buf.data());
+    int64_t *slot = tok + S;
+    int32_t *len = reinterpret_cast<int32_t *>(slot + S);
+    int32_t *gstart = len + S;
+    int32_t *grp = gstart + kGroups + 1;
+    int32_t *order = grp + kGroups * (maxn + 1);
+    std::vector<int32_t> nch(S);
+    int64_t base = 0;
+    for (int64_t s = 0; s < S; ++s) {
+        const int64_t l = cu[s + 1] - cu[s];
+        tok[s] = cu[s];
+        slot[s] = base;
+        len[s] = (int32_t)l;
+        nch[s] = (int32_t)((l + Q - 1) / Q);
+        base += H * nch[s];
+    }
+    int32_t at = 0;
+    for (int y = 0; y < kGroups; ++y) {
+        gstart[y] = at;
+        std::vector<int32_t> mine;
+        for (int64_t sl = y; sl < nsl; sl += kGroups) mine.push_back((int32_t)sl);
+        std::stable_sort(mine.begin(), mine.end(),
+                         [&](int32_t a, int32_t b) { return nch[a / H] > nch[b / H]; });
+        for (int32_t sl : mine) order[at++] = sl;
+        // items below level c: the slices with more than c' chunks, c' < c
+        // (a prefix of the list, shrinking as c grows)
+        int32_t *gy = grp + y * (maxn + 1);
+        gy[0] = 0;
+        size_t pre = mine.size();
+        for (int64_t c = 0; c < maxn; ++c) {
+            while (pre > 0 && nch[mine[pre - 1] / H] <= c) --pre;
+            gy[c + 1] = gy[c] + (int32_t)pre;
+        }
+    }
+    gstart[kGroups] = at;
+}
+
+}  // namespace
+}  // namespace m3
+
+// The single launch of a checked varlen batch (every run's arguments passed
+// m3_scan_fwd's checks): tables copied into the workspace, then the kernel.
+static m3_status varlen_single(const m3_dims *d, const int64_t *cu, const VarlenPlan &plan,
+                               const void *x, const void *B, const void *C, const float *dt,
+                               const float *A, const float *lambda, const float *theta,
+                               const float *D, const void *z, const float *init_state,
+                               const void *init_carryB, const void *init_carryX, void *y,
+                               float *final_state, void *carryB, void *carryX, void *workspace,
+                               void *stream) {
+    static thread_local std::vector<char> tab;
+    varlen_tables(d, cu, plan, tab);
+    char *ws = static_cast<char *>(workspace);
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    // (pageable source: the call returns once the bytes are staged)
+    hipError_t e = hipMemcpyAsync(ws + plan.off_tab, tab.data(), plan.tab_bytes, hipMemcpyHostToDevice, st);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return M3_ERR_HIP;
+    }
+    ScanArgs a = {};
+    a.x = x; a.B = B; a.C = C;
+    a.dt = dt; a.A = A; a.lam = lambda; a.theta = theta; a.D = D;
+    a.init_state = init_state; a.init_cB = init_carryB; a.init_cX = init_carryX;
+    a.y = y; a.z = z; a.final_state = final_state; a.cB = carryB; a.cX = carryX;
+    a.theta_ph = (d->flags & M3_THETA_PER_HEAD) ? 1 : 0;
+    a.ctl = reinterpret_cast<uint32_t *>(ws);
+    a.flags = reinterpret_cast<uint32_t *>(ws + plan.off_flags);
+    a.tot = ws + plan.off_tot;
+    a.agg = reinterpret_cast<float *>(ws + plan.off_agg);
+    a.inc = reinterpret_cast<float *>(ws + plan.off_inc);
+    a.batch = d->batch; a.L = d->seqlen; a.H = d->nheads; a.nchunks = plan.maxn;
+    a.a_sb = 0; a.a_st = d->a_stride_t; a.a_sh = d->a_stride_h;
+    const int64_t S = d->batch;
+    const char *tb = ws + plan.off_tab;
+    a.vl_tok = reinterpret_cast<const int64_t *>(tb);
+    a.vl_slot = a.vl_tok + S;
+    a.vl_len = reinterpret_cast<const int32_t *>(a.vl_slot + S);
+    a.vl_gstart = a.vl_len + S;
+    a.vl_grp = a.vl_gstart + kGroups + 1;
+    a.vl_order = a.vl_grp + kGroups * (plan.maxn + 1);
+    a.vl_maxn = (int)plan.maxn;
+    a.vl_slots = plan.slots;
+    a.spin_max = g_spin_max.load(std::memory_order_relaxed);
+    e = plan.launch(a, st);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return M3_ERR_HIP;
+    }
+    return M3_OK;
+}
+
+extern "C" size_t m3_scan_varlen_workspace_bytes(const m3_dims *d, const int64_t *cu_seqlens) {
+    if (check_dims_common(d) != M3_OK || !cu_seqlens || d->seqlen < 0 || d->a_stride_b != 0 ||
+        cu_seqlens[0] != 0 || cu_seqlens[d->batch] != d->seqlen)
+        return 0;
+    for (int64_t i = 0; i < d->batch; ++i)
+        if (cu_seqlens[i + 1] < cu_seqlens[i]) return 0;
+    return varlen_plan(d, cu_seqlens).total;
+}
+
 extern "C" m3_status m3_scan_fwd_varlen(const m3_dims *d, const int64_t *cu_seqlens,
                                         const void *x, const void *B, const void *C,
                                         const float *dt, const float *A, const float *lambda,
@@ -304,6 +466,13 @@ extern "C" m3_status m3_scan_fwd_varlen(const m3_dims *d, const int64_t *cu_seql
         return j;
     };
     for (int pass = 0; pass < 2; ++pass) {   // 0: every call checked, 1: launched
+        if (pass == 1) {   // one launch for the whole batch, where it applies and fits
+            const VarlenPlan plan = varlen_plan(d, cu_seqlens);
+            if (plan.launch && workspace_bytes >= plan.total)
+                return varlen_single(d, cu_seqlens, plan, x, B, C, dt, A, lambda, theta, D, z,
+                                     init_state, init_carryB, init_carryX, y, final_state, carryB,
+                                     carryX, workspace, stream);
+        }
         for (int64_t i = 0, j = 0; i < d->batch; i = j) {
             j = run_end(i);
             const int64_t t0 = cu_seqlens[i], len = cu_seqlens[i + 1] - t0;
@@ -477,6 +646,25 @@ extern "C" void m3_set_wait_limit(uint32_t polls) {
     g_spin_max.store(polls ? polls : kSpinMaxDefault, std::memory_order_relaxed);
 }
 
+// The last finished single-pass call's timeout count from the control block.
+static m3_status read_timeouts(const void *workspace, uint32_t *timeouts, void *stream) {
+    // the control words up to group 0's ticket counter: the last finished
+    // call ran with epoch (group 0's epoch - 1) and counted its timeouts in
+    // that epoch's word (a call without look-back zeroes both words)
+    const char *ctl = static_cast<const char *>(workspace);
+    uint32_t w[kGroupStride + 2] = {};
+    const hipStream_t st = static_cast<hipStream_t>(stream);
+    hipError_t e = hipMemcpyAsync(w, ctl, sizeof(w), hipMemcpyDeviceToHost, st);
+    if (e == hipSuccess) e = hipStreamSynchronize(st);
+    if (e != hipSuccess) {
+        g_last_hip_error = (int)e;
+        return M3_ERR_HIP;
+    }
+    const uint32_t last_epoch = w[kGroupStride + 1] - 1u;
+    *timeouts = w[(last_epoch & 1u) ? kCtlTimeouts1 : kCtlTimeouts0];
+    return M3_OK;
+}
+
 extern "C" m3_status m3_scan_check(const m3_dims *d, const void *workspace, size_t workspace_bytes,
                                    uint32_t *timeouts, void *stream) {
     ScanImpl impl;
@@ -493,22 +681,40 @@ extern "C" m3_status m3_scan_check(const m3_dims *d, const void *workspace, size
                                                          impl.acc_bytes, impl.fused);
     if (!workspace || workspace_bytes < wl.total) return M3_ERR_WORKSPACE;
     if (!aligned16(workspace)) return M3_ERR_ALIGN;
-    // the control words up to group 0's ticket counter: the last finished
-    // call ran with epoch (group 0's epoch - 1) and counted its timeouts in
-    // that epoch's word (a call without look-back zeroes both words)
-    const char *ctl = static_cast<const char *>(workspace) + wl.off_ctl;
-    uint32_t w[kGroupStride + 2] = {};
-    const hipStream_t st = static_cast<hipStream_t>(stream);
-    hipError_t e = hipMemcpyAsync(w, ctl, sizeof(w), hipMemcpyDeviceToHost, st);
-    if (e == hipSuccess) e = hipStreamSynchronize(st);
-    if (e != hipSuccess) {
-        g_last_hip_error = (int)e;
-        return M3_ERR_HIP;
-    }
-    const uint32_t last_epoch = w[kGroupStride + 1] - 1u;
-    *timeouts = w[(last_epoch & 1u) ? kCtlTimeouts1 : kCtlTimeouts0];
-    return M3_OK;
+    return read_timeouts(workspace, timeouts, stream);
 }
+
+extern "C" m3_status m3_scan_varlen_check(const m3_dims *d, const int64_t *cu_seqlens,
+                                          const void *workspace, size_t workspace_bytes,
+                                          uint32_t *timeouts, void *stream) {
+    m3_status s = check_dims_common(d);
+    if (s != M3_OK) return s;
+    if (!cu_seqlens || !timeouts) return M3_ERR_NULL;
+    if (d->seqlen < 0 || d->a_stride_b != 0 || cu_seqlens[0] != 0 || cu_seqlens[d->batch] != d->seqlen)
+        return M3_ERR_SHAPE;
+    for (int64_t i = 0; i < d->batch; ++i)
+        if (cu_seqlens[i + 1] < cu_seqlens[i]) return M3_ERR_SHAPE;
+    const VarlenPlan plan = varlen_plan(d, cu_seqlens);
+    if (plan.launch && workspace_bytes >= plan.total) {   // the call was one launch
+        if (!workspace) return M3_ERR_WORKSPACE;
+        if (!aligned16(workspace)) return M3_ERR_ALIGN;
+        return read_timeouts(workspace, timeouts, stream);
+    }
+    if (d->batch == 0) {
+        *timeouts = 0;
+        return M3_OK;
+    }
+    // else its last launch: the last sequence (batched with the equal-length
+    // run it ends, as far as the workspace held it; that run's launch wrote
+    // the control block either way)
+    const int64_t S = d->batch, len = cu_seqlens[S] - cu_seqlens[S - 1];
+    m3_dims dl = *d;
+    dl.batch = 1;
+    dl.seqlen = len;
+    dl.a_stride_b = 0;
+    return m3_scan_check(&dl, workspace, workspace_bytes, timeouts, stream);
+}
+
 
 // ---------------------------------------------------------------------------
 // Allocation-free prefill: the workspace is a library-owned device array.

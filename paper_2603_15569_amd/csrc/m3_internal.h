@@ -38,20 +38,31 @@ struct ScanArgs {
     void *Sin;       // [BH][nchunks][P][N] io    state entering each chunk
     void *tot;       // [BH][nchunks][1+N/2] acc  chunk log-decay and angle totals
     // single-pass (look-back) scan only
-    uint32_t *ctl;   // [0] ticket counter, [1] look-back timeouts
+    uint32_t *ctl;   // control block (ticket counters, epoch, timeout counts)
     uint32_t *flags; // [BH][nchunks] 0 / aggregate ready / inclusive state ready
     float *agg;      // [BH][nchunks][N*P] chunk aggregates (owner's lane layout)
     float *inc;      // [BH][nchunks][N*P] inclusive states (same layout)
     int64_t batch, L, H, nchunks;
     int64_t a_sb, a_st, a_sh;
+    // varlen single launch (per-chunk kernel, sequences packed along the
+    // token axis; batch = sequences, L = packed tokens): item and sequence
+    // tables in the workspace (null: a uniform batch)
+    const int32_t *vl_grp;     // [kGroups][vl_maxn + 1] items of group y with chunk index < c
+    const int32_t *vl_gstart;  // [kGroups + 1] start of group y's slices in vl_order
+    const int32_t *vl_order;   // [batch * H] each group's slices by decreasing chunk count
+    const int64_t *vl_tok;     // [batch] first packed token of each sequence
+    const int64_t *vl_slot;    // [batch] first flag slot of each sequence (H x its chunks)
+    const int32_t *vl_len;     // [batch] tokens of each sequence (all > 0)
+    int vl_maxn;               // chunks of the longest sequence
+    int64_t vl_slots;          // flag slots in all
     // segmented kernel: chunks per segment (0 = chosen at launch), segments
     // per slice (set at launch), and the one-chunk-per-workgroup kernel it
     // hands over to when its own choice would give short chunks several
     // segments per slice (null: none)
     int64_t G, nseg;
     hipError_t (*per_chunk)(const ScanArgs &, hipStream_t);
-    // polls of a look-back wait before it gives up (counts a timeout in
-    // ctl[1] and makes the entering state NaN)
+    // polls of a look-back wait before it gives up (counts a timeout in the
+    // control block and makes the entering state NaN)
     uint32_t spin_max;
     Prologue pro;
 };
@@ -115,6 +126,8 @@ struct ScanImpl {
 ScanImpl find_scan_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 step_launch_fn find_step_impl(int io, int64_t N, int64_t P, int64_t R);
 scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+// the per-chunk kernel over varlen tables (null: not built for the shape)
+scan_launch_fn find_fused_var_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 scan_launch_fn find_seg_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 // warp-specialised kernel for one segment per slice (null: none for the shape)
 scan_launch_fn find_ws_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);

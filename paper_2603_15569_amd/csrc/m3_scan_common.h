@@ -325,6 +325,46 @@ __device__ __forceinline__ void take_item(uint32_t *ctl, int64_t nsl, int64_t nc
     *ready = false;
 }
 
+// The same for sequences of different lengths (varlen tables): group y hands
+// out its items chunk-major too, chunk level c holding the group's slices
+// with more than c chunks; listed by decreasing chunk count, those are the
+// first grp[y][c+1] - grp[y][c] slices of the group's list, so ticket k is
+// chunk level c (the last with grp[y][c] <= k) and list entry k - grp[y][c].
+// Every predecessor of an item again holds an earlier ticket of its counter.
+// janitor: the item of group 0's last ticket.
+__device__ __forceinline__ void take_item_var(uint32_t *ctl, const int32_t *grp, const int32_t *gstart,
+                                              const int32_t *order, int maxn, int64_t *c, int64_t *sl,
+                                              uint32_t *epoch, bool *ready, bool *janitor) {
+    const int x = (int)(__builtin_amdgcn_s_getreg((3 << 11) | 20) & (kGroups - 1));   // XCC id
+    for (int tries = 0; tries < kGroups; ++tries) {
+        const int y = (x + tries) & (kGroups - 1);
+        const int32_t *gy = grp + y * (maxn + 1);
+        const int32_t items = gy[maxn];
+        if (items <= 0) continue;
+        const unsigned long long w =
+            __hip_atomic_fetch_add(group_counter(ctl, y), 1ull, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int32_t k = (int32_t)((uint32_t)w & ~kTicketReady);
+        if (k < items) {
+            int lo = 0, hi = maxn - 1;   // last level c with gy[c] <= k (gy[0] = 0)
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) / 2;
+                if (gy[mid] <= k) lo = mid; else hi = mid - 1;
+            }
+            *c = lo;
+            *sl = order[gstart[y] + (k - gy[lo])];
+            *epoch = (uint32_t)(w >> 32);
+            *ready = ((uint32_t)w & kTicketReady) != 0;
+            *janitor = y == 0 && k == items - 1;
+            return;
+        }
+    }
+    *c = -1;   // unreachable with one workgroup per item
+    *sl = -1;
+    *epoch = 0;
+    *ready = false;
+    *janitor = false;
+}
+
 // The call's first item clears the look-back flags [0, n) (all threads of the
 // workgroup), then marks them cleared: the ready bit of every group's counter
 // (seen by the items that take their tickets after), and, once those have
@@ -373,18 +413,26 @@ __device__ __forceinline__ bool wait_flags_ready(uint32_t *ctl, uint32_t epoch, 
 // next epoch's timeout word, so the next call on the workspace starts from a
 // clean block without a reset launch.  The wait is bounded by at least the
 // default limit; one that gives up counts a timeout and resets all the same.
+// Items of group y: (nsl - y + kGroups - 1) / kGroups slices of nunits each
+// (0 past the last slice), or the varlen table's count.
+__device__ __forceinline__ int64_t group_items(int y, int64_t nsl, int64_t nunits, const int32_t *grp, int maxn) {
+    if (grp) return grp[y * (maxn + 1) + maxn];
+    const int64_t items = (nsl - y + kGroups - 1) / kGroups * nunits;
+    return items > 0 ? items : 0;
+}
+
 __device__ __forceinline__ void janitor_reset(uint32_t *ctl, int64_t nsl, int64_t nunits, uint32_t epoch,
-                                              uint32_t spin_max) {
+                                              uint32_t spin_max, const int32_t *grp = nullptr, int maxn = 0) {
     const uint32_t lim = spin_max > kSpinMaxDefault ? spin_max : kSpinMaxDefault;
     bool all = false;
     for (uint32_t spin = 0; spin < lim && !all; ++spin) {
         all = __hip_atomic_load(ctl + kCtlReady, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == epoch + 1u;
 #pragma unroll
         for (int y = 0; y < kGroups; ++y) {
-            const int64_t items = (nsl - y + kGroups - 1) / kGroups * nunits;   // (0 past the last slice)
+            const int64_t items = group_items(y, nsl, nunits, grp, maxn);
             const uint32_t w = __hip_atomic_load(reinterpret_cast<uint32_t *>(group_counter(ctl, y)),
                                                  __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            all = all && (int64_t)(w & ~kTicketReady) >= (items > 0 ? items : 0);
+            all = all && (int64_t)(w & ~kTicketReady) >= items;
         }
         if (!all) __builtin_amdgcn_s_sleep(2);
     }

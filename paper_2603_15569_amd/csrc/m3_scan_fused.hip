@@ -53,13 +53,14 @@ namespace {
 
 using namespace scan;
 
-template <typename T, int Q, int R, bool kGate, bool kPro>
+template <typename T, int Q, int R, bool kGate, bool kPro, bool kVar = false>
 // Two waves per SIMD: two 4-wave workgroups or one 8-wave workgroup per CU
 // (more waves spill the tile registers of the output phase).  kGate: the
 // stored y is multiplied by SiLU(z) (the block's output gate).  kPro: the
 // block prologue is applied as the rows arrive (B and C: RMS norm over N,
 // gain, bias; x and z: X = W_X o X', Z = W_Z o Z'), from per-head tables in
-// LDS.
+// LDS.  kVar: sequences of different lengths packed along the token axis,
+// items and sequences from the varlen tables.
 __global__ __launch_bounds__((FShape<T, Q, R>::NTHR), 2)
 void k_scan_fused(ScanArgs a) {
     typedef FShape<T, Q, R> S;
@@ -117,14 +118,19 @@ void k_scan_fused(ScanArgs a) {
     if (tid == 0) {
         int64_t ci, si;
         uint32_t ep;
-        bool rd;
-        take_item(a.ctl, nsl, a.nchunks, &ci, &si, &ep, &rd);
+        bool rd, jan;
+        if constexpr (kVar) {
+            take_item_var(a.ctl, a.vl_grp, a.vl_gstart, a.vl_order, a.vl_maxn, &ci, &si, &ep, &rd, &jan);
+        } else {
+            take_item(a.ctl, nsl, a.nchunks, &ci, &si, &ep, &rd);
+            jan = is_janitor(ci, si, nsl, a.nchunks);
+        }
         s_i[0] = (int)ci;
         s_i[1] = (int)si;
         s_i[2] = (int)ep;
         s_i[3] = rd ? 1 : 0;
         s_ctl[0] = ep;
-        s_ctl[1] = is_janitor(ci, si, nsl, a.nchunks) ? 1u : 0u;
+        s_ctl[1] = jan ? 1u : 0u;
     }
     __syncthreads();
     const int64_t c = s_i[0], sl = s_i[1];
@@ -133,16 +139,32 @@ void k_scan_fused(ScanArgs a) {
     __syncthreads();
     if (c < 0) return;   // (cannot happen: one workgroup per item)
     if (c == 0 && sl == 0) {   // the call's first item clears the look-back flags
-        clear_flags(a.ctl, a.flags, nsl * a.nchunks, epoch, tid, S::NTHR);
+        clear_flags(a.ctl, a.flags, kVar ? a.vl_slots : nsl * a.nchunks, epoch, tid, S::NTHR);
         flags_ready = true;
     }
     const int64_t b = sl / a.H, h = sl % a.H;
+    // the item's sequence: its first token in the token arrays, its length,
+    // its chunks, the first flag slot of the slice, and A's offset for it
+    int64_t seq_tok, seq_len, seq_n, seq_slot, a_off;
+    if constexpr (kVar) {
+        seq_tok = a.vl_tok[b];
+        seq_len = a.vl_len[b];
+        seq_n = (seq_len + Q - 1) / Q;
+        seq_slot = a.vl_slot[b] + h * seq_n;
+        a_off = seq_tok * a.a_st;   // (a_sb = 0: A runs over the packed tokens)
+    } else {
+        seq_tok = b * a.L;
+        seq_len = a.L;
+        seq_n = a.nchunks;
+        seq_slot = sl * a.nchunks;
+        a_off = b * a.a_sb;
+    }
     const int64_t t0 = c * Q;
-    const int nvalid = (int)min((int64_t)Q, a.L - t0);
-    const int64_t slot = sl * a.nchunks + c;
-    const int64_t tok0 = (b * a.L + t0) * a.H + h;       // (b, t0, h) flat token-head index
+    const int nvalid = (int)min((int64_t)Q, seq_len - t0);
+    const int64_t slot = seq_slot + c;
+    const int64_t tok0 = (seq_tok + t0) * a.H + h;       // (token, head) flat index of the chunk's first row
     const int64_t tstr = a.H;                             // token stride in token-heads
-    const bool last = (c == a.nchunks - 1);
+    const bool last = (c == seq_n - 1);
 
     const T *Cg = static_cast<const T *>(a.C) + tok0 * (R * N);
     const T *Bg = static_cast<const T *>(a.B) + tok0 * (R * N);
@@ -327,7 +349,7 @@ void k_scan_fused(ScanArgs a) {
         float th[S::TPS];
 #pragma unroll
         for (int k = 0; k < S::TPS; ++k) th[k] = buf_load<float>(rth, tok_off(seg * S::TPS + k, thstr_b) + i * 4);
-        const int nvn = nvalid + (t0 + nvalid < a.L ? 1 : 0);
+        const int nvn = nvalid + (t0 + nvalid < seq_len ? 1 : 0);
         const Rsrc rdt = make_rsrc(a.dt + tok0, (uint32_t)(((nvn - 1) * tstr + 1) * 4));
         float dts[S::TPS];
         if (a.theta_ph) {
@@ -340,7 +362,7 @@ void k_scan_fused(ScanArgs a) {
         const float dtv = buf_load<float>(rdt, o), lamv = buf_load<float>(rlam, o);
         const float dtn = buf_load<float>(rdt, o + tstr_b), lamn = buf_load<float>(rlam, o + tstr_b);
         const int64_t tg = t0 + min(tid, nvalid - 1);
-        const float Av = a.A[b * a.a_sb + tg * a.a_st + h * a.a_sh];
+        const float Av = a.A[a_off + tg * a.a_st + h * a.a_sh];
         // the first blocks' loads go out after the prologue's own loads (memory
         // counters retire in order), so they overlap the prologue's arithmetic
         __builtin_amdgcn_sched_barrier(0);
@@ -638,7 +660,7 @@ void k_scan_fused(ScanArgs a) {
         const float *ist = a.init_state ? a.init_state + sl * SZ : nullptr;
         float wb = 0.f;
         if (a.init_cB) {
-            const int64_t k0 = (b * a.L) * a.H + h;
+            const int64_t k0 = seq_tok * a.H + h;
             wb = (1.f - a.lam[k0]) * a.dt[k0];
         }
         const T *iB = a.init_cB ? static_cast<const T *>(a.init_cB) + sl * (R * N) : nullptr;
@@ -675,7 +697,7 @@ void k_scan_fused(ScanArgs a) {
     if (c == 0) {
         load_init(Sin);
     } else {
-        const int64_t sbase = sl * a.nchunks;
+        const int64_t sbase = seq_slot;
         int64_t j = c - 1;        // next predecessor to probe
         int64_t jt = flags_lost ? c - 1 : -2;   // terminal: -1 sequence start, >= 0 inclusive state
         bool timed_out = flags_lost;
@@ -835,7 +857,7 @@ void k_scan_fused(ScanArgs a) {
             }
             T *cB = static_cast<T *>(a.cB) + sl * (R * N);
             T *cX = static_cast<T *>(a.cX) + sl * (R * P);
-            const int64_t kl = (b * a.L + a.L - 1) * a.H + h;
+            const int64_t kl = (seq_tok + seq_len - 1) * a.H + h;
             const T *Bl = static_cast<const T *>(a.B) + kl * (R * N);
             const T *Xl = static_cast<const T *>(a.x) + kl * xin_tok;
             if constexpr (kPro) {   // the carry holds the B and X the recurrence used
@@ -995,7 +1017,8 @@ void k_scan_fused(ScanArgs a) {
         }
         asm volatile("" ::: "memory");
     }
-    if (tid == 0 && s_ctl[1]) janitor_reset(a.ctl, nsl, a.nchunks, s_ctl[0], a.spin_max);
+    if (tid == 0 && s_ctl[1])
+        janitor_reset(a.ctl, nsl, a.nchunks, s_ctl[0], a.spin_max, kVar ? a.vl_grp : nullptr, a.vl_maxn);
 }
 
 template <typename T, int Q, int R, bool kPro = false>
@@ -1007,6 +1030,19 @@ hipError_t launch_fused(const ScanArgs &a, hipStream_t stream) {
                            dim3(S::NTHR), 0, stream, a);
     else
         hipLaunchKernelGGL((k_scan_fused<T, Q, R, false, kPro>), dim3((unsigned)(nsl * a.nchunks)),
+                           dim3(S::NTHR), 0, stream, a);
+    return hipGetLastError();
+}
+
+// Varlen single launch: one workgroup per (sequence, head, chunk) item.
+template <typename T, int Q, int R>
+hipError_t launch_fused_var(const ScanArgs &a, hipStream_t stream) {
+    typedef FShape<T, Q, R> S;
+    if (a.z)
+        hipLaunchKernelGGL((k_scan_fused<T, Q, R, true, false, true>), dim3((unsigned)a.vl_slots),
+                           dim3(S::NTHR), 0, stream, a);
+    else
+        hipLaunchKernelGGL((k_scan_fused<T, Q, R, false, false, true>), dim3((unsigned)a.vl_slots),
                            dim3(S::NTHR), 0, stream, a);
     return hipGetLastError();
 }
@@ -1030,6 +1066,15 @@ scan_launch_fn find_fused_impl(int io, int64_t N, int64_t P, int64_t R, int64_t 
     if (N != 128 || P != 64) return nullptr;
 #define M3_CASE(IO, T, R_, Q_) \
     if (io == IO && R == R_ && Q == Q_) return &launch_fused<T, Q_, R_>;
+    M3_FUSED_SHAPES(M3_CASE)
+#undef M3_CASE
+    return nullptr;
+}
+
+scan_launch_fn find_fused_var_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q) {
+    if (N != 128 || P != 64) return nullptr;
+#define M3_CASE(IO, T, R_, Q_) \
+    if (io == IO && R == R_ && Q == Q_) return &launch_fused_var<T, Q_, R_>;
     M3_FUSED_SHAPES(M3_CASE)
 #undef M3_CASE
     return nullptr;

@@ -54,6 +54,7 @@ class M3Error(RuntimeError):
 
 
 EXPORTS = ("m3_scan_workspace_bytes", "m3_scan_fwd", "m3_scan_fwd_gated", "m3_scan_fwd_varlen",
+           "m3_scan_varlen_workspace_bytes", "m3_scan_varlen_check",
            "m3_step", "m3_step_gated", "m3_scan_check", "m3_set_wait_limit", "m3_scan_fwd_noalloc",
            "m3_scan_fwd_pro", "m3_step_pro", "m3_scan_bwd", "m3_scan_bwd_workspace_bytes",
            "m3_status_string", "m3_last_hip_error")
@@ -80,6 +81,12 @@ def lib() -> ctypes.CDLL:
         L.m3_scan_fwd_varlen.argtypes = ([dims_p, ctypes.POINTER(ctypes.c_int64)] + [vp] * 16
                                          + [vp, ctypes.c_size_t, vp])
         L.m3_scan_fwd_varlen.restype = ctypes.c_int
+        i64p = ctypes.POINTER(ctypes.c_int64)
+        L.m3_scan_varlen_workspace_bytes.argtypes = [dims_p, i64p]
+        L.m3_scan_varlen_workspace_bytes.restype = ctypes.c_size_t
+        L.m3_scan_varlen_check.argtypes = [dims_p, i64p, vp, ctypes.c_size_t,
+                                           ctypes.POINTER(ctypes.c_uint32), vp]
+        L.m3_scan_varlen_check.restype = ctypes.c_int
         L.m3_step.argtypes = [dims_p] + [vp] * 12 + [vp]
         L.m3_step.restype = ctypes.c_int
         L.m3_step_gated.argtypes = [dims_p] + [vp] * 13 + [vp]
@@ -247,13 +254,56 @@ def scan_fwd_noalloc(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, out,
     return y, fs, (cB, cX)
 
 
+def varlen_dims(x, Bm, A, chunk: int, cu, split: bool = False, per_chunk: bool = False,
+                seg: int = 0, theta=None) -> M3Dims:
+    T, nheads, rank, headdim = x.shape
+    dstate = Bm.shape[-1]
+    S = len(cu) - 1
+    if A.dim() == 1 and A.shape[0] == nheads:
+        sb, st, sh = 0, 0, 1
+    elif A.dim() == 2 and tuple(A.shape) == (T, nheads):
+        sb, (st, sh) = 0, A.stride()
+    else:
+        raise ValueError(f"A must be [H] or [T, H], got {tuple(A.shape)}")
+    ph = theta is not None and _theta_per_head(theta, nheads, dstate)
+    flags = ((M3_SCAN_SPLIT if split else 0) | (M3_SCAN_PER_CHUNK if per_chunk else 0)
+             | (M3_THETA_PER_HEAD if ph else 0))
+    return M3Dims(S, T, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags, sb, st, sh,
+                  int(seg))
+
+
+def _cu_list(cu_seqlens):
+    return [int(v) for v in (cu_seqlens.tolist() if hasattr(cu_seqlens, "tolist") else cu_seqlens)]
+
+
+def varlen_workspace_bytes(dims: M3Dims, cu_seqlens) -> int:
+    """m3_scan_varlen_workspace_bytes: the workspace of the one-launch varlen
+    scan (0: it does not apply)."""
+    cu = _cu_list(cu_seqlens)
+    return int(lib().m3_scan_varlen_workspace_bytes(ctypes.byref(dims), (ctypes.c_int64 * len(cu))(*cu)))
+
+
+def varlen_check(dims: M3Dims, cu_seqlens, workspace, stream=None) -> int:
+    """m3_scan_varlen_check: look-back timeouts of the last varlen call on
+    `workspace` (synchronises the stream)."""
+    cu = _cu_list(cu_seqlens)
+    n = ctypes.c_uint32(0)
+    wsb = workspace.numel() if workspace is not None else 0
+    _check(lib().m3_scan_varlen_check(ctypes.byref(dims), (ctypes.c_int64 * len(cu))(*cu),
+                                      _p(workspace), wsb, ctypes.byref(n), _stream(stream)))
+    return int(n.value)
+
+
 def scan_fwd_varlen(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, cu_seqlens,
                     init_state=None, init_carry=None, z=None, workspace=None, stream=None,
-                    split: bool = False, per_chunk: bool = False, seg: int = 0):
+                    split: bool = False, per_chunk: bool = False, seg: int = 0,
+                    check: bool = False):
     """m3_scan_fwd_varlen: sequences packed along the token axis, x [T,H,R,P],
     Bm/Cm [T,H,R,N], dt/lam [T,H], theta [T,H,N/2] (or [H,N/2] frequencies),
     A [H] or [T,H]; `cu_seqlens` (S + 1 offsets, host list or tensor).  Returns
-    y [T,H,R,P], final_state [S,H,N,P] and the carry ([S,H,R,N], [S,H,R,P])."""
+    y [T,H,R,P], final_state [S,H,N,P] and the carry ([S,H,R,N], [S,H,R,P]).
+    Without a workspace one is allocated (zero-filled) for the one-launch
+    scan where that applies, else for the largest sequence."""
     cu = [int(v) for v in (cu_seqlens.tolist() if hasattr(cu_seqlens, "tolist") else cu_seqlens)]
     T, nheads, rank, headdim = x.shape
     dstate = Bm.shape[-1]
@@ -274,16 +324,23 @@ def scan_fwd_varlen(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, cu_seqlens,
     cB = torch.empty((S, nheads, rank, dstate), dtype=x.dtype, device=dev)
     cX = torch.empty((S, nheads, rank, headdim), dtype=x.dtype, device=dev)
     if workspace is None:
-        longest = max([cu[i + 1] - cu[i] for i in range(S)] + [0])
-        d1 = M3Dims(1, longest, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags,
-                    0, st, sh, int(seg))
-        workspace = torch.zeros(max(workspace_bytes(d1), 16), dtype=torch.uint8, device=dev)
+        one = varlen_workspace_bytes(d, cu)
+        if one == 0:
+            longest = max([cu[i + 1] - cu[i] for i in range(S)] + [0])
+            d1 = M3Dims(1, longest, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags,
+                        0, st, sh, int(seg))
+            one = workspace_bytes(d1)
+        workspace = torch.zeros(max(one, 16), dtype=torch.uint8, device=dev)
     icB, icX = (None, None) if init_carry is None else init_carry
     cu_arr = (ctypes.c_int64 * len(cu))(*cu)
     _check(lib().m3_scan_fwd_varlen(ctypes.byref(d), cu_arr, _p(x), _p(Bm), _p(Cm), _p(dt), _p(A),
                                     _p(lam), _p(theta), _p(D), _p(z), _p(init_state), _p(icB),
                                     _p(icX), _p(y), _p(fs), _p(cB), _p(cX), _p(workspace),
                                     workspace.numel(), _stream(stream)))
+    if check:
+        n = varlen_check(d, cu, workspace, stream)
+        if n:
+            raise LookBackTimeout(f"{n} look-back wait(s) gave up: y and the final state are invalid")
     return y, fs, (cB, cX)
 
 

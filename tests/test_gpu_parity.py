@@ -746,6 +746,129 @@ def test_varlen_equal_length_runs(variant):
             assert np.array_equal(oracle._np(cB[i, h]), rb[h]) and np.array_equal(oracle._np(cX[i, h]), rx[h])
 
 
+def varlen_oracle_check(inp, y, fs, cB, cX, cu, seqs, H, R, N, P, io, init=None, icB=None, icX=None,
+                        z=None, A_tok=None, label=""):
+    """Every listed sequence of a packed batch against the oracle from its own
+    initial state and carry."""
+    for i in seqs:
+        t0, t1 = cu[i], cu[i + 1]
+        sl = [(0, h) for h in range(H)]
+        ref = oracle.slices_of_scan(inp.x, inp.Bm, inp.Cm, inp.dt, inp.A, inp.lam, inp.theta,
+                                    inp.D, sl, t0, t1)
+        if A_tok is not None:
+            ref["A"] = np.stack([A_tok[t0:t1, h].double().cpu().numpy() for h in range(H)])
+        kw = {}
+        if init is not None:
+            kw = dict(init_state=oracle._np(init[i]), init_B=oracle._np(icB[i]), init_X=oracle._np(icX[i]))
+        ry, rs, rb, rx = oracle.scan(**ref, **kw)
+        for h in range(H):
+            ref_y = ry[h] if z is None else oracle.gate(ry[h], oracle._np(z[t0:t1, h]))
+            e = oracle.rel_err(y[t0:t1, h].double().cpu().numpy(), ref_y)
+            assert e <= TOL[io], f"{label} seq {i} head {h} y rel err {e:.3g}"
+            e = oracle.rel_err(fs[i, h].cpu().numpy(), rs[h])
+            assert e <= TOL[io], f"{label} seq {i} head {h} state rel err {e:.3g}"
+            assert np.array_equal(oracle._np(cB[i, h]), rb[h]) and np.array_equal(oracle._np(cX[i, h]), rx[h])
+
+
+@pytest.mark.parametrize("R,Q,gated,per_head,per_token_A", [
+    (1, 64, False, False, False), (4, 128, True, False, False), (2, 32, False, True, False),
+    (4, 64, False, False, True), (1, 128, True, True, False),
+])
+def test_varlen_one_launch(R, Q, gated, per_head, per_token_A):
+    """29 packed sequences of ragged lengths (1 .. 5Q, some whole chunks) in
+    one launch of the per-chunk kernel: every sequence against the oracle
+    from its own initial state and carry; the same bits as each sequence
+    scanned alone with the per-chunk kernel; a second call gives the same
+    bits."""
+    io, N, P, H = "bf16", 128, 64, 3
+    rng = np.random.default_rng(200 + R + Q)
+    lens = [int(v) for v in rng.integers(1, 5 * Q + 1, 29)]
+    lens[3], lens[7], lens[11] = 1, Q, 2 * Q
+    cu = [0]
+    for n in lens:
+        cu.append(cu[-1] + n)
+    T, S = cu[-1], len(lens)
+    say(f"varlen one launch R={R} Q={Q} T={T} gated={gated} per_head={per_head} A per token={per_token_A}")
+    inp = make_scan_inputs(1, T, H, P, N, R, io=io, seed=211 + R + Q, device=DEV, chunk=Q)
+    flat = lambda t: t[0].contiguous()
+    x, Bm, Cm, dt, lam, theta = (flat(inp.x), flat(inp.Bm), flat(inp.Cm), flat(inp.dt),
+                                 flat(inp.lam), flat(inp.theta))
+    th_in = inp.omega.contiguous() if per_head else theta
+    z = make_gate_input(x, 4) if gated else None
+    A_in = (-torch.rand(T, H, device=DEV) * 4 - 0.1).contiguous() if per_token_A else inp.A
+    init = torch.randn(S, H, N, P, device=DEV)
+    icB = torch.randn(S, H, R, N, device=DEV).to(x.dtype)
+    icX = torch.randn(S, H, R, P, device=DEV).to(x.dtype)
+    d = m3.varlen_dims(x, Bm, A_in, Q, cu, theta=th_in)
+    need = m3.varlen_workspace_bytes(d, cu)
+    assert need > 0, "the one-launch scan applies"
+    ws = torch.zeros(need, dtype=torch.uint8, device=DEV)
+    args = (x, Bm, Cm, dt, A_in, lam, th_in, inp.D, Q, cu)
+    kw = dict(init_state=init, init_carry=(icB, icX), z=z, workspace=ws, check=True)
+    y, fs, (cB, cX) = m3.scan_fwd_varlen(*args, **kw)
+    torch.cuda.synchronize()
+    varlen_oracle_check(inp, y, fs, cB, cX, cu, range(S), H, R, N, P, io, init, icB, icX, z,
+                        A_in if per_token_A else None, label="one launch")
+    # each sequence alone, one chunk per workgroup: the same launches' arithmetic
+    for i in sorted({0, 3, 7, 11, S - 1, int(rng.integers(0, S))}):
+        t0, t1 = cu[i], cu[i + 1]
+        one = lambda t: t[None, t0:t1].contiguous()
+        A1 = A_in[t0:t1].contiguous()[None] if per_token_A else inp.A
+        y1, fs1, (cB1, cX1) = m3.scan_fwd(one(x), one(Bm), one(Cm), one(dt), A1, one(lam),
+                                          th_in if per_head else one(theta), inp.D, chunk=Q,
+                                          init_state=init[i:i + 1].contiguous(),
+                                          init_carry=(icB[i:i + 1].contiguous(), icX[i:i + 1].contiguous()),
+                                          z=None if z is None else one(z), per_chunk=True)
+        torch.cuda.synchronize()
+        assert torch.equal(y1[0], y[t0:t1]) and torch.equal(fs1[0], fs[i]), f"seq {i}: not bit-identical"
+        assert torch.equal(cB1[0], cB[i]) and torch.equal(cX1[0], cX[i])
+    y2, fs2, _ = m3.scan_fwd_varlen(*args, **kw)
+    torch.cuda.synchronize()
+    assert torch.equal(y2, y) and torch.equal(fs2, fs), "second call differs"
+
+
+def test_varlen_many_short_sequences():
+    """600 packed sequences of 1 .. 40 tokens (SISO, chunk 64): one launch
+    against the oracle on a sample of sequences (the first, the last and
+    30 more), and against the sequence-by-sequence launches the same call
+    makes with a workspace too small for one launch."""
+    io, N, P, R, Q, H = "bf16", 128, 64, 1, 64, 4
+    rng = np.random.default_rng(300)
+    lens = [int(v) for v in rng.integers(1, 41, 600)]
+    cu = [0]
+    for n in lens:
+        cu.append(cu[-1] + n)
+    T, S = cu[-1], len(lens)
+    say(f"varlen many short sequences S={S} T={T}")
+    inp = make_scan_inputs(1, T, H, P, N, R, io=io, seed=301, device=DEV, chunk=Q)
+    flat = lambda t: t[0].contiguous()
+    args = (flat(inp.x), flat(inp.Bm), flat(inp.Cm), flat(inp.dt), inp.A, flat(inp.lam),
+            flat(inp.theta), inp.D, Q, cu)
+    d = m3.varlen_dims(args[0], args[1], inp.A, Q, cu)
+    need = m3.varlen_workspace_bytes(d, cu)
+    assert need > 0
+    ws = torch.zeros(need, dtype=torch.uint8, device=DEV)
+    y, fs, (cB, cX) = m3.scan_fwd_varlen(*args, workspace=ws, check=True)
+    torch.cuda.synchronize()
+    seqs = sorted({0, S - 1} | {int(v) for v in rng.integers(0, S, 30)})
+    varlen_oracle_check(inp, y, fs, cB, cX, cu, seqs, H, R, N, P, io, label="many short")
+    small = torch.zeros(m3.workspace_bytes(m3.M3Dims(1, 40, H, P, N, R, Q, 1, 0, 0, 0, 1, 0)),
+                        dtype=torch.uint8, device=DEV)
+    y2, fs2, (cB2, cX2) = m3.scan_fwd_varlen(*args, workspace=small, check=True)
+    torch.cuda.synchronize()
+    varlen_oracle_check(inp, y2, fs2, cB2, cX2, cu, seqs, H, R, N, P, io, label="per sequence")
+    # timing of the two (reported, not asserted)
+    for name, w in (("one launch", ws), ("per sequence", small)):
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(3):
+            m3.scan_fwd_varlen(*args, workspace=w)
+        e1.record()
+        torch.cuda.synchronize()
+        say(f"varlen {S} sequences, {name}: {e0.elapsed_time(e1) / 3:.3f} ms")
+
+
 @pytest.mark.parametrize("mode,seg,R,Q", [("per_chunk", 0, 1, 64), ("per_chunk", 0, 4, 128),
                                           ("seg", 2, 4, 64), ("seg", 4, 1, 64)])
 def test_determinism_many_items(mode, seg, R, Q):

@@ -216,6 +216,41 @@ def test_varlen_host_validation(L):
     assert L.m3_last_hip_error() == 0
 
 
+def test_varlen_one_launch_host(L):
+    """m3_scan_varlen_workspace_bytes: the one-launch workspace (control block,
+    a flag, the totals and two state maps per (sequence, head, chunk) slot,
+    the tables) where the per-chunk kernel serves the shape and every
+    sequence is non-empty, else 0; m3_scan_varlen_check's argument errors on
+    the host."""
+    bf = dict(io=m3.M3_BF16, headdim=64, dstate=128, rank=1, chunk=64, nheads=4)
+
+    def nb(d, cu):
+        return L.m3_scan_varlen_workspace_bytes(ctypes.byref(d), (ctypes.c_int64 * len(cu))(*cu))
+    cu = [0, 100, 101, 357]
+    d = dims(batch=3, seqlen=357, **bf)
+    n = nb(d, cu)
+    slots = 4 * (2 + 1 + 4)
+    assert n >= m3.CTL_BYTES + slots * (4 + 65 * 4 + 2 * 128 * 64 * 4) and n % 256 == 0
+    assert nb(dims(batch=3, seqlen=357, **dict(bf, rank=4, chunk=128)), cu) > 0
+    assert nb(d, [0, 100, 100, 357]) == 0                                   # an empty sequence
+    assert nb(d, [0, 100, 50, 357]) == 0                                    # bad offsets
+    assert nb(dims(batch=3, seqlen=357, flags=m3.M3_SCAN_SPLIT, **bf), cu) == 0
+    assert nb(dims(batch=3, seqlen=357, seg_chunks=2, **bf), cu) == 0
+    assert nb(dims(batch=3, seqlen=357, **dict(bf, dstate=64)), cu) == 0    # three-kernel shape
+    assert nb(dims(batch=3, seqlen=357), cu) == 0                          # fp32 16 x 16
+    t = ctypes.c_uint32(7)
+    arr = (ctypes.c_int64 * 4)(*cu)
+    chk = L.m3_scan_varlen_check
+    assert chk(ctypes.byref(d), None, FAKE, n, ctypes.byref(t), None) == m3.M3_ERR_NULL
+    assert chk(ctypes.byref(d), arr, FAKE, n, None, None) == m3.M3_ERR_NULL
+    bad = (ctypes.c_int64 * 4)(0, 100, 50, 357)
+    assert chk(ctypes.byref(d), bad, FAKE, n, ctypes.byref(t), None) == m3.M3_ERR_SHAPE
+    assert chk(ctypes.byref(d), arr, FAKE + 4, n, ctypes.byref(t), None) == m3.M3_ERR_ALIGN
+    # too small for the one launch: the last sequence's launch is the one checked
+    assert chk(ctypes.byref(d), arr, None, 0, ctypes.byref(t), None) == m3.M3_ERR_WORKSPACE
+    assert L.m3_last_hip_error() == 0
+
+
 def test_scan_check_host_validation(L):
     """m3_scan_check: argument errors on the host; the three-kernel path and
     the empty sequence report zero waits without touching the device."""
