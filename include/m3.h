@@ -393,8 +393,8 @@ m3_status m3_step_pro(const m3_dims *dims, const m3_prologue *pro,
  * overwritten.  Supported (else M3_ERR_UNSUPPORTED): io bf16, dstate 128,
  * headdim 64, chunk * rank = 64 (rank 1 chunk 64, rank 2 chunk 32, rank 4
  * chunk 16), no M3_THETA_PER_HEAD; A strided per head or per token.
- * Workspace: m3_scan_bwd_workspace_bytes(dims) bytes (16-byte aligned; four
- * fp32 N x P maps per chunk, after the scans' control block of M3_CTL_BYTES, which
+ * Workspace: m3_scan_bwd_workspace_bytes(dims) bytes (16-byte aligned; two
+ * fp32 and two bf16 N x P maps per chunk, after the scans' control block of M3_CTL_BYTES, which
  * this call neither reads nor writes; no initialisation).  Token arrays may be NULL when seqlen == 0.
  * Alignment: x, B, C, dy, dx, dB, dC, the states and the workspace 16 bytes,
  * the rest 4 bytes (else M3_ERR_ALIGN).  Outputs must not overlap inputs.

@@ -264,6 +264,7 @@ __global__ __launch_bounds__(kThr) void k_bwd_pass(BwdArgs a, int per) {
     const int64_t NP = kN * kP, base = bh * a.nchunks;
     const int o_re = i * kP + p, o_im = (i + kNH) * kP + p;
     constexpr int DEPTH = 8;   // chunks whose loads are issued together
+    bf16 *Sb = reinterpret_cast<bf16 *>(a.Sst);   // (bf16: an MFMA operand, and the decay term below)
     float sre = 0.f, sim = 0.f;
     if (a.init_state) {
         sre = a.init_state[bh * NP + o_re];
@@ -283,8 +284,8 @@ __global__ __launch_bounds__(kThr) void k_bwd_pass(BwdArgs a, int per) {
         for (int d = 0; d < DEPTH; ++d) {
             if (c0 + d >= a.nchunks) break;
             const int64_t s = base + c0 + d;
-            a.Sst[s * NP + o_re] = sre;
-            a.Sst[s * NP + o_im] = sim;
+            Sb[s * NP + o_re] = (bf16)sre;
+            Sb[s * NP + o_im] = (bf16)sim;
             const float e = __expf(ce[d]);
             float sn, cs;
             sincos_fast(ps[d], &sn, &cs);
@@ -307,8 +308,8 @@ __global__ __launch_bounds__(kThr) void k_bwd_pass(BwdArgs a, int per) {
             const int64_t s = base + max(c1 - d, (int64_t)0);
             ce[d] = a.tot[s * (1 + kNH)];
             ps[d] = a.tot[s * (1 + kNH) + 1 + i];
-            pre[d] = a.Sst[s * NP + o_re];
-            pim[d] = a.Sst[s * NP + o_im];
+            pre[d] = (float)Sb[s * NP + o_re];
+            pim[d] = (float)Sb[s * NP + o_im];
             mre[d] = a.Mb[s * NP + o_re];
             mim[d] = a.Mb[s * NP + o_im];
         }
@@ -393,14 +394,11 @@ __global__ __launch_bounds__(kThrC) void k_bwd_chunk(BwdArgs a) {
     stage_rows<R, kThrC>(s_dY, static_cast<const bf16 *>(a.dy) + tok0 * (R * kP), xstr, nvalid, nullptr);
     {
         const int64_t NP = kN * kP;
-        const float4 *Sg = reinterpret_cast<const float4 *>(a.Sst + slot * NP);
+        const bf16x4 *Sg = reinterpret_cast<const bf16x4 *>(reinterpret_cast<const bf16 *>(a.Sst) + slot * NP);
         const bf16x4 *Ug = reinterpret_cast<const bf16x4 *>(reinterpret_cast<const bf16 *>(a.Ust) + slot * NP);
         for (int q = tid; q < kN * kP / 4; q += kThrC) {
             const int n = (4 * q) / kP, p = (4 * q) % kP;
-            const float4 sv = Sg[q];
-            bf16x4 s4;
-            s4[0] = (bf16)sv.x; s4[1] = (bf16)sv.y; s4[2] = (bf16)sv.z; s4[3] = (bf16)sv.w;
-            *reinterpret_cast<bf16x4 *>(&s_S[n * LDP + p]) = s4;
+            *reinterpret_cast<bf16x4 *>(&s_S[n * LDP + p]) = Sg[q];
             *reinterpret_cast<bf16x4 *>(&s_U[n * LDP + p]) = Ug[q];
         }
     }
@@ -810,8 +808,8 @@ BwdWorkspaceLayout bwd_workspace_layout(int64_t BH, int64_t nchunks, int64_t N, 
     w.off_Af = kCtlBytes;   // (the scans' control block, left untouched in a shared workspace)
     w.off_Mb = up(w.off_Af + st);
     w.off_Sst = up(w.off_Mb + st);
-    w.off_Ust = up(w.off_Sst + st);
-    w.off_tot = up(w.off_Ust + st);
+    w.off_Ust = up(w.off_Sst + st / 2);   // (bf16 maps)
+    w.off_tot = up(w.off_Ust + st / 2);
     w.off_pst = up(w.off_tot + per * (size_t)(1 + N / 2) * sizeof(float));
     w.off_dsig = up(w.off_pst + per * (size_t)N * sizeof(float));
     w.off_dA = up(w.off_dsig + per * sizeof(float));

@@ -92,7 +92,7 @@ struct BwdArgs {
     float *Af;      // [N][P] chunk aggregate R(psi_e) sum_j v_j B^_j x_j^T
     float *Mb;      // [N][P] sum_t e^{cum_t} C^_t dy_t^T
     float *tot;     // [1 + N/2] cum_e, psi_e
-    float *Sst;     // [N][P] state entering the chunk
+    float *Sst;     // [N][P] state entering the chunk, stored as bf16 (an MFMA operand; the decay term)
     float *Ust;     // [N][P] R(-psi_e) dJ/dS_out, stored as bf16 (an MFMA operand only)
     float *pst;     // [2][N/2] state terms of dpsi_e and dcum_e (per pair)
     float *dsig;    // [1] dJ/dsigma of the chunk's last token

@@ -370,7 +370,7 @@ def test_backward_host_validation(L):
     d = dims(**bf)
     need = L.m3_scan_bwd_workspace_bytes(ctypes.byref(d))
     nc = (300 + 63) // 64
-    assert need >= 2 * nc * 4 * 128 * 64 * 4          # four fp32 N x P maps per chunk and slice
+    assert need >= 2 * nc * 3 * 128 * 64 * 4          # two fp32 and two bf16 N x P maps per chunk and slice
     assert call(dims(**dict(bf, rank=4, chunk=64))) == m3.M3_ERR_UNSUPPORTED   # chunk*rank 256
     assert L.m3_scan_bwd_workspace_bytes(ctypes.byref(dims(**dict(bf, rank=4, chunk=16)))) > 0
     assert call(dims()) == m3.M3_ERR_UNSUPPORTED                                  # fp32 not built
