@@ -215,7 +215,7 @@ def main():
         "decode_us_p10_p90": [round(float(np.percentile(step_ms, 10)) * 1e3, 3),
                               round(float(np.percentile(step_ms, 90)) * 1e3, 3)],
         # the dominant kernel of the step: the long-context scan (one
-        # m3_scan_fwd = the per-chunk kernel, after its reset launch)
+        # m3_scan_fwd = one launch of the per-chunk kernel)
         "roofline": {
             "kernel": "m3_scan_fwd long-context MIMO prefill (k_scan_fused<bf16,128,4>)",
             "bound": "mfma", "achieved": round(pre_tfs, 2), "peak": peak_tfs, "unit": "TFLOP/s",
@@ -270,6 +270,10 @@ def main():
         result["backward_siso"] = bw.figures(roofline, ms, peak_gbs, peak_tfs)
         result["backward_siso"]["traffic"] = measured_traffic("backward_siso")
         del bw
+        torch.cuda.empty_cache()
+        log("extras: decode at state size 64")
+        result["decode_state64"] = decode_state64_figures(m3, roofline, torch, stream, dev,
+                                                          wd, dec_us, peak_gbs)
         torch.cuda.empty_cache()
 
     if not args.no_cpu:
@@ -476,6 +480,43 @@ def prologue_figures(m3, roofline, torch, stream, dev, W, workload_inputs, peak_
         del inp, pin, ws, o
         torch.cuda.empty_cache()
     return out
+
+
+def decode_state64_figures(m3, roofline, torch, stream, dev, wd, dec_us_128, peak_gbs):
+    """The decode workload's batch, heads and rank at state size 64 (the
+    paper's MIMO state-size point): microseconds per step from a random fp32
+    state and carry, seeded step inputs, against the state-128 step."""
+    from paper_2603_15569_amd.inputs import make_scan_inputs, make_step_inputs
+    B, H, R, P, N = wd["batch"], wd["nheads"], wd["rank"], wd["headdim"], 64
+    layer = make_scan_inputs(B, 1, H, P, N, R, io="bf16", seed=4400, device=dev, chunk=64)
+    g = torch.Generator(dev).manual_seed(4401)
+    state = torch.randn((B, H, N, P), device=dev, generator=g) * 0.1
+    cB = torch.randn((B, H, R, N), device=dev, generator=g).to(torch.bfloat16)
+    cX = torch.randn((B, H, R, P), device=dev, generator=g).to(torch.bfloat16)
+    steps = [make_step_inputs(layer, s, device=dev) for s in range(8)]
+    y = torch.empty_like(steps[0].x)
+
+    def step(i):
+        st = steps[i % len(steps)]
+        m3.step(state, (cB, cX), st.x, st.Bm, st.Cm, st.dt, layer.A, st.lam, st.theta, layer.D, y=y)
+    for i in range(5):
+        step(i)
+    n = 100
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record(stream)
+    for i in range(n):
+        step(i)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) / n * 1e3
+    nbytes = B * H * roofline.decode_bytes_per_slice(N, P, R, 2)
+    gbs = nbytes / (us * 1e-6) / 1e9
+    return {"workload": f"decode step B={B} H={H} P={P} N={N} R={R} fp32 state",
+            "us_per_step": round(us, 3), "achieved_gbs": round(gbs, 1),
+            "hbm_frac": round(gbs / peak_gbs, 4), "bytes_per_launch": nbytes,
+            "state128_us_per_step": round(dec_us_128, 3),
+            "ratio_to_state128": round(us / dec_us_128, 3)}
 
 
 class BackwardCase:
