@@ -295,32 +295,6 @@ void k_scan_fused(ScanArgs a) {
             for (int kk = 0; kk < NK; ++kk) cf[m][kk] = buf_load<Frag>(rc, off + kk * MM::K * sizeof(T));
         }
     };
-    // Block prologue on the C fragments: C = g o C' / rms(C') + b, applied in
-    // place and rounded to the operand type before the rotation (a row sits
-    // in lanes l16 + 16 g).  Chunks of several row blocks do it at the end of
-    // the prologue, while the registers of the later phases are still free.
-    auto norm_cf = [&]() {
-#pragma unroll
-        for (int m = 0; m < TPW; ++m) {
-            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R;
-            float ss = 0.f;
-#pragma unroll
-            for (int kk = 0; kk < NK; ++kk) ss += sumsq(cf[m][kk]);
-            ss += __shfl_xor(ss, 16, kWave);
-            ss += __shfl_xor(ss, 32, kWave);
-            const bool ok = t < nvalid;
-            const float sc = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
-            const float bsc = ok ? 1.f : 0.f;
-            const int pcr = kPC + (row % R) * N + MM::KPL * g;
-#pragma unroll
-            for (int kk = 0; kk < NK; ++kk)
-#pragma unroll
-                for (int e = 0; e < MM::KPL; ++e) {
-                    const int pc = pcr + kk * MM::K + e;
-                    fset(cf[m][kk], e, sc * s_pro[pc] * fget(cf[m][kk], e) + bsc * s_pro[pc - kPC + kPCb]);
-                }
-        }
-    };
     // ---- 2. prologue ----
     if constexpr (kPro) {   // the head's prologue tables (read after the prologue's barriers)
         const int64_t hn = h * (R * N), hp = h * (R * P);
@@ -421,7 +395,6 @@ void k_scan_fused(ScanArgs a) {
             const Acc cum_e = s_cum[nvalid - 1];
             s_w[tid] = (tid < nvalid) ? (float)(exp_fast(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
         }
-        if constexpr (kPro && kEarlyC) norm_cf();
         __syncthreads();
     }
 
@@ -430,19 +403,59 @@ void k_scan_fused(ScanArgs a) {
     using False = std::integral_constant<bool, false>;
 
     // C^ fragments of the owned row tiles, rotated by -psi_t (rows past the
-    // end of the sequence were loaded as zeros)
+    // end of the sequence were loaded as zeros).  With the prologue the
+    // rotation first normalises each element, c = sc g c + b in fp32 (sc the
+    // row's RMS scale from a sum of squares over its fragments; a row sits in
+    // lanes l16 + 16 g), so the fragments are rounded once.  A lane's rank
+    // row r = l16 % R is the same in all its tiles, so the gain and bias of
+    // its elements are read once per fragment pair (16-byte reads) and serve
+    // every tile.
     auto rotate_cf = [&]() {
-        if constexpr (kPro && !kEarlyC) norm_cf();
+        float scm[TPW], bscm[TPW];
+        if constexpr (kPro) {
 #pragma unroll
-        for (int m = 0; m < TPW; ++m) {
-            const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R;
+            for (int m = 0; m < TPW; ++m) {
+                const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
+                float ss = 0.f;
 #pragma unroll
-            for (int kk = 0; kk < NK / 2; ++kk) {
+                for (int kk = 0; kk < NK; ++kk) ss += sumsq(cf[m][kk]);
+                ss += __shfl_xor(ss, 16, kWave);
+                ss += __shfl_xor(ss, 32, kWave);
+                const bool ok = t < nvalid;
+                scm[m] = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
+                bscm[m] = ok ? 1.f : 0.f;
+            }
+        }
+#pragma unroll
+        for (int kk = 0; kk < NK / 2; ++kk) {
+            float gu[MM::KPL], gw[MM::KPL], bu[MM::KPL], bw[MM::KPL];
+            if constexpr (kPro) {
+                static_assert(MM::KPL % 4 == 0 && 16 % R == 0, "16-byte table reads; r = l16 % R");
+                const int pu = (l16 % R) * N + kk * MM::K + MM::KPL * g, pw = pu + NH;
+#pragma unroll
+                for (int e4 = 0; e4 < MM::KPL; e4 += 4) {
+                    const float4 a0 = *reinterpret_cast<const float4 *>(&s_pro[kPC + pu + e4]);
+                    const float4 a1 = *reinterpret_cast<const float4 *>(&s_pro[kPC + pw + e4]);
+                    const float4 c0 = *reinterpret_cast<const float4 *>(&s_pro[kPCb + pu + e4]);
+                    const float4 c1 = *reinterpret_cast<const float4 *>(&s_pro[kPCb + pw + e4]);
+                    gu[e4] = a0.x; gu[e4 + 1] = a0.y; gu[e4 + 2] = a0.z; gu[e4 + 3] = a0.w;
+                    gw[e4] = a1.x; gw[e4 + 1] = a1.y; gw[e4 + 2] = a1.z; gw[e4 + 3] = a1.w;
+                    bu[e4] = c0.x; bu[e4 + 1] = c0.y; bu[e4 + 2] = c0.z; bu[e4 + 3] = c0.w;
+                    bw[e4] = c1.x; bw[e4 + 1] = c1.y; bw[e4 + 2] = c1.z; bw[e4 + 3] = c1.w;
+                }
+            }
+#pragma unroll
+            for (int m = 0; m < TPW; ++m) {
+                const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
                 float csv[MM::KPL], snv[MM::KPL];
                 cs_getn<MM::KPL>(&s_cs[t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
 #pragma unroll
                 for (int e = 0; e < MM::KPL; ++e) {
-                    const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
+                    float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
+                    if constexpr (kPro) {
+                        u = scm[m] * gu[e] * u + bscm[m] * bu[e];
+                        w = scm[m] * gw[e] * w + bscm[m] * bw[e];
+                    }
                     fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
                     fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
                 }
