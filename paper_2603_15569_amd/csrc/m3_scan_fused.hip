@@ -177,6 +177,13 @@ void k_scan_fused(ScanArgs a) {
     const T *Xg = static_cast<const T *>(a.x) + tok0 * xin_tok;
     const int64_t xin_str = tstr * xin_tok;
 
+    // K consecutive prologue-table floats (16-byte LDS reads; p a multiple of 4)
+    auto tab = [&](int p, float *v, int K) {
+        for (int q = 0; q < K; q += 4) {
+            const float4 f = *reinterpret_cast<const float4 *>(&s_pro[p + q]);
+            v[q] = f.x; v[q + 1] = f.y; v[q + 2] = f.z; v[q + 3] = f.w;
+        }
+    };
     // Rows jb*64 .. of the chunk are staged in two steps so that the global
     // loads of the next block overlap the MFMA work on this one: fetch()
     // issues the loads into registers, commit() rotates B^ = R(-psi_t) B and
@@ -246,7 +253,7 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
                 float u = fget(lo, e), w = fget(hi, e);
-                if constexpr (kPro) {
+                if constexpr (kPro) {   // (scalar table reads: fewer live registers in the block loop)
                     u = sc * s_pro[kPB + pb + e] * u + bsc * s_pro[kPBb + pb + e];
                     w = sc * s_pro[kPB + pb + NH + e] * w + bsc * s_pro[kPBb + pb + NH + e];
                 }
@@ -263,8 +270,10 @@ void k_scan_fused(ScanArgs a) {
             if constexpr (kPro) {   // X = W_X o X' (ones without structured input)
                 int pw = kPWX + ((jb * S::JB + jr) % R) * P + pc * S::CE;
                 asm volatile("" : "+v"(pw));
+                float wv[S::CE];
+                tab(pw, wv, S::CE);
 #pragma unroll
-                for (int e = 0; e < S::CE; ++e) fset(xv, e, fget(xv, e) * s_pro[pw + e]);
+                for (int e = 0; e < S::CE; ++e) fset(xv, e, fget(xv, e) * wv[e]);
             }
             if constexpr (decltype(kOut)::value) *reinterpret_cast<V16 *>(&sX[jr * LDP + pc * S::CE]) = xv;
             if constexpr (decltype(kAgg)::value) {
@@ -996,11 +1005,12 @@ void k_scan_fused(ScanArgs a) {
                 // (a row's RP pieces are RP consecutive lanes), so its sum of
                 // squares is a lane sum (rows past the end of the sequence
                 // hold finite values and are not stored)
-                float yf[S::CE], gz[S::CE];
+                float yf[S::CE], gz[S::CE], wz[S::CE];
+                if constexpr (kGate) tab(kPWZ + r * P + col, wz, S::CE);
 #pragma unroll
                 for (int e = 0; e < S::CE; ++e) {
                     yf[e] = fget(yv, e);
-                    gz[e] = kGate ? silu(fget(zp[m][i], e) * s_pro[kPWZ + r * P + col + e]) : 1.f;
+                    gz[e] = kGate ? silu(fget(zp[m][i], e) * wz[e]) : 1.f;
                 }
                 if (a.pro.onorm) {   // (uniform)
                     const bool post = a.pro.onorm == 2;
@@ -1012,9 +1022,11 @@ void k_scan_fused(ScanArgs a) {
                     }
                     for (int o = 1; o < a.pro.ogroup / S::CE; o <<= 1) ss += __shfl_xor(ss, o, kWave);
                     const float sc = rsqrtf(ss / (float)a.pro.ogroup + a.pro.oeps);
+                    float gy[S::CE];
+                    tab(kPGY + r * P + col, gy, S::CE);
 #pragma unroll
                     for (int e = 0; e < S::CE; ++e) {
-                        yf[e] *= sc * s_pro[kPGY + r * P + col + e];
+                        yf[e] *= sc * gy[e];
                         if (!post) yf[e] *= gz[e];
                     }
                 } else {
