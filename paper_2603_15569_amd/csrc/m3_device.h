@@ -73,6 +73,8 @@ __device__ __forceinline__ void sincos_fast(float x, float *s, float *c) {
 }
 __device__ __forceinline__ void sincos_fast(double x, double *s, double *c) { sincos(x, s, c); }
 __device__ __forceinline__ float exp_fast(float x) { return __expf(x); }
+// 2^x on the hardware exp unit (v_exp_f32)
+__device__ __forceinline__ float exp2_fast(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ double exp_fast(double x) { return exp(x); }
 
 // SiLU(u) = u / (1 + e^{-u}), the output gate's activation (App. "MIMO for

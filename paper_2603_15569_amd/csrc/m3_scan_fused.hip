@@ -78,6 +78,7 @@ void k_scan_fused(ScanArgs a) {
     constexpr int LDT = NH + 32 / (int)sizeof(typename S::CS);
 
     __shared__ Acc s_cum[Q];
+    __shared__ float s_c2[Q];   // cum_t log2(e): the causal weights are 2^{c2_t - c2_j} sigma_j
     __shared__ Acc s_wtot[NW];
     __shared__ Acc s_psie[NH];
     __shared__ float s_gam[Q], s_sig[Q], s_w[Q];
@@ -99,12 +100,19 @@ void k_scan_fused(ScanArgs a) {
     __shared__ __attribute__((aligned(16))) T s_S[P * S::LDN];        // S_in^T [p][n] (io dtype)
     __shared__ int s_i[4];
     __shared__ uint32_t s_ctl[2];   // call epoch, whether this item is the janitor
-    // block prologue tables of the head (fp32): B gain, B bias, C gain, C bias
+    // block prologue tables of the head (fp32): B gain and bias as 16-byte
+    // entries (gain, bias of element i, gain, bias of element i + N/2 of rank
+    // row r: one read serves a rotation pair) at bgb(r, i), C gain, C bias
     // [R][N], then W_X, W_Z and the output norm's gain [R][P] (ones / zeros
     // where not given)
-    constexpr int kPB = 0, kPBb = R * N, kPC = 2 * R * N, kPCb = 3 * R * N, kPWX = 4 * R * N,
+    constexpr int kPB = 0, kPC = 2 * R * N, kPCb = 3 * R * N, kPWX = 4 * R * N,
                   kPWZ = 4 * R * N + R * P, kPGY = 4 * R * N + 2 * R * P;
     __shared__ __attribute__((aligned(16))) float s_pro[kPro ? 4 * R * N + 3 * R * P : 4];
+    // B table entry of (rank row r, element i = piece * CE + e): ordered by
+    // (e, piece, r), so that the lanes staging one element of their pieces
+    // (consecutive pieces, all ranks) read consecutive entries
+    constexpr int BPR = NH / S::CE;   // 16-byte pieces per half row
+    auto bgb = [](int r, int i) { return kPB + 4 * (((i % S::CE) * BPR + i / S::CE) * R + r); };
     Acc *s_segtot = reinterpret_cast<Acc *>(s_B);              // prologue only
     static_assert(sizeof(Acc) * S::NSEG * NH <= sizeof(T) * S::JB * S::LDN, "alias");
     static_assert(P <= S::JB && NW * 16 <= 2 * NBUF * S::JB, "y staging fits in the x / W x buffers");
@@ -207,7 +215,6 @@ void k_scan_fused(ScanArgs a) {
     // B row pieces: consecutive lanes take consecutive rows (conflict-free
     // cos/sin reads); with the prologue the NH / CE pieces of a row sit in
     // consecutive lanes of one wave instead, so that its norm is a lane sum.
-    constexpr int BPR = NH / S::CE;   // 16-byte pieces per half row
     auto brow = [](int task) { return kPro ? task / BPR : task % S::JB; };
     auto bpiece = [](int task) { return kPro ? task % BPR : task / S::JB; };
     auto fetch = [&](int jb, Blk &f) {
@@ -226,6 +233,13 @@ void k_scan_fused(ScanArgs a) {
             f.xv[k] = buf_load<V16>(rx, tok_off(t, xin_b) + (uint32_t)((r * xr_el + pc * S::CE) * sizeof(T)));
         }
     };
+    // A thread's B tasks have the same rank rows and pieces in every block
+    // (JB is a multiple of R): chunks of up to 256 rows hold their table
+    // entries in registers for the whole chunk; the 512-row chunks need those
+    // registers for their tiles and read the entries per block.
+    constexpr bool kHoldB = kPro && S::QR <= 256;
+    static_assert(S::JB % R == 0, "rank row of a B task independent of the block");
+    float4 bgr[kHoldB ? TB : 1][kHoldB ? S::CE : 1];
     // kAgg: stage W x too (operand of M); kOut: stage x too (operand of y)
     auto commit = [&](int jb, const Blk &f, auto kAgg, auto kOut) {
         T *sB = s_B + (jb % NBUF) * kSB, *sX = s_XW + (jb % NBUF) * kSXr, *sWX = s_XW + (NBUF + jb % NBUF) * kSXr;
@@ -245,17 +259,17 @@ void k_scan_fused(ScanArgs a) {
                 const bool ok = t < nvalid;
                 sc = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
                 bsc = ok ? 1.f : 0.f;
-                pb = ((jb * S::JB + jr) % R) * N + cp * S::CE;
-                // (opaque per block: table reads that do not depend on the
-                // block are not hoisted out of the block loop and held)
-                asm volatile("" : "+v"(pb));
+                pb = bgb(jr % R, cp * S::CE);
+                // (opaque per block: the reads stay in the block loop)
+                if constexpr (!kHoldB) asm volatile("" : "+v"(pb));
             }
 #pragma unroll
             for (int e = 0; e < S::CE; ++e) {
                 float u = fget(lo, e), w = fget(hi, e);
-                if constexpr (kPro) {   // (scalar table reads: fewer live registers in the block loop)
-                    u = sc * s_pro[kPB + pb + e] * u + bsc * s_pro[kPBb + pb + e];
-                    w = sc * s_pro[kPB + pb + NH + e] * w + bsc * s_pro[kPBb + pb + NH + e];
+                if constexpr (kPro) {   // (one 16-byte table entry a pair)
+                    const float4 gb = kHoldB ? bgr[k][e] : *reinterpret_cast<const float4 *>(&s_pro[pb + 4 * BPR * R * e]);
+                    u = sc * gb.x * u + bsc * gb.y;
+                    w = sc * gb.z * w + bsc * gb.w;
                 }
                 fset(lo, e, csv[e] * u + snv[e] * w);
                 fset(hi, e, csv[e] * w - snv[e] * u);
@@ -308,8 +322,10 @@ void k_scan_fused(ScanArgs a) {
     if constexpr (kPro) {   // the head's prologue tables (read after the prologue's barriers)
         const int64_t hn = h * (R * N), hp = h * (R * P);
         for (int e = tid; e < R * N; e += S::NTHR) {
-            s_pro[kPB + e] = a.pro.gB ? a.pro.gB[hn + e] : 1.f;
-            s_pro[kPBb + e] = a.pro.bB ? a.pro.bB[hn + e] : 0.f;
+            const int r = e / N, n = e % N;
+            const int q = bgb(r, n % NH) + (n < NH ? 0 : 2);
+            s_pro[q] = a.pro.gB ? a.pro.gB[hn + e] : 1.f;
+            s_pro[q + 1] = a.pro.bB ? a.pro.bB[hn + e] : 0.f;
             s_pro[kPC + e] = a.pro.gC ? a.pro.gC[hn + e] : 1.f;
             s_pro[kPCb + e] = a.pro.bC ? a.pro.bC[hn + e] : 0.f;
         }
@@ -385,6 +401,7 @@ void k_scan_fused(ScanArgs a) {
             Acc off = 0;
             for (int w2 = 0; w2 < wave; ++w2) off += s_wtot[w2];
             s_cum[tid] = v + off;
+            s_c2[tid] = (float)((v + off) * (Acc)1.4426950408889634);
         }
         Acc off = 0;
         for (int s2 = 0; s2 < seg; ++s2) off += s_segtot[s2 * NH + i];
@@ -405,6 +422,15 @@ void k_scan_fused(ScanArgs a) {
             s_w[tid] = (tid < nvalid) ? (float)(exp_fast(cum_e - s_cum[tid]) * (Acc)s_sig[tid]) : 0.f;
         }
         __syncthreads();
+    }
+    if constexpr (kHoldB) {   // the B table entries of this thread's tasks (tables written before the barriers above)
+#pragma unroll
+        for (int k = 0; k < TB; ++k) {
+            const int task = tid + k * S::NTHR;
+#pragma unroll
+            for (int e = 0; e < S::CE; ++e)
+                bgr[k][e] = *reinterpret_cast<const float4 *>(&s_pro[bgb(brow(task) % R, bpiece(task) * S::CE + e)]);
+        }
     }
 
 
@@ -523,7 +549,7 @@ void k_scan_fused(ScanArgs a) {
                 const int TT = owned_tile<S>(wave, m);
                 if (tile_above(m) || (!tile_below(m) && J0 > TT)) continue;
                 const int tt = (TT * 16 + l16) / R;
-                const float cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
+                const float c2_t = s_c2[tt], cum_t = (float)s_cum[tt], gam_t = s_gam[tt];
                 // the lane's 4 rows 4g+v of a j-tile span NV tokens (one when R >= 4)
                 constexpr int NV = R >= 4 ? 1 : 4 / R;
 #pragma unroll
@@ -532,7 +558,11 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
                     for (int u = 0; u < NV; ++u) {
                         const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
-                        const float e = exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj];
+                        // (above the diagonal the exponent may be large: the select drops
+                        // it; rank 4 keeps the base-e form, whose register allocation in
+                        // the 512-row chunks measured faster)
+                        const float e = R >= 4 ? exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj]
+                                               : exp2_fast(c2_t - s_c2[tj]) * s_sig[tj];
                         wv[u] = (tile_below(m) || tj < tt) ? e : (tj == tt ? gam_t : 0.f);
                     }
 #pragma unroll
@@ -890,9 +920,10 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
                     for (int o = 1; o < kWave; o <<= 1) ss += __shfl_xor(ss, o, kWave);
                     const float sc = a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f;
-                    const int e0 = r * N + lane, e1 = e0 + kWave;
-                    cB[e0] = from_f32<T>(sc * s_pro[kPB + e0] * v0 + s_pro[kPBb + e0]);
-                    cB[e1] = from_f32<T>(sc * s_pro[kPB + e1] * v1 + s_pro[kPBb + e1]);
+                    const int e0 = r * N + lane, e1 = e0 + kWave;   // elements lane and lane + N/2
+                    const float4 gb = *reinterpret_cast<const float4 *>(&s_pro[bgb(r, lane)]);
+                    cB[e0] = from_f32<T>(sc * gb.x * v0 + gb.y);
+                    cB[e1] = from_f32<T>(sc * gb.z * v1 + gb.w);
                 }
                 for (int e = tid; e < R * P; e += S::NTHR)
                     cX[e] = from_f32<T>(to_f32(Xl[sx ? e % P : e]) * s_pro[kPWX + e]);

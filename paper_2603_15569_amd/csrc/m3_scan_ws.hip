@@ -71,7 +71,8 @@ void k_scan_ws(ScanArgs a) {
 
     // Per-chunk scalars and tables, by chunk parity: the state waves write
     // chunk c + 1's while chunk c's are in use.
-    __shared__ float s_cum[2][Q], s_gam[2][Q], s_sig[2][Q], s_w[2][Q], s_psie[2][NH];
+    // s_c2: the log-decay prefix sums in base 2 (cum_t log2(e)): e^{cum} = 2^{c2}
+    __shared__ float s_c2[2][Q], s_gam[2][Q], s_sig[2][Q], s_w[2][Q], s_psie[2][NH];
     __shared__ __attribute__((aligned(16))) CS s_cs[2][Q * LDT];
     // Row blocks, double-buffered: B^ [row][n], x and W x [row][p].
     __shared__ __attribute__((aligned(16))) T s_B[2][S::JB * LDN];
@@ -172,13 +173,13 @@ void k_scan_ws(ScanArgs a) {
 #pragma unroll
                     for (int m = 0; m < TPW; ++m) acc[m][pt] = MM::mma(sf, cf[m][kk], acc[m][pt]);
                 }
-            float cum_t[TPW], gam_t[TPW];
+            float c2_t[TPW], gam_t[TPW];
 #pragma unroll
             for (int m = 0; m < TPW; ++m) {
                 const int t = (TT[m] * 16 + l16) / R;
-                cum_t[m] = s_cum[par][t];
+                c2_t[m] = s_c2[par][t];
                 gam_t[m] = s_gam[par][t];
-                const float ec = exp_fast(cum_t[m]);
+                const float ec = exp2_fast(c2_t[m]);
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
@@ -233,7 +234,7 @@ void k_scan_ws(ScanArgs a) {
 #pragma unroll
                         for (int u = 0; u < NV; ++u) {
                             const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
-                            cj[q][u] = s_cum[par][tj];
+                            cj[q][u] = s_c2[par][tj];
                             sj[q][u] = s_sig[par][tj];
                         }
                         Frag bfr[NK];
@@ -258,7 +259,8 @@ void k_scan_ws(ScanArgs a) {
                             float wv[NV];
 #pragma unroll
                             for (int u = 0; u < NV; ++u) {
-                                const float e = exp_fast(fminf(cum_t[m] - cj[q][u], 0.f)) * sj[q][u];
+                                // (above the diagonal the exponent may be large: the select drops it)
+                                const float e = exp2_fast(c2_t[m] - cj[q][u]) * sj[q][u];
                                 if (m > jb || J0 + q < TT[m]) {
                                     wv[u] = e;
                                 } else {
@@ -419,7 +421,7 @@ void k_scan_ws(ScanArgs a) {
             const float sig = gam + (1.f - p.lamn) * p.dtn;
             const float cum = lane_scan(lg);
             const float cum_e = lane_bcast(cum, nv - 1);
-            s_cum[par][lane] = cum;
+            s_c2[par][lane] = cum * 1.44269504f;
             s_gam[par][lane] = gam;
             s_sig[par][lane] = sig;
             s_w[par][lane] = (lane < nv) ? exp_fast(cum_e - cum) * sig : 0.f;
@@ -538,7 +540,7 @@ void k_scan_ws(ScanArgs a) {
             const int64_t cn = min(c + 1, nch - 1);
             f32x4 ms[PT][2];
             {
-                const float de = exp_fast(s_cum[par][nv - 1]);
+                const float de = exp2_fast(s_c2[par][nv - 1]);
 #pragma unroll
                 for (int pt = 0; pt < PT; ++pt)
 #pragma unroll
