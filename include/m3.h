@@ -342,8 +342,11 @@ typedef struct {
  * prologue `pro` (not NULL) applied to B, C, x and z as they are read.  x
  * (and z with w_z) is [batch][seqlen][nheads][headdim] when w_x (w_z) is
  * given, else as in m3_scan_fwd.  Runs the one-chunk-per-workgroup
- * single-pass kernel (M3_SCAN_PER_CHUNK; the workspace is sized by
- * m3_scan_workspace_bytes(dims) as usual).  Supported shapes: io bf16,
+ * single-pass kernel, except where the default choice (flags without
+ * M3_SCAN_PER_CHUNK, seg_chunks as for m3_scan_fwd) gives one segment per
+ * slice at rank 4 and chunk 64: then the warp-specialised kernel runs with
+ * the prologue (the workspace is sized by m3_scan_workspace_bytes(dims) as
+ * usual).  Supported shapes: io bf16,
  * dstate 128, headdim 64, rank 1/2/4 and chunk 32/64/128 with chunk*rank a
  * multiple of 64 and at most 512 (else M3_ERR_UNSUPPORTED, also with
  * M3_SCAN_SPLIT).  Errors as m3_scan_fwd; M3_ERR_NULL for a NULL pro, or

@@ -165,14 +165,22 @@ static m3_status scan_fwd(const m3_dims *d, const void *x, const void *B, const 
     Prologue pr;
     s = check_prologue(pro, gated, d->headdim, &pr);
     if (s != M3_OK) return s;
-    if (pr.on) {   // the block prologue runs in the per-chunk kernel (same workspace layout)
+    if (pr.on) {
+        // the block prologue runs in the per-chunk kernel (same workspace
+        // layout), or, where the segmented kernel's launcher would choose the
+        // warp-specialised kernel (one segment per slice), in that kernel
+        // built with the prologue: the launcher then hands everything else to
+        // the per-chunk kernel with the prologue
         scan_launch_fn f = (d->flags & M3_SCAN_SPLIT) ? nullptr
                                                       : find_fused_pro_impl(d->io, d->dstate, d->headdim,
                                                                             d->rank, d->chunk);
         if (!f) return M3_ERR_UNSUPPORTED;
         if (nc > 0) {
             if (!impl.fused) return M3_ERR_UNSUPPORTED;
-            impl.launch = f;
+            const bool seg = impl.launch != impl.per_chunk &&
+                             find_ws_pro_impl(d->io, d->dstate, d->headdim, d->rank, d->chunk) != nullptr;
+            if (!seg) impl.launch = f;
+            impl.per_chunk = f;
         }
     }
     // token arrays may be NULL only for an empty sequence (empty tensors)

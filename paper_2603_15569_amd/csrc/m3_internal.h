@@ -58,7 +58,10 @@ struct ScanArgs {
     // segmented kernel: chunks per segment (0 = chosen at launch), segments
     // per slice (set at launch), and the one-chunk-per-workgroup kernel it
     // hands over to when its own choice would give short chunks several
-    // segments per slice (null: none)
+    // segments per slice (null: none).  With the block prologue (pro.on) the
+    // segmented kernel itself never runs: one segment per slice goes to the
+    // warp-specialised kernel with the prologue, anything else to per_chunk
+    // (then the per-chunk kernel with the prologue).
     int64_t G, nseg;
     hipError_t (*per_chunk)(const ScanArgs &, hipStream_t);
     // polls of a look-back wait before it gives up (counts a timeout in the
@@ -133,6 +136,7 @@ scan_launch_fn find_seg_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q)
 scan_launch_fn find_ws_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 // kernels built with the block prologue (null: none for the shape)
 scan_launch_fn find_fused_pro_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
+scan_launch_fn find_ws_pro_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q);
 step_launch_fn find_step_pro_impl(int io, int64_t N, int64_t P, int64_t R);
 
 // Control block of the single-pass scans (the first kCtlBytes of every scan

@@ -1051,7 +1051,13 @@ void k_scan_fused(ScanArgs a) {
                         if (post) yf[e] *= gz[e];
                         ss += yf[e] * yf[e];
                     }
-                    for (int o = 1; o < a.pro.ogroup / S::CE; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+                    // (a fixed count of lane steps, those past the group adding nothing:
+                    // a loop of constant length stays unrolled)
+#pragma unroll
+                    for (int o = 1; o < RP; o <<= 1) {
+                        const float so = __shfl_xor(ss, o, kWave);
+                        ss += o < a.pro.ogroup / S::CE ? so : 0.f;
+                    }
                     const float sc = rsqrtf(ss / (float)a.pro.ogroup + a.pro.oeps);
                     float gy[S::CE];
                     tab(kPGY + r * P + col, gy, S::CE);

@@ -1011,8 +1011,10 @@ hipError_t launch_seg(const ScanArgs &a0, hipStream_t stream) {
     a.nseg = (a.nchunks + G - 1) / G;
     // one segment per slice: the warp-specialised kernel, where built
     if (a.nseg == 1 && std::is_same<T, bf16>::value) {
-        if (scan_launch_fn f = find_ws_impl(1, S::N, S::P, R, Q)) return f(a, stream);
+        if (scan_launch_fn f = a.pro.on ? find_ws_pro_impl(1, S::N, S::P, R, Q) : find_ws_impl(1, S::N, S::P, R, Q))
+            return f(a, stream);
     }
+    if (a.pro.on) return a.per_chunk ? a.per_chunk(a0, stream) : hipErrorInvalidValue;   // (no prologue here)
     if (gate)
         hipLaunchKernelGGL((k_scan_seg<T, Q, R, true>), dim3((unsigned)(nsl * a.nseg)), dim3(S::NTHR), 0, stream, a);
     else

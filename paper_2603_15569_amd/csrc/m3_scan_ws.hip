@@ -21,6 +21,13 @@
 //     M = B^T (W x) per block and update the state at the end of the chunk.
 // A chunk is four steps (one per 64-row block) separated by workgroup
 // barriers; both roles pass the same barriers.
+//
+// With the block prologue (Sec. 3.4 "BCNorm" and "B, C Biases"; App. "MIMO for
+// Mamba-3", structured MIMO input and gate) the rows are transformed as they
+// arrive, from per-head tables in LDS: the state waves normalise and bias B
+// while staging it and scale x' by W_X; the output waves normalise and bias C
+// inside its rotation, scale z' by W_Z and apply the optional output norm at
+// the store.
 #include <type_traits>
 
 #include "m3_device.h"
@@ -53,7 +60,9 @@ struct WsShape {
 };
 
 // kGate: the stored y is multiplied by SiLU(z) (the block's output gate).
-template <int Q, int R, bool kGate>
+// kPro: the block prologue (B and C: RMS norm over N, gain, bias; x and z:
+// X = W_X o X', Z = W_Z o Z'; the output norm).
+template <int Q, int R, bool kGate, bool kPro>
 __global__ __launch_bounds__(512, 1)
 void k_scan_ws(ScanArgs a) {
     typedef bf16 T;
@@ -82,6 +91,24 @@ void k_scan_ws(ScanArgs a) {
     __shared__ __attribute__((aligned(16))) T s_S[P * LDN];
     // y staging, one 16-row tile per output wave.
     __shared__ __attribute__((aligned(16))) T s_Y[S::NWO][16 * LDP];
+    // Block prologue tables of the head (fp32): B gain and bias as 16-byte
+    // entries at bgb(r, i) (gain and bias of element i, then of element
+    // i + N/2, of rank row r: one read serves a rotation pair; ordered so that
+    // the lanes staging one element of consecutive pieces of all rank rows
+    // read consecutive entries), C gain and bias [R][N], then W_X, W_Z and
+    // the output norm's gain [R][P] (ones / zeros where not given).
+    constexpr int kPB = 0, kPC = 2 * R * N, kPCb = 3 * R * N, kPWX = 4 * R * N, kPWZ = kPWX + R * P,
+                  kPGY = kPWZ + R * P;
+    __shared__ __attribute__((aligned(16))) float s_pro[kPro ? 4 * R * N + 3 * R * P : 4];
+    constexpr int BPR = NH / CE;   // 16-byte pieces of a half row
+    auto bgb = [](int r, int i) { return kPB + 4 * (((i % CE) * BPR + i / CE) * R + r); };
+    // K consecutive table floats (16-byte reads; p a multiple of 4)
+    auto tab = [&](int p, float *v, int K) {
+        for (int q = 0; q < K; q += 4) {
+            const float4 f = *reinterpret_cast<const float4 *>(&s_pro[p + q]);
+            v[q] = f.x; v[q + 1] = f.y; v[q + 2] = f.z; v[q + 3] = f.w;
+        }
+    };
 
     // Lane indices are re-derived from an opaque copy of the thread index at
     // the top of every chunk (relane), so that the compiler recomputes
@@ -103,7 +130,7 @@ void k_scan_ws(ScanArgs a) {
     const int64_t nch = a.nchunks;
     const int64_t tstr = a.H;
     const int64_t bstr = tstr * R * N, xstr = tstr * R * P;
-    const uint32_t bstr_b = (uint32_t)(bstr * sizeof(T)), xstr_b = (uint32_t)(xstr * sizeof(T));
+    const uint32_t bstr_b = (uint32_t)(bstr * sizeof(T));
     const T *Bs = static_cast<const T *>(a.B);
     const T *Cs = static_cast<const T *>(a.C);
     const T *Xs = static_cast<const T *>(a.x);
@@ -117,6 +144,29 @@ void k_scan_ws(ScanArgs a) {
     };
     auto sched_fence = []() { __builtin_amdgcn_sched_barrier(0); };
     const int64_t SZ = (int64_t)N * P;
+    // x and z as read: P x R per token-head, or (structured input) the
+    // P-vector X' (Z') that every rank row reads (row offset 0)
+    const bool sx = kPro && a.pro.wx != nullptr, sz = kPro && a.pro.wz != nullptr;
+    const int64_t xin_tok = sx ? (int64_t)P : (int64_t)(R * P), zin_tok = sz ? (int64_t)P : (int64_t)(R * P);
+    const int xr_el = sx ? 0 : P, zr_el = sz ? 0 : P;
+    const int64_t xin_str = tstr * xin_tok, zin_str = tstr * zin_tok;
+    const uint32_t xin_b = (uint32_t)(xin_str * sizeof(T)), zin_b = (uint32_t)(zin_str * sizeof(T));
+    if constexpr (kPro) {   // the head's tables (read after the first barrier of both roles)
+        const int64_t hn = h * (R * N), hp = h * (R * P);
+        for (int e = tid; e < R * N; e += S::NTHR) {
+            const int r = e / N, n = e % N;
+            const int q = bgb(r, n % NH) + (n < NH ? 0 : 2);
+            s_pro[q] = a.pro.gB ? a.pro.gB[hn + e] : 1.f;
+            s_pro[q + 1] = a.pro.bB ? a.pro.bB[hn + e] : 0.f;
+            s_pro[kPC + e] = a.pro.gC ? a.pro.gC[hn + e] : 1.f;
+            s_pro[kPCb + e] = a.pro.bC ? a.pro.bC[hn + e] : 0.f;
+        }
+        for (int e = tid; e < R * P; e += S::NTHR) {
+            s_pro[kPWX + e] = a.pro.wx ? a.pro.wx[hp + e] : 1.f;
+            s_pro[kPWZ + e] = a.pro.wz ? a.pro.wz[hp + e] : 1.f;
+            s_pro[kPGY + e] = a.pro.og ? a.pro.og[hp + e] : 1.f;
+        }
+    }
 
     if (wave < S::NWO) {
         // ================= output waves =================
@@ -143,18 +193,62 @@ void k_scan_ws(ScanArgs a) {
             const int nv = nvalid_of(c);
             const int64_t cn = min(c + 1, nch - 1);
             // C^ = R(-psi_t) C of the owned rows
+            if constexpr (kPro) {
+                // each element first normalised, c = sc g c + b in fp32 (sc the
+                // row's RMS scale from a sum of squares over its fragments: a
+                // row sits in lanes l16 + 16 g; zero past the end of the
+                // sequence); a lane's rank row l16 % R is the same in all its
+                // tiles, so its gains and biases are read once per fragment pair
+                float scm[TPW], bscm[TPW];
 #pragma unroll
-            for (int m = 0; m < TPW; ++m) {
-                const int t = (TT[m] * 16 + l16) / R;
+                for (int m = 0; m < TPW; ++m) {
+                    const int t = (TT[m] * 16 + l16) / R;
+                    float ss = 0.f;
+#pragma unroll
+                    for (int kk = 0; kk < NK; ++kk) ss += sumsq(cf[m][kk]);
+                    ss += __shfl_xor(ss, 16, kWave);
+                    ss += __shfl_xor(ss, 32, kWave);
+                    const bool ok = t < nv;
+                    scm[m] = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
+                    bscm[m] = ok ? 1.f : 0.f;
+                }
 #pragma unroll
                 for (int kk = 0; kk < NK / 2; ++kk) {
-                    float csv[MM::KPL], snv[MM::KPL];
-                    cs_getn<MM::KPL>(&s_cs[par][t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
+                    static_assert(MM::KPL % 4 == 0, "16-byte table reads");
+                    const int pu = (l16 % R) * N + kk * MM::K + MM::KPL * g, pw = pu + NH;
+                    float gu[MM::KPL], gw[MM::KPL], bu[MM::KPL], bw[MM::KPL];
+                    tab(kPC + pu, gu, MM::KPL);
+                    tab(kPC + pw, gw, MM::KPL);
+                    tab(kPCb + pu, bu, MM::KPL);
+                    tab(kPCb + pw, bw, MM::KPL);
 #pragma unroll
-                    for (int e = 0; e < MM::KPL; ++e) {
-                        const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
-                        fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
-                        fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
+                    for (int m = 0; m < TPW; ++m) {
+                        const int t = (TT[m] * 16 + l16) / R;
+                        float csv[MM::KPL], snv[MM::KPL];
+                        cs_getn<MM::KPL>(&s_cs[par][t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
+#pragma unroll
+                        for (int e = 0; e < MM::KPL; ++e) {
+                            const float u = scm[m] * gu[e] * fget(cf[m][kk], e) + bscm[m] * bu[e];
+                            const float w = scm[m] * gw[e] * fget(cf[m][kk + NK / 2], e) + bscm[m] * bw[e];
+                            fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
+                            fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
+                        }
+                    }
+                }
+            } else {
+#pragma unroll
+                for (int m = 0; m < TPW; ++m) {
+                    const int t = (TT[m] * 16 + l16) / R;
+#pragma unroll
+                    for (int kk = 0; kk < NK / 2; ++kk) {
+                        float csv[MM::KPL], snv[MM::KPL];
+                        cs_getn<MM::KPL>(&s_cs[par][t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
+#pragma unroll
+                        for (int e = 0; e < MM::KPL; ++e) {
+                            const float u = fget(cf[m][kk], e), w = fget(cf[m][kk + NK / 2], e);
+                            fset(cf[m][kk], e, csv[e] * u + snv[e] * w);
+                            fset(cf[m][kk + NK / 2], e, csv[e] * w - snv[e] * u);
+                        }
                     }
                 }
             }
@@ -197,14 +291,14 @@ void k_scan_ws(ScanArgs a) {
                 const T *sBc = s_B[jb & 1], *sXc = s_X[jb & 1];
                 if constexpr (kGate) {
                     if (jb == NJB - 1) {
-                        const Rsrc rz = rows_rsrc(static_cast<const T *>(a.z), c, xstr, R * P);
+                        const Rsrc rz = rows_rsrc(static_cast<const T *>(a.z), c, zin_str, (int)zin_tok);
 #pragma unroll
                         for (int m = 0; m < TPW; ++m)
 #pragma unroll
                             for (int i = 0; i < NPC; ++i) {
                                 const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * CE;
                                 const int row = TT[m] * 16 + rl, t = row / R, r = row % R;
-                                zp[m][i] = buf_load<V16>(rz, tok_off(t, xstr_b) + (uint32_t)((r * P + col) * sizeof(T)));
+                                zp[m][i] = buf_load<V16>(rz, tok_off(t, zin_b) + (uint32_t)((r * zr_el + col) * sizeof(T)));
                             }
                     }
                 }
@@ -306,7 +400,51 @@ void k_scan_ws(ScanArgs a) {
                         for (int i = 0; i < NPC; ++i) {
                             const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * CE;
                             const int row = TT[m] * 16 + rl, t = row / R, r = row % R;
-                            if (t < nv) {
+                            if constexpr (kPro) {
+                                // gate factor SiLU(W_Z o Z') in fp32, then
+                                // (optionally) the output norm: a row's RP
+                                // pieces are RP consecutive lanes, so a group's
+                                // sum of squares is a lane sum (all lanes take
+                                // part; rows past the end are not stored)
+                                V16 yv = *reinterpret_cast<const V16 *>(&sy[rl * LDP + col]);
+                                float yf[CE], gz[CE], wz[CE];
+                                if constexpr (kGate) tab(kPWZ + r * P + col, wz, CE);
+#pragma unroll
+                                for (int e = 0; e < CE; ++e) {
+                                    yf[e] = fget(yv, e);
+                                    gz[e] = kGate ? silu(fget(zp[m][i], e) * wz[e]) : 1.f;
+                                }
+                                if (a.pro.onorm) {   // (uniform)
+                                    const bool post = a.pro.onorm == 2;
+                                    float ss = 0.f;
+#pragma unroll
+                                    for (int e = 0; e < CE; ++e) {
+                                        if (post) yf[e] *= gz[e];
+                                        ss += yf[e] * yf[e];
+                                    }
+                                    // (a fixed count of lane steps, those past the group adding nothing:
+                                    // a loop of constant length stays unrolled)
+#pragma unroll
+                                    for (int o = 1; o < RP; o <<= 1) {
+                                        const float so = __shfl_xor(ss, o, kWave);
+                                        ss += o < a.pro.ogroup / CE ? so : 0.f;
+                                    }
+                                    const float sc = rsqrtf(ss / (float)a.pro.ogroup + a.pro.oeps);
+                                    float gy[CE];
+                                    tab(kPGY + r * P + col, gy, CE);
+#pragma unroll
+                                    for (int e = 0; e < CE; ++e) {
+                                        yf[e] *= sc * gy[e];
+                                        if (!post) yf[e] *= gz[e];
+                                    }
+                                } else {
+#pragma unroll
+                                    for (int e = 0; e < CE; ++e) yf[e] *= gz[e];
+                                }
+#pragma unroll
+                                for (int e = 0; e < CE; ++e) fset(yv, e, yf[e]);
+                                if (t < nv) *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) = yv;
+                            } else if (t < nv) {
                                 V16 yv = *reinterpret_cast<const V16 *>(&sy[rl * LDP + col]);
                                 if constexpr (kGate) yv = gate_piece<T>(yv, zp[m][i]);
                                 *reinterpret_cast<V16 *>(Yg + t * xstr + r * P + col) = yv;
@@ -325,11 +463,16 @@ void k_scan_ws(ScanArgs a) {
         constexpr int TX = S::JB * (P / CE) / S::NST;    // x tasks per thread
         static_assert(TB * S::NST == S::JB * (NH / CE) && TX * S::NST == S::JB * (P / CE), "tasks");
         struct Blk { V16 lo[TB], hi[TB], xv[TX]; };
+        // B row pieces: consecutive lanes take consecutive rows (conflict-free
+        // cos/sin reads); with the prologue the BPR pieces of a half row sit in
+        // consecutive lanes instead, so that the row's norm is a lane sum.
+        auto brow = [](int task) { return kPro ? task / BPR : task % S::JB; };
+        auto bpiece = [](int task) { return kPro ? task % BPR : task / S::JB; };
         auto fetch = [&](int64_t c, int jb, Blk &f) {
-            const Rsrc rb = rows_rsrc(Bs, c, bstr, R * N), rx = rows_rsrc(Xs, c, xstr, R * P);
+            const Rsrc rb = rows_rsrc(Bs, c, bstr, R * N), rx = rows_rsrc(Xs, c, xin_str, (int)xin_tok);
 #pragma unroll
             for (int k = 0; k < TB; ++k) {
-                const int task = (tid - S::NWO * kWave) + k * S::NST, jr = task % S::JB, cp = task / S::JB;
+                const int task = (tid - S::NWO * kWave) + k * S::NST, jr = brow(task), cp = bpiece(task);
                 const int row = jb * S::JB + jr, t = row / R, r = row % R;
                 const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + cp * CE) * sizeof(T));
                 f.lo[k] = buf_load<V16>(rb, off);
@@ -339,22 +482,40 @@ void k_scan_ws(ScanArgs a) {
             for (int k = 0; k < TX; ++k) {
                 const int task = (tid - S::NWO * kWave) + k * S::NST, jr = task % S::JB, pc = task / S::JB;
                 const int row = jb * S::JB + jr, t = row / R, r = row % R;
-                f.xv[k] = buf_load<V16>(rx, tok_off(t, xstr_b) + (uint32_t)((r * P + pc * CE) * sizeof(T)));
+                f.xv[k] = buf_load<V16>(rx, tok_off(t, xin_b) + (uint32_t)((r * xr_el + pc * CE) * sizeof(T)));
             }
         };
-        // stage block jb of a chunk (tables of parity par) into buffer jb & 1
-        auto commit = [&](int jb, int par, const Blk &f) {
+        // stage block jb of a chunk with nvs valid tokens (tables of parity
+        // par) into buffer jb & 1
+        auto commit = [&](int jb, int par, int nvs, const Blk &f) {
             T *sB = s_B[jb & 1], *sX = s_X[jb & 1], *sWX = s_WX[jb & 1];
 #pragma unroll
             for (int k = 0; k < TB; ++k) {
-                const int task = (tid - S::NWO * kWave) + k * S::NST, jr = task % S::JB, cp = task / S::JB;
+                const int task = (tid - S::NWO * kWave) + k * S::NST, jr = brow(task), cp = bpiece(task);
                 const int t = (jb * S::JB + jr) / R;
                 V16 lo = f.lo[k], hi = f.hi[k];
                 float csv[CE], snv[CE];
                 cs_getn<CE>(&s_cs[par][t * LDT + cp * CE], csv, snv);
+                float sc = 1.f, bsc = 1.f;
+                int pb = 0;
+                if constexpr (kPro) {   // B = g o B' / rms(B') + b (rows past the end stay zero)
+                    float ss = sumsq(lo) + sumsq(hi);
+#pragma unroll
+                    for (int o = 1; o < BPR; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+                    const bool ok = t < nvs;
+                    sc = !ok ? 0.f : (a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f);
+                    bsc = ok ? 1.f : 0.f;
+                    static_assert(S::JB % R == 0, "rank row of a task independent of the block");
+                    pb = bgb(jr % R, cp * CE);
+                }
 #pragma unroll
                 for (int e = 0; e < CE; ++e) {
-                    const float u = fget(lo, e), w = fget(hi, e);
+                    float u = fget(lo, e), w = fget(hi, e);
+                    if constexpr (kPro) {   // (one 16-byte table entry a pair)
+                        const float4 gb = *reinterpret_cast<const float4 *>(&s_pro[pb + 4 * BPR * R * e]);
+                        u = sc * gb.x * u + bsc * gb.y;
+                        w = sc * gb.z * w + bsc * gb.w;
+                    }
                     fset(lo, e, csv[e] * u + snv[e] * w);
                     fset(hi, e, csv[e] * w - snv[e] * u);
                 }
@@ -365,10 +526,17 @@ void k_scan_ws(ScanArgs a) {
             for (int k = 0; k < TX; ++k) {
                 const int task = (tid - S::NWO * kWave) + k * S::NST, jr = task % S::JB, pc = task / S::JB;
                 const float wt = s_w[par][(jb * S::JB + jr) / R];
-                *reinterpret_cast<V16 *>(&sX[jr * LDP + pc * CE]) = f.xv[k];
+                V16 xv = f.xv[k];
+                if constexpr (kPro) {   // X = W_X o X' (ones without structured input)
+                    float wv[CE];
+                    tab(kPWX + (jr % R) * P + pc * CE, wv, CE);
+#pragma unroll
+                    for (int e = 0; e < CE; ++e) fset(xv, e, fget(xv, e) * wv[e]);
+                }
+                *reinterpret_cast<V16 *>(&sX[jr * LDP + pc * CE]) = xv;
                 V16 wx;
 #pragma unroll
-                for (int e = 0; e < CE; ++e) fset(wx, e, wt * fget(f.xv[k], e));
+                for (int e = 0; e < CE; ++e) fset(wx, e, wt * fget(xv, e));
                 *reinterpret_cast<V16 *>(&sWX[jr * LDP + pc * CE]) = wx;
             }
         };
@@ -503,9 +671,25 @@ void k_scan_ws(ScanArgs a) {
             T *cX = static_cast<T *>(a.cX) + sl * (R * P);
             const int64_t kl = (b * a.L + a.L - 1) * a.H + h;
             const T *Bl = Bs + kl * (R * N);
-            const T *Xl = Xs + kl * (R * P);
-            for (int e = (tid - S::NWO * kWave); e < R * N; e += S::NST) cB[e] = Bl[e];
-            for (int e = (tid - S::NWO * kWave); e < R * P; e += S::NST) cX[e] = Xl[e];
+            const T *Xl = Xs + kl * xin_tok;
+            if constexpr (kPro) {   // the carry holds the B and X the recurrence used
+                static_assert(N == 2 * kWave, "two elements of a B row per lane");
+                for (int r = sw; r < R; r += S::NSW) {
+                    const float v0 = to_f32(Bl[r * N + lane]), v1 = to_f32(Bl[r * N + kWave + lane]);
+                    float ss = v0 * v0 + v1 * v1;
+#pragma unroll
+                    for (int o = 1; o < kWave; o <<= 1) ss += __shfl_xor(ss, o, kWave);
+                    const float sc = a.pro.bcnorm ? rsqrtf(ss * (1.f / N) + a.pro.eps) : 1.f;
+                    const float4 gb = *reinterpret_cast<const float4 *>(&s_pro[bgb(r, lane)]);
+                    cB[r * N + lane] = from_f32<T>(sc * gb.x * v0 + gb.y);
+                    cB[r * N + kWave + lane] = from_f32<T>(sc * gb.z * v1 + gb.w);
+                }
+                for (int e = (tid - S::NWO * kWave); e < R * P; e += S::NST)
+                    cX[e] = from_f32<T>(to_f32(Xl[sx ? e % P : e]) * s_pro[kPWX + e]);
+            } else {
+                for (int e = (tid - S::NWO * kWave); e < R * N; e += S::NST) cB[e] = Bl[e];
+                for (int e = (tid - S::NWO * kWave); e < R * P; e += S::NST) cX[e] = Xl[e];
+            }
         };
 
         // Blocks are numbered k = c * NJB + jb; the ring holds the loads of
@@ -528,7 +712,7 @@ void k_scan_ws(ScanArgs a) {
         load_pro(min((int64_t)1, nch - 1), pro);
         sched_fence();
         __syncthreads();   // prologue of chunk 0 written
-        commit(0, 0, ring[0]);
+        commit(0, 0, nvalid_of(0), ring[0]);
         sched_fence();
         fetch_k(2, ring[0]);
         sched_fence();
@@ -555,8 +739,8 @@ void k_scan_ws(ScanArgs a) {
                 // and load block k + 3
                 const int64_t k = c * NJB + jb;
                 sched_fence();
-                if (jb + 1 < NJB) commit(jb + 1, par, ring[(jb + 1) & 1]);
-                else commit(0, (int)(cn & 1), ring[(jb + 1) & 1]);
+                if (jb + 1 < NJB) commit(jb + 1, par, nv, ring[(jb + 1) & 1]);
+                else commit(0, (int)(cn & 1), nvalid_of(cn), ring[(jb + 1) & 1]);
                 sched_fence();
                 fetch_k(k + 3, ring[(jb + 1) & 1]);
                 sched_fence();
@@ -594,14 +778,14 @@ void k_scan_ws(ScanArgs a) {
     }
 }
 
-template <int Q, int R>
+template <int Q, int R, bool kPro = false>
 hipError_t launch_ws(const ScanArgs &a, hipStream_t stream) {
     typedef WsShape<Q, R> S;
     const int64_t nsl = a.batch * a.H;
     if (a.z)
-        hipLaunchKernelGGL((k_scan_ws<Q, R, true>), dim3((unsigned)nsl), dim3(S::NTHR), 0, stream, a);
+        hipLaunchKernelGGL((k_scan_ws<Q, R, true, kPro>), dim3((unsigned)nsl), dim3(S::NTHR), 0, stream, a);
     else
-        hipLaunchKernelGGL((k_scan_ws<Q, R, false>), dim3((unsigned)nsl), dim3(S::NTHR), 0, stream, a);
+        hipLaunchKernelGGL((k_scan_ws<Q, R, false, kPro>), dim3((unsigned)nsl), dim3(S::NTHR), 0, stream, a);
     return hipGetLastError();
 }
 
@@ -611,6 +795,13 @@ hipError_t launch_ws(const ScanArgs &a, hipStream_t stream) {
 scan_launch_fn find_ws_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q) {
     if (io != 1 || N != 128 || P != 64) return nullptr;
     if (Q == 64 && R == 4) return &launch_ws<64, 4>;
+    return nullptr;
+}
+
+// The same kernels built with the block prologue.
+scan_launch_fn find_ws_pro_impl(int io, int64_t N, int64_t P, int64_t R, int64_t Q) {
+    if (io != 1 || N != 128 || P != 64) return nullptr;
+    if (Q == 64 && R == 4) return &launch_ws<64, 4, true>;
     return nullptr;
 }
 

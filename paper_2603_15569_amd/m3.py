@@ -397,11 +397,13 @@ def prologue(bc_norm: bool = False, eps: float = 1e-6, norm_B=None, norm_C=None,
 
 def scan_fwd_pro(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, pro: M3Prologue, rank: int,
                  z=None, init_state=None, init_carry=None, out=None, workspace=None,
-                 stream=None, check: bool = False):
+                 stream=None, check: bool = False, seg: int = 0):
     """m3_scan_fwd_pro: the scan with the block prologue `pro` applied to the
     raw B', C' [B,L,H,R,N] and to x (X' [B,L,H,P] when pro.w_x is set, else
     [B,L,H,R,P]) and z as they are read.  Returns y [B,L,H,R,P], the final
-    state and the carry (the prologue's B_{L-1}, X_{L-1})."""
+    state and the carry (the prologue's B_{L-1}, X_{L-1}).  `seg` is the
+    dims' seg_chunks (0: chosen at launch; at least the chunk count: one
+    segment per slice, the warp-specialised kernel where it is built)."""
     batch, seqlen, nheads = x.shape[:3]
     headdim, dstate = x.shape[-1], Bm.shape[-1]
     if tuple(Bm.shape) != (batch, seqlen, nheads, rank, dstate):
@@ -409,7 +411,7 @@ def scan_fwd_pro(x, Bm, Cm, dt, A, lam, theta, D, chunk: int, pro: M3Prologue, r
     sb, st, sh = _a_strides(A, batch, seqlen, nheads)
     flags = M3_THETA_PER_HEAD if _theta_per_head(theta, nheads, dstate) else 0
     d = M3Dims(batch, seqlen, nheads, headdim, dstate, rank, int(chunk), _IO[x.dtype], flags,
-               sb, st, sh, 0)
+               sb, st, sh, int(seg))
     dev = x.device
     if out is None:
         y = torch.empty((batch, seqlen, nheads, rank, headdim), dtype=x.dtype, device=dev)

@@ -94,7 +94,8 @@ def oracle_prologue(inp, pin, variant, slices, zfull=None, t0=0, t1=None):
     return ref, zref
 
 
-def run_pro(inp, pin, variant, Q, zfull=None, init_state=None, init_carry=None, t0=0, t1=None):
+def run_pro(inp, pin, variant, Q, zfull=None, init_state=None, init_carry=None, t0=0, t1=None,
+            seg=0):
     x, z = gpu_args(inp, pin, variant, zfull)
     sl = slice(t0, t1)
 
@@ -104,7 +105,7 @@ def run_pro(inp, pin, variant, Q, zfull=None, init_state=None, init_carry=None, 
     y, fs, (cB, cX) = m3.scan_fwd_pro(cut(x), cut(pin.Bp), cut(pin.Cp), cut(inp.dt), inp.A,
                                       cut(inp.lam), cut(inp.theta), inp.D, Q,
                                       pro_of(pin, variant), R, z=cut(z), init_state=init_state,
-                                      init_carry=init_carry, check=True)
+                                      init_carry=init_carry, check=True, seg=seg)
     torch.cuda.synchronize()
     return y, fs, cB, cX
 
@@ -155,6 +156,38 @@ def test_prologue_continuation(R, Q):
     slices = [(0, 0), (0, 1)]
     ref, _ = oracle_prologue(inp, pin, "full", slices)
     compare(y, fb, cBb, cXb, ref, None, slices, f"pro continuation R={R} Q={Q}")
+
+
+# One segment per slice (seg at least the chunk count) runs the
+# warp-specialised kernel with the prologue (rank 4, chunk 64): every
+# variant, a ragged last chunk, and a continuation from a state and carry.
+WS = 1 << 20
+
+
+@pytest.mark.parametrize("variant", list(VARIANTS))
+@pytest.mark.parametrize("L", [200, 64, 1])
+def test_prologue_scan_ws(L, variant):
+    say(f"prologue scan warp-specialised R=4 Q=64 L={L} {variant}")
+    inp, pin = make_case(2, L, 3, 4, 64, seed=400 + L)
+    zfull = torch.randn(inp.x.shape, device=DEV, generator=torch.Generator(DEV).manual_seed(11)
+                        ).to(torch.bfloat16)
+    y, fs, cB, cX = run_pro(inp, pin, variant, 64, zfull=zfull, seg=WS)
+    slices = [(b, h) for b in range(2) for h in range(3)]
+    ref, zref = oracle_prologue(inp, pin, variant, slices, zfull=zfull)
+    compare(y, fs, cB, cX, ref, zref, slices, f"pro ws L={L} {variant}")
+
+
+def test_prologue_continuation_ws():
+    say("prologue continuation warp-specialised R=4 Q=64")
+    L, L1 = 333, 190
+    inp, pin = make_case(1, L, 2, 4, 64, seed=81)
+    ya, fa, cBa, cXa = run_pro(inp, pin, "full", 64, t0=0, t1=L1, seg=WS)
+    yb, fb, cBb, cXb = run_pro(inp, pin, "full", 64, init_state=fa, init_carry=(cBa, cXa),
+                               t0=L1, t1=L, seg=WS)
+    y = torch.cat([ya, yb], dim=1)
+    slices = [(0, 0), (0, 1)]
+    ref, _ = oracle_prologue(inp, pin, "full", slices)
+    compare(y, fb, cBb, cXb, ref, None, slices, "pro continuation ws")
 
 
 @pytest.mark.parametrize("gated", [False, True])
@@ -313,9 +346,10 @@ def check_onorm(got, want, bound, label):
 
 
 @pytest.mark.parametrize("name", list(ONORM))
-@pytest.mark.parametrize("R,Q,L", [(1, 64, 300), (4, 64, 200), (2, 32, 77), (4, 128, 130)])
-def test_out_norm_scan(R, Q, L, name):
-    say(f"output norm scan R={R} Q={Q} L={L} {name}")
+@pytest.mark.parametrize("R,Q,L,seg", [(1, 64, 300, 0), (4, 64, 200, 0), (2, 32, 77, 0), (4, 128, 130, 0),
+                                       (4, 64, 200, 1 << 20)])
+def test_out_norm_scan(R, Q, L, seg, name):
+    say(f"output norm scan R={R} Q={Q} L={L} seg={seg} {name}")
     B, H = 2, 3
     inp, pin = make_case(B, L, H, R, Q, seed=R * 50 + Q + L + 7)
     zfull = torch.randn(inp.x.shape, device=DEV, generator=torch.Generator(DEV).manual_seed(19)
@@ -324,7 +358,7 @@ def test_out_norm_scan(R, Q, L, name):
     p, variant = onorm_pro(pin, name, gain_t)
     x, z = gpu_args(inp, pin, variant, zfull)
     y, fs, (cB, cX) = m3.scan_fwd_pro(x, pin.Bp, pin.Cp, inp.dt, inp.A, inp.lam, inp.theta, inp.D,
-                                      Q, p, R, z=z, check=True)
+                                      Q, p, R, z=z, check=True, seg=seg)
     torch.cuda.synchronize()
     slices = [(b, h) for b in range(B) for h in range(H)]
     ref, zref = oracle_prologue(inp, pin, variant, slices, zfull=zfull)
