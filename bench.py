@@ -423,8 +423,10 @@ def prologue_figures(m3, roofline, torch, stream, dev, W, workload_inputs, peak_
     """The prefill with the block prologue fused (BCNorm with gains, B/C
     biases, structured MIMO input X = W_X o X') on the three prefill
     workloads' shapes, against the plain scan of the same shape (the
-    library's default kernel, and the one-chunk-per-workgroup kernel that the
-    prologue runs in)."""
+    library's default kernel, and the one-chunk-per-workgroup kernel; the
+    prologue scan runs in the warp-specialised kernel where the default
+    choice is that kernel, workload 2, else in the one-chunk-per-workgroup
+    kernel)."""
     from paper_2603_15569_amd.inputs import make_prologue_inputs
     out = {}
     for k in (1, 2, 3):

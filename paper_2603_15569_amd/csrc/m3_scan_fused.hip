@@ -953,14 +953,18 @@ void k_scan_fused(ScanArgs a) {
                 s_S[(pt * 16 + l16) * S::LDN + 16 * (ntl + 4 * half) + 4 * g + v] = from_f32<T>(Sin[m2][half][v]);
     }
     // y leaves in 16-byte pieces of its rows (NPC per lane and owned tile);
-    // with the gate, the matching pieces of z are loaded now and arrive
-    // during the inter-chunk products
+    // with the gate, the matching pieces of z are loaded before the
+    // inter-chunk products and arrive during them (the 512-row chunks with
+    // the prologue load a tile's pieces once its products are done, when its
+    // C^ fragments are dead: their registers are full until then)
     constexpr int RP = P / S::CE;                   // 16-byte pieces of a row
     constexpr int NPC = 16 * RP / kWave;
     static_assert(NPC * kWave == 16 * RP, "store pieces");
+    constexpr bool kLateZ = kPro && S::QR > 256;
     V16 zp[kGate ? TPW : 1][NPC];
-    if constexpr (kGate) {
-        // z as read: like x, or (structured) the P-vector Z' of each token
+    // z as read: like x, or (structured) the P-vector Z' of each token;
+    // the pieces of owned tile m, or of all (m < 0)
+    auto load_z = [&](int m) {
         const int64_t zin_tok = sz ? (int64_t)P : (int64_t)(R * P);
         const int zr_el = sz ? 0 : P;
         const uint32_t zin_b = (uint32_t)(tstr * zin_tok * sizeof(T));
@@ -968,14 +972,16 @@ void k_scan_fused(ScanArgs a) {
                                   (uint32_t)(((nvalid - 1) * tstr * zin_tok + (R - 1) * zr_el + P) *
                                              (int64_t)sizeof(T)));
 #pragma unroll
-        for (int m = 0; m < TPW; ++m)
+        for (int mm = 0; mm < TPW; ++mm)
 #pragma unroll
             for (int i = 0; i < NPC; ++i) {
+                if (m >= 0 && mm != m) continue;
                 const int k = lane + i * kWave, rl = k / RP, col = (k % RP) * S::CE;
-                const int row = owned_tile<S>(wave, m) * 16 + rl, t = row / R, r = row % R;
-                zp[m][i] = buf_load<V16>(rz, tok_off(t, zin_b) + (uint32_t)((r * zr_el + col) * sizeof(T)));
+                const int row = owned_tile<S>(wave, mm) * 16 + rl, t = row / R, r = row % R;
+                zp[mm][i] = buf_load<V16>(rz, tok_off(t, zin_b) + (uint32_t)((r * zr_el + col) * sizeof(T)));
             }
-    }
+    };
+    if constexpr (kGate && !kLateZ) load_z(-1);
     if constexpr (!kMerged) {
         if constexpr (!kEarlyC) load_c();
         rotate_cf();
@@ -998,6 +1004,7 @@ void k_scan_fused(ScanArgs a) {
                 else acc[m][pt][v] = ecum * tmp[v];
             }
         }
+        if constexpr (kGate && kLateZ) load_z(m);
     }
     if constexpr (!kMerged) {
         // intra-chunk term over the row blocks at or below each owned tile
