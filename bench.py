@@ -80,7 +80,7 @@ def main():
         return
 
     if args.bwd_calls is not None:
-        bw = BackwardCase(m3, torch, dev, WORKLOADS[1], workload_inputs)
+        bw = BackwardCase(m3, torch, dev, WORKLOADS, workload_inputs)
         bw.call()
         ms = bw.time(stream, args.bwd_calls)
         print(json.dumps({"bwd_workload": 1, "calls": args.bwd_calls, "ms_per_call": round(ms, 5)}),
@@ -263,13 +263,17 @@ def main():
                                               workload_inputs, peak_gbs, peak_tfs)
         torch.cuda.empty_cache()
         log("extras: backward")
-        bw = BackwardCase(m3, torch, dev, WORKLOADS[1], workload_inputs)
+        bw = BackwardCase(m3, torch, dev, WORKLOADS, workload_inputs)
         for _ in range(3):
             bw.call()
         ms = bw.time(stream, 20)
         result["backward_siso"] = bw.figures(roofline, ms, peak_gbs, peak_tfs)
         result["backward_siso"]["traffic"] = measured_traffic("backward_siso")
         del bw
+        torch.cuda.empty_cache()
+        log("extras: backward at rank 4 and SISO, workload 2's batch, length and heads")
+        result["backward_mimo"] = backward_mimo_figures(torch, stream, dev, WORKLOADS, workload_inputs,
+                                                        m3, roofline, peak_gbs, peak_tfs)
         torch.cuda.empty_cache()
         log("extras: decode at state size 64")
         result["decode_state64"] = decode_state64_figures(m3, roofline, torch, stream, dev,
@@ -522,15 +526,16 @@ def decode_state64_figures(m3, roofline, torch, stream, dev, wd, dec_us_128, pea
 
 
 class BackwardCase:
-    """m3_scan_bwd on the SISO prefill workload's shape (B=4, L=2048, H=16,
-    P=64, N=128, chunk 64): inputs, dy, dJ/d(final state) and the outputs
-    and workspace allocated once."""
+    """m3_scan_bwd on prefill workload k's shape (by default the SISO one:
+    B=4, L=2048, H=16, P=64, N=128, chunk 64; `override` changes fields such
+    as the rank and the chunk): inputs, dy, dJ/d(final state) and the
+    outputs and workspace allocated once."""
 
-    def __init__(self, m3, torch, dev, w, workload_inputs):
+    def __init__(self, m3, torch, dev, W, workload_inputs, k=1, **override):
         import ctypes
         self.m3, self.torch, self.ctypes = m3, torch, ctypes
-        self.inp = inp = workload_inputs(1, device=dev)
-        self.chunk = w["chunk"]
+        self.inp = inp = workload_inputs(k, device=dev, **override)
+        self.chunk = override.get("chunk", W[k]["chunk"])
         g = torch.Generator(dev).manual_seed(77)
         B, L, H, R, P = inp.x.shape
         N = inp.Bm.shape[-1]
@@ -576,6 +581,27 @@ class BackwardCase:
                 "bound": "hbm", "achieved_gbs": round(gbs, 1), "frac": round(gbs / peak_gbs, 4),
                 "bytes_per_launch": nbytes, "flops_per_launch": flops,
                 "mfma_tflops": round(flops / (ms * 1e-3) / 1e12, 2)}
+
+
+def backward_mimo_figures(torch, stream, dev, W, workload_inputs, m3, roofline, peak_gbs, peak_tfs):
+    """The backward at rank 4 (chunk 16: 64 rows a chunk, the backward's
+    tile) on workload 2's batch, length and heads, and the SISO backward
+    (chunk 64) of the same batch, length and heads: the paper puts MIMO
+    training at rank 4 about twice as slow as SISO (Sec. 3.3)."""
+    out = {}
+    for name, ov in (("mimo", dict(chunk=16)), ("siso", dict(rank=1, chunk=64))):
+        bw = BackwardCase(m3, torch, dev, W, workload_inputs, k=2, **ov)
+        for _ in range(2):
+            bw.call()
+        ms = bw.time(stream, 5)
+        out[name] = bw.figures(roofline, ms, peak_gbs, peak_tfs)
+        del bw
+        torch.cuda.empty_cache()
+    res = dict(out["mimo"])
+    res["siso_same_shape_ms"] = out["siso"]["ms"]
+    res["siso_same_shape_tokens_per_s"] = out["siso"]["tokens_per_s"]
+    res["time_ratio_to_siso"] = round(out["mimo"]["ms"] / out["siso"]["ms"], 3)
+    return res
 
 
 def measured_traffic(key):
