@@ -306,12 +306,22 @@ void k_scan_fused(ScanArgs a) {
     constexpr int DC = S::NJB < 1 ? S::NJB : 1;
     constexpr int DR = DA > DC ? DA : DC;
     Blk ring[DR];
+    // The merged pass takes the row blocks last to first: the first blocks
+    // worked on need the C^ fragments of few owned tiles (the last rows'), so
+    // each tile's C rows are waited for and rotated only when its first block
+    // comes, inside the block loop, instead of all before it (the sums of the
+    // aggregate and of the outputs are taken in that order too).  With the
+    // prologue the rotation also normalises, and the blocks keep their order:
+    // the per-tile normalisations measured slower there.
+    constexpr bool kRev = kMerged && !kPro;
+    auto blk = [](int sb) { return kRev ? S::NJB - 1 - sb : sb; };
 
     Frag cf[TPW][NK];   // C rows of the owned output tiles (rotated in the output phase)
     constexpr bool kEarlyC = S::NJB > 1;
     auto load_c = [&]() {
 #pragma unroll
-        for (int m = 0; m < TPW; ++m) {
+        for (int mi = 0; mi < TPW; ++mi) {
+            const int m = kRev ? TPW - 1 - mi : mi;   // (in the order the tiles are first used)
             const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
             const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + MM::KPL * g) * sizeof(T));
 #pragma unroll
@@ -366,7 +376,7 @@ void k_scan_fused(ScanArgs a) {
         // counters retire in order), so they overlap the prologue's arithmetic
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int d = 0; d < DA; ++d) fetch(d, ring[d]);
+        for (int d = 0; d < DA; ++d) fetch(blk(d), ring[d]);
         __builtin_amdgcn_sched_barrier(0);
         // chunks of several row blocks load the C rows of their output tiles
         // now too: the round trip overlaps the aggregate and the look-back
@@ -444,12 +454,13 @@ void k_scan_fused(ScanArgs a) {
     // lanes l16 + 16 g), so the fragments are rounded once.  A lane's rank
     // row r = l16 % R is the same in all its tiles, so the gain and bias of
     // its elements are read once per fragment pair (16-byte reads) and serve
-    // every tile.
-    auto rotate_cf = [&]() {
+    // every tile.  `only` >= 0 rotates that owned tile alone.
+    auto rotate_cf = [&](int only) {
         float scm[TPW], bscm[TPW];
         if constexpr (kPro) {
 #pragma unroll
             for (int m = 0; m < TPW; ++m) {
+                if (only >= 0 && m != only) continue;
                 const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
                 float ss = 0.f;
 #pragma unroll
@@ -481,6 +492,7 @@ void k_scan_fused(ScanArgs a) {
             }
 #pragma unroll
             for (int m = 0; m < TPW; ++m) {
+                if (only >= 0 && m != only) continue;
                 const int t = (owned_tile<S>(wave, m) * 16 + l16) / R;
                 float csv[MM::KPL], snv[MM::KPL];
                 cs_getn<MM::KPL>(&s_cs[t * LDT + kk * MM::K + MM::KPL * g], csv, snv);
@@ -602,21 +614,22 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     if constexpr (kMerged) {
-        rotate_cf();
+        if constexpr (!kRev) rotate_cf(-1);
 #pragma unroll
         for (int m = 0; m < TPW; ++m)
 #pragma unroll
             for (int pt = 0; pt < PT; ++pt) acc[m][pt] = f32x4{0.f, 0.f, 0.f, 0.f};
-        commit(0, ring[0], True{}, True{});
+        commit(blk(0), ring[0], True{}, True{});
         __syncthreads();
-        if (DA < S::NJB) fetch(DA, ring[0]);
+        if (DA < S::NJB) fetch(blk(DA), ring[0]);
     }
 #pragma unroll
-    for (int jb = 0; jb < S::NJB; ++jb) {
+    for (int sb = 0; sb < S::NJB; ++sb) {
+        const int jb = blk(sb);
         if constexpr (NBUF == 2) {
-            if (jb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
-                commit(jb + 1, ring[(jb + 1) % DA], True{}, True{});
-                if (jb + 1 + DA < S::NJB) fetch(jb + 1 + DA, ring[(jb + 1) % DA]);
+            if (sb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
+                commit(blk(sb + 1), ring[(sb + 1) % DA], True{}, True{});
+                if (sb + 1 + DA < S::NJB) fetch(blk(sb + 1 + DA), ring[(sb + 1) % DA]);
             }
         } else {
             if constexpr (S::NJB == 1) commit(jb, ring[0], True{}, True{});   // one block: keep B^ for the outputs
@@ -644,7 +657,17 @@ void k_scan_fused(ScanArgs a) {
                 for (int half = 0; half < 2; ++half) ms[m2][half] = MM::mma(af[half], bf, ms[m2][half]);
             }
         }
-        if constexpr (kMerged) out_block(jb);
+        if constexpr (kMerged) {
+            // an owned tile's C^ fragments are rotated just before the first
+            // block (in the reversed order) that works on it: its own last
+            // block, whose rows reach the tile's
+            if constexpr (kRev) {
+#pragma unroll
+                for (int m = 0; m < TPW; ++m)
+                    if (((m + 1) * S::NWO - 1) / 4 == jb) rotate_cf(m);
+            }
+            out_block(jb);
+        }
         __syncthreads();
     }
 
@@ -984,7 +1007,7 @@ void k_scan_fused(ScanArgs a) {
     if constexpr (kGate && !kLateZ) load_z(-1);
     if constexpr (!kMerged) {
         if constexpr (!kEarlyC) load_c();
-        rotate_cf();
+        rotate_cf(-1);
     }
     __syncthreads();   // s_S complete
     // inter-chunk term e^{cum_t} C^_t . S_in
