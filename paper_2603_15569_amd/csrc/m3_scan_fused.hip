@@ -571,10 +571,10 @@ void k_scan_fused(ScanArgs a) {
                     for (int u = 0; u < NV; ++u) {
                         const int tj = ((J0 + q) * 16 + 4 * g + u * R) / R;
                         // (above the diagonal the exponent may be large: the select drops
-                        // it; rank 4 keeps the base-e form, whose register allocation in
-                        // the 512-row chunks measured faster)
-                        const float e = R >= 4 ? exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj]
-                                               : exp2_fast(c2_t - s_c2[tj]) * s_sig[tj];
+                        // it; rank 4 with the prologue keeps the base-e form, whose
+                        // register allocation there spills less)
+                        const float e = (R >= 4 && kPro) ? exp_fast(fminf(cum_t - (float)s_cum[tj], 0.f)) * s_sig[tj]
+                                                         : exp2_fast(c2_t - s_c2[tj]) * s_sig[tj];
                         wv[u] = (tile_below(m) || tj < tt) ? e : (tj == tt ? gam_t : 0.f);
                     }
 #pragma unroll
