@@ -977,13 +977,13 @@ void k_scan_fused(ScanArgs a) {
     }
     // y leaves in 16-byte pieces of its rows (NPC per lane and owned tile);
     // with the gate, the matching pieces of z are loaded before the
-    // inter-chunk products and arrive during them (the 512-row chunks with
-    // the prologue load a tile's pieces once its products are done, when its
-    // C^ fragments are dead: their registers are full until then)
+    // inter-chunk products and arrive during them (the 512-row chunks load a
+    // tile's pieces once its products are done, when its C^ fragments are
+    // dead: their registers are full until then)
     constexpr int RP = P / S::CE;                   // 16-byte pieces of a row
     constexpr int NPC = 16 * RP / kWave;
     static_assert(NPC * kWave == 16 * RP, "store pieces");
-    constexpr bool kLateZ = kPro && S::QR > 256;
+    constexpr bool kLateZ = S::QR > 256;
     V16 zp[kGate ? TPW : 1][NPC];
     // z as read: like x, or (structured) the P-vector Z' of each token;
     // the pieces of owned tile m, or of all (m < 0)
