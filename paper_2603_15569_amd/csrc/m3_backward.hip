@@ -378,6 +378,7 @@ __global__ __launch_bounds__(kThrC) void k_bwd_chunk(BwdArgs a) {
     __shared__ float s_dv[kRows], s_dcy[kRows];                   // dJ/dv_j, y state term of cum_t
     __shared__ float s_tok[3][kWave];                             // per token: dcum, dsigma, dgamma
     __shared__ float s_red[2][4];
+    __shared__ float s_segd[kThrC / kWave - 1][kNH];                // dtheta: segment totals
 
     const int64_t slot = blockIdx.x, bh = slot / a.nchunks, c = slot % a.nchunks;
     const int64_t b = bh / a.H, h = bh % a.H, t0 = c * Q;
@@ -722,18 +723,40 @@ __global__ __launch_bounds__(kThrC) void k_bwd_chunk(BwdArgs a) {
             a.dApart[slot] = dAt;
             a.dDpart[slot] = s_red[0][0] + s_red[0][1] + s_red[0][2] + s_red[0][3];
         }
-    } else if (tid < 2 * kWave) {   // dtheta: suffix sums of dpsi per pair
-        const int i = tid - kWave;
+    }
+    // dtheta: suffix sums over the chunk's tokens of dpsi per pair (lane i),
+    // by waves 1 .. 7, one segment of TSD consecutive tokens each: the
+    // segment's own suffix sums, then the totals of the later segments
+    // through LDS
+    constexpr int NSD = kThrC / kWave - 1, TSD = (Q + NSD - 1) / NSD;
+    const int sd = wave - 1, i = lane;
+    float dl[TSD];
+    if (wave >= 1) {
         float acc = 0.f;
-        float *dth = a.dtheta + tok0 * kNH + i;
-        for (int t = nvalid - 1; t >= 0; --t) {
-            float d = 0.f;
 #pragma unroll
-            for (int r = 0; r < R; ++r)
-                d += s_dpsi[0][(t * R + r) * kNH + i] + s_dpsi[1][(t * R + r) * kNH + i];
-            if (t == nvalid - 1) d += pst[i];
+        for (int k = TSD - 1; k >= 0; --k) {
+            const int t = sd * TSD + k;
+            float d = 0.f;
+            if (t < nvalid) {
+#pragma unroll
+                for (int r = 0; r < R; ++r)
+                    d += s_dpsi[0][(t * R + r) * kNH + i] + s_dpsi[1][(t * R + r) * kNH + i];
+                if (t == nvalid - 1) d += pst[i];
+            }
             acc += d;
-            dth[(int64_t)t * a.H * kNH] = acc;
+            dl[k] = acc;
+        }
+        s_segd[sd][i] = acc;
+    }
+    __syncthreads();
+    if (wave >= 1) {
+        float off = 0.f;
+        for (int s2 = sd + 1; s2 < NSD; ++s2) off += s_segd[s2][i];
+        float *dth = a.dtheta + tok0 * kNH + i;
+#pragma unroll
+        for (int k = 0; k < TSD; ++k) {
+            const int t = sd * TSD + k;
+            if (t < nvalid) dth[(int64_t)t * a.H * kNH] = dl[k] + off;
         }
     }
 }
