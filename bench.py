@@ -106,7 +106,7 @@ def main():
     peak_gbs = roofline.HBM_BYTES_PER_S / 1e9
     peak_tfs = roofline.MFMA_BF16_FLOPS / 1e12
 
-    # ---------------- headline prefill: long-context MIMO (workload 3) ----------------
+    # ---------------- headline prefill: long-context MIMO, B=1 L=65536 H=32 R=4 ----------------
     log("inputs: long-context prefill")
     w3 = WORKLOADS[3]
     Q3 = w3["chunk"]
@@ -240,7 +240,7 @@ def main():
 
     if not args.no_extras:
         del ev
-        # ---------------- rank-4 prefill (workload 2) ----------------
+        # ---------------- rank-4 prefill, B=8 L=4096 H=32 ----------------
         log("extras: rank-4 prefill")
         w2 = WORKLOADS[2]
         p2 = workload_inputs(2, device=dev)
@@ -251,7 +251,7 @@ def main():
             "warp-specialised kernel, one workgroup per slice", measured_traffic("k_scan_ws_w2"))
         del p2
         torch.cuda.empty_cache()
-        # ---------------- SISO prefill (workload 1), gated and per-head variants ----------------
+        # ---------------- SISO prefill B=4 L=2048 H=16, gated and per-head variants ----------------
         log("extras: SISO prefill")
         result.update(siso_figures(m3, roofline, torch, np, stream, dev, WORKLOADS[1],
                                    workload_inputs, make_gate_input, step_in, dstep, dstate,
@@ -271,7 +271,7 @@ def main():
         result["backward_siso"]["traffic"] = measured_traffic("backward_siso")
         del bw
         torch.cuda.empty_cache()
-        log("extras: backward at rank 4 and SISO, workload 2's batch, length and heads")
+        log("extras: backward at rank 4 and SISO, B=8 L=4096 H=32")
         result["backward_mimo"] = backward_mimo_figures(torch, stream, dev, WORKLOADS, workload_inputs,
                                                         m3, roofline, peak_gbs, peak_tfs)
         torch.cuda.empty_cache()
@@ -429,8 +429,8 @@ def prologue_figures(m3, roofline, torch, stream, dev, W, workload_inputs, peak_
     workloads' shapes, against the plain scan of the same shape (the
     library's default kernel, and the one-chunk-per-workgroup kernel; the
     prologue scan runs in the warp-specialised kernel where the default
-    choice is that kernel, workload 2, else in the one-chunk-per-workgroup
-    kernel)."""
+    choice is that kernel, the rank-4 B=8 L=4096 prefill, else in the
+    one-chunk-per-workgroup kernel)."""
     from paper_2603_15569_amd.inputs import make_prologue_inputs
     out = {}
     for k in (1, 2, 3):
@@ -585,7 +585,8 @@ class BackwardCase:
 
 def backward_mimo_figures(torch, stream, dev, W, workload_inputs, m3, roofline, peak_gbs, peak_tfs):
     """The backward at rank 4 (chunk 16: 64 rows a chunk, the backward's
-    tile) on workload 2's batch, length and heads, and the SISO backward
+    tile) on the rank-4 prefill's batch, length and heads (B=8 L=4096 H=32),
+    and the SISO backward
     (chunk 64) of the same batch, length and heads: the paper puts MIMO
     training at rank 4 about twice as slow as SISO (Sec. 3.3)."""
     out = {}

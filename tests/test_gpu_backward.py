@@ -135,17 +135,17 @@ def test_backward_per_token_A_no_final_no_init(R, Q):
                 assert out[key][b, 0, h].abs().max().item() <= TOL * full, (key, b, h)
 
 
-def test_backward_workload1_shape():
+def test_backward_siso_prefill_shape():
     """The SISO prefill workload's shape (B=4, L=2048, H=16, chunk 64): every
     slice."""
     w = WORKLOADS[1]
-    say("backward workload 1 shape, all 64 slices")
+    say("backward SISO B=4 L=2048 H=16, all 64 slices")
     inp = workload_inputs(1, device=DEV)
     out, dy, dfin, h0, A = grads_case(inp, w["chunk"], seed=11)
     slices = [(b, h) for b in range(w["batch"]) for h in range(w["nheads"])]
     ref = oracle_grads(inp, A, dy, dfin, h0, slices)
-    compare(out, ref, slices, "bwd workload 1", A, w["nheads"])
-    check_head_sums(out, ref, slices, w["nheads"], "bwd workload 1")
+    compare(out, ref, slices, "bwd SISO B=4 L=2048", A, w["nheads"])
+    check_head_sums(out, ref, slices, w["nheads"], "bwd SISO B=4 L=2048")
 
 
 def test_backward_deterministic():

@@ -250,8 +250,8 @@ def sample_slices(batch, nheads, count, seed):
 def test_prologue_workloads(k):
     """The prefill workloads' shapes with the whole prologue (norm, gains,
     biases, structured input; raw B', C', X' drawn by make_prologue_inputs):
-    workload 1 on every slice, workloads 2 and 3 on 16 seeded slices plus the
-    first and the last."""
+    the SISO B=4 L=2048 prefill on every slice, the rank-4 B=8 L=4096 and
+    B=1 L=65536 prefills on 16 seeded slices plus the first and the last."""
     w = WORKLOADS[k]
     say(f"prologue workload {k}")
     inp = workload_inputs(k, device=DEV)
