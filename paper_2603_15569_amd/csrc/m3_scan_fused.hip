@@ -318,10 +318,19 @@ void k_scan_fused(ScanArgs a) {
 
     Frag cf[TPW][NK];   // C rows of the owned output tiles (rotated in the output phase)
     constexpr bool kEarlyC = S::NJB > 1;
-    auto load_c = [&]() {
+    // In the reversed order, owned tile m is first used (and rotated) in
+    // block pass c_rot(m); its C rows are loaded two passes before that,
+    // after that pass's prefetch of the next block (so the block waits do
+    // not wait for them), and only the tiles used in the first two passes
+    // load with the prologue: its burst of loads stays small.
+    auto c_rot = [](int m) { return S::NJB - 1 - ((m + 1) * S::NWO - 1) / 4; };
+    auto c_issue = [&](int m) { return kRev && c_rot(m) >= 2 ? c_rot(m) - 2 : -1; };
+    // the owned tiles' C rows issued at pass `at` (-1: the prologue)
+    auto load_c = [&](int at) {
 #pragma unroll
         for (int mi = 0; mi < TPW; ++mi) {
             const int m = kRev ? TPW - 1 - mi : mi;   // (in the order the tiles are first used)
+            if (c_issue(m) != at) continue;
             const int row = owned_tile<S>(wave, m) * 16 + l16, t = row / R, r = row % R;
             const uint32_t off = tok_off(t, bstr_b) + (uint32_t)((r * N + MM::KPL * g) * sizeof(T));
 #pragma unroll
@@ -379,9 +388,10 @@ void k_scan_fused(ScanArgs a) {
         for (int d = 0; d < DA; ++d) fetch(blk(d), ring[d]);
         __builtin_amdgcn_sched_barrier(0);
         // chunks of several row blocks load the C rows of their output tiles
-        // now too: the round trip overlaps the aggregate and the look-back
+        // now too (in the reversed block order only those of the tiles used
+        // first): the round trip overlaps the aggregate and the look-back
         // (single-block chunks have no registers to spare for them)
-        if constexpr (kEarlyC) load_c();
+        if constexpr (kEarlyC) load_c(-1);
         __builtin_amdgcn_sched_barrier(0);
         // dt and lambda are zero past the end of the sequence, so
         // sigma_{L-1} = gamma_{L-1} and rows past the end carry zeros
@@ -630,6 +640,7 @@ void k_scan_fused(ScanArgs a) {
             if (sb + 1 < S::NJB) {   // stage the next block while this one feeds the MFMAs
                 commit(blk(sb + 1), ring[(sb + 1) % DA], True{}, True{});
                 if (sb + 1 + DA < S::NJB) fetch(blk(sb + 1 + DA), ring[(sb + 1) % DA]);
+                if constexpr (kRev) load_c(sb);
             }
         } else {
             if constexpr (S::NJB == 1) commit(jb, ring[0], True{}, True{});   // one block: keep B^ for the outputs
@@ -1006,7 +1017,7 @@ void k_scan_fused(ScanArgs a) {
     };
     if constexpr (kGate && !kLateZ) load_z(-1);
     if constexpr (!kMerged) {
-        if constexpr (!kEarlyC) load_c();
+        if constexpr (!kEarlyC) load_c(-1);
         rotate_cf(-1);
     }
     __syncthreads();   // s_S complete
