@@ -311,8 +311,10 @@ void k_scan_fused(ScanArgs a) {
     // each tile's C rows are waited for and rotated only when its first block
     // comes, inside the block loop, instead of all before it (the sums of the
     // aggregate and of the outputs are taken in that order too).  With the
-    // prologue the rotation also normalises, and the blocks keep their order:
-    // the per-tile normalisations measured slower there.
+    // prologue the rotation also normalises, and the blocks keep their order
+    // (the per-tile normalisations measured slower there): all tiles are
+    // rotated at once, after the first block's aggregate products, with
+    // their C rows loaded once the first block is staged.
     constexpr bool kRev = kMerged && !kPro;
     auto blk = [](int sb) { return kRev ? S::NJB - 1 - sb : sb; };
 
@@ -389,9 +391,10 @@ void k_scan_fused(ScanArgs a) {
         __builtin_amdgcn_sched_barrier(0);
         // chunks of several row blocks load the C rows of their output tiles
         // now too (in the reversed block order only those of the tiles used
-        // first): the round trip overlaps the aggregate and the look-back
-        // (single-block chunks have no registers to spare for them)
-        if constexpr (kEarlyC) load_c(-1);
+        // first; in the forward order, with the prologue, after the first
+        // block is staged): the round trip overlaps the aggregate and the
+        // look-back (single-block chunks have no registers to spare for them)
+        if constexpr (kEarlyC && !(kMerged && !kRev)) load_c(-1);
         __builtin_amdgcn_sched_barrier(0);
         // dt and lambda are zero past the end of the sequence, so
         // sigma_{L-1} = gamma_{L-1} and rows past the end carry zeros
@@ -624,7 +627,6 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
     for (int m2 = 0; m2 < PTW; ++m2) ms[m2][0] = ms[m2][1] = f32x4{0.f, 0.f, 0.f, 0.f};
     if constexpr (kMerged) {
-        if constexpr (!kRev) rotate_cf(-1);
 #pragma unroll
         for (int m = 0; m < TPW; ++m)
 #pragma unroll
@@ -632,6 +634,7 @@ void k_scan_fused(ScanArgs a) {
         commit(blk(0), ring[0], True{}, True{});
         __syncthreads();
         if (DA < S::NJB) fetch(blk(DA), ring[0]);
+        if constexpr (!kRev) load_c(-1);
     }
 #pragma unroll
     for (int sb = 0; sb < S::NJB; ++sb) {
@@ -676,6 +679,8 @@ void k_scan_fused(ScanArgs a) {
 #pragma unroll
                 for (int m = 0; m < TPW; ++m)
                     if (((m + 1) * S::NWO - 1) / 4 == jb) rotate_cf(m);
+            } else if (sb == 0) {
+                rotate_cf(-1);   // (after the first block's aggregate: the C rows arrive meanwhile)
             }
             out_block(jb);
         }
