@@ -340,22 +340,55 @@ void k_scan_fused(ScanArgs a) {
         }
     };
     // ---- 2. prologue ----
-    if constexpr (kPro) {   // the head's prologue tables (read after the prologue's barriers)
+    // The head's prologue tables: every thread's entries are loaded at once,
+    // ahead of the item's other loads (buffer loads: a table that is not
+    // given reads as zeros through an empty range and takes its default
+    // below), and written to LDS before the prologue's first barrier; they
+    // are read after the prologue's barriers.
+    constexpr int TEN = (R * N + S::NTHR - 1) / S::NTHR, TEP = (R * P + S::NTHR - 1) / S::NTHR;
+    float pvn[kPro ? TEN : 1][4], pvp[kPro ? TEP : 1][3];
+    if constexpr (kPro) {
         const int64_t hn = h * (R * N), hp = h * (R * P);
-        for (int e = tid; e < R * N; e += S::NTHR) {
-            const int r = e / N, n = e % N;
-            const int q = bgb(r, n % NH) + (n < NH ? 0 : 2);
-            s_pro[q] = a.pro.gB ? a.pro.gB[hn + e] : 1.f;
-            s_pro[q + 1] = a.pro.bB ? a.pro.bB[hn + e] : 0.f;
-            s_pro[kPC + e] = a.pro.gC ? a.pro.gC[hn + e] : 1.f;
-            s_pro[kPCb + e] = a.pro.bC ? a.pro.bC[hn + e] : 0.f;
-        }
-        for (int e = tid; e < R * P; e += S::NTHR) {
-            s_pro[kPWX + e] = a.pro.wx ? a.pro.wx[hp + e] : 1.f;
-            s_pro[kPWZ + e] = a.pro.wz ? a.pro.wz[hp + e] : 1.f;
-            s_pro[kPGY + e] = a.pro.og ? a.pro.og[hp + e] : 1.f;
-        }
+        auto trs = [&](const float *t, int64_t off, int n) {
+            return make_rsrc(t ? t + off : a.D, t ? (uint32_t)(n * 4) : 0u);
+        };
+        const Rsrc rt[4] = {trs(a.pro.gB, hn, R * N), trs(a.pro.bB, hn, R * N), trs(a.pro.gC, hn, R * N),
+                            trs(a.pro.bC, hn, R * N)};
+        const Rsrc rp[3] = {trs(a.pro.wx, hp, R * P), trs(a.pro.wz, hp, R * P), trs(a.pro.og, hp, R * P)};
+#pragma unroll
+        for (int k = 0; k < TEN; ++k)
+#pragma unroll
+            for (int u = 0; u < 4; ++u) pvn[k][u] = buf_load<float>(rt[u], (uint32_t)((tid + k * S::NTHR) * 4));
+#pragma unroll
+        for (int k = 0; k < TEP; ++k)
+#pragma unroll
+            for (int u = 0; u < 3; ++u) pvp[k][u] = buf_load<float>(rp[u], (uint32_t)((tid + k * S::NTHR) * 4));
     }
+    auto write_tables = [&]() {
+        if constexpr (kPro) {
+#pragma unroll
+            for (int k = 0; k < TEN; ++k) {
+                const int e = tid + k * S::NTHR;
+                if (e < R * N) {
+                    const int r = e / N, n = e % N;
+                    const int q = bgb(r, n % NH) + (n < NH ? 0 : 2);
+                    s_pro[q] = a.pro.gB ? pvn[k][0] : 1.f;
+                    s_pro[q + 1] = a.pro.bB ? pvn[k][1] : 0.f;
+                    s_pro[kPC + e] = a.pro.gC ? pvn[k][2] : 1.f;
+                    s_pro[kPCb + e] = a.pro.bC ? pvn[k][3] : 0.f;
+                }
+            }
+#pragma unroll
+            for (int k = 0; k < TEP; ++k) {
+                const int e = tid + k * S::NTHR;
+                if (e < R * P) {
+                    s_pro[kPWX + e] = a.pro.wx ? pvp[k][0] : 1.f;
+                    s_pro[kPWZ + e] = a.pro.wz ? pvp[k][1] : 1.f;
+                    s_pro[kPGY + e] = a.pro.og ? pvp[k][2] : 1.f;
+                }
+            }
+        }
+    };
     {
         // angles first (the largest prologue load): thread (pair i, segment seg)
         const int i = tid % NH, seg = tid / NH;
@@ -419,6 +452,7 @@ void k_scan_fused(ScanArgs a) {
             ps[k] = run;
         }
         s_segtot[seg * NH + i] = run;
+        if constexpr (kPro) write_tables();
         __syncthreads();
         if (tid < Q) {
             Acc off = 0;
