@@ -2,6 +2,8 @@
 // and G chunks per workgroup): shape traits of the N = 128, P = 64 tiling,
 // element helpers, coherent accesses of the look-back, the control block.
 #pragma once
+#include <type_traits>
+
 #include "m3_device.h"
 #include "m3_internal.h"
 
@@ -467,6 +469,41 @@ inline int resident_capacity(const void *fn, int nthr, int *cache) {
     v = ncu * (per > 0 ? per : 1);
     __atomic_store_n(&cache[dev], v, __ATOMIC_RELAXED);
     return v;
+}
+
+// Initial state plus the carried previous-input term of token 0 for the K
+// state elements a lane owns (element k at row n_of(k), column p_of(k) of the
+// N x P state): h_{-1}[n][p] + wb sum_r B_{-1}[r][n] X_{-1}[r][p], with either
+// part absent when its pointer is null (the carry's B and X come together).
+// The null tests are taken once, outside the element loop, so that each
+// case's element loads are issued together instead of one round trip each.
+template <typename T, int R, int N, int P, int K, class FN, class FP>
+__device__ __forceinline__ void init_elems(const float *ist, const T *iB, const T *iX, float wb, FN n_of,
+                                           FP p_of, float *out) {
+    auto fill = [&](auto kI, auto kB) {
+#pragma unroll
+        for (int k = 0; k < K; ++k) {
+            const int n = n_of(k), p = p_of(k);
+            float sv = 0.f;
+            if constexpr (decltype(kI)::value) sv = ist[n * P + p];
+            if constexpr (decltype(kB)::value) {
+                float u = 0.f;
+#pragma unroll
+                for (int r = 0; r < R; ++r) u += to_f32(iB[r * N + n]) * to_f32(iX[r * P + p]);
+                sv += wb * u;
+            }
+            out[k] = sv;
+        }
+    };
+    using Yes = std::integral_constant<bool, true>;
+    using No = std::integral_constant<bool, false>;
+    if (ist) {
+        if (iB) fill(Yes{}, Yes{});
+        else fill(Yes{}, No{});
+    } else {
+        if (iB) fill(No{}, Yes{});
+        else fill(No{}, No{});
+    }
 }
 
 }  // namespace scan

@@ -444,23 +444,11 @@ void k_scan_seg(ScanArgs a) {
         }
         const T *iB = a.init_cB ? static_cast<const T *>(a.init_cB) + sl * (R * N) : nullptr;
         const T *iX = a.init_cX ? static_cast<const T *>(a.init_cX) + sl * (R * P) : nullptr;
-#pragma unroll
-        for (int m2 = 0; m2 < PTW; ++m2) {
-            const int k = wave + NW * m2, ntl = k % 4, pt = k / 4, p = pt * 16 + l16;
-#pragma unroll
-            for (int half = 0; half < 2; ++half)
-#pragma unroll
-                for (int v = 0; v < 4; ++v) {
-                    const int n = 16 * (ntl + 4 * half) + 4 * g + v;
-                    float sv = ist ? ist[n * P + p] : 0.f;
-                    if (iB) {
-                        float u = 0.f;
-                        for (int r = 0; r < R; ++r) u += to_f32(iB[r * N + n]) * to_f32(iX[r * P + p]);
-                        sv += wb * u;
-                    }
-                    Si[m2][half][v] = sv;
-                }
-        }
+        // element (m2, half, v): row 16 (ntl + 4 half) + 4g + v, column 16 pt + l16
+        init_elems<T, R, N, P, PTW * 8>(
+            ist, iB, iX, wb,
+            [&](int e) { return 16 * ((wave + NW * (e / 8)) % 4 + 4 * ((e / 4) % 2)) + 4 * g + e % 4; },
+            [&](int e) { return (wave + NW * (e / 8)) / 4 * 16 + l16; }, &Si[0][0][0]);
     };
 
     using True = std::integral_constant<bool, true>;

@@ -631,21 +631,10 @@ void k_scan_ws(ScanArgs a) {
             }
             const T *iB = a.init_cB ? static_cast<const T *>(a.init_cB) + sl * (R * N) : nullptr;
             const T *iX = a.init_cX ? static_cast<const T *>(a.init_cX) + sl * (R * P) : nullptr;
-#pragma unroll
-            for (int pt = 0; pt < PT; ++pt)
-#pragma unroll
-                for (int half = 0; half < 2; ++half)
-#pragma unroll
-                    for (int v = 0; v < 4; ++v) {
-                        const int n = 16 * (sw + 4 * half) + 4 * g + v, p = 16 * pt + l16;
-                        float sv = ist ? ist[n * P + p] : 0.f;
-                        if (iB) {
-                            float u = 0.f;
-                            for (int r = 0; r < R; ++r) u += to_f32(iB[r * N + n]) * to_f32(iX[r * P + p]);
-                            sv += wb * u;
-                        }
-                        Sst[pt][half][v] = sv;
-                    }
+            // element (pt, half, v): row 16 (sw + 4 half) + 4g + v, column 16 pt + l16
+            init_elems<T, R, N, P, PT * 8>(
+                ist, iB, iX, wb, [&](int e) { return 16 * (sw + 4 * ((e / 4) % 2)) + 4 * g + e % 4; },
+                [&](int e) { return 16 * (e / 8) + l16; }, &Sst[0][0][0]);
         }
         auto write_st = [&]() {   // S^T [p][n] in bf16, 8-byte pieces
 #pragma unroll
