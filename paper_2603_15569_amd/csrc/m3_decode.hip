@@ -59,6 +59,7 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     T *cB = static_cast<T *>(a.cB) + bh * (R * N);
     T *cX = static_cast<T *>(a.cX) + bh * (R * P);
     const float dtv = a.dt[bh], lamv = a.lam[bh], Av = a.A[b * a.a_sb + h * a.a_sh];
+    const float Dh = a.D[h];   // (loaded with the step's scalars: used only by the last stage)
     // B_t, C_t, the carry and X in 16-byte pieces; the loaded B_t and X_t
     // pieces are also the new carry (written after the barrier below)
     typedef typename Vec8<T>::type V8;
@@ -271,7 +272,6 @@ __global__ __launch_bounds__(NT) void k_step(StepArgs a) {
     }
     __syncthreads();
     T *yt = static_cast<T *>(a.y) + bh * (R * P);
-    const float Dh = a.D[h];
 #pragma unroll
     for (int k = 0; k < TZ; ++k) {
         const int e = tid + k * NT, ec = min(e, R * P - 1);
