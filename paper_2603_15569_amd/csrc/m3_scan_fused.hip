@@ -23,7 +23,10 @@
 //      a cos/sin table in LDS;
 //   3. aggregate first: per 64-row block, B^ and W x staged row-major in LDS
 //      and M += B^T W x (MFMA, K = rows, operands read with transposing LDS
-//      reads); A_c published (flag AGG);
+//      reads); A_c published (flag AGG) unless the predecessor is already
+//      inclusive.  bf16 chunks of several blocks (two LDS buffers) form the
+//      intra-chunk outputs of step 5 in this same pass (the merged pass),
+//      taking the blocks last to first without the prologue;
 //   4. decoupled look-back: predecessors' flags probed 16 at a time back to
 //      the nearest inclusive state (flag INC) or the sequence start, then the
 //      aggregates after it folded forward with the step the owners use for
@@ -36,7 +39,8 @@
 //      G^T = B^ C^T (MFMA, K = N) masked by w_tj, y += (w o G) x (MFMA,
 //      K = rows); D x added; y staged per wave from the (transposed)
 //      accumulator tiles and stored.  A chunk of a single 64-row block
-//      stages B^ once for both uses; longer chunks restage it from cache.
+//      stages B^ once for both uses; merged chunks only add the inter-chunk
+//      term here; other longer chunks (fp32) restage their blocks.
 // The workspace's control block carries the tickets from call to call: the
 // call's first item clears the flags (every other item waits for that before
 // its first flag access), every item counts itself done after its last flag
@@ -426,7 +430,8 @@ void k_scan_fused(ScanArgs a) {
         // now too (in the reversed block order only those of the tiles used
         // first; in the forward order, with the prologue, after the first
         // block is staged): the round trip overlaps the aggregate and the
-        // look-back (single-block chunks have no registers to spare for them)
+        // look-back (single-block chunks load them in the output phase: earlier
+        // loads measured slower there, their waits delaying the publications)
         if constexpr (kEarlyC && !(kMerged && !kRev)) load_c(-1);
         __builtin_amdgcn_sched_barrier(0);
         // dt and lambda are zero past the end of the sequence, so
