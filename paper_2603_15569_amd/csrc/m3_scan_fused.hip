@@ -761,12 +761,15 @@ void k_scan_fused(ScanArgs a) {
         flags_lost = s_i[0] != 0;
         __syncthreads();
     }
-    bool publish_agg = c > 0 && !last && !flags_lost;
-    if (S::NJB > 1 && publish_agg) {
+    // (chunks of several blocks read the predecessor's flag first: if it is
+    // inclusive, the look-back below takes that state without probing)
+    bool publish_agg = c > 0 && !last && !flags_lost, pred_inc = false;
+    if (S::NJB > 1 && c > 0 && !flags_lost) {
         if (tid == 0)
-            s_i[0] = __hip_atomic_load(a.flags + slot - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != kFlagInc;
+            s_i[0] = __hip_atomic_load(a.flags + slot - 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == kFlagInc;
         __syncthreads();
-        publish_agg = s_i[0] != 0;
+        pred_inc = s_i[0] != 0;
+        publish_agg = publish_agg && !pred_inc;
     }
     if (publish_agg) {
         unsigned long long *dst = reinterpret_cast<unsigned long long *>(a.agg + slot * SZ);
@@ -817,7 +820,7 @@ void k_scan_fused(ScanArgs a) {
     } else {
         const int64_t sbase = seq_slot;
         int64_t j = c - 1;        // next predecessor to probe
-        int64_t jt = flags_lost ? c - 1 : -2;   // terminal: -1 sequence start, >= 0 inclusive state
+        int64_t jt = (flags_lost || pred_inc) ? c - 1 : -2;   // terminal: -1 sequence start, >= 0 inclusive state
         bool timed_out = flags_lost;
         while (jt == -2) {
             // probe predecessors j, j-1, ..., j-15 at once (lanes of wave 0)
